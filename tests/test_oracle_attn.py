@@ -1,0 +1,303 @@
+"""Pins for the oracle's attention (no GPU).
+
+The oracle follows Algorithm 1 (without smoothing Q) with the two-level
+quantization of P~ (Sec. 3.2).  Nothing here compares the oracle with itself:
+each test checks it against a textbook definition (softmax attention in fp64),
+a closed form, an invariance the mathematics guarantees, or a claim the paper
+states (Table 1, smoothing ablation).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2505_11594_amd import workloads as wl
+
+E2M1 = np.array([0, .5, 1, 1.5, 2, 3, 4, 6, -0., -.5, -1, -1.5, -2, -3, -4, -6])
+
+
+def textbook_attention(q, k, v, causal):
+    """fp64 softmax(q k^T / sqrt(D)) v for one head; inputs float arrays [N, D]."""
+    N, D = q.shape
+    s = (q.astype(np.float64) @ k.astype(np.float64).T) / np.sqrt(D)
+    if causal:
+        s = np.where(np.tril(np.ones((N, N), bool)), s, -np.inf)
+    s -= s.max(axis=1, keepdims=True)
+    p = np.exp(s)
+    return (p / p.sum(axis=1, keepdims=True)) @ v.astype(np.float64)
+
+
+def widen(bits, dt):
+    return wl.from_bits(bits, dt)
+
+
+@pytest.mark.parametrize("bkv", [16, 64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("N", [200, 256])
+def test_identity_quantizer_equals_textbook_softmax(bkv, causal, N):
+    """fmt NONE (no quantization) reduces Algorithm 1 + two-level scaling to softmax attention."""
+    q, k, v = wl.make_inputs(1, 2, N, 64, wl.IN_BF16, seed=11, k_bias_var=4.0)
+    out, tol, cnt = oracle.attn(q, k, v, wl.IN_BF16, causal, oracle.FMT_NONE, bkv)
+    out = out.reshape(1, 2, N, 64)
+    for h in range(2):
+        ref = textbook_attention(widen(q[0, h], 1), widen(k[0, h], 1), widen(v[0, h], 1), causal)
+        err = np.abs(out[0, h] - ref).max() / np.abs(ref).max()
+        assert err < 2e-6, err
+
+
+def test_identity_quantizer_direct_mode_and_no_smoothing_agree():
+    q, k, v = wl.make_inputs(1, 1, 160, 64, wl.IN_FP16, seed=12)
+    a, _, _ = oracle.attn(q, k, v, wl.IN_FP16, False, oracle.FMT_NONE, 32)
+    b, _, _ = oracle.attn(q, k, v, wl.IN_FP16, False, oracle.FMT_NONE, 32, flags=oracle.DIRECT_P)
+    c, _, _ = oracle.attn(q, k, v, wl.IN_FP16, False, oracle.FMT_NONE, 32, flags=oracle.NO_SMOOTH_K)
+    assert np.abs(a - b).max() < 1e-6 and np.abs(a - c).max() < 1e-6
+
+
+@pytest.mark.parametrize("fmt", [oracle.FMT_MX, oracle.FMT_NV16])
+def test_closed_form_q_zero_gives_mean_of_dequantized_v(fmt):
+    """Q = 0: every score is 0, so P~2 = R on every key, every P code is 6 at a
+    unit (MX) / 448 (NV16) scale and O is the mean of the dequantized V."""
+    N, D = 192, 64
+    q, k, v = wl.make_inputs(1, 1, N, D, wl.IN_BF16, seed=13)
+    q[:] = 0
+    out, _, _ = oracle.attn(q, k, v, wl.IN_BF16, False, fmt, 64)
+    vc, vs, _, _ = oracle.quant(v, wl.IN_BF16, oracle.ROLE_V, fmt)
+    n = oracle.block_size(fmt)
+    sv = (2.0 ** (vs.astype(np.float64) - 127)) if fmt == oracle.FMT_MX else \
+        np.array([oracle.e4m3_decode(c) for c in range(256)])[vs]
+    vdeq = E2M1[vc[0, 0]] * np.repeat(sv[0, 0], n, axis=1)      # [D, Np]
+    expect = vdeq[:, :N].mean(axis=1)
+    assert np.abs(out[0] - expect).max() <= 1e-6 * np.abs(vdeq).max()
+    # l = N up to rounding, so the mean is exact to a few ulps in every row
+    assert np.allclose(out, expect[None, :], rtol=0, atol=1e-6 * np.abs(vdeq).max())
+    r = oracle.p_tile(np.zeros(64, np.float32), -np.inf, D, fmt)
+    assert np.all(r["codes"] == 7)
+    assert np.all(r["sbytes"] == (127 if fmt == oracle.FMT_MX else 0x7E))
+
+
+def _onehot_inputs(N=128, D=64, a=32.0, seed=14):
+    rng = np.random.default_rng(seed)
+    perm = rng.permutation(64)
+    q = np.zeros((1, 1, N, D), np.float32)
+    k = np.zeros((1, 1, N, D), np.float32)
+    for i in range(N):
+        q[0, 0, i, perm[i % 64]] = a
+    for j in range(64):
+        k[0, 0, j, j] = a          # keys 0..63 one-hot, keys 64.. zero
+    v = rng.standard_normal((1, 1, N, D)).astype(np.float32)
+    return perm, wl.to_bits(q, 1), wl.to_bits(k, 1), wl.to_bits(v, 1)
+
+
+@pytest.mark.parametrize("fmt", [oracle.FMT_MX, oracle.FMT_NV16])
+@pytest.mark.parametrize("bkv", [32, 64])
+def test_closed_form_one_hot_scores_select_one_value_row(fmt, bkv):
+    """Q_i and K_j are FP4-exact one-hot vectors (32 = 4 x 2^3); query i matches
+    key perm(i % 64) with a score gap of 32*32/8 = 128 natural-log units, so
+    O_i = deq(V^)[perm(i % 64)] up to fp32 rounding."""
+    perm, q, k, v = _onehot_inputs()
+    out, _, _ = oracle.attn(q, k, v, wl.IN_BF16, False, fmt, bkv, flags=oracle.NO_SMOOTH_K)
+    vc, vs, _, _ = oracle.quant(v, wl.IN_BF16, oracle.ROLE_V, fmt)
+    n = oracle.block_size(fmt)
+    sv = (2.0 ** (vs.astype(np.float64) - 127)) if fmt == oracle.FMT_MX else \
+        np.array([oracle.e4m3_decode(c) for c in range(256)])[vs]
+    vdeq = (E2M1[vc[0, 0]] * np.repeat(sv[0, 0], n, axis=1)).T   # [Np, D]
+    expect = vdeq[perm[np.arange(128) % 64]]
+    # P~2 at the tile max is exp2 of log2(6) plus the rounding of t*c2 (t = 1024,
+    # c2 = log2(e)/8): relative error <= ulp(184.7)/2 * ln 2 = 5.3e-6
+    assert np.abs(out - expect).max() <= 1e-5 * np.abs(vdeq).max()
+
+
+def test_closed_form_two_keys_in_two_tiles():
+    """Only two keys carry weight, one per KV tile, both tile maxima (so their
+    P codes are exactly 6 at scale 1 after the first level): O is the exact
+    two-term softmax average.  Pins alpha, s_P1, l and the V/K block indexing."""
+    N, D, bkv = 128, 64, 64
+    a = 32.0
+    q = np.zeros((1, 1, N, D), np.float32)
+    k = np.zeros((1, 1, N, D), np.float32)
+    q[0, 0, :, 0] = a            # every query: channel 0 = 32, channel 1 = 4
+    q[0, 0, :, 1] = 4.0
+    k[0, 0, 10, 0] = 4.0         # key 10 (tile 0): score 128
+    k[0, 0, 100, 0] = 4.0        # key 100 (tile 1): score 128 + 4*1 = 132
+    k[0, 0, 100, 1] = 1.0
+    k[0, 0, [j for j in range(N) if j not in (10, 100)], 0] = -4.0   # others: score -128
+    rng = np.random.default_rng(15)
+    v = np.zeros((1, 1, N, D), np.float32)
+    v[0, 0] = rng.standard_normal((N, D))                             # compared via deq(V^)
+    qb, kb, vb = wl.to_bits(q, 1), wl.to_bits(k, 1), wl.to_bits(v, 1)
+    out, _, _ = oracle.attn(qb, kb, vb, wl.IN_BF16, False, oracle.FMT_MX, bkv, flags=oracle.NO_SMOOTH_K)
+    vc, vs, _, _ = oracle.quant(vb, wl.IN_BF16, oracle.ROLE_V, oracle.FMT_MX)
+    vdeq = (E2M1[vc[0, 0]] * np.repeat(2.0 ** (vs[0, 0].astype(np.float64) - 127), 32, axis=1)).T
+    s10, s100 = 128.0 / 8.0, 132.0 / 8.0                 # S / sqrt(64)
+    w10 = 1.0 / (1.0 + np.exp(s100 - s10))
+    expect = w10 * vdeq[10] + (1 - w10) * vdeq[100]
+    # fused exponent argument: relative error <= ulp(t c2)/2 ln 2 with t c2 = 23.8
+    assert np.abs(out - expect[None, :]).max() < 4e-6 * np.abs(vdeq).max()
+
+
+@pytest.mark.parametrize("fmt", [oracle.FMT_MX, oracle.FMT_NV16])
+def test_permutation_within_blocks_and_of_tiles(fmt):
+    """Permuting keys together with their values inside each n-token block
+    leaves every block max, scale and code set unchanged (FP4MM sums are exact),
+    so O changes only by fp32 summation order; permuting whole KV tiles changes
+    only the order of the online-softmax merges."""
+    N, D, bkv = 256, 64, 64
+    n = oracle.block_size(fmt)
+    q, k, v = wl.make_inputs(1, 1, N, D, wl.IN_BF16, seed=16)
+    base, _, _ = oracle.attn(q, k, v, wl.IN_BF16, False, fmt, bkv)
+    rng = np.random.default_rng(17)
+    perm = np.concatenate([b0 + rng.permutation(n) for b0 in range(0, N, n)])
+    o1, _, _ = oracle.attn(q, k[:, :, perm], v[:, :, perm], wl.IN_BF16, False, fmt, bkv)
+    assert np.abs(o1 - base).max() < 1e-6 * np.abs(base).max()
+    tperm = np.concatenate([t * bkv + np.arange(bkv) for t in rng.permutation(N // bkv)])
+    o2, _, _ = oracle.attn(q, k[:, :, tperm], v[:, :, tperm], wl.IN_BF16, False, fmt, bkv)
+    assert np.abs(o2 - base).max() < 4e-6 * np.abs(base).max()
+
+
+def test_smoothing_k_removes_a_channel_bias_exactly():
+    """K with zero column means plus a per-channel bias b: smoothing K maps
+    both to the same K' (K + b - b), so the outputs are bit-identical; without
+    smoothing they differ (Algorithm 1 preprocessing; softmax is invariant to
+    the bias, which only shifts each row's scores)."""
+    N, D = 128, 64
+    rng = np.random.default_rng(18)
+    half = np.round(rng.standard_normal((1, 1, N // 2, D)) * 4) / 4
+    k0 = np.concatenate([half, -half], axis=2).astype(np.float32)      # column sums exactly 0
+    bias = rng.integers(-6, 7, (1, 1, 1, D)).astype(np.float32)
+    q, _, v = wl.make_inputs(1, 1, N, D, wl.IN_BF16, seed=19)
+    kb0, kb1 = wl.to_bits(k0, 1), wl.to_bits(k0 + bias, 1)
+    assert np.array_equal(wl.from_bits(kb1, 1), k0 + bias)               # exact in bf16
+    for fmt in (oracle.FMT_MX, oracle.FMT_NV16):
+        a, _, _ = oracle.attn(q, kb0, v, wl.IN_BF16, False, fmt, 64)
+        b, _, _ = oracle.attn(q, kb1, v, wl.IN_BF16, False, fmt, 64)
+        assert np.array_equal(a, b)
+        c, _, _ = oracle.attn(q, kb1, v, wl.IN_BF16, False, fmt, 64, flags=oracle.NO_SMOOTH_K)
+        assert not np.array_equal(a, c)
+
+
+def test_kmean_exact_and_order_independent():
+    q, k, v = wl.make_inputs(2, 3, 1000, 64, wl.IN_BF16, seed=20, k_bias_var=4.0)
+    mu, inexact = oracle.kmean(k, wl.IN_BF16)
+    assert inexact == 0
+    kf = wl.from_bits(k, 1).astype(np.float64)
+    ref = (kf.sum(axis=2) / 1000).astype(np.float32)   # fp64 sum is exact here, any order
+    assert np.array_equal(mu, ref)
+    rng = np.random.default_rng(21)
+    mu2, _ = oracle.kmean(np.ascontiguousarray(k[:, :, rng.permutation(1000)]), wl.IN_BF16)
+    assert np.array_equal(mu, mu2)
+
+
+# ------------------------------------------------------------------ P tile
+@pytest.mark.parametrize("fmt", [oracle.FMT_MX, oracle.FMT_NV16])
+def test_p_tile_two_level_properties(fmt):
+    """Sec. 3.2: s_P1 = rowmax(P~)/R, P~2 = P~/s_P1 = R 2^{c2 (S - t)}; the tile
+    max lands on code 6 at the top scale (E8M0 2^0, or E4M3 448); rowsum is the
+    unquantized sum; alpha = 2^{c2 (m_old - m_new)}."""
+    D = 128
+    c2 = np.float32(1.0 / (np.log(2.0) * np.sqrt(D)))
+    R = 6.0 if fmt == oracle.FMT_MX else 2688.0
+    n = oracle.block_size(fmt)
+    rng = np.random.default_rng(22)
+    for trial in range(200):
+        S = (rng.standard_normal(128) * rng.uniform(1, 60)).astype(np.float32)
+        S[rng.random(128) < 0.1] = -np.inf
+        if np.all(S == -np.inf):
+            S[0] = 0
+        t = float(S[S > -np.inf].max())
+        m_old = t + float(rng.uniform(-30, 30)) if trial % 3 else -np.inf
+        r = oracle.p_tile(S, m_old, D, fmt)
+        m_new = max(m_old, t)
+        assert r["m_new"] == np.float32(m_new)
+        valid = S > -np.inf
+        exact_p2 = R * np.exp2(np.float64(c2) * (S[valid].astype(np.float64) - t))
+        # the fp32 exponent argument carries a few roundings of size |S c2|, |t c2|, log2 R
+        rtol = (2 + np.abs(S[valid]) * c2 + abs(t) * c2 + np.log2(R)) * 2.0 ** -23 * np.log(2) + 2.0 ** -23
+        assert np.all(np.abs(r["p2"][valid] - exact_p2) <= rtol * exact_p2)
+        assert np.all(r["p2"][~valid] == 0)
+        rho = np.exp2(np.float64(c2) * (t - m_new))
+        # exponent arguments are differences of fp32 products t c2, m c2
+        e_tm = (2 + abs(t) * c2 + abs(m_new) * c2) * 2.0 ** -23 * np.log(2) + 2.0 ** -22
+        assert abs(r["s1"] * R - rho) <= e_tm * rho
+        assert abs(r["rowsum"] - rho / R * exact_p2.sum()) <= 2e-5 * rho / R * exact_p2.sum()
+        if m_old == -np.inf:
+            assert r["alpha"] == 0.0
+        else:
+            e_mm = (2 + abs(m_old) * c2 + abs(m_new) * c2) * 2.0 ** -23 * np.log(2) + 2.0 ** -22
+            a_ex = np.exp2(np.float64(c2) * (m_old - m_new))
+            assert abs(r["alpha"] - a_ex) <= e_mm * a_ex
+        kmax = int(np.argmax(np.where(valid, S, -np.inf)))
+        assert r["codes"][kmax] == 7
+        assert r["sbytes"][kmax // n] == (127 if fmt == oracle.FMT_MX else 0x7E)
+        # each block scale obeys the value-domain rule of phi up to fp32 rounding
+        for b in range(128 // n):
+            blk = slice(b * n, b * n + n)
+            am = r["p2"][blk].max()
+            if fmt == oracle.FMT_MX:
+                e = int(r["sbytes"][b]) - 127
+                if am > 6 * 2.0 ** -126:
+                    eps = (2 + 2 * abs(t) * c2 + np.log2(R)) * 2.0 ** -23 * np.log(2) + 2.0 ** -23
+                    assert 6 * 2.0 ** e >= am * (1 - eps) and 3 * 2.0 ** e < am * (1 + eps)
+            else:
+                assert r["sbytes"][b] == oracle.e4m3_encode(float(np.float32(am / np.float32(6))))
+
+
+def test_two_level_scales_use_the_e4m3_range():
+    """Appendix (two-level analysis): direct quantization keeps E4M3 P scales
+    in [0, 0.167] (35 values); two-level moves them up to 448 (127 values)."""
+    rng = np.random.default_rng(23)
+    direct, two = set(), set()
+    for trial in range(300):
+        S = (rng.standard_normal(128) * 20).astype(np.float32)
+        r1 = oracle.p_tile(S, float(S.max()), 128, oracle.FMT_NV16, flags=oracle.DIRECT_P)
+        r2 = oracle.p_tile(S, float(S.max()) + 5, 128, oracle.FMT_NV16)
+        direct |= set(r1["sbytes"].tolist())
+        two |= set(r2["sbytes"].tolist())
+    dv = [oracle.e4m3_decode(b) for b in direct]
+    tv = [oracle.e4m3_decode(b) for b in two]
+    assert max(dv) <= 0.1875 and max(tv) == 448.0
+    assert len(direct) <= 35 + 1 and len(two) > 60
+
+
+# ------------------------------------------------------------------ accuracy
+def _acc(fmt, flags=0, k_bias_var=0.0, seed=24, N=512, D=128):
+    q, k, v = wl.make_inputs(1, 2, N, D, wl.IN_BF16, seed=seed, k_bias_var=k_bias_var)
+    out, _, cnt = oracle.attn(q, k, v, wl.IN_BF16, False, fmt, 128, flags=flags)
+    ex = oracle.exact_attn(q, k, v, wl.IN_BF16, False)
+    return oracle.metrics(ex, out), cnt
+
+
+def test_accuracy_against_exact_attention():
+    mx, cnt = _acc(oracle.FMT_MX)
+    nv, _ = _acc(oracle.FMT_NV16)
+    assert cnt["inexact_s"] == 0
+    # i.i.d. N(0,1) data has flat softmax rows (|O| ~ 0.1), so FP4 errors are
+    # large relative to O; the paper's 99.5% is on real, peaked attention
+    assert mx["cossim"] > 0.95 and nv["cossim"] > 0.97
+    # Table 1(a): NVFP4 is more accurate than MXFP4
+    assert nv["cossim"] > mx["cossim"] and nv["l1"] < mx["l1"] and nv["rmse"] < mx["rmse"]
+    # Table 1(b): two-level beats direct quantization of P~ (NVFP4)
+    nvd, _ = _acc(oracle.FMT_NV16, flags=oracle.DIRECT_P)
+    assert nv["l1"] < nvd["l1"] and nv["cossim"] > nvd["cossim"]
+    mxd, _ = _acc(oracle.FMT_MX, flags=oracle.DIRECT_P)
+    assert mx["l1"] < mxd["l1"] and mx["cossim"] > mxd["cossim"]
+    # smoothing K (Algorithm 1 preprocessing; smoothing ablation) helps when K has a channel bias
+    sm, _ = _acc(oracle.FMT_MX, k_bias_var=4.0)
+    ns, _ = _acc(oracle.FMT_MX, flags=oracle.NO_SMOOTH_K, k_bias_var=4.0)
+    assert sm["l1"] < ns["l1"]
+
+
+def test_exact_attention_matches_textbook():
+    q, k, v = wl.make_inputs(1, 1, 96, 64, wl.IN_FP16, seed=25)
+    for causal in (False, True):
+        ex = oracle.exact_attn(q, k, v, wl.IN_FP16, causal)
+        ref = textbook_attention(widen(q[0, 0], 0), widen(k[0, 0], 0), widen(v[0, 0], 0), causal)
+        assert np.abs(ex - ref).max() < 1e-12
+
+
+def test_rows_subset_and_causal_skip_counts():
+    q, k, v = wl.make_inputs(1, 2, 300, 64, wl.IN_BF16, seed=26)
+    full, _, _ = oracle.attn(q, k, v, wl.IN_BF16, True, oracle.FMT_MX, 64)
+    rows = np.array([0, 63, 64, 299, 300, 599], dtype=np.int64)
+    sub, _, cnt = oracle.attn(q, k, v, wl.IN_BF16, True, oracle.FMT_MX, 64, rows=rows)
+    assert np.array_equal(sub, full[rows])
+    # row 0 sees only tile 0 (4 tiles skipped), row 299 sees all 5 tiles
+    assert cnt["skipped_tiles"] == 4 + 4 + 3 + 0 + 4 + 0
