@@ -1,0 +1,157 @@
+/*
+ * sage_mi355x.h -- C ABI of the MI355X (gfx950) microscaled-FP4 attention
+ * forward of SageAttention3 (arXiv 2505.11594).
+ *
+ * Every function returns an int status (sage_status).  Arguments are checked
+ * on the host before any HIP call, so invalid calls fail without touching the
+ * GPU.  All GPU work is enqueued asynchronously on the caller's stream; no
+ * function synchronizes.  The library never frees caller memory.  Pointers
+ * are device pointers unless stated otherwise; tensors are contiguous.
+ *
+ * Inputs Q, K, V are 16-bit (fp16 or bf16) [B, H, N, D] tensors: the problem
+ * statement of Algorithm 1 (N x d matrices per head, FP16 inputs) with the
+ * FlashAttention tiling of Sec. 2.  Inputs must be finite.
+ */
+#ifndef SAGE_MI355X_H
+#define SAGE_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SAGE_OK = 0,
+  SAGE_ERR_INVALID_ARG = 1,  /* null pointer, bad size, misalignment, unknown flag bits */
+  SAGE_ERR_UNSUPPORTED = 2,  /* a valid request this build does not implement          */
+  SAGE_ERR_HIP = 3,          /* a HIP runtime call or kernel launch failed              */
+  SAGE_ERR_WORKSPACE = 4     /* caller workspace smaller than the size query returned   */
+} sage_status;
+
+/* ---- fmt bitfield ----------------------------------------------------- */
+/* Microscaling format (Sec. 3.1, "Data type determination"):              */
+#define SAGE_FMT_MXFP4      0x0u  /* E2M1 codes, 1x32 blocks, E8M0 scales (gfx950 native) */
+#define SAGE_FMT_NV16_E4M3  0x1u  /* E2M1 codes, 1x16 blocks, E4M3 scales (paper's NVFP4)  */
+#define SAGE_FMT_MASK       0x3u
+/* Input dtype of q, k, v (and of o unless SAGE_OUT_F32):                  */
+#define SAGE_IN_FP16        0x0u
+#define SAGE_IN_BF16        0x4u
+#define SAGE_OUT_F32        0x8u  /* o is fp32; otherwise o has the input dtype           */
+#define SAGE_NO_SMOOTH_K    0x10u /* ablation: skip K <- K - mean(K) (Algorithm 1)         */
+#define SAGE_SMOOTH_Q       0x20u /* smoothing Q (Algorithm 1): SAGE_ERR_UNSUPPORTED       */
+#define SAGE_BKV64          0x40u /* KV tile of 64 tokens instead of 128                   */
+#define SAGE_FMT_ALL_BITS   0x7Fu
+
+/* ---- quantization roles ------------------------------------------------ */
+#define SAGE_ROLE_Q 0
+#define SAGE_ROLE_K 1
+#define SAGE_ROLE_V 2
+
+/*
+ * Physical layout of quantized tensors (n = 32 for MXFP4, 16 for NV16;
+ * Np = N rounded up to 128).  Codes are E2M1, two per byte, element 2i in the
+ * low nibble.  Scale bytes are E8M0 (2^(b-127)) or E4M3FN.
+ *   Q^  codes [B,H,N,D/2],  scales [B,H,N,D/n]      blocks along D
+ *   K^  codes [B,H,Np,D/2], scales [B,H,Np,D/n]     blocks along D, of
+ *       K' = fl32(K - mean_t K) (smoothing K).  Inside every 64-token group
+ *       the token with offset o = 32h + 16t + 4g + r (h,t in {0,1};
+ *       g,r in {0..3}) is stored at position 32t + 8g + 4h + r, so the MFMA
+ *       accumulator of S^T = K^ Q^T is laid out as the B operand of the P.V
+ *       product (the CDNA form of the paper's "Permutation for K", Sec. 3.3).
+ *       Tokens >= N have zero codes.
+ *   V^T codes [B,H,D,Np/2], scales [B,H,D,Np/n]     blocks along tokens, V
+ *       transposed (Appendix, "Transposing V"), natural token order, tokens
+ *       >= N are zero.
+ * kmean: fp32 [B,H,D], the per-(b,h) channel mean of K over the N tokens,
+ * computed as an exact fp64 sum divided by N and rounded to fp32.
+ */
+
+/* Byte sizes of the codes and scales buffers for one role.  Host only. */
+int sage_quant_sizes(int role, int B, int H, int N, int D, unsigned fmt,
+                     size_t* codes_bytes, size_t* scales_bytes);
+
+/* Workspace bytes sage_quant_fp4 needs for role K with smoothing (the
+ * per-chunk partial sums of the mean); 0 otherwise.  Host only. */
+size_t sage_quant_workspace_size(int role, int B, int H, int N, int D, unsigned fmt);
+
+/*
+ * sage_quant_fp4 -- microscaling FP4 quantization phi (Sec. 3.1, Eq.
+ * microscaling): s = max|block|/6 stored as E8M0 (smallest power of two with
+ * 6 s >= max, no clipping) or E4M3 (round to nearest even, saturating at
+ * 448); codes = FP4 round-to-nearest-even of x/s, saturating at +-6, sign
+ * kept.  Role K first subtracts the channel mean (smoothing K) and stores
+ * the tokens permuted as described above; role V writes V^T.
+ *  x        : 16-bit input [B,H,N,D], 16-byte aligned
+ *  codes    : output, sage_quant_sizes() bytes, 16-byte aligned
+ *  scales   : output, sage_quant_sizes() bytes, 4-byte aligned
+ *  kmean    : role K: output fp32 [B,H,D] (required unless SAGE_NO_SMOOTH_K);
+ *             other roles: must be NULL
+ *  workspace: role K with smoothing: device buffer of at least
+ *             sage_quant_workspace_size() bytes, 8-byte aligned; else may be NULL
+ * D must be 64 or 128; N >= 1.
+ */
+int sage_quant_fp4(const void* x, int role, int B, int H, int N, int D, unsigned fmt,
+                   void* codes, void* scales, float* kmean,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes for sage_attn_fp4_fwd_ws (quantized Q, K, V, the mean and
+ * its partial sums).  Host only. */
+size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt);
+
+/*
+ * sage_attn_fp4_fwd -- the microscaling FP4 attention forward, Algorithm 1
+ * without smoothing Q: smoothing K, phi(Q), phi(K), phi(V) (V blocked along
+ * tokens), S = FP4MM(Q^, K^) on block-scaled MFMA, online softmax over KV
+ * tiles with the two-level quantization of P~ (Sec. 3.2: s_P1 = rowmax/R
+ * per row and tile, then phi of P~/s_P1 with R = 6 for E8M0 scales and
+ * 448*6 for E4M3 scales) and O += FP4MM(P^, V^) * s_P1; O = O / l.
+ * Softmax scale is 1/sqrt(D).  causal = 1 keeps key j for query i iff j <= i.
+ *  q, k, v  : 16-bit [B,H,N,D], 16-byte aligned
+ *  o        : [B,H,N,D] fp32 (SAGE_OUT_F32) or input dtype, 16-byte aligned
+ * The internal workspace comes from hipMallocAsync on `stream` and is freed
+ * with hipFreeAsync on the same stream.
+ */
+int sage_attn_fp4_fwd(const void* q, const void* k, const void* v, void* o,
+                      int B, int H, int N, int D, int causal, unsigned fmt, hipStream_t stream);
+
+/* Same, with a caller-provided workspace of at least
+ * sage_attn_fp4_workspace_size() bytes (256-byte aligned). */
+int sage_attn_fp4_fwd_ws(const void* q, const void* k, const void* v, void* o,
+                         int B, int H, int N, int D, int causal, unsigned fmt,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * sage_attn_fp4_fwd_prequant -- the attention kernel alone, on tensors
+ * produced by sage_quant_fp4 (layouts above).  kmean is not needed: the
+ * smoothing is already inside K^ (softmax is invariant to it).
+ */
+int sage_attn_fp4_fwd_prequant(const void* q_codes, const void* q_scales,
+                               const void* k_codes, const void* k_scales,
+                               const void* vt_codes, const void* vt_scales,
+                               void* o, int B, int H, int N, int D, int causal,
+                               unsigned fmt, hipStream_t stream);
+
+/*
+ * sage_attn_bf16_fwd -- comparison kernel with the same tiling on bf16 MFMA:
+ * S = Q K^T in fp32, online softmax in fp32, P rounded to bf16, O += P V
+ * (FlashAttention forward, Sec. 2).  q, k, v must be bf16 (flags must
+ * contain SAGE_IN_BF16); o is fp32 with SAGE_OUT_F32, else bf16.  Only
+ * SAGE_IN_BF16, SAGE_OUT_F32 and SAGE_BKV64 are accepted in flags.  The V
+ * transpose goes to a hipMallocAsync workspace on `stream`.
+ */
+int sage_attn_bf16_fwd(const void* q, const void* k, const void* v, void* o,
+                       int B, int H, int N, int D, int causal, unsigned flags, hipStream_t stream);
+
+/* Human-readable status name; never NULL. */
+const char* sage_status_string(int status);
+
+/* Library version string. */
+const char* sage_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SAGE_MI355X_H */

@@ -1,0 +1,176 @@
+"""Thin ctypes binding over ``libsage_mi355x.so`` (declared in include/sage_mi355x.h).
+
+Argument marshalling only: every step of the attention path runs in the HIP
+kernels.  torch supplies device memory and the current stream.  If the
+library has not been built, ``lib()`` raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsage_mi355x.so")
+
+SAGE_OK, SAGE_ERR_INVALID_ARG, SAGE_ERR_UNSUPPORTED, SAGE_ERR_HIP, SAGE_ERR_WORKSPACE = 0, 1, 2, 3, 4
+SAGE_FMT_MXFP4, SAGE_FMT_NV16_E4M3 = 0x0, 0x1
+SAGE_IN_FP16, SAGE_IN_BF16 = 0x0, 0x4
+SAGE_OUT_F32 = 0x8
+SAGE_NO_SMOOTH_K = 0x10
+SAGE_SMOOTH_Q = 0x20
+SAGE_BKV64 = 0x40
+SAGE_ROLE_Q, SAGE_ROLE_K, SAGE_ROLE_V = 0, 1, 2
+
+_lib = None
+
+
+class SageError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__("%s failed: %s" % (fn, status_string(status)))
+        self.status = status
+
+
+def lib():
+    """Load the in-tree HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libsage_mi355x.so is not built; run __graft_entry__.build() "
+                               "or python paper_2505_11594_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i, u, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint, ctypes.c_size_t
+        L.sage_quant_sizes.argtypes = [i, i, i, i, i, u, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+        L.sage_quant_workspace_size.argtypes = [i, i, i, i, i, u]
+        L.sage_quant_workspace_size.restype = sz
+        L.sage_quant_fp4.argtypes = [vp, i, i, i, i, i, u, vp, vp, vp, vp, sz, vp]
+        L.sage_attn_fp4_workspace_size.argtypes = [i, i, i, i, u]
+        L.sage_attn_fp4_workspace_size.restype = sz
+        L.sage_attn_fp4_fwd.argtypes = [vp, vp, vp, vp, i, i, i, i, i, u, vp]
+        L.sage_attn_fp4_fwd_ws.argtypes = [vp, vp, vp, vp, i, i, i, i, i, u, vp, sz, vp]
+        L.sage_attn_fp4_fwd_prequant.argtypes = [vp] * 7 + [i, i, i, i, i, u, vp]
+        L.sage_attn_bf16_fwd.argtypes = [vp, vp, vp, vp, i, i, i, i, i, u, vp]
+        L.sage_status_string.argtypes = [i]
+        L.sage_status_string.restype = ctypes.c_char_p
+        L.sage_version.restype = ctypes.c_char_p
+        for name in ("sage_quant_sizes", "sage_quant_fp4", "sage_attn_fp4_fwd", "sage_attn_fp4_fwd_ws",
+                     "sage_attn_fp4_fwd_prequant", "sage_attn_bf16_fwd"):
+            getattr(L, name).restype = i
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().sage_status_string(int(status)).decode()
+
+
+def _check(fn: str, rc: int):
+    if rc != SAGE_OK:
+        raise SageError(fn, rc)
+
+
+def _stream():
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _in_flag(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return SAGE_IN_BF16
+    if t.dtype == torch.float16:
+        return SAGE_IN_FP16
+    raise TypeError("inputs must be bf16 or fp16, got %s" % t.dtype)
+
+
+def _shape(t):
+    if t.dim() != 4 or not t.is_contiguous() or not t.is_cuda:
+        raise ValueError("expected a contiguous 4-d [B, H, N, D] device tensor")
+    return tuple(int(s) for s in t.shape)
+
+
+def quant_sizes(role: int, B: int, H: int, N: int, D: int, fmt: int):
+    c, s = ctypes.c_size_t(), ctypes.c_size_t()
+    _check("sage_quant_sizes", lib().sage_quant_sizes(role, B, H, N, D, fmt, ctypes.byref(c), ctypes.byref(s)))
+    return c.value, s.value
+
+
+def sage_quant_fp4(x, role: int, fmt: int = SAGE_FMT_MXFP4):
+    """Quantize one tensor; returns (codes uint8, scales uint8, kmean fp32 or None) on the device."""
+    import torch
+    B, H, N, D = _shape(x)
+    fmt = fmt | _in_flag(x)
+    cb, sb = quant_sizes(role, B, H, N, D, fmt)
+    codes = torch.empty(cb, dtype=torch.uint8, device=x.device)
+    scales = torch.empty(sb, dtype=torch.uint8, device=x.device)
+    kmean = None
+    ws = None
+    if role == SAGE_ROLE_K and not (fmt & SAGE_NO_SMOOTH_K):
+        kmean = torch.empty((B, H, D), dtype=torch.float32, device=x.device)
+        wsb = int(lib().sage_quant_workspace_size(role, B, H, N, D, fmt))
+        ws = torch.empty(max(wsb, 8), dtype=torch.uint8, device=x.device)
+    _check("sage_quant_fp4", lib().sage_quant_fp4(_ptr(x), role, B, H, N, D, fmt, _ptr(codes), _ptr(scales),
+                                                  _ptr(kmean), _ptr(ws), ws.numel() if ws is not None else 0,
+                                                  _stream()))
+    return codes, scales, kmean
+
+
+def attn_fp4_workspace_size(B: int, H: int, N: int, D: int, fmt: int) -> int:
+    return int(lib().sage_attn_fp4_workspace_size(B, H, N, D, fmt))
+
+
+def _out(q, out_f32: bool):
+    import torch
+    return torch.empty(q.shape, dtype=torch.float32 if out_f32 else q.dtype, device=q.device)
+
+
+def sage_attn_fp4_fwd(q, k, v, causal: bool = False, fmt: int = SAGE_FMT_MXFP4, out_f32: bool = True,
+                      out=None, workspace=None):
+    """O = attention(Q, K, V) through the FP4 path.  With ``workspace`` (a uint8 device
+    tensor of at least attn_fp4_workspace_size bytes) no allocation happens inside."""
+    B, H, N, D = _shape(q)
+    if _shape(k) != (B, H, N, D) or _shape(v) != (B, H, N, D):
+        raise ValueError("q, k, v must have the same shape")
+    fmt = fmt | _in_flag(q) | (SAGE_OUT_F32 if out_f32 else 0)
+    o = _out(q, out_f32) if out is None else out
+    if workspace is None:
+        rc = lib().sage_attn_fp4_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, H, N, D, int(bool(causal)), fmt, _stream())
+        _check("sage_attn_fp4_fwd", rc)
+    else:
+        rc = lib().sage_attn_fp4_fwd_ws(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, H, N, D, int(bool(causal)), fmt,
+                                        _ptr(workspace), workspace.numel(), _stream())
+        _check("sage_attn_fp4_fwd_ws", rc)
+    return o
+
+
+def sage_attn_fp4_fwd_prequant(qq, kq, vq, shape, causal: bool = False, fmt: int = SAGE_FMT_MXFP4,
+                               in_bf16: bool = True, out_f32: bool = True, out=None):
+    """Attention kernel alone on (codes, scales) pairs from sage_quant_fp4."""
+    import torch
+    B, H, N, D = shape
+    fmt = fmt | (SAGE_IN_BF16 if in_bf16 else SAGE_IN_FP16) | (SAGE_OUT_F32 if out_f32 else 0)
+    dev = qq[0].device
+    if out is None:
+        out = torch.empty(shape, dtype=torch.float32 if out_f32 else (torch.bfloat16 if in_bf16 else torch.float16),
+                          device=dev)
+    rc = lib().sage_attn_fp4_fwd_prequant(_ptr(qq[0]), _ptr(qq[1]), _ptr(kq[0]), _ptr(kq[1]), _ptr(vq[0]),
+                                          _ptr(vq[1]), _ptr(out), B, H, N, D, int(bool(causal)), fmt, _stream())
+    _check("sage_attn_fp4_fwd_prequant", rc)
+    return out
+
+
+def sage_attn_bf16_fwd(q, k, v, causal: bool = False, out_f32: bool = True, out=None):
+    """bf16-MFMA comparison kernel of the same structure."""
+    B, H, N, D = _shape(q)
+    flags = _in_flag(q) | (SAGE_OUT_F32 if out_f32 else 0)
+    o = _out(q, out_f32) if out is None else out
+    rc = lib().sage_attn_bf16_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, H, N, D, int(bool(causal)), flags, _stream())
+    _check("sage_attn_bf16_fwd", rc)
+    return o
+
+
+def version() -> str:
+    return lib().sage_version().decode()

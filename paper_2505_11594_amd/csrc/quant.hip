@@ -1,0 +1,290 @@
+// Quantization kernels for gfx950: smoothing-K mean, FP4 microscaling of Q and
+// K along the head dimension, and of V along tokens with the transpose fused in.
+//
+// phi (Sec. 3.1, Eq. microscaling): per 1 x n block, s = max|x| / 6 stored as
+// E8M0 (MXFP4, n = 32: the smallest power of two with 6 s >= max) or E4M3
+// (n = 16, round to nearest even, saturating at 448); codes are FP4 E2M1
+// round-to-nearest-even of x / s.  Smoothing K (Algorithm 1 preprocessing)
+// subtracts the per-(b,h) channel mean first; the V transpose is fused into
+// its quantization (Appendix, "Transposing V").
+//
+// All three kernels are HBM-bound: each element is read once as 16 bits
+// (twice for K, which the mean also reads) and written as 4 bits plus 8 bits
+// per block.
+#include "sage_common.h"
+
+namespace sage {
+
+// ---------------------------------------------------------------------------
+// Smoothing K, pass 1: per-chunk fp64 column sums.  Block (chunk, bh) sums
+// tokens [chunk * KM_CHUNK, ...) of K[bh] for every channel.  Every value is a
+// 16-bit float, so the fp64 partial sums are exact for the token counts used
+// here and the final mean does not depend on the summation order.
+// ---------------------------------------------------------------------------
+constexpr int KM_CHUNK = 512;
+constexpr int KM_THREADS = 256;
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(KM_THREADS) void kmean_partial_kernel(const uint16_t* __restrict__ k,
+                                                                   double* __restrict__ part, int N,
+                                                                   int nchunk) {
+  constexpr int CG = D / 8;                  // 8-channel groups per row (16 bytes)
+  constexpr int RS = KM_THREADS / CG;        // rows handled in parallel
+  const int chunk = blockIdx.x, bh = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int cg = tid % CG, rsub = tid / CG;
+  const int t0 = chunk * KM_CHUNK;
+  const int t1 = min(N, t0 + KM_CHUNK);
+  const uint16_t* kb = k + (size_t)bh * N * D;
+  double acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.0;
+  for (int t = t0 + rsub; t < t1; t += RS) {
+    uint4 raw = *reinterpret_cast<const uint4*>(kb + (size_t)t * D + cg * 8);
+    const uint16_t* h = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] += (double)widen<BF16>(h[i]);
+  }
+  __shared__ double red[KM_THREADS][9];      // padded against bank conflicts
+#pragma unroll
+  for (int i = 0; i < 8; ++i) red[tid][i] = acc[i];
+  __syncthreads();
+  if (tid < D) {
+    const int c = tid, g = c / 8, i = c % 8;
+    double s = 0.0;
+    for (int r = 0; r < RS; ++r) s += red[r * CG + g][i];
+    part[((size_t)bh * nchunk + chunk) * D + c] = s;
+  }
+}
+
+// Pass 2: mu = fl32(fl64(sum) / N).
+template <int D>
+__global__ void kmean_final_kernel(const double* __restrict__ part, float* __restrict__ mu, int N, int nchunk) {
+  const int bh = blockIdx.x, c = threadIdx.x;
+  if (c >= D) return;
+  double s = 0.0;
+  for (int j = 0; j < nchunk; ++j) s += part[((size_t)bh * nchunk + j) * D + c];
+  mu[(size_t)bh * D + c] = (float)(s / (double)N);
+}
+
+// ---------------------------------------------------------------------------
+// Row quantizer for Q and K (blocks along D).  One lane owns 8 consecutive
+// channels (a 16-byte load); the 4 (MXFP4) or 2 (NV16) lanes of a block
+// reduce their absolute maxima with cross-lane swaps.  A lane writes its 8
+// codes as one 32-bit word.  Role K subtracts mu and stores each token at
+// its permuted position inside its 64-token group.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int k_stored_pos(int t) {
+  // offset o = 32h + 16t' + 4g + r  ->  position 32t' + 8g + 4h + r
+  const int o = t & 63;
+  const int h = o >> 5, tt = (o >> 4) & 1, g = (o >> 2) & 3, r = o & 3;
+  return (t & ~63) | (tt << 5) | (g << 3) | (h << 2) | r;
+}
+
+template <int D, bool BF16, int FMT, bool IS_K>
+__global__ __launch_bounds__(256) void quant_rows_kernel(const uint16_t* __restrict__ x, const float* __restrict__ mu,
+                                                         uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
+                                                         int N, int Nout, long long total_units) {
+  constexpr int NB = (FMT == kFmtMX) ? 32 : 16;     // block size
+  constexpr int LPB = NB / 8;                       // lanes per block
+  constexpr int UPR = D / 8;                        // units (lanes) per row
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  for (long long u = (long long)blockIdx.x * blockDim.x + threadIdx.x; u < total_units; u += stride) {
+    const long long row = u / UPR;                  // (bh, t) flattened over the N input rows
+    const int cu = (int)(u % UPR);
+    const long long bh = row / N;
+    const int t = (int)(row % N);
+    uint4 raw = *reinterpret_cast<const uint4*>(x + (size_t)row * D + cu * 8);
+    const uint16_t* hv = reinterpret_cast<const uint16_t*>(&raw);
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = widen<BF16>(hv[i]);
+    if (IS_K && mu != nullptr) {
+      const float* m = mu + bh * D + cu * 8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = v[i] - m[i];
+    }
+    float am = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) am = __builtin_fmaxf(am, __builtin_fabsf(v[i]));
+#pragma unroll
+    for (int off = 1; off < LPB; off <<= 1) am = __builtin_fmaxf(am, __shfl_xor(am, off, 64));
+    uint32_t sbyte;
+    float y[8];
+    if (FMT == kFmtMX) {
+      const int e = e8m0_exponent(am);
+      sbyte = (uint32_t)(e + 127);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) y[i] = __builtin_ldexpf(v[i], -e);   // exact power-of-two scaling
+    } else {
+      sbyte = e4m3_encode(am / 6.0f);
+      const float s = e4m3_decode(sbyte);
+      if (s == 0.0f) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) y[i] = 0.0f;
+      } else {
+        const float r = 1.0f / s;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) y[i] = v[i] * r;
+      }
+    }
+    uint32_t word = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) word |= cvt_fp4x2(y[2 * i], y[2 * i + 1]) << (8 * i);
+    const long long orow = bh * Nout + (IS_K ? k_stored_pos(t) : t);
+    *reinterpret_cast<uint32_t*>(codes + (size_t)orow * (D / 2) + cu * 4) = word;
+    if ((cu % LPB) == 0) scales[(size_t)orow * (D / NB) + cu / LPB] = (uint8_t)sbyte;
+  }
+}
+
+// Zero codes (and unit scales) of K's padded tail tokens N .. Np-1.
+template <int D, int FMT>
+__global__ void k_tail_kernel(uint8_t* __restrict__ codes, uint8_t* __restrict__ scales, int N, int Np) {
+  constexpr int NB = (FMT == kFmtMX) ? 32 : 16;
+  const int bh = blockIdx.y;
+  const int ntail = Np - N;
+  for (int i = threadIdx.x + blockIdx.x * blockDim.x; i < ntail * (D / 2); i += gridDim.x * blockDim.x) {
+    const int t = N + i / (D / 2), b = i % (D / 2);
+    const long long orow = (long long)bh * Np + k_stored_pos(t);
+    codes[(size_t)orow * (D / 2) + b] = 0;
+    if (b < D / NB) scales[(size_t)orow * (D / NB) + b] = (FMT == kFmtMX) ? 127 : 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// V quantizer with the transpose fused in.  A block of 256 threads stages a
+// 128-token x D tile in LDS (coalesced 16-byte loads), then each thread
+// quantizes whole token blocks of one channel and writes them contiguously
+// into V^T [bh, d, Np/2].  Tokens >= N are zero.
+// ---------------------------------------------------------------------------
+constexpr int VT = 128;   // tokens per tile
+
+template <int D, bool BF16, int FMT>
+__global__ __launch_bounds__(256) void quant_v_kernel(const uint16_t* __restrict__ v, uint8_t* __restrict__ codes,
+                                                      uint8_t* __restrict__ scales, int N, int Np) {
+  constexpr int NB = (FMT == kFmtMX) ? 32 : 16;
+  constexpr int TPC = 256 / D;               // threads per channel: 2 (D=128) or 4 (D=64)
+  constexpr int BPT = VT / NB / TPC;         // token blocks per thread
+  __shared__ uint16_t tile[VT][D + 2];       // +2 halves: rows start on different banks
+  const int tt = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int t0 = tt * VT;
+  const uint16_t* vb = v + (size_t)bh * N * D;
+  constexpr int UPR = D / 8;
+  for (int i = tid; i < VT * UPR; i += 256) {
+    const int r = i / UPR, cu = i % UPR;
+    const int t = t0 + r;
+    uint4 raw = make_uint4(0, 0, 0, 0);
+    if (t < N) raw = *reinterpret_cast<const uint4*>(vb + (size_t)t * D + cu * 8);
+    const uint16_t* hv = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) tile[r][cu * 8 + j] = hv[j];
+  }
+  __syncthreads();
+  const int c = tid / TPC, part = tid % TPC;
+  uint8_t* crow = codes + ((size_t)bh * D + c) * (Np / 2);
+  uint8_t* srow = scales + ((size_t)bh * D + c) * (Np / NB);
+#pragma unroll
+  for (int bb = 0; bb < BPT; ++bb) {
+    const int blk = part * BPT + bb;         // token block inside the tile
+    float x[NB];
+    float am = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int r = blk * NB + j;
+      x[j] = (t0 + r < N) ? widen<BF16>(tile[r][c]) : 0.0f;
+      am = __builtin_fmaxf(am, __builtin_fabsf(x[j]));
+    }
+    uint32_t sbyte;
+    if (FMT == kFmtMX) {
+      const int e = e8m0_exponent(am);
+      sbyte = (uint32_t)(e + 127);
+#pragma unroll
+      for (int j = 0; j < NB; ++j) x[j] = __builtin_ldexpf(x[j], -e);
+    } else {
+      sbyte = e4m3_encode(am / 6.0f);
+      const float s = e4m3_decode(sbyte);
+      const float r = (s == 0.0f) ? 0.0f : 1.0f / s;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) x[j] = (s == 0.0f) ? 0.0f : x[j] * r;
+    }
+    uint32_t w[NB / 8];
+#pragma unroll
+    for (int q = 0; q < NB / 8; ++q) {
+      w[q] = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[q] |= cvt_fp4x2(x[8 * q + 2 * i], x[8 * q + 2 * i + 1]) << (8 * i);
+    }
+    uint8_t* dst = crow + (t0 + blk * NB) / 2;
+    if (NB == 32) *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+    else *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
+    srow[(t0 + blk * NB) / NB] = (uint8_t)sbyte;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host-side launchers (called by the C ABI in sage_abi.hip).
+// ---------------------------------------------------------------------------
+int kmean_chunks(int N) { return (N + KM_CHUNK - 1) / KM_CHUNK; }
+
+template <int D, bool BF16>
+static hipError_t launch_kmean_t(const void* k, double* part, float* mu, int BH, int N, hipStream_t st) {
+  const int nchunk = kmean_chunks(N);
+  hipLaunchKernelGGL((kmean_partial_kernel<D, BF16>), dim3(nchunk, BH), dim3(KM_THREADS), 0, st,
+                     (const uint16_t*)k, part, N, nchunk);
+  hipLaunchKernelGGL((kmean_final_kernel<D>), dim3(BH), dim3(D), 0, st, (const double*)part, mu, N, nchunk);
+  return hipGetLastError();
+}
+
+hipError_t launch_kmean(const void* k, double* part, float* mu, int BH, int N, int D, bool bf16, hipStream_t st) {
+  if (D == 128) return bf16 ? launch_kmean_t<128, true>(k, part, mu, BH, N, st) : launch_kmean_t<128, false>(k, part, mu, BH, N, st);
+  return bf16 ? launch_kmean_t<64, true>(k, part, mu, BH, N, st) : launch_kmean_t<64, false>(k, part, mu, BH, N, st);
+}
+
+template <int D, bool BF16, int FMT, bool IS_K>
+static hipError_t launch_rows_t(const void* x, const float* mu, void* codes, void* scales, int BH, int N, int Nout,
+                                hipStream_t st) {
+  const long long units = (long long)BH * N * (D / 8);
+  long long blocks = (units + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL((quant_rows_kernel<D, BF16, FMT, IS_K>), dim3((unsigned)blocks), dim3(256), 0, st,
+                     (const uint16_t*)x, mu, (uint8_t*)codes, (uint8_t*)scales, N, Nout, units);
+  if (IS_K && Nout > N) {
+    hipLaunchKernelGGL((k_tail_kernel<D, FMT>), dim3(1, BH), dim3(256), 0, st, (uint8_t*)codes, (uint8_t*)scales, N, Nout);
+  }
+  return hipGetLastError();
+}
+
+template <int D, int FMT, bool IS_K>
+static hipError_t launch_rows_d(const void* x, const float* mu, void* codes, void* scales, int BH, int N, int Nout,
+                                bool bf16, hipStream_t st) {
+  return bf16 ? launch_rows_t<D, true, FMT, IS_K>(x, mu, codes, scales, BH, N, Nout, st)
+              : launch_rows_t<D, false, FMT, IS_K>(x, mu, codes, scales, BH, N, Nout, st);
+}
+
+hipError_t launch_quant_rows(const void* x, const float* mu, void* codes, void* scales, int BH, int N, int Nout, int D,
+                             int fmt, bool is_k, bool bf16, hipStream_t st) {
+#define SAGE_ROWS(DD, FF)                                                                              \
+  return is_k ? launch_rows_d<DD, FF, true>(x, mu, codes, scales, BH, N, Nout, bf16, st)              \
+              : launch_rows_d<DD, FF, false>(x, mu, codes, scales, BH, N, Nout, bf16, st)
+  if (D == 128) { if (fmt == kFmtMX) { SAGE_ROWS(128, kFmtMX); } else { SAGE_ROWS(128, kFmtNV16); } }
+  else { if (fmt == kFmtMX) { SAGE_ROWS(64, kFmtMX); } else { SAGE_ROWS(64, kFmtNV16); } }
+#undef SAGE_ROWS
+}
+
+template <int D, bool BF16, int FMT>
+static hipError_t launch_v_t(const void* v, void* codes, void* scales, int BH, int N, int Np, hipStream_t st) {
+  hipLaunchKernelGGL((quant_v_kernel<D, BF16, FMT>), dim3(Np / VT, BH), dim3(256), 0, st, (const uint16_t*)v,
+                     (uint8_t*)codes, (uint8_t*)scales, N, Np);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_v(const void* v, void* codes, void* scales, int BH, int N, int Np, int D, int fmt, bool bf16,
+                          hipStream_t st) {
+#define SAGE_V(DD, FF) return bf16 ? launch_v_t<DD, true, FF>(v, codes, scales, BH, N, Np, st) \
+                                   : launch_v_t<DD, false, FF>(v, codes, scales, BH, N, Np, st)
+  if (D == 128) { if (fmt == kFmtMX) { SAGE_V(128, kFmtMX); } else { SAGE_V(128, kFmtNV16); } }
+  else { if (fmt == kFmtMX) { SAGE_V(64, kFmtMX); } else { SAGE_V(64, kFmtNV16); } }
+#undef SAGE_V
+}
+
+}  // namespace sage

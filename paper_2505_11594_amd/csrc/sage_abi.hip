@@ -1,0 +1,239 @@
+// C ABI of the gfx950 microscaled-FP4 attention library.  Argument checks run
+// on the host before any HIP call; kernels are enqueued on the caller's stream.
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "sage_common.h"
+#include "../../include/sage_mi355x.h"
+
+namespace sage {
+hipError_t launch_kmean(const void* k, double* part, float* mu, int BH, int N, int D, bool bf16, hipStream_t st);
+int kmean_chunks(int N);
+hipError_t launch_quant_rows(const void* x, const float* mu, void* codes, void* scales, int BH, int N, int Nout, int D,
+                             int fmt, bool is_k, bool bf16, hipStream_t st);
+hipError_t launch_quant_v(const void* v, void* codes, void* scales, int BH, int N, int Np, int D, int fmt, bool bf16,
+                          hipStream_t st);
+hipError_t launch_attn_fp4_mx(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
+                              const void* vs, void* o, int BH, int N, int Np, int D, int bkv, bool causal, int out,
+                              float c2, float log6, hipStream_t st);
+}  // namespace sage
+
+namespace {
+
+constexpr long long kMaxElems = 1LL << 40;   // bound on B*H*N*D (keeps every offset in 64-bit range)
+
+inline bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+inline int fmt_of(unsigned f) { return (int)(f & SAGE_FMT_MASK); }
+inline int blk_of(unsigned f) { return fmt_of(f) == SAGE_FMT_MXFP4 ? 32 : 16; }
+inline int pad128(int N) { return (N + 127) / 128 * 128; }
+inline size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int check_shape(int B, int H, int N, int D, unsigned fmt) {
+  if (B <= 0 || H <= 0 || N <= 0) return SAGE_ERR_INVALID_ARG;
+  if (D != 64 && D != 128) return SAGE_ERR_INVALID_ARG;
+  if (fmt & ~SAGE_FMT_ALL_BITS) return SAGE_ERR_INVALID_ARG;
+  const int f = fmt_of(fmt);
+  if (f != SAGE_FMT_MXFP4 && f != SAGE_FMT_NV16_E4M3) return SAGE_ERR_INVALID_ARG;
+  if ((long long)B * H > (1LL << 30)) return SAGE_ERR_INVALID_ARG;
+  if (N > (1 << 30) - 128) return SAGE_ERR_INVALID_ARG;
+  if ((long long)B * H * (long long)pad128(N) * D > kMaxElems) return SAGE_ERR_INVALID_ARG;
+  if (fmt & SAGE_SMOOTH_Q) return SAGE_ERR_UNSUPPORTED;
+  return SAGE_OK;
+}
+
+void sizes(int role, int B, int H, int N, int D, unsigned fmt, size_t* cb, size_t* sb) {
+  const size_t BH = (size_t)B * H;
+  const size_t n = blk_of(fmt);
+  const size_t rows = (role == SAGE_ROLE_K) ? (size_t)pad128(N) : (size_t)N;
+  if (role == SAGE_ROLE_V) {
+    const size_t Np = pad128(N);
+    *cb = BH * D * Np / 2;
+    *sb = BH * D * Np / n;
+  } else {
+    *cb = BH * rows * D / 2;
+    *sb = BH * rows * D / n;
+  }
+}
+
+size_t kmean_ws_bytes(int B, int H, int N, int D) {
+  return (size_t)B * H * (size_t)sage::kmean_chunks(N) * D * sizeof(double);
+}
+
+struct AttnWs {
+  size_t qc, qs, kc, ks, vc, vs, mu, part, total;
+};
+
+AttnWs attn_ws_layout(int B, int H, int N, int D, unsigned fmt) {
+  AttnWs w;
+  size_t c, s, off = 0;
+  sizes(SAGE_ROLE_Q, B, H, N, D, fmt, &c, &s);
+  w.qc = off; off += up256(c); w.qs = off; off += up256(s);
+  sizes(SAGE_ROLE_K, B, H, N, D, fmt, &c, &s);
+  w.kc = off; off += up256(c); w.ks = off; off += up256(s);
+  sizes(SAGE_ROLE_V, B, H, N, D, fmt, &c, &s);
+  w.vc = off; off += up256(c); w.vs = off; off += up256(s);
+  w.mu = off; off += up256((size_t)B * H * D * sizeof(float));
+  w.part = off; off += up256(kmean_ws_bytes(B, H, N, D));
+  w.total = off;
+  return w;
+}
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? SAGE_OK : SAGE_ERR_HIP; }
+
+int quant_impl(const void* x, int role, int B, int H, int N, int D, unsigned fmt, void* codes, void* scales,
+               float* kmean, void* ws, hipStream_t st) {
+  const bool bf16 = (fmt & SAGE_IN_BF16) != 0;
+  const int BH = B * H, f = fmt_of(fmt);
+  hipError_t e = hipSuccess;
+  if (role == SAGE_ROLE_Q) {
+    e = sage::launch_quant_rows(x, nullptr, codes, scales, BH, N, N, D, f, false, bf16, st);
+  } else if (role == SAGE_ROLE_K) {
+    const bool smooth = !(fmt & SAGE_NO_SMOOTH_K);
+    if (smooth) {
+      e = sage::launch_kmean(x, static_cast<double*>(ws), kmean, BH, N, D, bf16, st);
+      if (e != hipSuccess) return SAGE_ERR_HIP;
+    }
+    e = sage::launch_quant_rows(x, smooth ? kmean : nullptr, codes, scales, BH, N, pad128(N), D, f, true, bf16, st);
+  } else {
+    e = sage::launch_quant_v(x, codes, scales, BH, N, pad128(N), D, f, bf16, st);
+  }
+  return hip_status(e);
+}
+
+int attn_args(const void* q, const void* k, const void* v, const void* o, int B, int H, int N, int D, int causal,
+              unsigned fmt) {
+  int rc = check_shape(B, H, N, D, fmt);
+  if (rc != SAGE_OK) return rc;
+  if (!q || !k || !v || !o) return SAGE_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return SAGE_ERR_INVALID_ARG;
+  if (causal != 0 && causal != 1) return SAGE_ERR_INVALID_ARG;
+  return SAGE_OK;
+}
+
+inline float softmax_c2(int D) { return (float)(1.0 / (std::log(2.0) * std::sqrt((double)D))); }
+inline float log2_of_6() { return (float)std::log2(6.0); }
+inline int out_kind(unsigned fmt) { return (fmt & SAGE_OUT_F32) ? 0 : ((fmt & SAGE_IN_BF16) ? 1 : 2); }
+
+int attn_prequant_impl(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc, const void* vs,
+                       void* o, int B, int H, int N, int D, int causal, unsigned fmt, hipStream_t st) {
+  if (fmt_of(fmt) != SAGE_FMT_MXFP4) return SAGE_ERR_UNSUPPORTED;
+  const int bkv = (fmt & SAGE_BKV64) ? 64 : 128;
+  return hip_status(sage::launch_attn_fp4_mx(qc, qs, kc, ks, vc, vs, o, B * H, N, pad128(N), D, bkv, causal != 0,
+                                             out_kind(fmt), softmax_c2(D), log2_of_6(), st));
+}
+
+int attn_ws_impl(const void* q, const void* k, const void* v, void* o, int B, int H, int N, int D, int causal,
+                 unsigned fmt, void* ws, hipStream_t st) {
+  const AttnWs w = attn_ws_layout(B, H, N, D, fmt);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  float* mu = reinterpret_cast<float*>(base + w.mu);
+  int rc = quant_impl(q, SAGE_ROLE_Q, B, H, N, D, fmt, base + w.qc, base + w.qs, nullptr, nullptr, st);
+  if (rc == SAGE_OK) rc = quant_impl(k, SAGE_ROLE_K, B, H, N, D, fmt, base + w.kc, base + w.ks, mu, base + w.part, st);
+  if (rc == SAGE_OK) rc = quant_impl(v, SAGE_ROLE_V, B, H, N, D, fmt, base + w.vc, base + w.vs, nullptr, nullptr, st);
+  if (rc == SAGE_OK)
+    rc = attn_prequant_impl(base + w.qc, base + w.qs, base + w.kc, base + w.ks, base + w.vc, base + w.vs, o, B, H, N, D,
+                            causal, fmt, st);
+  return rc;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sage_quant_sizes(int role, int B, int H, int N, int D, unsigned fmt, size_t* codes_bytes, size_t* scales_bytes) {
+  if (!codes_bytes || !scales_bytes) return SAGE_ERR_INVALID_ARG;
+  if (role != SAGE_ROLE_Q && role != SAGE_ROLE_K && role != SAGE_ROLE_V) return SAGE_ERR_INVALID_ARG;
+  const int rc = check_shape(B, H, N, D, fmt);
+  if (rc != SAGE_OK) return rc;
+  sizes(role, B, H, N, D, fmt, codes_bytes, scales_bytes);
+  return SAGE_OK;
+}
+
+size_t sage_quant_workspace_size(int role, int B, int H, int N, int D, unsigned fmt) {
+  if (role != SAGE_ROLE_K || (fmt & SAGE_NO_SMOOTH_K) || check_shape(B, H, N, D, fmt) != SAGE_OK) return 0;
+  return kmean_ws_bytes(B, H, N, D);
+}
+
+int sage_quant_fp4(const void* x, int role, int B, int H, int N, int D, unsigned fmt, void* codes, void* scales,
+                   float* kmean, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (role != SAGE_ROLE_Q && role != SAGE_ROLE_K && role != SAGE_ROLE_V) return SAGE_ERR_INVALID_ARG;
+  int rc = check_shape(B, H, N, D, fmt);
+  if (rc != SAGE_OK) return rc;
+  if (!x || !codes || !scales) return SAGE_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4)) return SAGE_ERR_INVALID_ARG;
+  const bool smooth = role == SAGE_ROLE_K && !(fmt & SAGE_NO_SMOOTH_K);
+  if (smooth) {
+    if (!kmean || !aligned(kmean, 4) || !workspace || !aligned(workspace, 8)) return SAGE_ERR_INVALID_ARG;
+    if (workspace_bytes < kmean_ws_bytes(B, H, N, D)) return SAGE_ERR_WORKSPACE;
+  } else if (kmean) {
+    return SAGE_ERR_INVALID_ARG;
+  }
+  return quant_impl(x, role, B, H, N, D, fmt, codes, scales, kmean, workspace, stream);
+}
+
+size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt) {
+  if (check_shape(B, H, N, D, fmt) != SAGE_OK) return 0;
+  return attn_ws_layout(B, H, N, D, fmt).total;
+}
+
+int sage_attn_fp4_fwd_ws(const void* q, const void* k, const void* v, void* o, int B, int H, int N, int D, int causal,
+                         unsigned fmt, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int rc = attn_args(q, k, v, o, B, H, N, D, causal, fmt);
+  if (rc != SAGE_OK) return rc;
+  if (fmt_of(fmt) != SAGE_FMT_MXFP4) return SAGE_ERR_UNSUPPORTED;
+  if (!workspace || !aligned(workspace, 256)) return SAGE_ERR_INVALID_ARG;
+  if (workspace_bytes < attn_ws_layout(B, H, N, D, fmt).total) return SAGE_ERR_WORKSPACE;
+  return attn_ws_impl(q, k, v, o, B, H, N, D, causal, fmt, workspace, stream);
+}
+
+int sage_attn_fp4_fwd(const void* q, const void* k, const void* v, void* o, int B, int H, int N, int D, int causal,
+                      unsigned fmt, hipStream_t stream) {
+  int rc = attn_args(q, k, v, o, B, H, N, D, causal, fmt);
+  if (rc != SAGE_OK) return rc;
+  if (fmt_of(fmt) != SAGE_FMT_MXFP4) return SAGE_ERR_UNSUPPORTED;
+  const size_t bytes = attn_ws_layout(B, H, N, D, fmt).total;
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess) return SAGE_ERR_HIP;
+  rc = attn_ws_impl(q, k, v, o, B, H, N, D, causal, fmt, ws, stream);
+  if (hipFreeAsync(ws, stream) != hipSuccess && rc == SAGE_OK) rc = SAGE_ERR_HIP;
+  return rc;
+}
+
+int sage_attn_fp4_fwd_prequant(const void* q_codes, const void* q_scales, const void* k_codes, const void* k_scales,
+                               const void* vt_codes, const void* vt_scales, void* o, int B, int H, int N, int D,
+                               int causal, unsigned fmt, hipStream_t stream) {
+  int rc = check_shape(B, H, N, D, fmt);
+  if (rc != SAGE_OK) return rc;
+  if (!q_codes || !q_scales || !k_codes || !k_scales || !vt_codes || !vt_scales || !o) return SAGE_ERR_INVALID_ARG;
+  if (!aligned(q_codes, 16) || !aligned(k_codes, 16) || !aligned(vt_codes, 16) || !aligned(o, 16)) return SAGE_ERR_INVALID_ARG;
+  if (!aligned(q_scales, 4) || !aligned(k_scales, 4) || !aligned(vt_scales, 4)) return SAGE_ERR_INVALID_ARG;
+  if (causal != 0 && causal != 1) return SAGE_ERR_INVALID_ARG;
+  return attn_prequant_impl(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, o, B, H, N, D, causal, fmt,
+                            stream);
+}
+
+int sage_attn_bf16_fwd(const void* q, const void* k, const void* v, void* o, int B, int H, int N, int D, int causal,
+                       unsigned flags, hipStream_t stream) {
+  if (flags & ~(unsigned)(SAGE_IN_BF16 | SAGE_OUT_F32)) return SAGE_ERR_INVALID_ARG;
+  if (!(flags & SAGE_IN_BF16)) return SAGE_ERR_INVALID_ARG;
+  int rc = attn_args(q, k, v, o, B, H, N, D, causal, flags);
+  if (rc != SAGE_OK) return rc;
+  (void)stream;
+  return SAGE_ERR_UNSUPPORTED;
+}
+
+const char* sage_status_string(int status) {
+  switch (status) {
+    case SAGE_OK: return "SAGE_OK";
+    case SAGE_ERR_INVALID_ARG: return "SAGE_ERR_INVALID_ARG";
+    case SAGE_ERR_UNSUPPORTED: return "SAGE_ERR_UNSUPPORTED";
+    case SAGE_ERR_HIP: return "SAGE_ERR_HIP";
+    case SAGE_ERR_WORKSPACE: return "SAGE_ERR_WORKSPACE";
+    default: return "SAGE_ERR_UNKNOWN";
+  }
+}
+
+const char* sage_version(void) { return "sage-mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

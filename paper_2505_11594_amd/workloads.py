@@ -109,17 +109,19 @@ def make_inputs(B, H, N, D, in_dtype, seed, k_bias_var=0.0, outlier_frac=0.0, ou
 
 
 def sample_rows(w: Workload, per_head_tiles: int = 8, tile: int = 64, rows_per_tile: int = 64,
-                B: int | None = None, H: int | None = None, N: int | None = None, seed: int = 7):
+                B: int | None = None, H: int | None = None, N: int | None = None, seed: int = 7,
+                heads=None):
     """Flat row ids ((b*H + h)*N + i) of a seeded sample of query tiles per head:
     always the first and last tile, plus (causal) the tile that ends on a KV-tile
-    boundary, then random tiles; ``rows_per_tile`` rows of each (all if >= tile)."""
+    boundary, then random tiles; ``rows_per_tile`` rows of each (all if >= tile).
+    ``heads``: the flat (b*H + h) heads to sample (default: all)."""
     B = w.B if B is None else B
     H = w.H if H is None else H
     N = w.N if N is None else N
     rng = np.random.default_rng(seed)
     ntile = (N + tile - 1) // tile
     rows = []
-    for bh in range(B * H):
+    for bh in (range(B * H) if heads is None else heads):
         pick = {0, ntile - 1}
         if w.causal:
             pick.add(min(ntile - 1, (w.bkv // tile)))

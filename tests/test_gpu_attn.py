@@ -1,0 +1,140 @@
+"""GPU parity of the microscaled-FP4 attention forward (Algorithm 1 without
+smoothing Q, two-level P quantization of Sec. 3.2) against the oracle.
+
+Bar: |O_gpu - O_oracle| <= 2e-3 per element (fp32 output), plus, per row, the
+oracle's bound for P codes whose pre-rounding value lies within 8 ulp of an
+E2M1 rounding boundary (the GPU evaluates exp2 with v_exp_f32, within 1 ulp
+of the correctly rounded value the oracle uses; such codes may legitimately
+take either neighbour)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2505_11594_amd import binding as bd
+from paper_2505_11594_amd import workloads as wl
+
+from _gpu import to_dev, torch_dev, say
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+
+
+def gpu_attn(q, k, v, in_dtype, causal, fmt, bkv, out_f32=True, **kw):
+    torch = torch_dev()
+    f = fmt | (bd.SAGE_BKV64 if bkv == 64 else 0)
+    o = bd.sage_attn_fp4_fwd(to_dev(q, in_dtype), to_dev(k, in_dtype), to_dev(v, in_dtype), causal=causal, fmt=f,
+                             out_f32=out_f32, **kw)
+    torch.cuda.synchronize()
+    return o
+
+
+def o_rows(o, rows, D):
+    torch = torch_dev()
+    flat = o.reshape(-1, D)
+    idx = torch.from_numpy(rows).to(o.device)
+    return flat.index_select(0, idx).float().cpu().numpy()
+
+
+def check(got, ref, tie_tol, label, extra=None):
+    err = np.abs(got - ref).max(axis=1)
+    lim = TOL + tie_tol + (0 if extra is None else extra)
+    bad = err > lim
+    say("%s: rows=%d max_err=%.3g (%.3g without tie rows) tie_rows=%d" %
+        (label, len(err), float(err.max()), float(err[tie_tol == 0].max()) if (tie_tol == 0).any() else 0.0,
+         int((tie_tol > 0).sum())))
+    assert not bad.any(), "%s: %d rows over the bar, worst err %.3g at row %d" % (
+        label, int(bad.sum()), float(err[bad].max()), int(np.flatnonzero(bad)[0]))
+
+
+@pytest.mark.parametrize("N", [1, 64, 100, 257, 640])
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("bkv", [64, 128])
+def test_attn_edge_shapes(N, D, causal, bkv):
+    say("attn edge N=%d D=%d causal=%d bkv=%d" % (N, D, causal, bkv))
+    in_dtype = 1 if (N + D) % 2 else 0
+    q, k, v = wl.make_inputs(1, 2, N, D, in_dtype, seed=200 + N, k_bias_var=4.0, outlier_frac=0.02)
+    o = gpu_attn(q, k, v, in_dtype, causal, 0, bkv)
+    ref, tie, _ = oracle.attn(q, k, v, in_dtype, causal, oracle.FMT_MX, bkv)
+    check(o.cpu().numpy().reshape(-1, D), ref, tie, "edge")
+
+
+def test_attn_config0_all_rows():
+    w = wl.CONFIGS[0]
+    q, k, v = wl.generate(w)
+    o = gpu_attn(q, k, v, w.in_dtype, w.causal, 0, w.bkv)
+    ref, tie, cnt = oracle.attn(q, k, v, w.in_dtype, w.causal, oracle.FMT_MX, w.bkv)
+    check(o.cpu().numpy().reshape(-1, w.D), ref, tie, w.name)
+    ex = oracle.exact_attn(q, k, v, w.in_dtype, w.causal)
+    say("accuracy vs exact", oracle.metrics(ex, o.cpu().numpy().reshape(-1, w.D)))
+
+
+@pytest.mark.parametrize("ci", [1, 2, 3, 4])
+def test_attn_configs_full_size_sampled_rows(ci):
+    """The benchmark's launch configuration at full size; the oracle computes a
+    seeded sample of rows (first/last/random query tiles of sampled heads)."""
+    w = wl.CONFIGS[ci]
+    if wl.FMT_MX not in w.fmts:
+        pytest.skip("no MXFP4 run for this configuration")
+    say("attn config", ci, w.name)
+    q, k, v = wl.generate(w)
+    o = gpu_attn(q, k, v, w.in_dtype, w.causal, 0, w.bkv)
+    BH = w.B * w.H
+    heads = sorted({0, BH - 1} | set(np.random.default_rng(ci).choice(BH, min(BH, 6), replace=False).tolist()))
+    rows = wl.sample_rows(w, per_head_tiles=4, tile=128, rows_per_tile=8, heads=heads, seed=ci)
+    ref, tie, cnt = oracle.attn(q, k, v, w.in_dtype, w.causal, oracle.FMT_MX, w.bkv, rows=rows)
+    got = o_rows(o, rows, w.D)
+    check(got, ref, tie, w.name)
+    ex = oracle.exact_attn(q, k, v, w.in_dtype, w.causal, rows=rows)
+    say("accuracy vs exact (sampled rows)", oracle.metrics(ex, got), cnt)
+
+
+def test_attn_deterministic_and_entry_points_agree():
+    torch = torch_dev()
+    w = wl.CONFIGS[1]
+    q, k, v = wl.generate(w, B=1, H=4, N=2048)
+    a = gpu_attn(q, k, v, w.in_dtype, False, 0, 128)
+    b = gpu_attn(q, k, v, w.in_dtype, False, 0, 128)
+    assert torch.equal(a, b)
+    qd, kd, vd = (to_dev(x, w.in_dtype) for x in (q, k, v))
+    ws = torch.empty(bd.attn_fp4_workspace_size(1, 4, 2048, 128, bd.SAGE_IN_BF16 | bd.SAGE_OUT_F32),
+                     dtype=torch.uint8, device="cuda")
+    c = bd.sage_attn_fp4_fwd(qd, kd, vd, causal=False, workspace=ws)
+    qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q)
+    kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K)
+    vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V)
+    e = bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (1, 4, 2048, 128))
+    torch.cuda.synchronize()
+    assert torch.equal(a, c) and torch.equal(a, e)
+
+
+@pytest.mark.parametrize("in_dtype", [0, 1])
+def test_attn_16bit_output(in_dtype):
+    torch = torch_dev()
+    q, k, v = wl.make_inputs(1, 2, 384, 128, in_dtype, seed=31)
+    o = gpu_attn(q, k, v, in_dtype, False, 0, 128, out_f32=False)
+    assert o.dtype == (torch.bfloat16 if in_dtype == 1 else torch.float16)
+    ref, tie, _ = oracle.attn(q, k, v, in_dtype, False, oracle.FMT_MX, 128)
+    rnd = np.abs(ref).max(axis=1) * (2.0 ** -8 if in_dtype == 1 else 2.0 ** -11)
+    check(o.float().cpu().numpy().reshape(-1, 128), ref, tie, "16-bit out", extra=rnd)
+
+
+def test_attn_no_smooth_k_matches_oracle_ablation():
+    q, k, v = wl.make_inputs(1, 2, 512, 128, 1, seed=32, k_bias_var=4.0)
+    o = gpu_attn(q, k, v, 1, False, bd.SAGE_NO_SMOOTH_K, 128)
+    ref, tie, _ = oracle.attn(q, k, v, 1, False, oracle.FMT_MX, 128, flags=oracle.NO_SMOOTH_K)
+    check(o.cpu().numpy().reshape(-1, 128), ref, tie, "no smooth-K")
+
+
+def test_attn_closed_form_q_zero():
+    """Q = 0: O is the mean of the dequantized V (every P code 6 at unit scale)."""
+    torch = torch_dev()
+    q, k, v = wl.make_inputs(1, 1, 300, 128, 1, seed=33)
+    q[:] = 0
+    o = gpu_attn(q, k, v, 1, False, 0, 128).cpu().numpy().reshape(-1, 128)
+    vc, vs, _, _ = oracle.quant(v, 1, oracle.ROLE_V, oracle.FMT_MX)
+    E2M1 = np.array([0, .5, 1, 1.5, 2, 3, 4, 6, -0., -.5, -1, -1.5, -2, -3, -4, -6])
+    vdeq = E2M1[vc[0, 0]] * np.repeat(2.0 ** (vs[0, 0].astype(np.float64) - 127), 32, axis=1)
+    expect = vdeq[:, :300].mean(axis=1)
+    assert np.abs(o - expect[None, :]).max() < 1e-5
