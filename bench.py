@@ -1,0 +1,211 @@
+#!/usr/bin/env python3
+"""Benchmark: microscaled-FP4 attention forward on one MI355X.
+
+One step = the whole hot path on one batch: smoothing-K mean, FP4 quantization
+of Q, K and V (V transposed), and the FP4 attention kernel, through the C ABI
+(sage_attn_fp4_fwd_ws, inputs resident in HBM, preallocated workspace).
+Workload: B=1, H=32, N=32768, D=128 non-causal, bf16 inputs with 1% of Q and K
+rows scaled by 20 (seeded synthetic data), MXFP4.
+
+Throughput is attention TOPS = 4 B H N^2 D / t.  The JSON line also carries
+the attention kernel's own rate (HIP events around repeated launches of the
+kernel alone on the same stream) as a fraction of the MXFP4 dense MFMA peak,
+the bf16-MFMA comparison kernel's rate when available, and the CPU oracle
+timed on a bounded sample of query rows on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "FP4 attention fwd TOPS at D=128,N=32768; % of MI355X MXFP4 MFMA peak"
+PEAK_FP4_TFLOPS = 10100.0      # MI355X dense MXFP4 MFMA, published
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+PEAK_HBM_GBS = 8000.0
+COUNTERS = os.path.join(ROOT, "profiles", "attn_fp4_mx_counters.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2505_11594_amd", "csrc", "attn_fp4.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def traffic_from_counters(n_launch_units: float):
+    """HBM bytes per launch from committed rocprofv3 FETCH_SIZE/WRITE_SIZE runs
+    (scaled by the copy-kernel calibration), or None when the kernel source
+    changed since they were taken."""
+    if not os.path.exists(COUNTERS):
+        return None
+    c = json.load(open(COUNTERS))
+    if c.get("source_sha") != kernel_source_sha():
+        return None
+    return float(c["hbm_bytes_per_launch"])
+
+
+def cpu_baseline(w, q, k, v, budget_s: float = 15.0):
+    """The oracle, as is, on a bounded sample of query rows of head 0."""
+    import oracle
+    threads = oracle.default_threads()
+    N, D = w.N, w.D
+    rng = np.random.default_rng(0)
+    # one query head's K/V are quantized once per call; take a small probe first
+    q1, k1, v1 = (np.ascontiguousarray(x[:1, :1]) for x in (q, k, v))
+
+    def run(nr):
+        rows = np.sort(rng.choice(N, size=nr, replace=False)).astype(np.int64)
+        t0 = time.perf_counter()
+        oracle.attn(q1, k1, v1, w.in_dtype, w.causal, oracle.FMT_MX, w.bkv, rows=rows, nthreads=threads)
+        return time.perf_counter() - t0
+
+    # per-row cost from two probes (the head's K/V quantization is a fixed cost)
+    t1, t2 = run(threads), run(4 * threads)
+    per_row = max((t2 - t1) / (3 * threads), 1e-6)
+    nrows = int(max(threads, min(N, (budget_s - t1) / per_row)))
+    rows = np.sort(rng.choice(N, size=nrows, replace=False)).astype(np.int64)
+    t0 = time.perf_counter()
+    oracle.attn(q1, k1, v1, w.in_dtype, w.causal, oracle.FMT_MX, w.bkv, rows=rows, nthreads=threads)
+    dt = time.perf_counter() - t0
+    ops = 4.0 * nrows * N * D * (0.5 if w.causal else 1.0)
+    return {"value": ops / dt / 1e12, "unit": "TOPS", "cores": threads, "kind": "oracle",
+            "sample": "%d random query rows of head 0 (of %d x %d), K/V quantization of that head included, %.1f s"
+                      % (nrows, w.B * w.H, N, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bf16", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only (the per-head work needs no communication; "
+              "see the sharding note in DESIGN.md); --gpus %d is not supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2505_11594_amd import binding as bd
+    from paper_2505_11594_amd import workloads as wl
+
+    w = wl.CONFIGS[2]
+    B, H, N, D = w.B, w.H, w.N, w.D
+    log("generating inputs", w.name)
+    q, k, v = wl.generate(w)
+    dt = torch.bfloat16 if w.in_dtype == wl.IN_BF16 else torch.float16
+    dev = torch.device("cuda:0")
+    to_dev = lambda a: torch.from_numpy(a.view(np.int16)).view(dt).to(dev)
+    qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)
+    fmt = bd.SAGE_FMT_MXFP4 | (bd.SAGE_IN_BF16 if w.in_dtype == wl.IN_BF16 else 0) | bd.SAGE_OUT_F32
+    ws = torch.empty(bd.attn_fp4_workspace_size(B, H, N, D, fmt), dtype=torch.uint8, device=dev)
+    o = torch.empty((B, H, N, D), dtype=torch.float32, device=dev)
+    ops = w.ops
+
+    def step():
+        bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=bd.SAGE_FMT_MXFP4, out_f32=True, out=o, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t_step = (time.perf_counter() - t0) / args.steps
+    log("step %.3f ms" % (t_step * 1e3))
+
+    # the attention kernel alone, timed with HIP events on the launch stream
+    qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q)
+    kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K)
+    vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V)
+
+    def attn_only():
+        bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, out=o)
+
+    for _ in range(2):
+        attn_only()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        attn_only()
+    e1.record()
+    torch.cuda.synchronize()
+    t_attn = e0.elapsed_time(e1) / 1e3 / args.steps
+    attn_tflops = ops / t_attn / 1e12
+    log("attention kernel %.3f ms = %.1f TFLOP/s (%.1f%% of MXFP4 peak)" % (t_attn * 1e3, attn_tflops,
+                                                                        100 * attn_tflops / PEAK_FP4_TFLOPS))
+    # quantization kernels alone (HBM-bound)
+    e0.record()
+    for _ in range(args.steps):
+        bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q)
+        bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K)
+        bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V)
+    e1.record()
+    torch.cuda.synchronize()
+    t_quant = e0.elapsed_time(e1) / 1e3 / args.steps
+    n_el = B * H * N * D
+    quant_bytes = n_el * (2 + 2 + 2 + 2) + 3 * n_el * (0.5 + 1.0 / 32)   # K read twice (mean + quantize)
+
+    bf16 = None
+    if not args.no_bf16:
+        try:
+            bd.sage_attn_bf16_fwd(qd, kd, vd, causal=w.causal, out_f32=True, out=o)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(args.steps):
+                bd.sage_attn_bf16_fwd(qd, kd, vd, causal=w.causal, out_f32=True, out=o)
+            e1.record()
+            torch.cuda.synchronize()
+            t_bf = e0.elapsed_time(e1) / 1e3 / args.steps
+            bf16 = {"tops": ops / t_bf / 1e12, "ms": t_bf * 1e3,
+                    "frac_of_bf16_peak": ops / t_bf / 1e12 / PEAK_BF16_TFLOPS}
+        except bd.SageError as ex:
+            log("bf16 kernel unavailable:", ex)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        cpu = cpu_baseline(w, q, k, v)
+
+    line = {
+        "metric": METRIC,
+        "value": ops / t_step / 1e12,
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": t_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "mxfp4",
+        "data": "synthetic (seeded normal Q/K/V, 1% of Q and K rows x20)",
+        "config": {"workload": w.name, "B": B, "H": H, "N": N, "D": D, "causal": w.causal,
+                   "format": "MXFP4 (E2M1, 1x32 blocks, E8M0 scales)", "kv_tile": w.bkv, "parallelism": "none",
+                   "step": "kmean + quantize Q/K/V + FP4 attention (sage_attn_fp4_fwd_ws)"},
+        "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
+                     "frac": attn_tflops / PEAK_FP4_TFLOPS, "traffic": traffic_from_counters(1),
+                     "kernel": "attn_fp4_mx_kernel<128,128,false,0>", "kernel_ms": t_attn * 1e3},
+        "quantize": {"ms": t_quant * 1e3, "algorithmic_GBs": quant_bytes / t_quant / 1e9,
+                     "frac_of_hbm_peak": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS},
+        "bf16_kernel": bf16,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

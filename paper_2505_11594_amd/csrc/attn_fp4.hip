@@ -49,65 +49,57 @@ struct Fp4Tile {
   static constexpr int VC_PER_T = (VC_UNITS + 255) / 256;
 };
 
+// Register staging of one KV tile: every thread issues the same fixed set of
+// 16-byte global loads (no divergent branches, so the loads stay in flight
+// while the current tile is computed) and later writes them to LDS.
 template <int D, int BKV>
-struct Prefetch {
-  uint4 kc[Fp4Tile<D, BKV>::KC_PER_T];
-  uint4 vc[Fp4Tile<D, BKV>::VC_PER_T];
+struct Stage {
+  using T = Fp4Tile<D, BKV>;
+  v4i kc[T::KC_PER_T];
+  v4i vc[T::VC_PER_T];
   uint32_t ks, vs;
-};
 
-template <int D, int BKV>
-__device__ __forceinline__ void tile_load(Prefetch<D, BKV>& pf, const uint8_t* __restrict__ kc,
-                                          const uint8_t* __restrict__ ks, const uint8_t* __restrict__ vc,
-                                          const uint8_t* __restrict__ vs, long long bh, int Np, int kb, int tid) {
-  using T = Fp4Tile<D, BKV>;
-  const uint8_t* kbase = kc + ((size_t)bh * Np + kb) * T::KROW;
+  __device__ __forceinline__ void load(const uint8_t* __restrict__ kcg, const uint8_t* __restrict__ ksg,
+                                       const uint8_t* __restrict__ vcg, const uint8_t* __restrict__ vsg, long long bh,
+                                       int Np, int kb, int tid) {
+    const uint8_t* kbase = kcg + ((size_t)bh * Np + kb) * T::KROW;
 #pragma unroll
-  for (int i = 0; i < T::KC_PER_T; ++i) {
-    const int u = tid + 256 * i;
-    if (u < T::KC_UNITS) pf.kc[i] = *reinterpret_cast<const uint4*>(kbase + (size_t)u * 16);
-  }
+    for (int i = 0; i < T::KC_PER_T; ++i) {
+      const int u = (tid + 256 * i) % T::KC_UNITS;        // units beyond the tile repeat a valid one
+      kc[i] = reinterpret_cast<const v4i*>(kbase)[u];
+    }
 #pragma unroll
-  for (int i = 0; i < T::VC_PER_T; ++i) {
-    const int u = tid + 256 * i;
-    if (u < T::VC_UNITS) {
+    for (int i = 0; i < T::VC_PER_T; ++i) {
+      const int u = (tid + 256 * i) % T::VC_UNITS;
       const int d = u / T::VCH, ch = u % T::VCH;
-      pf.vc[i] = *reinterpret_cast<const uint4*>(vc + ((size_t)bh * D + d) * (Np / 2) + kb / 2 + ch * 16);
+      vc[i] = *reinterpret_cast<const v4i*>(vcg + ((size_t)bh * D + d) * (Np / 2) + kb / 2 + ch * 16);
     }
+    const int key = tid % BKV;
+    const uint8_t* pk = ksg + ((size_t)bh * Np + kb + key) * (D / 32);
+    ks = (D == 128) ? *reinterpret_cast<const uint32_t*>(pk) : (uint32_t)*reinterpret_cast<const uint16_t*>(pk);
+    const int d = tid % D;
+    const uint8_t* pv = vsg + ((size_t)bh * D + d) * (Np / 32) + kb / 32;
+    vs = (BKV == 128) ? *reinterpret_cast<const uint32_t*>(pv) : (uint32_t)*reinterpret_cast<const uint16_t*>(pv);
   }
-  if (tid < BKV) {
-    const uint8_t* p = ks + ((size_t)bh * Np + kb + tid) * (D / 32);
-    pf.ks = (D == 128) ? *reinterpret_cast<const uint32_t*>(p) : (uint32_t)*reinterpret_cast<const uint16_t*>(p);
-  }
-  if (tid >= 128 && tid < 128 + D) {
-    const int d = tid - 128;
-    const uint8_t* p = vs + ((size_t)bh * D + d) * (Np / 32) + kb / 32;
-    pf.vs = (BKV == 128) ? *reinterpret_cast<const uint32_t*>(p) : (uint32_t)*reinterpret_cast<const uint16_t*>(p);
-  }
-}
 
-template <int D, int BKV>
-__device__ __forceinline__ void tile_store(const Prefetch<D, BKV>& pf, uint8_t* lds, int tid) {
-  using T = Fp4Tile<D, BKV>;
+  __device__ __forceinline__ void store(uint8_t* lds, int tid) const {
 #pragma unroll
-  for (int i = 0; i < T::KC_PER_T; ++i) {
-    const int u = tid + 256 * i;
-    if (u < T::KC_UNITS) {
+    for (int i = 0; i < T::KC_PER_T; ++i) {
+      const int u = (tid + 256 * i) % T::KC_UNITS;
       const int row = u / T::KCH, ch = u % T::KCH;
-      *reinterpret_cast<uint4*>(lds + T::KC_OFF + row * T::KROW + swz<T::KCH>(row, ch) * 16) = pf.kc[i];
+      *reinterpret_cast<v4i*>(lds + T::KC_OFF + row * T::KROW + swz<T::KCH>(row, ch) * 16) = kc[i];
     }
-  }
 #pragma unroll
-  for (int i = 0; i < T::VC_PER_T; ++i) {
-    const int u = tid + 256 * i;
-    if (u < T::VC_UNITS) {
+    for (int i = 0; i < T::VC_PER_T; ++i) {
+      const int u = (tid + 256 * i) % T::VC_UNITS;
       const int row = u / T::VCH, ch = u % T::VCH;
-      *reinterpret_cast<uint4*>(lds + T::VC_OFF + row * T::VROW + swz<T::VCH>(row, ch) * 16) = pf.vc[i];
+      *reinterpret_cast<v4i*>(lds + T::VC_OFF + row * T::VROW + swz<T::VCH>(row, ch) * 16) = vc[i];
     }
+    // duplicate writers store identical values
+    *reinterpret_cast<uint32_t*>(lds + T::KS_OFF + (tid % BKV) * 4) = ks;
+    *reinterpret_cast<uint32_t*>(lds + T::VS_OFF + (tid % D) * 4) = vs;
   }
-  if (tid < BKV) *reinterpret_cast<uint32_t*>(lds + T::KS_OFF + tid * 4) = pf.ks;
-  if (tid >= 128 && tid < 128 + D) *reinterpret_cast<uint32_t*>(lds + T::VS_OFF + (tid - 128) * 4) = pf.vs;
-}
+};
 
 __device__ __forceinline__ v8i as_op(const v4i x) { return v8i{x[0], x[1], x[2], x[3], 0, 0, 0, 0}; }
 
@@ -165,15 +157,28 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
   for (int db = 0; db < NDB; ++db) oacc[db] = v16f{};
   float m = -INFINITY, mc_old = -INFINITY, f_old = 0.0f, lsum_acc = 0.0f;
 
-  Prefetch<D, BKV> pf;
-  tile_load<D, BKV>(pf, kc, ks, vc, vs, bh, Np, 0, tid);
-  tile_store<D, BKV>(pf, lds[0], tid);
+  // Per-lane LDS byte offsets, the same for every tile: A-operand chunk
+  // (2s + hi) of row col (the swizzle depends on row bits 1..2 only, which
+  // the 32-row subtile offset leaves unchanged).
+  int koff[NKS], voff[NG];
+#pragma unroll
+  for (int s = 0; s < NKS; ++s) koff[s] = T::KC_OFF + col * T::KROW + swz<T::KCH>(col, 2 * s + hi) * 16;
+#pragma unroll
+  for (int g = 0; g < NG; ++g) voff[g] = T::VC_OFF + col * T::VROW + swz<T::VCH>(col, 2 * g + hi) * 16;
+  const int ksoff = T::KS_OFF + col * 4, vsoff = T::VS_OFF + col * 4;
+  const int hsh = 8 * hi;
+
+  Stage<D, BKV> stg;
+  stg.load(kc, ks, vc, vs, bh, Np, 0, tid);
+  stg.store(lds[0], tid);
   __syncthreads();
 
-  for (int j = 0; j < ntiles; ++j) {
+  auto tile = [&](auto BUF_, int j) {
+    constexpr int buf = decltype(BUF_)::value;
+    const uint8_t* L = lds[buf];
     const int kb = j * BKV;
-    const uint8_t* L = lds[j & 1];
-    if (j + 1 < ntiles) tile_load<D, BKV>(pf, kc, ks, vc, vs, bh, Np, kb + BKV, tid);
+    const bool more = j + 1 < ntiles;
+    if (more) stg.load(kc, ks, vc, vs, bh, Np, kb + BKV, tid);
 
     const bool active = !CAUSAL || kb <= qw + 31;
     if (active) {
@@ -181,12 +186,11 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
       v16f sacc[NSUB];
 #pragma unroll
       for (int t = 0; t < NSUB; ++t) {
-        const int row = 32 * t + col;
-        const uint32_t ksc = *reinterpret_cast<const uint32_t*>(L + T::KS_OFF + row * 4) >> (8 * hi);
+        const uint32_t ksc = *reinterpret_cast<const uint32_t*>(L + ksoff + 32 * t * 4) >> hsh;
         v16f acc = v16f{};
         static_for<NKS>([&](auto S_) {
           constexpr int s = decltype(S_)::value;
-          const v4i a = *reinterpret_cast<const v4i*>(L + T::KC_OFF + row * T::KROW + swz<T::KCH>(row, 2 * s + hi) * 16);
+          const v4i a = *reinterpret_cast<const v4i*>(L + koff[s] + 32 * t * T::KROW);
           acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(qreg[s]), acc, 4, 4, 2 * s, (int)ksc,
                                                                 2 * s, (int)qsc);
         });
@@ -258,7 +262,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
           }
         }
         pw[g] = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
-        int sb = e + kfold + 127;
+        const int sb = e + kfold + 127;
         psb[g] = sb < 0 ? 0 : sb;
       }
       // ---- rescale and O^T += V^T . P^T ------------------------------------
@@ -269,11 +273,10 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
       lsum_acc = lsum_acc * gam + __builtin_ldexpf(psum, kfold);
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const int row = 32 * db + col;
-        const uint32_t vsc = *reinterpret_cast<const uint32_t*>(L + T::VS_OFF + row * 4) >> (8 * hi);
+        const uint32_t vsc = *reinterpret_cast<const uint32_t*>(L + vsoff + 32 * db * 4) >> hsh;
         static_for<NG>([&](auto G_) {
           constexpr int g = decltype(G_)::value;
-          const v4i a = *reinterpret_cast<const v4i*>(L + T::VC_OFF + row * T::VROW + swz<T::VCH>(row, 2 * g + hi) * 16);
+          const v4i a = *reinterpret_cast<const v4i*>(L + voff[g] + 32 * db * T::VROW);
           oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(pw[g]), oacc[db], 4, 4, 2 * g,
                                                                      (int)vsc, 0, psb[g]);
         });
@@ -282,8 +285,13 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
       mc_old = mc;
       f_old = f;
     }
-    if (j + 1 < ntiles) tile_store<D, BKV>(pf, lds[(j + 1) & 1], tid);
+    if (more) stg.store(lds[buf ^ 1], tid);
     __syncthreads();
+  };
+
+  for (int j = 0; j < ntiles; j += 2) {
+    tile(ic<0>{}, j);
+    if (j + 1 < ntiles) tile(ic<1>{}, j + 1);
   }
 
   // ---- epilogue: O = O^T / l, stored row-major ----------------------------
