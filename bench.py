@@ -91,6 +91,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true")
+    ap.add_argument("--mode", choices=["full", "attn", "copy"], default="full",
+                    help="attn: only the attention kernel (for counter runs); "
+                         "copy: a plain 1 GiB device copy (calibrates FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only (the per-head work needs no communication; "
@@ -100,6 +103,16 @@ def main():
     import torch
     from paper_2505_11594_amd import binding as bd
     from paper_2505_11594_amd import workloads as wl
+
+    if args.mode == "copy":
+        nbytes = 1 << 30
+        src = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup + args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "copy", "bytes_per_copy": nbytes, "copies": args.warmup + args.steps}))
+        return
 
     w = wl.CONFIGS[2]
     B, H, N, D = w.B, w.H, w.N, w.D
@@ -116,6 +129,16 @@ def main():
 
     def step():
         bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=bd.SAGE_FMT_MXFP4, out_f32=True, out=o, workspace=ws)
+
+    if args.mode == "attn":
+        qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q)
+        kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K)
+        vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V)
+        for _ in range(args.warmup + args.steps):
+            bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, out=o)
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "attn", "launches": args.warmup + args.steps, "ops_per_launch": ops}))
+        return
 
     for _ in range(args.warmup):
         step()

@@ -29,8 +29,12 @@ namespace sage {
 
 constexpr int AQ = 128;   // queries per workgroup (4 waves x 32)
 
+// 16-byte-chunk XOR swizzle of LDS rows (64 or 32 bytes long).  An MFMA
+// operand read has consecutive lanes on consecutive rows at one chunk; rows
+// r and r + 4k must land in different chunks for 64 banks (16 lanes per pass)
+// and rows r and r + 2k for 32 banks (8 lanes per pass).
 template <int NCH>
-__device__ __forceinline__ int swz(int row, int ch) { return ch ^ ((row >> 1) & (NCH - 1)); }
+__device__ __forceinline__ int swz(int row, int ch) { return ch ^ (((row >> 1) ^ (row >> 3)) & (NCH - 1)); }
 
 template <int D, int BKV>
 struct Fp4Tile {
@@ -40,9 +44,9 @@ struct Fp4Tile {
   static constexpr int VCH = BKV / 32;        // 16-byte chunks per V^T tile row
   static constexpr int KC_OFF = 0;
   static constexpr int KS_OFF = KC_OFF + BKV * KROW;
-  static constexpr int VC_OFF = KS_OFF + BKV * 4;
+  static constexpr int VC_OFF = KS_OFF + BKV * 8;   // K scales: 2 dwords per key
   static constexpr int VS_OFF = VC_OFF + D * VROW;
-  static constexpr int BYTES = VS_OFF + D * 4;
+  static constexpr int BYTES = VS_OFF + D * 8;      // V scales: 2 dwords per row
   static constexpr int KC_UNITS = BKV * KCH;  // 16-byte units
   static constexpr int VC_UNITS = D * VCH;
   static constexpr int KC_PER_T = (KC_UNITS + 255) / 256;
@@ -95,9 +99,14 @@ struct Stage {
       const int row = u / T::VCH, ch = u % T::VCH;
       *reinterpret_cast<v4i*>(lds + T::VC_OFF + row * T::VROW + swz<T::VCH>(row, ch) * 16) = vc[i];
     }
-    // duplicate writers store identical values
-    *reinterpret_cast<uint32_t*>(lds + T::KS_OFF + (tid % BKV) * 4) = ks;
-    *reinterpret_cast<uint32_t*>(lds + T::VS_OFF + (tid % D) * 4) = vs;
+    // Scale bytes of a row are split by lane half: the half-hi lanes of an
+    // MFMA need bytes hi, hi+2 (blocks 2s + hi), so slot hi holds them as
+    // bytes 0 and 1 and the MFMA op_sel picks byte s directly.  Duplicate
+    // writers store identical values.
+    const uint32_t k0 = (ks & 0xFFu) | ((ks >> 8) & 0xFF00u), k1 = ((ks >> 8) & 0xFFu) | ((ks >> 16) & 0xFF00u);
+    const uint32_t v0 = (vs & 0xFFu) | ((vs >> 8) & 0xFF00u), v1 = ((vs >> 8) & 0xFFu) | ((vs >> 16) & 0xFF00u);
+    *reinterpret_cast<uint2*>(lds + T::KS_OFF + (tid % BKV) * 8) = make_uint2(k0, k1);
+    *reinterpret_cast<uint2*>(lds + T::VS_OFF + (tid % D) * 8) = make_uint2(v0, v1);
   }
 };
 
@@ -158,15 +167,14 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
   float m = -INFINITY, mc_old = -INFINITY, f_old = 0.0f, lsum_acc = 0.0f;
 
   // Per-lane LDS byte offsets, the same for every tile: A-operand chunk
-  // (2s + hi) of row col (the swizzle depends on row bits 1..2 only, which
+  // (2s + hi) of row col (the swizzle depends on row bits 1..4 only, which
   // the 32-row subtile offset leaves unchanged).
   int koff[NKS], voff[NG];
 #pragma unroll
   for (int s = 0; s < NKS; ++s) koff[s] = T::KC_OFF + col * T::KROW + swz<T::KCH>(col, 2 * s + hi) * 16;
 #pragma unroll
   for (int g = 0; g < NG; ++g) voff[g] = T::VC_OFF + col * T::VROW + swz<T::VCH>(col, 2 * g + hi) * 16;
-  const int ksoff = T::KS_OFF + col * 4, vsoff = T::VS_OFF + col * 4;
-  const int hsh = 8 * hi;
+  const int ksoff = T::KS_OFF + col * 8 + hi * 4, vsoff = T::VS_OFF + col * 8 + hi * 4;
 
   Stage<D, BKV> stg;
   stg.load(kc, ks, vc, vs, bh, Np, 0, tid);
@@ -186,12 +194,12 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
       v16f sacc[NSUB];
 #pragma unroll
       for (int t = 0; t < NSUB; ++t) {
-        const uint32_t ksc = *reinterpret_cast<const uint32_t*>(L + ksoff + 32 * t * 4) >> hsh;
+        const uint32_t ksc = *reinterpret_cast<const uint32_t*>(L + ksoff + 32 * t * 8);
         v16f acc = v16f{};
         static_for<NKS>([&](auto S_) {
           constexpr int s = decltype(S_)::value;
           const v4i a = *reinterpret_cast<const v4i*>(L + koff[s] + 32 * t * T::KROW);
-          acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(qreg[s]), acc, 4, 4, 2 * s, (int)ksc,
+          acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(qreg[s]), acc, 4, 4, s, (int)ksc,
                                                                 2 * s, (int)qsc);
         });
         sacc[t] = acc;
@@ -212,6 +220,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
       float bm[NG];
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
+        // a serial chain: the compiler fuses it into v_max3 (a tree costs more)
         float x = sacc[2 * g][0];
 #pragma unroll
         for (int v = 1; v < 16; ++v) x = __builtin_fmaxf(x, sacc[2 * g][v]);
@@ -222,7 +231,9 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
       float tl = bm[0];
 #pragma unroll
       for (int g = 1; g < NG; ++g) tl = __builtin_fmaxf(tl, bm[g]);
-      const float t = __builtin_fmaxf(tl, __shfl_xor(tl, 32, 64));
+      // row max over the two lane halves that share a query
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(tl), __float_as_uint(tl), false, false);
+      const float t = __builtin_fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
       const float m_new = __builtin_fmaxf(m, t);
       const float tc = t * c2;
       const float mc = m_new * c2;
@@ -234,7 +245,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
       const float bias = log6 - tc;                      // P~2 = 2^{fma(S, c2, log2 6 - t c2)}
 
       // ---- P~2, unquantized row sum, FP4 pack with E8M0 block scales ----
-      float psum = 0.0f;
+      float ps[4] = {0.0f, 0.0f, 0.0f, 0.0f};            // independent partial row sums
       v4i pw[NG];
       int psb[NG];
 #pragma unroll
@@ -254,8 +265,8 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
               constexpr int i = decltype(I_)::value;
               const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[tt][8 * q + 2 * i], c2, bias));
               const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[tt][8 * q + 2 * i + 1], c2, bias));
-              psum += p0;
-              psum += p1;
+              ps[(2 * half + q) & 3] += p0;
+              ps[(2 * half + q) & 3] += p1;
               word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, p0, p1, escale, i);
             });
             w[2 * half + q] = word;
@@ -270,14 +281,15 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int v = 0; v < 16; ++v) oacc[db][v] *= gam;
+      const float psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
       lsum_acc = lsum_acc * gam + __builtin_ldexpf(psum, kfold);
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const uint32_t vsc = *reinterpret_cast<const uint32_t*>(L + vsoff + 32 * db * 4) >> hsh;
+        const uint32_t vsc = *reinterpret_cast<const uint32_t*>(L + vsoff + 32 * db * 8);
         static_for<NG>([&](auto G_) {
           constexpr int g = decltype(G_)::value;
           const v4i a = *reinterpret_cast<const v4i*>(L + voff[g] + 32 * db * T::VROW);
-          oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(pw[g]), oacc[db], 4, 4, 2 * g,
+          oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(pw[g]), oacc[db], 4, 4, g,
                                                                      (int)vsc, 0, psb[g]);
         });
       }

@@ -157,7 +157,7 @@ __global__ void k_tail_kernel(uint8_t* __restrict__ codes, uint8_t* __restrict__
 // quantizes whole token blocks of one channel and writes them contiguously
 // into V^T [bh, d, Np/2].  Tokens >= N are zero.
 // ---------------------------------------------------------------------------
-constexpr int VT = 128;   // tokens per tile
+constexpr int VT = 128;   // tokens per tile (a V^T row segment of 64 bytes)
 
 template <int D, bool BF16, int FMT>
 __global__ __launch_bounds__(256) void quant_v_kernel(const uint16_t* __restrict__ v, uint8_t* __restrict__ codes,
@@ -165,8 +165,20 @@ __global__ __launch_bounds__(256) void quant_v_kernel(const uint16_t* __restrict
   constexpr int NB = (FMT == kFmtMX) ? 32 : 16;
   constexpr int TPC = 256 / D;               // threads per channel: 2 (D=128) or 4 (D=64)
   constexpr int BPT = VT / NB / TPC;         // token blocks per thread
-  __shared__ uint16_t tile[VT][D + 2];       // +2 halves: rows start on different banks
-  const int tt = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  static_assert(BPT >= 1, "tile shape");
+  // all lanes of a wave read one row (consecutive channels): no padding needed
+  __shared__ uint16_t tile[VT][D];
+  // Workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous
+  // range of (bh, tile) so the two 64-byte halves of every 128-byte V^T line
+  // are written through the same L2 at nearly the same time.
+  const int ntt = (Np + VT - 1) / VT;
+  const int total = ntt * gridDim.y;
+  int lin = blockIdx.y * ntt + blockIdx.x;
+  if ((total & 7) == 0) {
+    const int w = blockIdx.y * gridDim.x + blockIdx.x;   // dispatch order
+    lin = (w & 7) * (total >> 3) + (w >> 3);
+  }
+  const int tt = lin % ntt, bh = lin / ntt, tid = threadIdx.x;
   const int t0 = tt * VT;
   const uint16_t* vb = v + (size_t)bh * N * D;
   constexpr int UPR = D / 8;
@@ -175,17 +187,16 @@ __global__ __launch_bounds__(256) void quant_v_kernel(const uint16_t* __restrict
     const int t = t0 + r;
     uint4 raw = make_uint4(0, 0, 0, 0);
     if (t < N) raw = *reinterpret_cast<const uint4*>(vb + (size_t)t * D + cu * 8);
-    const uint16_t* hv = reinterpret_cast<const uint16_t*>(&raw);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) tile[r][cu * 8 + j] = hv[j];
+    *reinterpret_cast<uint4*>(&tile[r][cu * 8]) = raw;
   }
   __syncthreads();
-  const int c = tid / TPC, part = tid % TPC;
+  const int c = tid % D, part = tid / D;
   uint8_t* crow = codes + ((size_t)bh * D + c) * (Np / 2);
   uint8_t* srow = scales + ((size_t)bh * D + c) * (Np / NB);
 #pragma unroll
   for (int bb = 0; bb < BPT; ++bb) {
     const int blk = part * BPT + bb;         // token block inside the tile
+    if (t0 + blk * NB >= Np) break;          // the last tile may end at Np (a multiple of 128)
     float x[NB];
     float am = 0.0f;
 #pragma unroll
@@ -273,7 +284,8 @@ hipError_t launch_quant_rows(const void* x, const float* mu, void* codes, void* 
 
 template <int D, bool BF16, int FMT>
 static hipError_t launch_v_t(const void* v, void* codes, void* scales, int BH, int N, int Np, hipStream_t st) {
-  hipLaunchKernelGGL((quant_v_kernel<D, BF16, FMT>), dim3(Np / VT, BH), dim3(256), 0, st, (const uint16_t*)v,
+  // Np is a multiple of 128; a last half tile is handled by the tile-range guard
+  hipLaunchKernelGGL((quant_v_kernel<D, BF16, FMT>), dim3((Np + VT - 1) / VT, BH), dim3(256), 0, st, (const uint16_t*)v,
                      (uint8_t*)codes, (uint8_t*)scales, N, Np);
   return hipGetLastError();
 }

@@ -5,7 +5,7 @@
 #include <cstring>
 
 #include "sage_common.h"
-#include "../../include/sage_mi355x.h"
+#include "sage_mi355x.h"
 
 namespace sage {
 hipError_t launch_kmean(const void* k, double* part, float* mu, int BH, int N, int D, bool bf16, hipStream_t st);
@@ -17,6 +17,9 @@ hipError_t launch_quant_v(const void* v, void* codes, void* scales, int BH, int 
 hipError_t launch_attn_fp4_mx(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
                               const void* vs, void* o, int BH, int N, int Np, int D, int bkv, bool causal, int out,
                               float c2, float log6, hipStream_t st);
+hipError_t launch_attn_bf16(const void* q, const void* k, const void* vt, void* o, int BH, int N, int Np, int D,
+                            bool causal, bool out_f32, float c2, hipStream_t st);
+hipError_t launch_transpose_v_bf16(const void* v, void* vt, int BH, int N, int Np, int D, hipStream_t st);
 }  // namespace sage
 
 namespace {
@@ -219,8 +222,17 @@ int sage_attn_bf16_fwd(const void* q, const void* k, const void* v, void* o, int
   if (!(flags & SAGE_IN_BF16)) return SAGE_ERR_INVALID_ARG;
   int rc = attn_args(q, k, v, o, B, H, N, D, causal, flags);
   if (rc != SAGE_OK) return rc;
-  (void)stream;
-  return SAGE_ERR_UNSUPPORTED;
+  const int Np = pad128(N);
+  const size_t bytes = (size_t)B * H * D * Np * 2;
+  void* vt = nullptr;
+  if (hipMallocAsync(&vt, bytes, stream) != hipSuccess) return SAGE_ERR_HIP;
+  hipError_t e = sage::launch_transpose_v_bf16(v, vt, B * H, N, Np, D, stream);
+  if (e == hipSuccess)
+    e = sage::launch_attn_bf16(q, k, vt, o, B * H, N, Np, D, causal != 0, (flags & SAGE_OUT_F32) != 0, softmax_c2(D),
+                               stream);
+  rc = hip_status(e);
+  if (hipFreeAsync(vt, stream) != hipSuccess && rc == SAGE_OK) rc = SAGE_ERR_HIP;
+  return rc;
 }
 
 const char* sage_status_string(int status) {
