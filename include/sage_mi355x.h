@@ -56,11 +56,13 @@ typedef enum {
  * low nibble.  Scale bytes are E8M0 (2^(b-127)) or E4M3FN.
  *   Q^  codes [B,H,N,D/2],  scales [B,H,N,D/n]      blocks along D
  *   K^  codes [B,H,Np,D/2], scales [B,H,Np,D/n]     blocks along D, of
- *       K' = fl32(K - mean_t K) (smoothing K).  Inside every 64-token group
- *       the token with offset o = 32h + 16t + 4g + r (h,t in {0,1};
- *       g,r in {0..3}) is stored at position 32t + 8g + 4h + r, so the MFMA
+ *       K' = fl32(K - mean_t K) (smoothing K), tokens permuted so the MFMA
  *       accumulator of S^T = K^ Q^T is laid out as the B operand of the P.V
- *       product (the CDNA form of the paper's "Permutation for K", Sec. 3.3).
+ *       product (the CDNA form of the paper's "Permutation for K", Sec. 3.3):
+ *       MXFP4: inside every 64-token group the token with offset
+ *       o = 32h + 16t + 4g + r (h,t in {0,1}; g,r in {0..3}) is stored at
+ *       position 32t + 8g + 4h + r;  NV16: inside every 32-token group the
+ *       offset o = 16h + 4g + r goes to position 8g + 4h + r.
  *       Tokens >= N have zero codes.
  *   V^T codes [B,H,D,Np/2], scales [B,H,D,Np/n]     blocks along tokens, V
  *       transposed (Appendix, "Transposing V"), natural token order, tokens
@@ -108,6 +110,9 @@ size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt);
  * tiles with the two-level quantization of P~ (Sec. 3.2: s_P1 = rowmax/R
  * per row and tile, then phi of P~/s_P1 with R = 6 for E8M0 scales and
  * 448*6 for E4M3 scales) and O += FP4MM(P^, V^) * s_P1; O = O / l.
+ * MXFP4 runs on block-scaled FP4 MFMA; NV16 (whose E4M3 scales at 16-element
+ * granularity the MFMA cannot take) dequantizes exactly to bf16 and runs on
+ * bf16 MFMA.
  * Softmax scale is 1/sqrt(D).  causal = 1 keeps key j for query i iff j <= i.
  *  q, k, v  : 16-bit [B,H,N,D], 16-byte aligned
  *  o        : [B,H,N,D] fp32 (SAGE_OUT_F32) or input dtype, 16-byte aligned

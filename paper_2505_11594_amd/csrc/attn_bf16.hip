@@ -11,11 +11,13 @@
 // 16-token group with offset bits 2 and 3 swapped, so the 8 scores a lane
 // holds for one 16-key K-step are exactly the keys its P operand slots need.
 #include "sage_common.h"
+#include "bf16_tile.h"
 
 namespace sage {
 
 constexpr int BQ = 128;        // queries per workgroup
 constexpr int BK = 64;         // keys per tile
+template <int D> using Bf16Tile = Bf16TileT<D, BK>;
 
 __device__ __forceinline__ int vt_pos(int t) {
   // offset bits (b3 b2) swapped inside each 16-token group (an involution)
@@ -50,29 +52,6 @@ __global__ __launch_bounds__(256) void transpose_v_kernel(const uint16_t* __rest
     w.z = o[4] | ((uint32_t)o[5] << 16); w.w = o[6] | ((uint32_t)o[7] << 16);
     *reinterpret_cast<uint4*>(vt + ((size_t)bh * D + d) * Np + t0 + p0) = w;
   }
-}
-
-template <int D>
-struct Bf16Tile {
-  static constexpr int KROW = D * 2;          // bytes per K row
-  static constexpr int KCH = KROW / 16;       // chunks per K row (16 or 8)
-  static constexpr int VROW = BK * 2;         // bytes per V^T tile row (128)
-  static constexpr int VCH = VROW / 16;       // 8
-  static constexpr int K_OFF = 0;
-  static constexpr int V_OFF = BK * KROW;
-  static constexpr int BYTES = V_OFF + D * VROW;
-  static constexpr int KU = BK * KCH, VU = D * VCH;
-  static constexpr int KPT = KU / 256, VPT = VU / 256;
-};
-
-// 16-byte chunk swizzle: lanes of one operand read sit on consecutive rows at
-// one chunk; keep 8 (32 banks) or 16 (64 banks) consecutive rows on distinct
-// bank groups.  Only row bits 0..4 matter, so a 32-row block offset does not
-// change the swizzle.
-template <int NCH>
-__device__ __forceinline__ int bswz(int row, int ch) {
-  if constexpr (NCH == 16) return ch ^ (row & 15);
-  else return ch ^ (((row & 31) ^ ((row & 31) >> 3)) & 7);
 }
 
 template <int D>
@@ -111,7 +90,6 @@ struct Bf16Stage {
   }
 };
 
-__device__ __forceinline__ v8bf as_bf(const v4i x) { return __builtin_bit_cast(v8bf, x); }
 
 template <int D, bool CAUSAL, bool OUT_F32>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,

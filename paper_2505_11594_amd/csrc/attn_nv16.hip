@@ -1,0 +1,312 @@
+// NV16 (E2M1 codes, 16-element blocks, E4M3 scales -- the paper's NVFP4,
+// Sec. 3.1) attention forward for gfx950.  The block-scaled MFMA only takes
+// E8M0 scales at 32-element granularity, so this path dequantizes exactly to
+// bf16 (an E2M1 value times an E4M3 scale has at most 6 significant bits) and
+// runs both products on v_mfma_f32_32x32x16_bf16:
+//   * Q^ is dequantized once into the B-operand registers;
+//   * each K^ / V^T tile arrives as codes + scales (4.5 bits per element),
+//     staged in registers a tile ahead and dequantized into bf16 LDS tiles;
+//   * P~ gets the two-level quantization of Sec. 3.2 with R = 448 * 6 in
+//     registers: the first level as in the MXFP4 kernel, the second level an
+//     E4M3 scale per 16 keys (round to nearest even of blockmax/6), E2M1 codes
+//     of P~2 / s, and the dequantized code * s fed to the MFMA in bf16.
+// K^ is stored with the tokens of every 32-token group permuted (offset
+// 16h + 4g + r at position 8g + 4h + r), so the 16 scores a lane holds for one
+// 32-key subtile are one 16-key block of original keys and, split in halves,
+// exactly the P operand of two 16-key K-steps; V^T stays in natural order.
+#include "sage_common.h"
+#include "bf16_tile.h"
+
+namespace sage {
+
+constexpr int NQ = 128;   // queries per workgroup (4 waves x 32)
+
+template <int D, int BKV>
+struct Nv16Stage {
+  using T = Bf16TileT<D, BKV>;
+  static constexpr int KU = BKV * D / 32, VU = D * BKV / 32;   // 32-element units
+  static constexpr int KPT = (KU + 255) / 256, VPT = (VU + 255) / 256;
+  v4i kc[KPT], vc[VPT];
+  uint32_t ksc[KPT], vsc[VPT];
+
+  __device__ __forceinline__ void load(const uint8_t* __restrict__ kcg, const uint8_t* __restrict__ ksg,
+                                       const uint8_t* __restrict__ vcg, const uint8_t* __restrict__ vsg, long long bh,
+                                       int Np, int kb, int tid) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int u = (tid + 256 * i) % KU;          // units past the tile repeat a valid one
+      const int row = u / (D / 32), c = u % (D / 32);
+      const size_t r = (size_t)bh * Np + kb + row;
+      kc[i] = *reinterpret_cast<const v4i*>(kcg + r * (D / 2) + c * 16);
+      ksc[i] = *reinterpret_cast<const uint16_t*>(ksg + r * (D / 16) + c * 2);
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int u = (tid + 256 * i) % VU;
+      const int d = u / (BKV / 32), c = u % (BKV / 32);
+      const size_t r = (size_t)bh * D + d;
+      vc[i] = *reinterpret_cast<const v4i*>(vcg + r * (Np / 2) + kb / 2 + c * 16);
+      vsc[i] = *reinterpret_cast<const uint16_t*>(vsg + r * (Np / 16) + kb / 16 + c * 2);
+    }
+  }
+
+  // 32 codes + two E4M3 scales -> 32 bf16 values in four 16-byte chunks
+  __device__ __forceinline__ static void dequant32(const v4i codes, uint32_t sc2, v4i out[4]) {
+    const float s0 = e4m3_decode(sc2 & 0xFFu), s1 = e4m3_decode((sc2 >> 8) & 0xFFu);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float s = (w < 2) ? s0 : s1;
+      const uint32_t word = (uint32_t)codes[w];
+      uint32_t o[4];
+      static_for<4>([&](auto B_) {
+        constexpr int b = decltype(B_)::value;
+        const auto f = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(word, 1.0f, b);   // exact E2M1 values
+        typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+        const v2bf pb = {(__bf16)(f[0] * s), (__bf16)(f[1] * s)};                 // exact in bf16
+        o[b] = __builtin_bit_cast(uint32_t, pb);
+      });
+      out[w] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+    }
+  }
+
+  __device__ __forceinline__ void store(uint8_t* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int u = (tid + 256 * i) % KU;
+      const int row = u / (D / 32), c = u % (D / 32);
+      v4i q[4];
+      dequant32(kc[i], ksc[i], q);
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        *reinterpret_cast<v4i*>(lds + T::K_OFF + row * T::KROW + bswz<T::KCH>(row, 4 * c + w) * 16) = q[w];
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int u = (tid + 256 * i) % VU;
+      const int d = u / (BKV / 32), c = u % (BKV / 32);
+      v4i q[4];
+      dequant32(vc[i], vsc[i], q);
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        *reinterpret_cast<v4i*>(lds + T::V_OFF + d * T::VROW + bswz<T::VCH>(d, 4 * c + w) * 16) = q[w];
+    }
+  }
+};
+
+template <int D, int BKV, bool CAUSAL, int OUT>   // OUT: 0 = fp32, 1 = bf16, 2 = fp16
+__global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
+    const uint8_t* __restrict__ qc, const uint8_t* __restrict__ qs, const uint8_t* __restrict__ kc,
+    const uint8_t* __restrict__ ks, const uint8_t* __restrict__ vc, const uint8_t* __restrict__ vs,
+    void* __restrict__ o, int BH, int N, int Np, int nqt, float c2, float logR) {
+  using T = Bf16TileT<D, BKV>;
+  constexpr int NSUB = BKV / 32;   // 32-key subtiles = P blocks per lane
+  constexpr int NKS = D / 16;      // QK K-steps
+  constexpr int NPK = BKV / 16;    // PV K-steps
+  constexpr int NDB = D / 32;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2][T::BYTES];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 31, hi = lane >> 5;
+
+  const int total = nqt * BH;
+  int lin = blockIdx.x;
+  if ((total & 7) == 0) lin = (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3);
+  const long long bh = lin / nqt;
+  int qt = lin % nqt;
+  if (CAUSAL) qt = nqt - 1 - qt;
+  const int q0 = qt * NQ, qw = q0 + wave * 32, qi = qw + col;
+
+  // Q^ dequantized into the B operand: K-step s holds dims [16s + 8hi, +8) (block s)
+  v4i qreg[NKS];
+  {
+    const int qr = min(qi, N - 1);
+    const uint8_t* crow = qc + ((size_t)bh * N + qr) * (D / 2);
+    const uint8_t* srow = qs + ((size_t)bh * N + qr) * (D / 16);
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) {
+      const uint32_t word = *reinterpret_cast<const uint32_t*>(crow + 8 * s + 4 * hi);
+      const float sc = (qi < N) ? e4m3_decode(srow[s]) : 0.0f;
+      uint32_t w[4];
+      static_for<4>([&](auto B_) {
+        constexpr int b = decltype(B_)::value;
+        const auto f = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(word, 1.0f, b);
+        typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+        const v2bf pb = {(__bf16)(f[0] * sc), (__bf16)(f[1] * sc)};
+        w[b] = __builtin_bit_cast(uint32_t, pb);
+      });
+      qreg[s] = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+    }
+  }
+  int ntiles = (N + BKV - 1) / BKV;
+  if (CAUSAL) ntiles = min(ntiles, min(q0 + NQ - 1, N - 1) / BKV + 1);
+
+  int vo[NPK];   // V^T operand offsets: K-step (t, w) reads keys 32t + 16hi + 8w + [0, 8)
+#pragma unroll
+  for (int u = 0; u < NPK; ++u)
+    vo[u] = T::V_OFF + col * T::VROW + bswz<T::VCH>(col, 4 * (u >> 1) + 2 * hi + (u & 1)) * 16;
+
+  v16f oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) oacc[db] = v16f{};
+  float m = -INFINITY, mc_old = -INFINITY, f_old = 0.0f, lsum_acc = 0.0f;
+
+  Nv16Stage<D, BKV> stg;
+  stg.load(kc, ks, vc, vs, bh, Np, 0, tid);
+  stg.store(lds[0], tid);
+  __syncthreads();
+
+  auto tile = [&](auto BUF_, int j) {
+    constexpr int buf = decltype(BUF_)::value;
+    const uint8_t* L = lds[buf];
+    const int kb = j * BKV;
+    const bool more = j + 1 < ntiles;
+    if (more) stg.load(kc, ks, vc, vs, bh, Np, kb + BKV, tid);
+    if (!CAUSAL || kb <= qw + 31) {
+      v16f sacc[NSUB];
+#pragma unroll
+      for (int t = 0; t < NSUB; ++t) {
+        const int row = 32 * t + col;
+        v16f acc = v16f{};
+#pragma unroll
+        for (int s = 0; s < NKS; ++s) {
+          const v4i a = *reinterpret_cast<const v4i*>(L + T::K_OFF + row * T::KROW + bswz<T::KCH>(row, 2 * s + hi) * 16);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf(a), as_bf(qreg[s]), acc, 0, 0, 0);
+        }
+        sacc[t] = acc;
+      }
+      if ((kb + BKV > N) || (CAUSAL && kb + BKV - 1 > qw)) {
+#pragma unroll
+        for (int t = 0; t < NSUB; ++t)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int key = kb + 32 * t + 16 * hi + v;
+            if (!(key < N && (!CAUSAL || key <= qi))) sacc[t][v] = -INFINITY;
+          }
+      }
+      float bm[NSUB];
+#pragma unroll
+      for (int t = 0; t < NSUB; ++t) {
+        float x = sacc[t][0];
+#pragma unroll
+        for (int v = 1; v < 16; ++v) x = __builtin_fmaxf(x, sacc[t][v]);
+        bm[t] = x;
+      }
+      float tl = bm[0];
+#pragma unroll
+      for (int t = 1; t < NSUB; ++t) tl = __builtin_fmaxf(tl, bm[t]);
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(tl), __float_as_uint(tl), false, false);
+      const float tmax = __builtin_fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+      const float m_new = __builtin_fmaxf(m, tmax);
+      const float tc = tmax * c2, mc = m_new * c2;
+      const float delta = tc - mc;
+      const float kf = __builtin_floorf(delta);
+      const float f = delta - kf;
+      const float gam = __builtin_amdgcn_exp2f((mc_old - mc) + (f_old - f));
+      const int kfold = (int)__builtin_fmaxf(kf, -300.0f);
+      const float bias = logR - tc;                    // P~2 = 2^{fma(S, c2, log2 R - t c2)}, R = 448 * 6
+      float ps[2] = {0.0f, 0.0f};
+      v4i pk[NPK];
+#pragma unroll
+      for (int t = 0; t < NSUB; ++t) {
+        // second level: E4M3 scale of this lane's 16-key block
+        const float amax = (bm[t] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(__builtin_fmaf(bm[t], c2, bias));
+        const uint32_t sb = e4m3_encode(amax / 6.0f);
+        const float s2 = e4m3_decode(sb);
+        const float r = (s2 == 0.0f) ? 0.0f : 1.0f / s2;
+        const float s2k = __builtin_ldexpf(s2, kfold);   // k_j folded into the dequantized P
+#pragma unroll
+        for (int w = 0; w < 2; ++w) {
+          uint32_t pw[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int v = 8 * w + 2 * i;
+            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v], c2, bias));
+            const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v + 1], c2, bias));
+            ps[i & 1] += p0;
+            ps[i & 1] += p1;
+            const uint32_t code = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, p0 * r, p1 * r, 1.0f, 0);
+            const auto dq = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(code, 1.0f, 0);
+            typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+            const v2bf pb = {(__bf16)(dq[0] * s2k), (__bf16)(dq[1] * s2k)};
+            pw[i] = __builtin_bit_cast(uint32_t, pb);
+          }
+          pk[2 * t + w] = v4i{(int)pw[0], (int)pw[1], (int)pw[2], (int)pw[3]};
+        }
+      }
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[db][v] *= gam;
+      lsum_acc = lsum_acc * gam + __builtin_ldexpf(ps[0] + ps[1], kfold);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int u = 0; u < NPK; ++u) {
+          const v4i a = *reinterpret_cast<const v4i*>(L + vo[u] + 32 * db * T::VROW);
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf(a), as_bf(pk[u]), oacc[db], 0, 0, 0);
+        }
+      m = m_new;
+      mc_old = mc;
+      f_old = f;
+    }
+    if (more) stg.store(lds[buf ^ 1], tid);
+    __syncthreads();
+  };
+  for (int j = 0; j < ntiles; j += 2) {
+    tile(ic<0>{}, j);
+    if (j + 1 < ntiles) tile(ic<1>{}, j + 1);
+  }
+
+  const float ltot = lsum_acc + __shfl_xor(lsum_acc, 32, 64);
+  const float inv = 1.0f / ltot;
+  if (qi < N) {
+    uint8_t* ob = reinterpret_cast<uint8_t*>(o);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int d0 = 32 * db + 8 * g + 4 * hi;
+        const size_t idx = ((size_t)bh * N + qi) * D + d0;
+        const float a0 = oacc[db][4 * g] * inv, a1 = oacc[db][4 * g + 1] * inv;
+        const float a2 = oacc[db][4 * g + 2] * inv, a3 = oacc[db][4 * g + 3] * inv;
+        if (OUT == 0) {
+          *reinterpret_cast<float4*>(ob + idx * 4) = make_float4(a0, a1, a2, a3);
+        } else {
+          uint16_t h0, h1, h2, h3;
+          if (OUT == 1) { h0 = f32_to_bf16_rne(a0); h1 = f32_to_bf16_rne(a1); h2 = f32_to_bf16_rne(a2); h3 = f32_to_bf16_rne(a3); }
+          else { h0 = f32_to_fp16_rne(a0); h1 = f32_to_fp16_rne(a1); h2 = f32_to_fp16_rne(a2); h3 = f32_to_fp16_rne(a3); }
+          *reinterpret_cast<uint2*>(ob + idx * 2) = make_uint2((uint32_t)h0 | ((uint32_t)h1 << 16), (uint32_t)h2 | ((uint32_t)h3 << 16));
+        }
+      }
+  }
+}
+
+template <int D, int BKV, bool CAUSAL, int OUT>
+static hipError_t launch_nv16_t(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
+                                const void* vs, void* o, int BH, int N, int Np, float c2, float logR, hipStream_t st) {
+  const int nqt = (N + NQ - 1) / NQ;
+  hipLaunchKernelGGL((attn_nv16_kernel<D, BKV, CAUSAL, OUT>), dim3((unsigned)(nqt * BH)), dim3(256), 0, st,
+                     (const uint8_t*)qc, (const uint8_t*)qs, (const uint8_t*)kc, (const uint8_t*)ks, (const uint8_t*)vc,
+                     (const uint8_t*)vs, o, BH, N, Np, nqt, c2, logR);
+  return hipGetLastError();
+}
+
+template <int D, int BKV, bool CAUSAL>
+static hipError_t launch_nv16_o(int out, const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
+                                const void* vs, void* o, int BH, int N, int Np, float c2, float logR, hipStream_t st) {
+  if (out == 0) return launch_nv16_t<D, BKV, CAUSAL, 0>(qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, logR, st);
+  if (out == 1) return launch_nv16_t<D, BKV, CAUSAL, 1>(qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, logR, st);
+  return launch_nv16_t<D, BKV, CAUSAL, 2>(qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, logR, st);
+}
+
+hipError_t launch_attn_nv16(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
+                            const void* vs, void* o, int BH, int N, int Np, int D, int bkv, bool causal, int out,
+                            float c2, float logR, hipStream_t st) {
+#define SAGE_N(DD, BB)                                                                                 \
+  return causal ? launch_nv16_o<DD, BB, true>(out, qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, logR, st) \
+                : launch_nv16_o<DD, BB, false>(out, qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, logR, st)
+  if (D == 128) { if (bkv == 128) { SAGE_N(128, 128); } else { SAGE_N(128, 64); } }
+  else { if (bkv == 128) { SAGE_N(64, 128); } else { SAGE_N(64, 64); } }
+#undef SAGE_N
+}
+
+}  // namespace sage

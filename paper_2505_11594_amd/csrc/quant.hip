@@ -74,11 +74,21 @@ __global__ void kmean_final_kernel(const double* __restrict__ part, float* __res
 // codes as one 32-bit word.  Role K subtracts mu and stores each token at
 // its permuted position inside its 64-token group.
 // ---------------------------------------------------------------------------
+// Stored row of K token t.  MXFP4 (32x32x64 block-scaled MFMA): inside each
+// 64-token group, offset o = 32h + 16t' + 4g + r goes to 32t' + 8g + 4h + r.
+// NV16 (32x32x16 bf16 MFMA after dequantization): inside each 32-token group,
+// o = 16h + 4g + r goes to 8g + 4h + r.
+template <int FMT>
 __device__ __forceinline__ int k_stored_pos(int t) {
-  // offset o = 32h + 16t' + 4g + r  ->  position 32t' + 8g + 4h + r
-  const int o = t & 63;
-  const int h = o >> 5, tt = (o >> 4) & 1, g = (o >> 2) & 3, r = o & 3;
-  return (t & ~63) | (tt << 5) | (g << 3) | (h << 2) | r;
+  if constexpr (FMT == kFmtMX) {
+    const int o = t & 63;
+    const int h = o >> 5, tt = (o >> 4) & 1, g = (o >> 2) & 3, r = o & 3;
+    return (t & ~63) | (tt << 5) | (g << 3) | (h << 2) | r;
+  } else {
+    const int o = t & 31;
+    const int h = o >> 4, g = (o >> 2) & 3, r = o & 3;
+    return (t & ~31) | (g << 3) | (h << 2) | r;
+  }
 }
 
 template <int D, bool BF16, int FMT, bool IS_K>
@@ -131,7 +141,7 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(const uint16_t* __restr
     uint32_t word = 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i) word |= cvt_fp4x2(y[2 * i], y[2 * i + 1]) << (8 * i);
-    const long long orow = bh * Nout + (IS_K ? k_stored_pos(t) : t);
+    const long long orow = bh * Nout + (IS_K ? k_stored_pos<FMT>(t) : t);
     *reinterpret_cast<uint32_t*>(codes + (size_t)orow * (D / 2) + cu * 4) = word;
     if ((cu % LPB) == 0) scales[(size_t)orow * (D / NB) + cu / LPB] = (uint8_t)sbyte;
   }
@@ -145,7 +155,7 @@ __global__ void k_tail_kernel(uint8_t* __restrict__ codes, uint8_t* __restrict__
   const int ntail = Np - N;
   for (int i = threadIdx.x + blockIdx.x * blockDim.x; i < ntail * (D / 2); i += gridDim.x * blockDim.x) {
     const int t = N + i / (D / 2), b = i % (D / 2);
-    const long long orow = (long long)bh * Np + k_stored_pos(t);
+    const long long orow = (long long)bh * Np + k_stored_pos<FMT>(t);
     codes[(size_t)orow * (D / 2) + b] = 0;
     if (b < D / NB) scales[(size_t)orow * (D / NB) + b] = (FMT == kFmtMX) ? 127 : 0;
   }

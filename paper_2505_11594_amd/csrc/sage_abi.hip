@@ -17,6 +17,9 @@ hipError_t launch_quant_v(const void* v, void* codes, void* scales, int BH, int 
 hipError_t launch_attn_fp4_mx(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
                               const void* vs, void* o, int BH, int N, int Np, int D, int bkv, bool causal, int out,
                               float c2, float log6, hipStream_t st);
+hipError_t launch_attn_nv16(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
+                            const void* vs, void* o, int BH, int N, int Np, int D, int bkv, bool causal, int out,
+                            float c2, float logR, hipStream_t st);
 hipError_t launch_attn_bf16(const void* q, const void* k, const void* vt, void* o, int BH, int N, int Np, int D,
                             bool causal, bool out_f32, float c2, hipStream_t st);
 hipError_t launch_transpose_v_bf16(const void* v, void* vt, int BH, int N, int Np, int D, hipStream_t st);
@@ -116,12 +119,15 @@ int attn_args(const void* q, const void* k, const void* v, const void* o, int B,
 
 inline float softmax_c2(int D) { return (float)(1.0 / (std::log(2.0) * std::sqrt((double)D))); }
 inline float log2_of_6() { return (float)std::log2(6.0); }
+inline float log2_of_2688() { return (float)std::log2(448.0 * 6.0); }
 inline int out_kind(unsigned fmt) { return (fmt & SAGE_OUT_F32) ? 0 : ((fmt & SAGE_IN_BF16) ? 1 : 2); }
 
 int attn_prequant_impl(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc, const void* vs,
                        void* o, int B, int H, int N, int D, int causal, unsigned fmt, hipStream_t st) {
-  if (fmt_of(fmt) != SAGE_FMT_MXFP4) return SAGE_ERR_UNSUPPORTED;
   const int bkv = (fmt & SAGE_BKV64) ? 64 : 128;
+  if (fmt_of(fmt) == SAGE_FMT_NV16_E4M3)
+    return hip_status(sage::launch_attn_nv16(qc, qs, kc, ks, vc, vs, o, B * H, N, pad128(N), D, bkv, causal != 0,
+                                             out_kind(fmt), softmax_c2(D), log2_of_2688(), st));
   return hip_status(sage::launch_attn_fp4_mx(qc, qs, kc, ks, vc, vs, o, B * H, N, pad128(N), D, bkv, causal != 0,
                                              out_kind(fmt), softmax_c2(D), log2_of_6(), st));
 }
@@ -184,7 +190,6 @@ int sage_attn_fp4_fwd_ws(const void* q, const void* k, const void* v, void* o, i
                          unsigned fmt, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   int rc = attn_args(q, k, v, o, B, H, N, D, causal, fmt);
   if (rc != SAGE_OK) return rc;
-  if (fmt_of(fmt) != SAGE_FMT_MXFP4) return SAGE_ERR_UNSUPPORTED;
   if (!workspace || !aligned(workspace, 256)) return SAGE_ERR_INVALID_ARG;
   if (workspace_bytes < attn_ws_layout(B, H, N, D, fmt).total) return SAGE_ERR_WORKSPACE;
   return attn_ws_impl(q, k, v, o, B, H, N, D, causal, fmt, workspace, stream);
@@ -194,7 +199,6 @@ int sage_attn_fp4_fwd(const void* q, const void* k, const void* v, void* o, int 
                       unsigned fmt, hipStream_t stream) {
   int rc = attn_args(q, k, v, o, B, H, N, D, causal, fmt);
   if (rc != SAGE_OK) return rc;
-  if (fmt_of(fmt) != SAGE_FMT_MXFP4) return SAGE_ERR_UNSUPPORTED;
   const size_t bytes = attn_ws_layout(B, H, N, D, fmt).total;
   void* ws = nullptr;
   if (hipMallocAsync(&ws, bytes, stream) != hipSuccess) return SAGE_ERR_HIP;

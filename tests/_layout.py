@@ -21,12 +21,18 @@ def unpack_nibbles(b):
     return out
 
 
-def k_stored_position(t):
-    """Stored row of token t (within its 64-token group: o = 32h + 16t' + 4g + r -> 32t' + 8g + 4h + r)."""
+def k_stored_position(t, fmt=0):
+    """Stored row of token t: MXFP4 permutes inside 64-token groups
+    (o = 32h + 16t' + 4g + r -> 32t' + 8g + 4h + r), NV16 inside 32-token groups
+    (o = 16h + 4g + r -> 8g + 4h + r)."""
     t = np.asarray(t)
-    o = t & 63
-    h, tt, g, r = o >> 5, (o >> 4) & 1, (o >> 2) & 3, o & 3
-    return (t & ~63) | (tt << 5) | (g << 3) | (h << 2) | r
+    if fmt == 0:
+        o = t & 63
+        h, tt, g, r = o >> 5, (o >> 4) & 1, (o >> 2) & 3, o & 3
+        return (t & ~63) | (tt << 5) | (g << 3) | (h << 2) | r
+    o = t & 31
+    h, g, r = o >> 4, (o >> 2) & 3, o & 3
+    return (t & ~31) | (g << 3) | (h << 2) | r
 
 
 def block_size(fmt):
@@ -46,7 +52,7 @@ def k_logical(codes, scales, B, H, N, D, fmt):
     Np = pad128(N)
     c = unpack_nibbles(np.asarray(codes).reshape(B, H, Np, D // 2))
     s = np.asarray(scales).reshape(B, H, Np, D // n)
-    pos = k_stored_position(np.arange(Np))
+    pos = k_stored_position(np.arange(Np), fmt)
     return c[:, :, pos[:N]], s[:, :, pos[:N]], c[:, :, pos[N:]], s[:, :, pos[N:]]
 
 

@@ -47,16 +47,17 @@ def check(got, ref, tie_tol, label, extra=None):
         label, int(bad.sum()), float(err[bad].max()), int(np.flatnonzero(bad)[0]))
 
 
+@pytest.mark.parametrize("fmt", [0, 1])
 @pytest.mark.parametrize("N", [1, 64, 100, 257, 640])
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("bkv", [64, 128])
-def test_attn_edge_shapes(N, D, causal, bkv):
-    say("attn edge N=%d D=%d causal=%d bkv=%d" % (N, D, causal, bkv))
+def test_attn_edge_shapes(fmt, N, D, causal, bkv):
+    say("attn edge fmt=%d N=%d D=%d causal=%d bkv=%d" % (fmt, N, D, causal, bkv))
     in_dtype = 1 if (N + D) % 2 else 0
     q, k, v = wl.make_inputs(1, 2, N, D, in_dtype, seed=200 + N, k_bias_var=4.0, outlier_frac=0.02)
-    o = gpu_attn(q, k, v, in_dtype, causal, 0, bkv)
-    ref, tie, _ = oracle.attn(q, k, v, in_dtype, causal, oracle.FMT_MX, bkv)
+    o = gpu_attn(q, k, v, in_dtype, causal, fmt, bkv)
+    ref, tie, _ = oracle.attn(q, k, v, in_dtype, causal, fmt, bkv)
     check(o.cpu().numpy().reshape(-1, D), ref, tie, "edge")
 
 
@@ -70,41 +71,41 @@ def test_attn_config0_all_rows():
     say("accuracy vs exact", oracle.metrics(ex, o.cpu().numpy().reshape(-1, w.D)))
 
 
-@pytest.mark.parametrize("ci", [1, 2, 3, 4])
-def test_attn_configs_full_size_sampled_rows(ci):
+@pytest.mark.parametrize("ci,fmt", [(1, 0), (2, 0), (3, 0), (4, 1), (4, 0)])
+def test_attn_configs_full_size_sampled_rows(ci, fmt):
     """The benchmark's launch configuration at full size; the oracle computes a
     seeded sample of rows (first/last/random query tiles of sampled heads)."""
     w = wl.CONFIGS[ci]
-    if wl.FMT_MX not in w.fmts:
-        pytest.skip("no MXFP4 run for this configuration")
-    say("attn config", ci, w.name)
+    assert fmt in w.fmts
+    say("attn config", ci, w.name, "fmt", fmt)
     q, k, v = wl.generate(w)
-    o = gpu_attn(q, k, v, w.in_dtype, w.causal, 0, w.bkv)
+    o = gpu_attn(q, k, v, w.in_dtype, w.causal, fmt, w.bkv)
     BH = w.B * w.H
     heads = sorted({0, BH - 1} | set(np.random.default_rng(ci).choice(BH, min(BH, 6), replace=False).tolist()))
     rows = wl.sample_rows(w, per_head_tiles=4, tile=128, rows_per_tile=8, heads=heads, seed=ci)
-    ref, tie, cnt = oracle.attn(q, k, v, w.in_dtype, w.causal, oracle.FMT_MX, w.bkv, rows=rows)
+    ref, tie, cnt = oracle.attn(q, k, v, w.in_dtype, w.causal, fmt, w.bkv, rows=rows)
     got = o_rows(o, rows, w.D)
     check(got, ref, tie, w.name)
     ex = oracle.exact_attn(q, k, v, w.in_dtype, w.causal, rows=rows)
     say("accuracy vs exact (sampled rows)", oracle.metrics(ex, got), cnt)
 
 
-def test_attn_deterministic_and_entry_points_agree():
+@pytest.mark.parametrize("fmt", [0, 1])
+def test_attn_deterministic_and_entry_points_agree(fmt):
     torch = torch_dev()
     w = wl.CONFIGS[1]
     q, k, v = wl.generate(w, B=1, H=4, N=2048)
-    a = gpu_attn(q, k, v, w.in_dtype, False, 0, 128)
-    b = gpu_attn(q, k, v, w.in_dtype, False, 0, 128)
+    a = gpu_attn(q, k, v, w.in_dtype, False, fmt, 128)
+    b = gpu_attn(q, k, v, w.in_dtype, False, fmt, 128)
     assert torch.equal(a, b)
     qd, kd, vd = (to_dev(x, w.in_dtype) for x in (q, k, v))
-    ws = torch.empty(bd.attn_fp4_workspace_size(1, 4, 2048, 128, bd.SAGE_IN_BF16 | bd.SAGE_OUT_F32),
+    ws = torch.empty(bd.attn_fp4_workspace_size(1, 4, 2048, 128, fmt | bd.SAGE_IN_BF16 | bd.SAGE_OUT_F32),
                      dtype=torch.uint8, device="cuda")
-    c = bd.sage_attn_fp4_fwd(qd, kd, vd, causal=False, workspace=ws)
-    qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q)
-    kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K)
-    vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V)
-    e = bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (1, 4, 2048, 128))
+    c = bd.sage_attn_fp4_fwd(qd, kd, vd, causal=False, fmt=fmt, workspace=ws)
+    qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q, fmt)
+    kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K, fmt)
+    vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V, fmt)
+    e = bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (1, 4, 2048, 128), fmt=fmt)
     torch.cuda.synchronize()
     assert torch.equal(a, c) and torch.equal(a, e)
 
