@@ -144,8 +144,9 @@ int sage_attn_fp4_fwd_prequant(const void* q_codes, const void* q_scales,
  * S = Q K^T in fp32, online softmax in fp32, P rounded to bf16, O += P V
  * (FlashAttention forward, Sec. 2).  q, k, v must be bf16 (flags must
  * contain SAGE_IN_BF16); o is fp32 with SAGE_OUT_F32, else bf16.  Only
- * SAGE_IN_BF16, SAGE_OUT_F32 and SAGE_BKV64 are accepted in flags.  The V
- * transpose goes to a hipMallocAsync workspace on `stream`.
+ * SAGE_IN_BF16 and SAGE_OUT_F32 are accepted in flags (the kernel uses
+ * 64-key tiles).  The V transpose goes to a hipMallocAsync workspace on
+ * `stream`.
  */
 int sage_attn_bf16_fwd(const void* q, const void* k, const void* v, void* o,
                        int B, int H, int N, int D, int causal, unsigned flags, hipStream_t stream);

@@ -23,91 +23,47 @@
 // an integer part k_j (folded exactly into P's E8M0 scale) and a fraction
 // f_j.  Each tile then rescales the accumulator once by
 // gamma_j = 2^{c2 (m_{j-1} - m_j) + f_{j-1} - f_j}.
+//
+// Data movement: KV tiles go from HBM straight into LDS with global loads
+// that write LDS (no staging registers).  LDS holds each tile in MFMA-operand
+// order -- one 1 KiB block per 64-lane operand read, lane l's 16 bytes at
+// 16 l -- so operand reads are linear and bank-conflict free.  Three LDS
+// stages and one barrier per tile: after the barrier of tile j every wave
+// has finished tile j-1, the loads of tile j+2 go to that stage, and the
+// S^T products of tile j+1 are issued between the row max of tile j and its
+// exponentials, so the MFMAs run under tile j's softmax.
 #include "sage_common.h"
 
 namespace sage {
 
 constexpr int AQ = 128;   // queries per workgroup (4 waves x 32)
 
-// 16-byte-chunk XOR swizzle of LDS rows (64 or 32 bytes long).  An MFMA
-// operand read has consecutive lanes on consecutive rows at one chunk; rows
-// r and r + 4k must land in different chunks for 64 banks (16 lanes per pass)
-// and rows r and r + 2k for 32 banks (8 lanes per pass).
-template <int NCH>
-__device__ __forceinline__ int swz(int row, int ch) { return ch ^ (((row >> 1) ^ (row >> 3)) & (NCH - 1)); }
+// HBM -> LDS loads (global_load_lds): lane l's bytes land at dst + l * size.
+__device__ __forceinline__ void lds_load16(const void* src, void* dst) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+}
+__device__ __forceinline__ void lds_load4(const void* src, void* dst) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 4, 0, 0);
+}
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
 
+// One LDS stage of a KV tile, in MFMA-operand order.
 template <int D, int BKV>
-struct Fp4Tile {
-  static constexpr int KROW = D / 2;          // bytes of one K^ row
-  static constexpr int KCH = D / 32;          // 16-byte chunks per K^ row
-  static constexpr int VROW = BKV / 2;        // bytes of one V^T row inside a tile
-  static constexpr int VCH = BKV / 32;        // 16-byte chunks per V^T tile row
+struct Fp4Stage {
+  static constexpr int NSUB = BKV / 32;        // 32-key subtiles (S^T rows)
+  static constexpr int NKS = D / 64;           // K-steps of S^T = K^ Q^T
+  static constexpr int NDB = D / 32;           // 32-dim blocks (O^T rows)
+  static constexpr int NG = BKV / 64;          // K-steps of O^T += V^T P^T
+  static constexpr int NKB = NSUB * NKS;       // K^ operand blocks, 1 KiB each
+  static constexpr int NVB = NDB * NG;         // V^T operand blocks, 1 KiB each
   static constexpr int KC_OFF = 0;
-  static constexpr int KS_OFF = KC_OFF + BKV * KROW;
-  static constexpr int VC_OFF = KS_OFF + BKV * 8;   // K scales: 2 dwords per key
-  static constexpr int VS_OFF = VC_OFF + D * VROW;
-  static constexpr int BYTES = VS_OFF + D * 8;      // V scales: 2 dwords per row
-  static constexpr int KC_UNITS = BKV * KCH;  // 16-byte units
-  static constexpr int VC_UNITS = D * VCH;
-  static constexpr int KC_PER_T = (KC_UNITS + 255) / 256;
-  static constexpr int VC_PER_T = (VC_UNITS + 255) / 256;
-};
-
-// Register staging of one KV tile: every thread issues the same fixed set of
-// 16-byte global loads (no divergent branches, so the loads stay in flight
-// while the current tile is computed) and later writes them to LDS.
-template <int D, int BKV>
-struct Stage {
-  using T = Fp4Tile<D, BKV>;
-  v4i kc[T::KC_PER_T];
-  v4i vc[T::VC_PER_T];
-  uint32_t ks, vs;
-
-  __device__ __forceinline__ void load(const uint8_t* __restrict__ kcg, const uint8_t* __restrict__ ksg,
-                                       const uint8_t* __restrict__ vcg, const uint8_t* __restrict__ vsg, long long bh,
-                                       int Np, int kb, int tid) {
-    const uint8_t* kbase = kcg + ((size_t)bh * Np + kb) * T::KROW;
-#pragma unroll
-    for (int i = 0; i < T::KC_PER_T; ++i) {
-      const int u = (tid + 256 * i) % T::KC_UNITS;        // units beyond the tile repeat a valid one
-      kc[i] = reinterpret_cast<const v4i*>(kbase)[u];
-    }
-#pragma unroll
-    for (int i = 0; i < T::VC_PER_T; ++i) {
-      const int u = (tid + 256 * i) % T::VC_UNITS;
-      const int d = u / T::VCH, ch = u % T::VCH;
-      vc[i] = *reinterpret_cast<const v4i*>(vcg + ((size_t)bh * D + d) * (Np / 2) + kb / 2 + ch * 16);
-    }
-    const int key = tid % BKV;
-    const uint8_t* pk = ksg + ((size_t)bh * Np + kb + key) * (D / 32);
-    ks = (D == 128) ? *reinterpret_cast<const uint32_t*>(pk) : (uint32_t)*reinterpret_cast<const uint16_t*>(pk);
-    const int d = tid % D;
-    const uint8_t* pv = vsg + ((size_t)bh * D + d) * (Np / 32) + kb / 32;
-    vs = (BKV == 128) ? *reinterpret_cast<const uint32_t*>(pv) : (uint32_t)*reinterpret_cast<const uint16_t*>(pv);
-  }
-
-  __device__ __forceinline__ void store(uint8_t* lds, int tid) const {
-#pragma unroll
-    for (int i = 0; i < T::KC_PER_T; ++i) {
-      const int u = (tid + 256 * i) % T::KC_UNITS;
-      const int row = u / T::KCH, ch = u % T::KCH;
-      *reinterpret_cast<v4i*>(lds + T::KC_OFF + row * T::KROW + swz<T::KCH>(row, ch) * 16) = kc[i];
-    }
-#pragma unroll
-    for (int i = 0; i < T::VC_PER_T; ++i) {
-      const int u = (tid + 256 * i) % T::VC_UNITS;
-      const int row = u / T::VCH, ch = u % T::VCH;
-      *reinterpret_cast<v4i*>(lds + T::VC_OFF + row * T::VROW + swz<T::VCH>(row, ch) * 16) = vc[i];
-    }
-    // Scale bytes of a row are split by lane half: the half-hi lanes of an
-    // MFMA need bytes hi, hi+2 (blocks 2s + hi), so slot hi holds them as
-    // bytes 0 and 1 and the MFMA op_sel picks byte s directly.  Duplicate
-    // writers store identical values.
-    const uint32_t k0 = (ks & 0xFFu) | ((ks >> 8) & 0xFF00u), k1 = ((ks >> 8) & 0xFFu) | ((ks >> 16) & 0xFF00u);
-    const uint32_t v0 = (vs & 0xFFu) | ((vs >> 8) & 0xFF00u), v1 = ((vs >> 8) & 0xFFu) | ((vs >> 16) & 0xFF00u);
-    *reinterpret_cast<uint2*>(lds + T::KS_OFF + (tid % BKV) * 8) = make_uint2(k0, k1);
-    *reinterpret_cast<uint2*>(lds + T::VS_OFF + (tid % D) * 8) = make_uint2(v0, v1);
-  }
+  static constexpr int VC_OFF = KC_OFF + NKB * 1024;
+  static constexpr int KS_OFF = VC_OFF + NVB * 1024;   // K^ scales: BKV rows x D/32 bytes, as in HBM
+  static constexpr int KS_BYTES = BKV * (D / 32);
+  static constexpr int VS_OFF = KS_OFF + KS_BYTES;      // V^T scales: one dword per dim row
+  static constexpr int BYTES = VS_OFF + D * 4;
+  static constexpr int NKSJ = (KS_BYTES / 4 + 63) / 64;   // dword loads of K^ scales (64 lanes each)
+  static constexpr int NVSJ = D / 64;                     // dword loads of V^T scales
 };
 
 __device__ __forceinline__ v8i as_op(const v4i x) { return v8i{x[0], x[1], x[2], x[3], 0, 0, 0, 0}; }
@@ -117,14 +73,12 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
     const uint8_t* __restrict__ qc, const uint8_t* __restrict__ qs, const uint8_t* __restrict__ kc,
     const uint8_t* __restrict__ ks, const uint8_t* __restrict__ vc, const uint8_t* __restrict__ vs,
     void* __restrict__ o, int BH, int N, int Np, int nqt, float c2, float log6) {
-  using T = Fp4Tile<D, BKV>;
-  constexpr int NSUB = BKV / 32;   // 32-key subtiles of S^T
-  constexpr int NG = BKV / 64;     // 64-key groups = PV K-steps
-  constexpr int NKS = D / 64;      // QK K-steps
-  constexpr int NDB = D / 32;      // 32-row blocks of O^T
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2][T::BYTES];
+  using T = Fp4Stage<D, BKV>;
+  constexpr int NSUB = T::NSUB, NKS = T::NKS, NDB = T::NDB, NG = T::NG;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[3][T::BYTES];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar branches
   const int col = lane & 31, hi = lane >> 5;
 
   // XCD-aware order: consecutive workgroups go round-robin over the 8 XCDs,
@@ -153,7 +107,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
 #pragma unroll
     for (int s = 0; s < NKS; ++s) qreg[s] = v4i{0, 0, 0, 0};
   }
-  qsc >>= 8 * hi;
+  qsc >>= 8 * hi;   // byte 2s = scale of block 2s + hi
 
   int ntiles = (N + BKV - 1) / BKV;
   if (CAUSAL) {
@@ -161,66 +115,120 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
     ntiles = min(ntiles, qlast / BKV + 1);
   }
 
+  // ---- tile loads: HBM -> LDS without registers ---------------------------
+  // Wave w loads K^ operand blocks w, w + 4, ... (block b = (t, s) = (b / NKS,
+  // b % NKS): key row 32t + col, bytes [32s + 16hi, +16)), V^T operand blocks
+  // w, w + 4, ... (b = (db, g) = (b / NG, b % NG): dim row 32db + col, bytes
+  // [32g + 16hi, +16) of the tile) and scale job w: K^ scale dwords c = w for
+  // w < NKSJ (64 per job), then V^T scale dwords (one per dim row).  Each
+  // load is a wave-uniform tile base plus a fixed 32-bit lane offset.
+  constexpr int KJ = (T::NKB + 3) / 4, VJ = (T::NVB + 3) / 4;
+  static_assert(T::NKSJ + T::NVSJ <= 4, "one scale job per wave");
+  const uint8_t* kbase = kc + (size_t)bh * Np * (D / 2);
+  const uint8_t* vbase = vc + (size_t)bh * D * (Np / 2);
+  const uint8_t* ksbase = ks + (size_t)bh * Np * (D / 32);
+  const uint8_t* vsbase = vs + (size_t)bh * D * (Np / 32);
+  uint32_t ko[KJ], vo[VJ], so;
+#pragma unroll
+  for (int i = 0; i < KJ; ++i) {
+    const int b = wave + 4 * i, t = b / NKS, s = b % NKS;
+    ko[i] = (32 * t + col) * (D / 2) + 32 * s + 16 * hi;
+  }
+#pragma unroll
+  for (int i = 0; i < VJ; ++i) {
+    const int b = wave + 4 * i, db = b / NG, g = b % NG;
+    vo[i] = (32 * db + col) * (Np / 2) + 32 * g + 16 * hi;
+  }
+  const bool ks_job = wave < T::NKSJ, vs_job = !ks_job && wave < T::NKSJ + T::NVSJ;
+  const bool ks_lane = 64 * (wave + 1) <= T::KS_BYTES / 4 || 64 * wave + lane < T::KS_BYTES / 4;
+  so = ks_job ? (64 * wave + lane) * 4 : (64 * (wave - T::NKSJ) + lane) * (Np / 32);
+  auto issue = [&](int j, int stage) {
+    const int kb = j * BKV;
+    uint8_t* L = lds[stage];
+    const uint8_t* kt = kbase + (size_t)kb * (D / 2);
+    const uint8_t* vt = vbase + kb / 2;
+#pragma unroll
+    for (int i = 0; i < KJ; ++i)
+      if (T::NKB % 4 == 0 || wave + 4 * i < T::NKB)
+        lds_load16(kt + ko[i], L + T::KC_OFF + (wave + 4 * i) * 1024);
+#pragma unroll
+    for (int i = 0; i < VJ; ++i)
+      if (T::NVB % 4 == 0 || wave + 4 * i < T::NVB)
+        lds_load16(vt + vo[i], L + T::VC_OFF + (wave + 4 * i) * 1024);
+    if (ks_job) {
+      if (ks_lane)
+        lds_load4(ksbase + (size_t)kb * (D / 32) + so, L + T::KS_OFF + wave * 256);
+    } else if (vs_job) {
+      // the aligned dword holding the tile's BKV/32 scale bytes of dim row 64c + lane
+      lds_load4(vsbase + ((kb / 32) & ~3) + so, L + T::VS_OFF + (wave - T::NKSJ) * 256);
+    }
+  };
+
   v16f oacc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) oacc[db] = v16f{};
   float m = -INFINITY, mc_old = -INFINITY, f_old = 0.0f, lsum_acc = 0.0f;
 
-  // Per-lane LDS byte offsets, the same for every tile: A-operand chunk
-  // (2s + hi) of row col (the swizzle depends on row bits 1..4 only, which
-  // the 32-row subtile offset leaves unchanged).
-  int koff[NKS], voff[NG];
+  // S^T = K^ . Q^T for one tile (LDS stage base L)
+  auto qk = [&](const uint8_t* L, v16f (&sacc)[NSUB]) {
 #pragma unroll
-  for (int s = 0; s < NKS; ++s) koff[s] = T::KC_OFF + col * T::KROW + swz<T::KCH>(col, 2 * s + hi) * 16;
-#pragma unroll
-  for (int g = 0; g < NG; ++g) voff[g] = T::VC_OFF + col * T::VROW + swz<T::VCH>(col, 2 * g + hi) * 16;
-  const int ksoff = T::KS_OFF + col * 8 + hi * 4, vsoff = T::VS_OFF + col * 8 + hi * 4;
+    for (int t = 0; t < NSUB; ++t) {
+      uint32_t ksc;
+      if constexpr (D == 128) ksc = *reinterpret_cast<const uint32_t*>(L + T::KS_OFF + (32 * t + col) * 4) >> (8 * hi);
+      else ksc = L[T::KS_OFF + (32 * t + col) * 2 + hi];
+      v16f acc = v16f{};
+      static_for<NKS>([&](auto S_) {
+        constexpr int s = decltype(S_)::value;
+        const v4i a = *reinterpret_cast<const v4i*>(L + T::KC_OFF + (t * NKS + s) * 1024 + lane * 16);
+        acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(qreg[s]), acc, 4, 4, 2 * s, (int)ksc,
+                                                              2 * s, (int)qsc);
+      });
+      sacc[t] = acc;
+    }
+  };
 
-  Stage<D, BKV> stg;
-  stg.load(kc, ks, vc, vs, bh, Np, 0, tid);
-  stg.store(lds[0], tid);
+  issue(0, 0);
+  if (ntiles > 1) issue(1, 1);
+  wait_loads();
   __syncthreads();
+  v16f sbuf[2][NSUB];
+  if (!CAUSAL || 0 <= qw + 31) qk(lds[0], sbuf[0]);
 
-  auto tile = [&](auto BUF_, int j) {
-    constexpr int buf = decltype(BUF_)::value;
-    const uint8_t* L = lds[buf];
+  auto tile = [&](auto P_, int j, int stage) {
+    constexpr int P = decltype(P_)::value;     // sbuf[P] holds this tile's S^T, sbuf[P ^ 1] gets the next
+    v16f (&sacc)[NSUB] = sbuf[P];
+    const uint8_t* L = lds[stage];
     const int kb = j * BKV;
-    const bool more = j + 1 < ntiles;
-    if (more) stg.load(kc, ks, vc, vs, bh, Np, kb + BKV, tid);
-
     const bool active = !CAUSAL || kb <= qw + 31;
+    float t = 0.f, m_new = 0.f, mc = 0.f, f = 0.f, gam = 1.f, bias = 0.f;
+    int kfold = 0;
+    float bm[NG];
+    float ps[4] = {0.0f, 0.0f, 0.0f, 0.0f};   // independent partial row sums
+    // V^T scale bytes of the tile for this lane's rows: byte 2g = block 2g + hi
+    const int vshift = 8 * (((kb / 32) & 3) + hi);
+
     if (active) {
-      // ---- S^T = K^ . Q^T ------------------------------------------------
-      v16f sacc[NSUB];
-#pragma unroll
-      for (int t = 0; t < NSUB; ++t) {
-        const uint32_t ksc = *reinterpret_cast<const uint32_t*>(L + ksoff + 32 * t * 8);
-        v16f acc = v16f{};
-        static_for<NKS>([&](auto S_) {
-          constexpr int s = decltype(S_)::value;
-          const v4i a = *reinterpret_cast<const v4i*>(L + koff[s] + 32 * t * T::KROW);
-          acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(qreg[s]), acc, 4, 4, s, (int)ksc,
-                                                                2 * s, (int)qsc);
-        });
-        sacc[t] = acc;
-      }
       // ---- masking (tail keys >= N; causal keys > query) ---------------
       const bool need_mask = (kb + BKV > N) || (CAUSAL && kb + BKV - 1 > qw);
       if (need_mask) {
+        // element (u, v) is key kb + 32 hi + c with c = 64 (u >> 1) + 16 (u & 1) + v;
+        // it is kept iff c < rem.  The sign bit of c - rem turns -inf into the
+        // bound +inf for kept keys, and min(S, bound) applies it -- plain bit
+        // arithmetic, so no per-element lane masks are formed.
+        const int rem = (CAUSAL ? min(N, qi + 1) : N) - kb - 32 * hi;
 #pragma unroll
-        for (int t = 0; t < NSUB; ++t)
+        for (int u = 0; u < NSUB; ++u)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            const int key = kb + 64 * (t >> 1) + 32 * hi + 16 * (t & 1) + v;
-            const bool ok = key < N && (!CAUSAL || key <= qi);
-            if (!ok) sacc[t][v] = -INFINITY;
+            const int c = 64 * (u >> 1) + 16 * (u & 1) + v;
+            const float bound = __uint_as_float(0xFF800000u ^ ((uint32_t)(c - rem) & 0x80000000u));
+            sacc[u][v] = __builtin_fminf(sacc[u][v], bound);
           }
       }
       // ---- tile row max (raw scores); block max is lane-local ----------
-      float bm[NG];
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
-        // a serial chain: the compiler fuses it into v_max3 (a tree costs more)
+        // a serial chain: the compiler fuses it into v_max3
         float x = sacc[2 * g][0];
 #pragma unroll
         for (int v = 1; v < 16; ++v) x = __builtin_fmaxf(x, sacc[2 * g][v]);
@@ -233,77 +241,84 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
       for (int g = 1; g < NG; ++g) tl = __builtin_fmaxf(tl, bm[g]);
       // row max over the two lane halves that share a query
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(tl), __float_as_uint(tl), false, false);
-      const float t = __builtin_fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-      const float m_new = __builtin_fmaxf(m, t);
+      t = __builtin_fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+      m_new = __builtin_fmaxf(m, t);
       const float tc = t * c2;
-      const float mc = m_new * c2;
+      mc = m_new * c2;
       const float delta = tc - mc;                       // c2 (t - m_new) <= 0
       const float kf = __builtin_floorf(delta);
-      const float f = delta - kf;                        // in [0, 1)
-      const float gam = __builtin_amdgcn_exp2f((mc_old - mc) + (f_old - f));
-      const int kfold = (int)__builtin_fmaxf(kf, -300.0f);
-      const float bias = log6 - tc;                      // P~2 = 2^{fma(S, c2, log2 6 - t c2)}
-
-      // ---- P~2, unquantized row sum, FP4 pack with E8M0 block scales ----
-      float ps[4] = {0.0f, 0.0f, 0.0f, 0.0f};            // independent partial row sums
-      v4i pw[NG];
-      int psb[NG];
-#pragma unroll
-      for (int g = 0; g < NG; ++g) {
-        // smallest e with 6 2^e >= blockmax(P~2) = 6 2^{c2 (bm - t)}; a fully
-        // masked block (bm = -inf) takes the floor -126
-        const int e = (int)__builtin_fmaxf(__builtin_ceilf((bm[g] - t) * c2), -126.0f);
-        const float escale = __builtin_ldexpf(1.0f, e);   // the convert divides by it exactly
-        uint32_t w[4];
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const int tt = 2 * g + half;
-#pragma unroll
-          for (int q = 0; q < 2; ++q) {
-            uint32_t word = 0;
-            static_for<4>([&](auto I_) {
-              constexpr int i = decltype(I_)::value;
-              const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[tt][8 * q + 2 * i], c2, bias));
-              const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[tt][8 * q + 2 * i + 1], c2, bias));
-              ps[(2 * half + q) & 3] += p0;
-              ps[(2 * half + q) & 3] += p1;
-              word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, p0, p1, escale, i);
-            });
-            w[2 * half + q] = word;
-          }
-        }
-        pw[g] = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
-        const int sb = e + kfold + 127;
-        psb[g] = sb < 0 ? 0 : sb;
-      }
-      // ---- rescale and O^T += V^T . P^T ------------------------------------
+      f = delta - kf;                                    // in [0, 1)
+      gam = __builtin_amdgcn_exp2f((mc_old - mc) + (f_old - f));
+      kfold = (int)__builtin_fmaxf(kf, -300.0f);
+      bias = log6 - tc;                                  // P~2 = 2^{fma(S, c2, log2 6 - t c2)}
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int v = 0; v < 16; ++v) oacc[db][v] *= gam;
-      const float psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
-      lsum_acc = lsum_acc * gam + __builtin_ldexpf(psum, kfold);
+    }
+
+    // ---- P~2, unquantized row sum, FP4 pack with E8M0 block scales; O^T += V^T . P^T
+    auto group = [&](auto G_) {
+      constexpr int g = decltype(G_)::value;
+      // smallest e with 6 2^e >= blockmax(P~2) = 6 2^{c2 (bm - t)}; a fully
+      // masked block (bm = -inf) takes the floor -126
+      const int e = (int)__builtin_fmaxf(__builtin_ceilf((bm[g] - t) * c2), -126.0f);
+      const float escale = __builtin_ldexpf(1.0f, e);   // the convert divides by it exactly
+      uint32_t w[4];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int tt = 2 * g + half;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          uint32_t word = 0;
+          static_for<4>([&](auto I_) {
+            constexpr int i = decltype(I_)::value;
+            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[tt][8 * q + 2 * i], c2, bias));
+            const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[tt][8 * q + 2 * i + 1], c2, bias));
+            ps[(2 * half + q) & 3] += p0;
+            ps[(2 * half + q) & 3] += p1;
+            word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, p0, p1, escale, i);
+          });
+          w[2 * half + q] = word;
+        }
+      }
+      const v4i pw = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+      const int sb = e + kfold + 127;
+      const int psb = sb < 0 ? 0 : sb;
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const uint32_t vsc = *reinterpret_cast<const uint32_t*>(L + vsoff + 32 * db * 8);
-        static_for<NG>([&](auto G_) {
-          constexpr int g = decltype(G_)::value;
-          const v4i a = *reinterpret_cast<const v4i*>(L + voff[g] + 32 * db * T::VROW);
-          oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(pw[g]), oacc[db], 4, 4, g,
-                                                                     (int)vsc, 0, psb[g]);
-        });
+        const uint32_t vsc = *reinterpret_cast<const uint32_t*>(L + T::VS_OFF + (32 * db + col) * 4) >> vshift;
+        const v4i a = *reinterpret_cast<const v4i*>(L + T::VC_OFF + (db * NG + g) * 1024 + lane * 16);
+        oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(pw), oacc[db], 4, 4, 2 * g,
+                                                                   (int)vsc, 0, psb);
       }
+    };
+
+    if (j + 1 < ntiles) {
+      wait_loads();                         // this wave's loads of tile j+1 have landed
+      __syncthreads();                      // everyone's have; every wave is past tile j-1
+      const int nstage = stage == 2 ? 0 : stage + 1;
+      if (j + 2 < ntiles) issue(j + 2, nstage == 2 ? 0 : nstage + 1);
+      if (!CAUSAL || kb + BKV <= qw + 31) qk(lds[nstage], sbuf[P ^ 1]);
+    }
+    if (active) {
+      static_for<NG>(group);
+      const float psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
+      lsum_acc = lsum_acc * gam + __builtin_ldexpf(psum, kfold);
       m = m_new;
       mc_old = mc;
       f_old = f;
     }
-    if (more) stg.store(lds[buf ^ 1], tid);
-    __syncthreads();
   };
 
+  int stage = 0;
   for (int j = 0; j < ntiles; j += 2) {
-    tile(ic<0>{}, j);
-    if (j + 1 < ntiles) tile(ic<1>{}, j + 1);
+    tile(ic<0>{}, j, stage);
+    stage = stage == 2 ? 0 : stage + 1;
+    if (j + 1 < ntiles) {
+      tile(ic<1>{}, j + 1, stage);
+      stage = stage == 2 ? 0 : stage + 1;
+    }
   }
 
   // ---- epilogue: O = O^T / l, stored row-major ----------------------------
