@@ -84,6 +84,93 @@ def cpu_baseline(w, q, k, v, budget_s: float = 15.0):
                       % (nrows, w.B * w.H, N, dt)}
 
 
+RATE_TESTS = [  # (name, what one loop iteration issues, instructions of the counted kind per iteration)
+    ("fma", "32 v_fma_f32", 32), ("exp", "8 v_exp_f32", 8), ("cvt_fp4", "8 v_cvt_scalef32_pk_fp4_f32", 8),
+    ("mfma_fp4", "4 v_mfma_scale_f32_32x32x64_f8f6f4 (FP4)", 4), ("mfma_fp4+fma", "4 FP4 MFMA + 32 v_fma_f32", 4),
+    ("mfma_fp4+exp", "4 FP4 MFMA + 8 v_exp_f32", 4), ("mfma_bf16", "4 v_mfma_f32_32x32x16_bf16", 4),
+    ("mfma_bf16+fma", "4 bf16 MFMA + 32 v_fma_f32", 4), ("mfma16_fp4", "8 v_mfma_scale_f32_16x16x128_f8f6f4 (FP4)", 8),
+    ("mfma16_fp4+fma", "8 FP4 16x16x128 MFMA + 32 v_fma_f32", 8),
+    ("split", "even SIMD slots: 4 FP4 MFMA; odd slots: 32 v_fma_f32", None)]
+
+
+def issue_rates(torch):
+    """Cycles per wave64 instruction per SIMD (at the 2.4 GHz peak clock) of the
+    instructions the FP4 attention kernel is made of, and how much VALU work
+    hides under FP4 MFMAs.  Prints one JSON line."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2505_11594_amd", "libsage_rates.so"))
+    lib.sage_rates_run.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                   ctypes.POINTER(ctypes.c_float)]
+    iters = lib.sage_rates_iterations()
+    out = torch.empty(1024 * 8 * 64, dtype=torch.float32, device="cuda:0")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    res = {}
+    for w in (2, 4):
+        for t, (name, what, _) in enumerate(RATE_TESTS):
+            ms = ctypes.c_float()
+            rc = lib.sage_rates_run(t, w, ctypes.c_void_p(out.data_ptr()), stream, ctypes.byref(ms))
+            if rc != 0:
+                raise RuntimeError("sage_rates_run(%d) failed: %d" % (t, rc))
+            cyc = ms.value * 1e-3 * 2.4e9 / (iters * w)     # cycles per loop iteration per SIMD
+            res["%s@%d" % (name, w)] = cyc
+            log("waves/SIMD %d  %-16s %-52s %8.1f cycles/iteration" % (w, name, what, cyc))
+    summary = {}
+    for w in (2, 4):
+        g = lambda k: res["%s@%d" % (k, w)]
+        summary["w%d" % w] = {
+            "fma_cycles": g("fma") / 32, "exp_cycles": g("exp") / 8, "cvt_fp4_cycles": g("cvt_fp4") / 8,
+            "mfma_fp4_32x32x64_cycles": g("mfma_fp4") / 4, "mfma_bf16_32x32x16_cycles": g("mfma_bf16") / 4,
+            "mfma_fp4_16x16x128_cycles": g("mfma16_fp4") / 8,
+            "fp4_mfma_tflops": 4 * 2 * 32 * 32 * 64 * 1024 * 2.4e9 / g("mfma_fp4") / 1e12,
+            # fraction of the VALU loop's time that disappears when it shares the wave with the MFMAs
+            "fma_hidden_under_fp4_mfma": (g("mfma_fp4") + g("fma") - g("mfma_fp4+fma")) / g("fma"),
+            "exp_hidden_under_fp4_mfma": (g("mfma_fp4") + g("exp") - g("mfma_fp4+exp")) / g("exp"),
+            "fma_hidden_under_bf16_mfma": (g("mfma_bf16") + g("fma") - g("mfma_bf16+fma")) / g("fma"),
+            "fma_hidden_under_fp4_16x16x128": (g("mfma16_fp4") + g("fma") - g("mfma16_fp4+fma")) / g("fma"),
+            # split: half the waves of a SIMD run only MFMAs, the other half only fma
+            "split_vs_serial": g("split") / ((g("mfma_fp4") + g("fma")) / 2)}
+    print(json.dumps({"mode": "rates", "clock_assumed_ghz": 2.4, "iterations": iters,
+                      "cycles_per_iteration": res, "derived": summary}), flush=True)
+
+
+def other_configs(torch, bd, wl, steps):
+    """Attention kernel alone (quantized operands resident) on the other workloads: the small
+    non-causal D=128 case, the causal case and the D=64 long-sequence case in both formats."""
+    res = {}
+    dev = torch.device("cuda:0")
+    for ci in (1, 3, 4):
+        w = wl.CONFIGS[ci]
+        q, k, v = wl.generate(w)
+        dt = torch.bfloat16 if w.in_dtype == wl.IN_BF16 else torch.float16
+        to_dev = lambda a: torch.from_numpy(a.view(np.int16)).view(dt).to(dev)
+        qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)
+        del q, k, v
+        o = torch.empty((w.B, w.H, w.N, w.D), dtype=torch.float32, device=dev)
+        for f in w.fmts:
+            fmt = bd.SAGE_FMT_MXFP4 if f == wl.FMT_MX else bd.SAGE_FMT_NV16_E4M3
+            qq, kq, vq = (bd.sage_quant_fp4(x, r, fmt) for x, r in ((qd, bd.SAGE_ROLE_Q), (kd, bd.SAGE_ROLE_K),
+                                                                    (vd, bd.SAGE_ROLE_V)))
+            run = lambda: bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (w.B, w.H, w.N, w.D), causal=w.causal,
+                                                         fmt=fmt, out=o)
+            run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            n = max(3, min(steps, 10))
+            e0.record()
+            for _ in range(n):
+                run()
+            e1.record()
+            torch.cuda.synchronize()
+            t = e0.elapsed_time(e1) / 1e3 / n
+            name = "%s_%s" % (w.name, "mxfp4" if f == wl.FMT_MX else "nv16")
+            res[name] = {"kernel_ms": t * 1e3, "tops": w.ops / t / 1e12, "frac_of_mxfp4_peak": w.ops / t / 1e12 / PEAK_FP4_TFLOPS}
+            log("%s: attention kernel %.3f ms = %.1f TOPS" % (name, t * 1e3, w.ops / t / 1e12))
+            del qq, kq, vq
+        del qd, kd, vd, o
+        torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -91,9 +178,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true")
-    ap.add_argument("--mode", choices=["full", "attn", "copy"], default="full",
+    ap.add_argument("--no-configs", action="store_true", help="skip the attention-kernel timings of the other workloads")
+    ap.add_argument("--mode", choices=["full", "attn", "copy", "rates"], default="full",
                     help="attn: only the attention kernel (for counter runs); "
-                         "copy: a plain 1 GiB device copy (calibrates FETCH_SIZE / WRITE_SIZE)")
+                         "copy: a plain 1 GiB device copy (calibrates FETCH_SIZE / WRITE_SIZE); "
+                         "rates: instruction issue-rate microbenchmarks behind the VALU co-bound")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only (the per-head work needs no communication; "
@@ -103,6 +192,10 @@ def main():
     import torch
     from paper_2505_11594_amd import binding as bd
     from paper_2505_11594_amd import workloads as wl
+
+    if args.mode == "rates":
+        issue_rates(torch)
+        return
 
     if args.mode == "copy":
         nbytes = 1 << 30
@@ -198,6 +291,10 @@ def main():
         except bd.SageError as ex:
             log("bf16 kernel unavailable:", ex)
 
+    others = None
+    if not args.no_configs:
+        others = other_configs(torch, bd, wl, args.steps)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
@@ -225,6 +322,7 @@ def main():
         "quantize": {"ms": t_quant * 1e3, "algorithmic_GBs": quant_bytes / t_quant / 1e9,
                      "frac_of_hbm_peak": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS},
         "bf16_kernel": bf16,
+        "other_configs": others,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

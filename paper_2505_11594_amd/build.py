@@ -1,4 +1,6 @@
-"""Build the gfx950 HIP library ``libsage_mi355x.so`` in-tree with hipcc.
+"""Build the gfx950 HIP library ``libsage_mi355x.so`` in-tree with hipcc, and
+the separate measurement library ``libsage_rates.so`` (instruction issue-rate
+microbenchmarks used by ``bench.py --mode rates``).
 
 Every HIP source is compiled for ``--offload-arch=gfx950`` only.  Packed FP32
 instructions are disabled (``-packed-fp32-ops``) and floating-point
@@ -16,6 +18,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsage_mi355x.so")
 SOURCES = ["sage_abi.hip", "quant.hip", "attn_fp4.hip", "attn_bf16.hip", "attn_nv16.hip"]
+RATES_LIB = os.path.join(HERE, "libsage_rates.so")
+RATES_SOURCES = ["issue_rates.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -27,9 +31,9 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp%d" % os.getpid()
+def _compile(lib: str, sources, verbose: bool) -> str:
+    srcs = [os.path.join(CSRC, s) for s in sources]
+    tmp = lib + ".tmp%d" % os.getpid()
     cmd = [HIPCC] + FLAGS + ["-o", tmp] + srcs
     r = subprocess.run(cmd, capture_output=True, text=True)
     # the host pass does not know the device-only feature name; that warning is harmless
@@ -38,8 +42,13 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
     if verbose and msgs:
         print("\n".join(msgs), file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
+
+
+def build(verbose: bool = False) -> str:
+    _compile(RATES_LIB, RATES_SOURCES, verbose)
+    return _compile(LIB, SOURCES, verbose)
 
 
 if __name__ == "__main__":

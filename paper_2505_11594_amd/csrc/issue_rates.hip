@@ -1,0 +1,146 @@
+// Instruction issue-rate microbenchmarks for gfx950, built into a separate
+// measurement library (not the attention library).  They ground the
+// co-bound of the FP4 attention kernel: how many cycles the VALU, the
+// transcendental unit, the FP4 pack convert and the block-scaled FP4 MFMA
+// take per wave64 instruction, and how much VALU work runs while FP4 MFMAs
+// execute.  Every wave runs register-only loops; nothing reads or writes
+// memory except one store per lane at the end.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+constexpr int kIters = 1024;
+
+enum Test {
+  kFma = 0,          // 32 independent v_fma_f32
+  kExp = 1,          // 8 v_exp_f32
+  kCvtFp4 = 2,       // 8 v_cvt_scalef32_pk_fp4_f32
+  kMfmaFp4 = 3,      // 4 v_mfma_scale_f32_32x32x64_f8f6f4 (FP4 x FP4, 4 accumulators)
+  kMfmaFp4Fma = 4,   // the same 4 MFMAs + 32 independent v_fma_f32 in the same wave
+  kMfmaFp4Exp = 5,   // the same 4 MFMAs + 8 v_exp_f32 in the same wave
+  kMfmaBf16 = 6,     // 4 v_mfma_f32_32x32x16_bf16
+  kMfmaBf16Fma = 7,  // the same + 32 v_fma_f32
+  kMfma16Fp4 = 8,    // 8 v_mfma_scale_f32_16x16x128_f8f6f4 (the same MACs as test 3)
+  kMfma16Fp4Fma = 9, // the same + 32 v_fma_f32
+  kSplit = 10,       // waves on even SIMD slots: test 3; odd slots: 32 v_fma_f32
+  kNumTests = 11
+};
+
+template <int T>
+__global__ __launch_bounds__(64) void rate_kernel(float* out, float seed) {
+  const int lane = threadIdx.x;
+  float x[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) x[i] = seed + 0.001f * (lane + i);
+  unsigned w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  v16f acc[4] = {};
+  v4f acc16[8] = {};
+  const v8i a = v8i{lane, lane + 1, lane + 2, lane + 3, 0, 0, 0, 0};
+  v8bf ab;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ab[i] = (__bf16)(0.01f * (lane + i));
+  // hardware wave slot on this SIMD (HW_ID[3:0], a read-only register)
+  const unsigned slot = __builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 4) & 15u;
+  const bool mfma_role = T != kSplit || (slot & 1u) == 0;
+  for (int it = 0; it < kIters; ++it) {
+    if (T == kMfmaFp4 || T == kMfmaFp4Fma || T == kMfmaFp4Exp || (T == kSplit && mfma_role)) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        acc[i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, a, acc[i], 4, 4, 0, 127, 0, 127);
+    }
+    if (T == kMfma16Fp4 || T == kMfma16Fp4Fma) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        acc16[i] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, a, acc16[i], 4, 4, 0, 127, 0, 127);
+    }
+    if (T == kMfmaBf16 || T == kMfmaBf16Fma) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ab, ab, acc[i], 0, 0, 0);
+    }
+    if (T == kFma || T == kMfmaFp4Fma || T == kMfmaBf16Fma || T == kMfma16Fp4Fma || (T == kSplit && !mfma_role)) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(x[i], 0.999f, 0.0001f);
+    }
+    if (T == kExp || T == kMfmaFp4Exp) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] = __builtin_amdgcn_exp2f(-x[i]);
+    }
+    if (T == kCvtFp4) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) w[i] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[i], x[i], x[(i + 1) & 7], 1.0f, 0);
+    }
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) s += x[i] + __uint_as_float(w[i] & 0x3fffffffu);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) s += acc[i][lane & 15];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) s += acc16[i][lane & 3];
+  out[blockIdx.x * 64 + lane] = s;
+}
+
+template <int T>
+hipError_t launch(float* out, int blocks, hipStream_t st) {
+  hipLaunchKernelGGL(rate_kernel<T>, dim3((unsigned)blocks), dim3(64), 0, st, out, 0.5f);
+  return hipGetLastError();
+}
+
+hipError_t launch_test(int test, float* out, int blocks, hipStream_t st) {
+  switch (test) {
+    case kFma: return launch<kFma>(out, blocks, st);
+    case kExp: return launch<kExp>(out, blocks, st);
+    case kCvtFp4: return launch<kCvtFp4>(out, blocks, st);
+    case kMfmaFp4: return launch<kMfmaFp4>(out, blocks, st);
+    case kMfmaFp4Fma: return launch<kMfmaFp4Fma>(out, blocks, st);
+    case kMfmaFp4Exp: return launch<kMfmaFp4Exp>(out, blocks, st);
+    case kMfmaBf16: return launch<kMfmaBf16>(out, blocks, st);
+    case kMfmaBf16Fma: return launch<kMfmaBf16Fma>(out, blocks, st);
+    case kMfma16Fp4: return launch<kMfma16Fp4>(out, blocks, st);
+    case kMfma16Fp4Fma: return launch<kMfma16Fp4Fma>(out, blocks, st);
+    default: return launch<kSplit>(out, blocks, st);
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+// Number of tests and loop iterations per wave (each iteration issues the
+// instruction mix named in the test table above).
+int sage_rates_num_tests(void) { return kNumTests; }
+int sage_rates_iterations(void) { return kIters; }
+
+// Runs test `test` with `waves_per_simd` one-wave workgroups per SIMD
+// (1024 * waves_per_simd workgroups: 256 CUs x 4 SIMDs) and writes the mean
+// duration of 5 launches after one warm-up launch, in milliseconds, to *ms.
+// `out` is a device buffer of at least 1024 * waves_per_simd * 64 floats.
+// Returns 0, 1 for bad arguments, 3 for a HIP error.  Synchronizes `stream`.
+int sage_rates_run(int test, int waves_per_simd, float* out, hipStream_t stream, float* ms) {
+  if (test < 0 || test >= kNumTests || waves_per_simd < 1 || waves_per_simd > 8 || !out || !ms) return 1;
+  const int blocks = 1024 * waves_per_simd;
+  hipEvent_t e0, e1;
+  if (hipEventCreate(&e0) != hipSuccess) return 3;
+  if (hipEventCreate(&e1) != hipSuccess) { (void)hipEventDestroy(e0); return 3; }
+  int rc = 0;
+  if (launch_test(test, out, blocks, stream) != hipSuccess || hipEventRecord(e0, stream) != hipSuccess) rc = 3;
+  for (int r = 0; r < 5 && rc == 0; ++r)
+    if (launch_test(test, out, blocks, stream) != hipSuccess) rc = 3;
+  if (rc == 0 && (hipEventRecord(e1, stream) != hipSuccess || hipEventSynchronize(e1) != hipSuccess)) rc = 3;
+  float t = 0.f;
+  if (rc == 0 && hipEventElapsedTime(&t, e0, e1) != hipSuccess) rc = 3;
+  *ms = t / 5.0f;
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  return rc;
+}
+
+}  // extern "C"
