@@ -23,7 +23,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 FMT_MX, FMT_NV16, FMT_NONE = 0, 1, 2
 IN_FP16, IN_BF16 = 0, 1
 ROLE_Q, ROLE_K, ROLE_V = 0, 1, 2
-NO_SMOOTH_K, DIRECT_P, R_LITERAL = 1, 2, 4
+NO_SMOOTH_K, DIRECT_P, R_LITERAL, SMOOTH_Q = 1, 2, 4, 8
 
 _lib = None
 
@@ -66,6 +66,13 @@ def lib():
         L.orc_quant.restype = ctypes.c_long
         L.orc_quant.argtypes = ([ctypes.c_void_p, ctypes.c_int, ctypes.c_int] + [ctypes.c_int] * 4 +
                                 [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p])
+        L.orc_attn2.restype = ctypes.c_int
+        L.orc_attn2.argtypes = ([ctypes.c_void_p] * 3 + [ctypes.c_int] * 9 + [ctypes.c_uint] +
+                                [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_int])
+        L.orc_quant_smooth_q.restype = None
+        L.orc_quant_smooth_q.argtypes = ([ctypes.c_void_p, ctypes.c_int] + [ctypes.c_int] * 6 +
+                                         [ctypes.c_void_p] * 3)
         L.orc_attn.restype = ctypes.c_int
         L.orc_attn.argtypes = ([ctypes.c_void_p] * 3 + [ctypes.c_int] * 8 + [ctypes.c_uint] +
                                [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
@@ -150,6 +157,19 @@ def kmean(k_bits: np.ndarray, in_dtype: int):
     return mu, int(inexact)
 
 
+def quant_smooth_q(q_bits: np.ndarray, in_dtype: int, fmt: int, bq: int = 128):
+    """phi(Q_i - mean(Q_i)) over query blocks of bq rows (smoothing Q, Algorithm 1).
+    Returns (codes [B,H,N,D] one per byte, scales [B,H,N,D/n], qbar fp32 [B,H,ceil(N/bq),D])."""
+    B, H, N, D = q_bits.shape
+    q_bits = np.ascontiguousarray(q_bits, dtype=np.uint16)
+    n = 32 if fmt == FMT_MX else 16
+    codes = np.zeros((B, H, N, D), dtype=np.uint8)
+    scales = np.zeros((B, H, N, D // n), dtype=np.uint8)
+    qbar = np.zeros((B, H, (N + bq - 1) // bq, D), dtype=np.float32)
+    lib().orc_quant_smooth_q(_ptr(q_bits), in_dtype, B, H, N, D, bq, fmt, _ptr(codes), _ptr(scales), _ptr(qbar))
+    return codes, scales, qbar
+
+
 def quant(x_bits: np.ndarray, in_dtype: int, role: int, fmt: int, smooth_k: bool = True):
     """Logical-layout quantization (one code per byte); see orc_quant in the C source.
 
@@ -171,8 +191,9 @@ def quant(x_bits: np.ndarray, in_dtype: int, role: int, fmt: int, smooth_k: bool
 
 
 def attn(q_bits, k_bits, v_bits, in_dtype: int, causal: bool, fmt: int, bkv: int,
-         rows=None, flags: int = 0, nthreads: int | None = None):
-    """Algorithm 1 (without smoothing Q) on the listed rows.
+         rows=None, flags: int = 0, nthreads: int | None = None, bq: int = 128):
+    """Algorithm 1 on the listed rows (smoothing Q when flags has SMOOTH_Q,
+    with query blocks of bq rows).
 
     rows: flat ids ((b*H + h)*N + i); None = every row.
     Returns (out [nrows, D] fp32, tie_tol [nrows] fp32, counters dict)."""
@@ -186,11 +207,11 @@ def attn(q_bits, k_bits, v_bits, in_dtype: int, causal: bool, fmt: int, bkv: int
     out = np.zeros((rows.size, D), dtype=np.float32)
     tol = np.zeros(rows.size, dtype=np.float32)
     cnt = np.zeros(4, dtype=np.int64)
-    rc = lib().orc_attn(_ptr(q_bits), _ptr(k_bits), _ptr(v_bits), in_dtype, B, H, N, D, int(bool(causal)),
-                        fmt, bkv, flags, _ptr(rows), rows.size, _ptr(out), _ptr(tol), _ptr(cnt),
-                        nthreads or default_threads())
+    rc = lib().orc_attn2(_ptr(q_bits), _ptr(k_bits), _ptr(v_bits), in_dtype, B, H, N, D, int(bool(causal)),
+                         fmt, bkv, bq, flags, _ptr(rows), rows.size, _ptr(out), _ptr(tol), _ptr(cnt),
+                         nthreads or default_threads())
     if rc != 0:
-        raise ValueError("orc_attn: invalid arguments")
+        raise ValueError("orc_attn2: invalid arguments")
     counters = dict(inexact_s=int(cnt[0]), inexact_o=int(cnt[1]), tie_codes=int(cnt[2]), skipped_tiles=int(cnt[3]))
     return out, tol, counters
 

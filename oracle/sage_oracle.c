@@ -53,6 +53,9 @@
 #define ORC_NO_SMOOTH_K 1u   /* ablation: skip K <- K - mean(K)                  */
 #define ORC_DIRECT_P 2u      /* ablation: quantize P~ directly (no first level) */
 #define ORC_R_LITERAL 4u     /* ablation: first-level constant 448*6 with E8M0  */
+#define ORC_SMOOTH_Q 8u      /* smoothing Q (Algorithm 1): quantize Q_i - mean(Q_i)
+                                over each block of B_q rows and add the GEMV
+                                mean(Q_i) . K_j^T to S                          */
 
 /* ------------------------------------------------------------------------ */
 /* 16-bit input widening (exact)                                             */
@@ -269,6 +272,48 @@ long orc_quant(const uint16_t* x, int in_dtype, int role, int B, int H, int N, i
 }
 
 /* ------------------------------------------------------------------------ */
+/* Smoothing Q (Algorithm 1, first step of the loop over query blocks):      */
+/* qbar_i = mean of the rows of block Q_i (B_q consecutive rows; the last    */
+/* block holds the remaining rows).  The sum is accumulated in fp64, where   */
+/* it is exact for 16-bit inputs and B_q <= 2^20 rows, and the quotient is   */
+/* rounded once to fp32.  qbar: [nqb][D] for one head.                       */
+/* ------------------------------------------------------------------------ */
+static void qmean_head(const uint16_t* qh, int in_dtype, int N, int D, int bq, float* qbar) {
+  const int nqb = (N + bq - 1) / bq;
+  for (int b = 0; b < nqb; ++b) {
+    const int r0 = b * bq, r1 = (r0 + bq < N) ? r0 + bq : N;
+    for (int c = 0; c < D; ++c) {
+      double s = 0.0;
+      for (int t = r0; t < r1; ++t) s += (double)orc_widen(qh[(long)t * D + c], in_dtype);
+      qbar[(long)b * D + c] = (float)(s / (double)(r1 - r0));
+    }
+  }
+}
+
+/* phi(Q_i - qbar_i) along D for every row (logical layout as orc_quant),    */
+/* and qbar [B,H,ceil(N/bq),D].                                              */
+void orc_quant_smooth_q(const uint16_t* q, int in_dtype, int B, int H, int N, int D, int bq, int fmt,
+                        uint8_t* codes, uint8_t* scales, float* qbar) {
+  const int n = block_of(fmt), nqb = (N + bq - 1) / bq;
+  float* work = (float*)malloc(sizeof(float) * (size_t)D);
+  for (long bh = 0; bh < (long)B * H; ++bh) {
+    const uint16_t* qh = q + bh * (long)N * D;
+    float* qm = qbar + bh * (long)nqb * D;
+    qmean_head(qh, in_dtype, N, D, bq, qm);
+    for (int t = 0; t < N; ++t) {
+      for (int c = 0; c < D; ++c) {
+        volatile float d = orc_widen(qh[(long)t * D + c], in_dtype) - qm[(long)(t / bq) * D + c];
+        work[c] = d;
+      }
+      for (int blk = 0; blk < D / n; ++blk)
+        scales[(bh * N + t) * (long)(D / n) + blk] =
+            orc_phi_block(work + blk * n, n, fmt, codes + (bh * N + t) * (long)D + blk * n);
+    }
+  }
+  free(work);
+}
+
+/* ------------------------------------------------------------------------ */
 /* Exact sums.  FP4MM (Sec. 3.1) equals the matmul of the dequantized        */
 /* operands.  With codes c (2c is an integer in [-12,12]) and scales s, a     */
 /* block's contribution is (sum_k (2c_a)(2c_b)) * s_a s_b / 4 -- an integer   */
@@ -291,14 +336,14 @@ typedef struct {
   float* ks;       /* [N][D/n] scale value of K^                              */
   int8_t* vc2;     /* [D][Np]  2*code value of V^T                            */
   float* vs;       /* [D][Np/n]                                               */
-  float* kf;       /* [N][D]   fp32 K' (fmt NONE)                             */
+  float* kf;       /* [N][D]   fp32 K' (fmt NONE, or smoothing Q: the GEMV)   */
   float* vf;       /* [N][D]   fp32 V  (fmt NONE)                             */
   double vabs_max; /* max |deq(V^)| (for the tie-tolerance bound)             */
 } head_t;
 
 typedef struct {
   const uint16_t *q, *k, *v;
-  int in_dtype, B, H, N, D, causal, fmt, bkv;
+  int in_dtype, B, H, N, D, causal, fmt, bkv, bq;
   unsigned flags;
   const int64_t* rows;
   int64_t nrows;
@@ -354,11 +399,13 @@ static void build_head(attn_job_t* J, long bh) {
   float* work = (float*)malloc(sizeof(float) * (size_t)(D > n ? D : n));
   h->kc2 = (int8_t*)malloc((size_t)N * D);
   h->ks = (float*)malloc(sizeof(float) * (size_t)N * (D / n));
+  if (J->flags & ORC_SMOOTH_Q) h->kf = (float*)malloc(sizeof(float) * (size_t)N * D);
   for (int t = 0; t < N; ++t) {
     for (int c = 0; c < D; ++c) {
       float kv = orc_widen(kb[(long)t * D + c], J->in_dtype);
       if (smooth) { volatile float d = kv - mu[c]; kv = d; }
       work[c] = kv;
+      if (h->kf) h->kf[(long)t * D + c] = kv;
     }
     for (int blk = 0; blk < D / n; ++blk) {
       uint8_t sb = orc_phi_block(work + blk * n, n, fmt, codes + (long)t * D + blk * n);
@@ -403,9 +450,13 @@ static void free_head(head_t* h) {
 static float exp2_f32(float x) { return (float)exp2((double)x); }
 
 /* ------------------------------------------------------------------------ */
-/* One query row of Algorithm 1 (without smoothing Q).                       */
+/* One query row of Algorithm 1 (smoothing Q optional, flag ORC_SMOOTH_Q).   */
 /*                                                                           */
 /* Readings (the paper does not fix these):                                  */
+/*  - smoothing Q: the block mean qbar_i is taken over the B_q rows of the   */
+/*    row's query block; the GEMV(qbar_i, K_j^T) uses the unquantized K' of  */
+/*    the smoothing-K step in fp32, its fp64 sum is rounded once to fp32 and */
+/*    added to the fp32 FP4MM result: S = fl32(fl32(FP4MM) + fl32(GEMV)).    */
 /*  - softmax scale 1/sqrt(D) is applied and exp is taken base 2:            */
 /*    P~_k = 2^{c2 (S_k - m)} with c2 = fl32(log2(e)/sqrt(D)).                */
 /*  - running max m and tile max t are kept in the raw score domain S.        */
@@ -561,9 +612,13 @@ int orc_p_tile(const float* S, int bkv, float m_old, int D, int fmt, unsigned fl
 }
 
 /* ------------------------------------------------------------------------ */
-/* One query row of Algorithm 1 (without smoothing Q).                       */
+/* One query row of Algorithm 1 (smoothing Q optional, flag ORC_SMOOTH_Q).   */
 /*                                                                           */
 /* Readings (the paper does not fix these):                                  */
+/*  - smoothing Q: the block mean qbar_i is taken over the B_q rows of the   */
+/*    row's query block; the GEMV(qbar_i, K_j^T) uses the unquantized K' of  */
+/*    the smoothing-K step in fp32, its fp64 sum is rounded once to fp32 and */
+/*    added to the fp32 FP4MM result: S = fl32(fl32(FP4MM) + fl32(GEMV)).    */
 /*  - softmax scale 1/sqrt(D) is applied and exp is taken base 2:            */
 /*    P~_k = 2^{c2 (S_k - m)} with c2 = fl32(log2(e)/sqrt(D)).                */
 /*  - running max m and tile max t are kept in the raw score domain S.        */
@@ -598,11 +653,20 @@ static void attn_row(attn_job_t* J, long bh, int i, float* out, float* tol_out, 
   const int nblk = bkv / n;
   const uint16_t* qb = J->q + (bh * (long)N + i) * D;
 
-  /* phi(Q_i) along D */
+  /* phi(Q_i) along D; with smoothing Q, phi(Q_i - qbar_i) (Algorithm 1) */
   float* qf = (float*)malloc(sizeof(float) * D);
   int* qc2 = (int*)malloc(sizeof(int) * D);
   float* qs = (float*)malloc(sizeof(float) * (D / n + 1));
+  float* qbar = NULL;
   for (int c = 0; c < D; ++c) qf[c] = orc_widen(qb[c], J->in_dtype);
+  if (J->flags & ORC_SMOOTH_Q) {
+    const int bq = J->bq, blk0 = (i / bq) * bq;
+    const int rows = (blk0 + bq < N) ? bq : N - blk0;
+    qbar = (float*)malloc(sizeof(float) * D);
+    /* the mean of this row's block only (same definition as qmean_head) */
+    qmean_head(J->q + (bh * (long)N + blk0) * D, J->in_dtype, rows, D, bq, qbar);
+    for (int c = 0; c < D; ++c) { volatile float d = qf[c] - qbar[c]; qf[c] = d; }
+  }
   if (fmt != ORC_FMT_NONE) {
     uint8_t cb[32];
     for (int blk = 0; blk < D / n; ++blk) {
@@ -644,6 +708,14 @@ static void attn_row(attn_job_t* J, long bh, int i, float* out, float* tol_out, 
       }
       if (acc.err != 0.0) cnt[0]++;
       S[kk] = (float)acc.s;
+      if (qbar) {
+        /* + GEMV(qbar_i, K_j^T): fp64 products (exact) summed in order of d,
+           rounded once to fp32, then added to the fp32 score */
+        double g = 0.0;
+        for (int c = 0; c < D; ++c) g += (double)qbar[c] * (double)h->kf[(long)k * D + c];
+        volatile float sb = S[kk] + (float)g;
+        S[kk] = sb;
+      }
     }
     if (nvalid == 0) { cnt[3]++; continue; }
 
@@ -698,7 +770,7 @@ static void attn_row(attn_job_t* J, long bh, int i, float* out, float* tol_out, 
   }
   for (int c = 0; c < D; ++c) { volatile float o = O[c] / l; out[c] = o; }
   if (tol_out) *tol_out = (float)(tol / (double)l);
-  free(qf); free(qc2); free(qs); free(S); free(P2); free(pc); free(psb); free(stie); free(tstep); free(O);
+  free(qf); free(qc2); free(qs); free(qbar); free(S); free(P2); free(pc); free(psb); free(stie); free(tstep); free(O);
 }
 
 static void* attn_worker(void* arg) {
@@ -734,7 +806,8 @@ static void* head_worker(void* arg) {
 }
 
 /* ------------------------------------------------------------------------ */
-/* orc_attn: Algorithm 1 (without smoothing Q) for a list of query rows.     */
+/* orc_attn2: Algorithm 1 for a list of query rows; smoothing Q (flag        */
+/* ORC_SMOOTH_Q) uses query blocks of bq rows.  orc_attn: bq = 128.          */
 /*  q, k, v : 16-bit [B,H,N,D] host arrays (in_dtype fp16/bf16)              */
 /*  rows    : flat row ids ((b*H + h)*N + i), nrows of them                   */
 /*  out     : [nrows][D] fp32;  tie_tol: [nrows] or NULL;                     */
@@ -742,16 +815,16 @@ static void* head_worker(void* arg) {
 /*            codes, skipped tiles)                                          */
 /* Returns 0, or -1 for invalid arguments.                                   */
 /* ------------------------------------------------------------------------ */
-int orc_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int in_dtype,
-             int B, int H, int N, int D, int causal, int fmt, int bkv, unsigned flags,
-             const int64_t* rows, int64_t nrows, float* out, float* tie_tol,
-             int64_t* counters, int nthreads) {
-  if (B <= 0 || H <= 0 || N <= 0 || D <= 0 || bkv <= 0) return -1;
+int orc_attn2(const uint16_t* q, const uint16_t* k, const uint16_t* v, int in_dtype,
+              int B, int H, int N, int D, int causal, int fmt, int bkv, int bq, unsigned flags,
+              const int64_t* rows, int64_t nrows, float* out, float* tie_tol,
+              int64_t* counters, int nthreads) {
+  if (B <= 0 || H <= 0 || N <= 0 || D <= 0 || bkv <= 0 || bq <= 0) return -1;
   if (fmt != ORC_FMT_NONE && (D % block_of(fmt) || bkv % block_of(fmt))) return -1;
   attn_job_t J;
   memset(&J, 0, sizeof(J));
   J.q = q; J.k = k; J.v = v; J.in_dtype = in_dtype; J.B = B; J.H = H; J.N = N; J.D = D;
-  J.causal = causal; J.fmt = fmt; J.bkv = bkv; J.flags = flags; J.rows = rows; J.nrows = nrows;
+  J.causal = causal; J.fmt = fmt; J.bkv = bkv; J.bq = bq; J.flags = flags; J.rows = rows; J.nrows = nrows;
   J.out = out; J.tie_tol = tie_tol;
   J.heads = (head_t*)calloc((size_t)B * H, sizeof(head_t));
   J.head_used = (char*)calloc((size_t)B * H, 1);
@@ -779,6 +852,14 @@ int orc_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int in_dty
   free(HJ.list); free(J.heads); free(J.head_used);
   pthread_mutex_destroy(&J.mu); pthread_mutex_destroy(&HJ.mu);
   return 0;
+}
+
+int orc_attn(const uint16_t* q, const uint16_t* k, const uint16_t* v, int in_dtype,
+             int B, int H, int N, int D, int causal, int fmt, int bkv, unsigned flags,
+             const int64_t* rows, int64_t nrows, float* out, float* tie_tol,
+             int64_t* counters, int nthreads) {
+  return orc_attn2(q, k, v, in_dtype, B, H, N, D, causal, fmt, bkv, 128, flags, rows, nrows, out, tie_tol,
+                   counters, nthreads);
 }
 
 /* ------------------------------------------------------------------------ */
