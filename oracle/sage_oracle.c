@@ -455,8 +455,9 @@ static float exp2_f32(float x) { return (float)exp2((double)x); }
 /* Readings (the paper does not fix these):                                  */
 /*  - smoothing Q: the block mean qbar_i is taken over the B_q rows of the   */
 /*    row's query block; the GEMV(qbar_i, K_j^T) uses the unquantized K' of  */
-/*    the smoothing-K step in fp32, its fp64 sum is rounded once to fp32 and */
-/*    added to the fp32 FP4MM result: S = fl32(fl32(FP4MM) + fl32(GEMV)).    */
+/*    the smoothing-K step in fp32, as a chain of fp32 fused multiply-adds   */
+/*    in order of d starting from 0, and is added to the fp32 FP4MM result:  */
+/*    S = fl32(fl32(FP4MM) + GEMV).                                          */
 /*  - softmax scale 1/sqrt(D) is applied and exp is taken base 2:            */
 /*    P~_k = 2^{c2 (S_k - m)} with c2 = fl32(log2(e)/sqrt(D)).                */
 /*  - running max m and tile max t are kept in the raw score domain S.        */
@@ -617,8 +618,9 @@ int orc_p_tile(const float* S, int bkv, float m_old, int D, int fmt, unsigned fl
 /* Readings (the paper does not fix these):                                  */
 /*  - smoothing Q: the block mean qbar_i is taken over the B_q rows of the   */
 /*    row's query block; the GEMV(qbar_i, K_j^T) uses the unquantized K' of  */
-/*    the smoothing-K step in fp32, its fp64 sum is rounded once to fp32 and */
-/*    added to the fp32 FP4MM result: S = fl32(fl32(FP4MM) + fl32(GEMV)).    */
+/*    the smoothing-K step in fp32, as a chain of fp32 fused multiply-adds   */
+/*    in order of d starting from 0, and is added to the fp32 FP4MM result:  */
+/*    S = fl32(fl32(FP4MM) + GEMV).                                          */
 /*  - softmax scale 1/sqrt(D) is applied and exp is taken base 2:            */
 /*    P~_k = 2^{c2 (S_k - m)} with c2 = fl32(log2(e)/sqrt(D)).                */
 /*  - running max m and tile max t are kept in the raw score domain S.        */
@@ -709,11 +711,11 @@ static void attn_row(attn_job_t* J, long bh, int i, float* out, float* tol_out, 
       if (acc.err != 0.0) cnt[0]++;
       S[kk] = (float)acc.s;
       if (qbar) {
-        /* + GEMV(qbar_i, K_j^T): fp64 products (exact) summed in order of d,
-           rounded once to fp32, then added to the fp32 score */
-        double g = 0.0;
-        for (int c = 0; c < D; ++c) g += (double)qbar[c] * (double)h->kf[(long)k * D + c];
-        volatile float sb = S[kk] + (float)g;
+        /* + GEMV(qbar_i, K_j^T) in fp32: a chain of fused multiply-adds in
+           order of d from 0, then added to the fp32 score */
+        float g = 0.0f;
+        for (int c = 0; c < D; ++c) g = fmaf(qbar[c], h->kf[(long)k * D + c], g);
+        volatile float sb = S[kk] + g;
         S[kk] = sb;
       }
     }
