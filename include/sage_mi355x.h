@@ -41,7 +41,7 @@ typedef enum {
 #define SAGE_IN_BF16        0x4u
 #define SAGE_OUT_F32        0x8u  /* o is fp32; otherwise o has the input dtype           */
 #define SAGE_NO_SMOOTH_K    0x10u /* ablation: skip K <- K - mean(K) (Algorithm 1)         */
-#define SAGE_SMOOTH_Q       0x20u /* smoothing Q (Algorithm 1): SAGE_ERR_UNSUPPORTED       */
+#define SAGE_SMOOTH_Q       0x20u /* smoothing Q (Algorithm 1), see below; MXFP4 attention  */
 #define SAGE_BKV64          0x40u /* KV tile of 64 tokens instead of 128                   */
 #define SAGE_FMT_ALL_BITS   0x7Fu
 
@@ -69,6 +69,14 @@ typedef enum {
  *       >= N are zero.
  * kmean: fp32 [B,H,D], the per-(b,h) channel mean of K over the N tokens,
  * computed as an exact fp64 sum divided by N and rounded to fp32.
+ *
+ * Smoothing Q (SAGE_SMOOTH_Q; Algorithm 1, "Smoothing Q of SageAttention2"):
+ * Q is split into blocks of 128 consecutive rows (the last block holds the
+ * rest); qbar[b,h,i,:] is the mean of block i (exact fp64 sum / rows, rounded
+ * to fp32) and Q^ = phi(fl32(Q - qbar)).  The attention adds the GEMV
+ * qbar_i . K'_k to every score of block i, with K' = fl32(K - kmean) (K when
+ * SAGE_NO_SMOOTH_K) and the dot product evaluated as a chain of fp32 fused
+ * multiply-adds in order of the channel: S = fl32(FP4MM + GEMV).
  */
 
 /* Byte sizes of the codes and scales buffers for one role.  Host only. */
@@ -90,7 +98,8 @@ size_t sage_quant_workspace_size(int role, int B, int H, int N, int D, unsigned 
  *  codes    : output, sage_quant_sizes() bytes, 16-byte aligned
  *  scales   : output, sage_quant_sizes() bytes, 4-byte aligned
  *  kmean    : role K: output fp32 [B,H,D] (required unless SAGE_NO_SMOOTH_K);
- *             other roles: must be NULL
+ *             role Q with SAGE_SMOOTH_Q: output qbar fp32 [B,H,ceil(N/128),D]
+ *             (required); otherwise must be NULL
  *  workspace: role K with smoothing: device buffer of at least
  *             sage_quant_workspace_size() bytes, 8-byte aligned; else may be NULL
  * D must be 64 or 128; N >= 1.
@@ -100,7 +109,9 @@ int sage_quant_fp4(const void* x, int role, int B, int H, int N, int D, unsigned
                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Workspace bytes for sage_attn_fp4_fwd_ws (quantized Q, K, V, the mean and
- * its partial sums).  Host only. */
+ * its partial sums; with SAGE_SMOOTH_Q also the query-block means and the
+ * GEMV term, B*H*ceil(N/128)*(D + Np)*4 bytes).  0 for invalid or unsupported
+ * arguments.  Host only. */
 size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt);
 
 /*
@@ -113,6 +124,8 @@ size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt);
  * MXFP4 runs on block-scaled FP4 MFMA; NV16 (whose E4M3 scales at 16-element
  * granularity the MFMA cannot take) dequantizes exactly to bf16 and runs on
  * bf16 MFMA.
+ * With SAGE_SMOOTH_Q the scores get the smoothing-Q GEMV term described above
+ * (MXFP4 only: SAGE_ERR_UNSUPPORTED with SAGE_FMT_NV16_E4M3).
  * Softmax scale is 1/sqrt(D).  causal = 1 keeps key j for query i iff j <= i.
  *  q, k, v  : 16-bit [B,H,N,D], 16-byte aligned
  *  o        : [B,H,N,D] fp32 (SAGE_OUT_F32) or input dtype, 16-byte aligned
@@ -131,7 +144,8 @@ int sage_attn_fp4_fwd_ws(const void* q, const void* k, const void* v, void* o,
 /*
  * sage_attn_fp4_fwd_prequant -- the attention kernel alone, on tensors
  * produced by sage_quant_fp4 (layouts above).  kmean is not needed: the
- * smoothing is already inside K^ (softmax is invariant to it).
+ * smoothing is already inside K^ (softmax is invariant to it).  SAGE_SMOOTH_Q
+ * returns SAGE_ERR_UNSUPPORTED (its GEMV term is not an input here).
  */
 int sage_attn_fp4_fwd_prequant(const void* q_codes, const void* q_scales,
                                const void* k_codes, const void* k_scales,

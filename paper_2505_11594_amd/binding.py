@@ -99,7 +99,9 @@ def quant_sizes(role: int, B: int, H: int, N: int, D: int, fmt: int):
 
 
 def sage_quant_fp4(x, role: int, fmt: int = SAGE_FMT_MXFP4):
-    """Quantize one tensor; returns (codes uint8, scales uint8, kmean fp32 or None) on the device."""
+    """Quantize one tensor; returns (codes uint8, scales uint8, mean fp32 or None) on the device:
+    role K with smoothing K: the channel mean [B,H,D]; role Q with SAGE_SMOOTH_Q: the query-block
+    means [B,H,ceil(N/128),D]."""
     import torch
     B, H, N, D = _shape(x)
     fmt = fmt | _in_flag(x)
@@ -108,6 +110,8 @@ def sage_quant_fp4(x, role: int, fmt: int = SAGE_FMT_MXFP4):
     scales = torch.empty(sb, dtype=torch.uint8, device=x.device)
     kmean = None
     ws = None
+    if role == SAGE_ROLE_Q and (fmt & SAGE_SMOOTH_Q):
+        kmean = torch.empty((B, H, (N + 127) // 128, D), dtype=torch.float32, device=x.device)
     if role == SAGE_ROLE_K and not (fmt & SAGE_NO_SMOOTH_K):
         kmean = torch.empty((B, H, D), dtype=torch.float32, device=x.device)
         wsb = int(lib().sage_quant_workspace_size(role, B, H, N, D, fmt))

@@ -47,8 +47,9 @@ __device__ __forceinline__ void lds_load4(const void* src, void* dst) {
 }
 __device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
 
-// One LDS stage of a KV tile, in MFMA-operand order.
-template <int D, int BKV>
+// One LDS stage of a KV tile, in MFMA-operand order (plus, with smoothing Q,
+// the tile's BKV entries of the query block's GEMV bias).
+template <int D, int BKV, bool SQ>
 struct Fp4Stage {
   static constexpr int NSUB = BKV / 32;        // 32-key subtiles (S^T rows)
   static constexpr int NKS = D / 64;           // K-steps of S^T = K^ Q^T
@@ -61,19 +62,23 @@ struct Fp4Stage {
   static constexpr int KS_OFF = VC_OFF + NVB * 1024;   // K^ scales: BKV rows x D/32 bytes, as in HBM
   static constexpr int KS_BYTES = BKV * (D / 32);
   static constexpr int VS_OFF = KS_OFF + KS_BYTES;      // V^T scales: one dword per dim row
-  static constexpr int BYTES = VS_OFF + D * 4;
+  static constexpr int BIAS_OFF = VS_OFF + D * 4;       // smoothing Q: fp32 bias of the tile's keys
+  static constexpr int BYTES = BIAS_OFF + (SQ ? BKV * 4 : 0);
   static constexpr int NKSJ = (KS_BYTES / 4 + 63) / 64;   // dword loads of K^ scales (64 lanes each)
   static constexpr int NVSJ = D / 64;                     // dword loads of V^T scales
 };
 
 __device__ __forceinline__ v8i as_op(const v4i x) { return v8i{x[0], x[1], x[2], x[3], 0, 0, 0, 0}; }
 
-template <int D, int BKV, bool CAUSAL, int OUT>  // OUT: 0 = fp32, 1 = bf16, 2 = fp16
+// OUT: 0 = fp32, 1 = bf16, 2 = fp16.  SQ: smoothing Q -- S += qkb[bh, query
+// block, key] (Algorithm 1's GEMV of the block mean with K', one row of Np
+// floats per 128-query block, which is this workgroup's query tile).
+template <int D, int BKV, bool CAUSAL, int OUT, bool SQ>
 __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
     const uint8_t* __restrict__ qc, const uint8_t* __restrict__ qs, const uint8_t* __restrict__ kc,
     const uint8_t* __restrict__ ks, const uint8_t* __restrict__ vc, const uint8_t* __restrict__ vs,
-    void* __restrict__ o, int BH, int N, int Np, int nqt, float c2, float log6) {
-  using T = Fp4Stage<D, BKV>;
+    const float* __restrict__ qkb, void* __restrict__ o, int BH, int N, int Np, int nqt, float c2, float log6) {
+  using T = Fp4Stage<D, BKV, SQ>;
   constexpr int NSUB = T::NSUB, NKS = T::NKS, NDB = T::NDB, NG = T::NG;
   __shared__ __attribute__((aligned(16))) uint8_t lds[3][T::BYTES];
 
@@ -142,6 +147,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
   const bool ks_job = wave < T::NKSJ, vs_job = !ks_job && wave < T::NKSJ + T::NVSJ;
   const bool ks_lane = 64 * (wave + 1) <= T::KS_BYTES / 4 || 64 * wave + lane < T::KS_BYTES / 4;
   so = ks_job ? (64 * wave + lane) * 4 : (64 * (wave - T::NKSJ) + lane) * (Np / 32);
+  const float* brow = SQ ? qkb + ((size_t)bh * nqt + qt) * Np : nullptr;   // this query block's bias row
   auto issue = [&](int j, int stage) {
     const int kb = j * BKV;
     uint8_t* L = lds[stage];
@@ -161,6 +167,9 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
     } else if (vs_job) {
       // the aligned dword holding the tile's BKV/32 scale bytes of dim row 64c + lane
       lds_load4(vsbase + ((kb / 32) & ~3) + so, L + T::VS_OFF + (wave - T::NKSJ) * 256);
+    }
+    if constexpr (SQ) {
+      if (wave == 0 && lane < BKV / 4) lds_load16(brow + kb + 4 * lane, L + T::BIAS_OFF);
     }
   };
 
@@ -208,6 +217,19 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
     const int vshift = 8 * (((kb / 32) & 3) + hi);
 
     if (active) {
+      if constexpr (SQ) {
+        // smoothing Q: S = fl32(S + bias); element (u, v) is key kb + 64 (u >> 1) + 32 hi + 16 (u & 1) + v
+#pragma unroll
+        for (int u = 0; u < NSUB; ++u) {
+          const float* bp = reinterpret_cast<const float*>(L + T::BIAS_OFF) + 64 * (u >> 1) + 32 * hi + 16 * (u & 1);
+#pragma unroll
+          for (int w4 = 0; w4 < 4; ++w4) {
+            const v4f b = *reinterpret_cast<const v4f*>(bp + 4 * w4);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sacc[u][4 * w4 + r] = sacc[u][4 * w4 + r] + b[r];
+          }
+        }
+      }
       // ---- masking (tail keys >= N; causal keys > query) ---------------
       const bool need_mask = (kb + BKV > N) || (CAUSAL && kb + BKV - 1 > qw);
       if (need_mask) {
@@ -346,30 +368,41 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
   }
 }
 
-template <int D, int BKV, bool CAUSAL, int OUT>
+template <int D, int BKV, bool CAUSAL, int OUT, bool SQ>
 static hipError_t launch_fp4_t(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                               const void* vs, void* o, int BH, int N, int Np, float c2, float log6, hipStream_t st) {
+                               const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2, float log6,
+                               hipStream_t st) {
   const int nqt = (N + AQ - 1) / AQ;
-  hipLaunchKernelGGL((attn_fp4_mx_kernel<D, BKV, CAUSAL, OUT>), dim3((unsigned)(nqt * BH)), dim3(256), 0, st,
+  hipLaunchKernelGGL((attn_fp4_mx_kernel<D, BKV, CAUSAL, OUT, SQ>), dim3((unsigned)(nqt * BH)), dim3(256), 0, st,
                      (const uint8_t*)qc, (const uint8_t*)qs, (const uint8_t*)kc, (const uint8_t*)ks, (const uint8_t*)vc,
-                     (const uint8_t*)vs, o, BH, N, Np, nqt, c2, log6);
+                     (const uint8_t*)vs, qkb, o, BH, N, Np, nqt, c2, log6);
   return hipGetLastError();
 }
 
-template <int D, int BKV, bool CAUSAL>
+template <int D, int BKV, bool CAUSAL, bool SQ>
 static hipError_t launch_fp4_o(int out, const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                               const void* vs, void* o, int BH, int N, int Np, float c2, float log6, hipStream_t st) {
-  if (out == 0) return launch_fp4_t<D, BKV, CAUSAL, 0>(qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, log6, st);
-  if (out == 1) return launch_fp4_t<D, BKV, CAUSAL, 1>(qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, log6, st);
-  return launch_fp4_t<D, BKV, CAUSAL, 2>(qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, log6, st);
+                               const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2, float log6,
+                               hipStream_t st) {
+  if (out == 0) return launch_fp4_t<D, BKV, CAUSAL, 0, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+  if (out == 1) return launch_fp4_t<D, BKV, CAUSAL, 1, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+  return launch_fp4_t<D, BKV, CAUSAL, 2, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
 }
 
+template <int D, int BKV, bool CAUSAL>
+static hipError_t launch_fp4_s(int out, const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
+                               const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2, float log6,
+                               hipStream_t st) {
+  return qkb ? launch_fp4_o<D, BKV, CAUSAL, true>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st)
+             : launch_fp4_o<D, BKV, CAUSAL, false>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+}
+
+// qkb: smoothing-Q bias [BH, ceil(N/128), Np] fp32, or null without smoothing Q.
 hipError_t launch_attn_fp4_mx(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                              const void* vs, void* o, int BH, int N, int Np, int D, int bkv, bool causal, int out,
-                              float c2, float log6, hipStream_t st) {
-#define SAGE_A(DD, BB)                                                                              \
-  return causal ? launch_fp4_o<DD, BB, true>(out, qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, log6, st) \
-                : launch_fp4_o<DD, BB, false>(out, qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, log6, st)
+                              const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
+                              bool causal, int out, float c2, float log6, hipStream_t st) {
+#define SAGE_A(DD, BB)                                                                                    \
+  return causal ? launch_fp4_s<DD, BB, true>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st) \
+                : launch_fp4_s<DD, BB, false>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st)
   if (D == 128) { if (bkv == 128) { SAGE_A(128, 128); } else { SAGE_A(128, 64); } }
   else { if (bkv == 128) { SAGE_A(64, 128); } else { SAGE_A(64, 64); } }
 #undef SAGE_A

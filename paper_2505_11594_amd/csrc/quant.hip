@@ -5,8 +5,10 @@
 // E8M0 (MXFP4, n = 32: the smallest power of two with 6 s >= max) or E4M3
 // (n = 16, round to nearest even, saturating at 448); codes are FP4 E2M1
 // round-to-nearest-even of x / s.  Smoothing K (Algorithm 1 preprocessing)
-// subtracts the per-(b,h) channel mean first; the V transpose is fused into
-// its quantization (Appendix, "Transposing V").
+// subtracts the per-(b,h) channel mean first, smoothing Q (Algorithm 1) the
+// mean of each block of QB query rows; the V transpose is fused into its
+// quantization (Appendix, "Transposing V").  For smoothing Q the GEMV of the
+// block means with K' is computed here as well.
 //
 // All three kernels are HBM-bound: each element is read once as 16 bits
 // (twice for K, which the mean also reads) and written as 4 bits plus 8 bits
@@ -68,11 +70,101 @@ __global__ void kmean_final_kernel(const double* __restrict__ part, float* __res
 }
 
 // ---------------------------------------------------------------------------
+// Smoothing Q (Algorithm 1): qbar[bh, b, c] = mean of Q[bh, t, c] over the QB
+// rows t of query block b (the last block holds the remaining rows), an fp64
+// sum -- exact for 16-bit inputs, so the order does not matter -- divided by
+// the row count and rounded once to fp32.  One workgroup per (block, bh).
+// ---------------------------------------------------------------------------
+constexpr int QB = 128;   // query rows per smoothing block (= the attention kernel's query tile)
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(KM_THREADS) void qmean_kernel(const uint16_t* __restrict__ q, float* __restrict__ qbar,
+                                                           int N, int nqb) {
+  constexpr int CG = D / 8, RS = KM_THREADS / CG;
+  const int b = blockIdx.x, bh = blockIdx.y, tid = threadIdx.x;
+  const int cg = tid % CG, rsub = tid / CG;
+  const int t0 = b * QB, t1 = min(N, t0 + QB);
+  const uint16_t* qh = q + (size_t)bh * N * D;
+  double acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = 0.0;
+  for (int t = t0 + rsub; t < t1; t += RS) {
+    uint4 raw = *reinterpret_cast<const uint4*>(qh + (size_t)t * D + cg * 8);
+    const uint16_t* h = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] += (double)widen<BF16>(h[i]);
+  }
+  __shared__ double red[KM_THREADS][9];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) red[tid][i] = acc[i];
+  __syncthreads();
+  if (tid < D) {
+    const int c = tid, g = c / 8, i = c % 8;
+    double s = 0.0;
+    for (int r = 0; r < RS; ++r) s += red[r * CG + g][i];
+    qbar[((size_t)bh * nqb + b) * D + c] = (float)(s / (double)(t1 - t0));
+  }
+}
+
+// GEMV of smoothing Q: bias[bh, b, k] = qbar[bh, b, :] . K'[bh, k, :] with
+// K' = fl32(K - mu) (K itself without smoothing K), as a chain of fp32 fused
+// multiply-adds in order of the channel from 0; keys k >= N get 0.  One
+// thread per key keeps K' in registers and runs QBG independent chains (query
+// blocks) at a time; the block means are wave-uniform scalar loads.
+constexpr int QBG = 8;
+
+template <int D, bool BF16>
+__global__ __launch_bounds__(128) void qk_bias_kernel(const uint16_t* __restrict__ k, const float* __restrict__ mu,
+                                                      const float* __restrict__ qbar, float* __restrict__ bias, int N,
+                                                      int Np, int nqb) {
+  const int bh = blockIdx.y;
+  const int key = blockIdx.x * 128 + threadIdx.x;   // < Np: the grid covers Np / 128 blocks exactly
+  float kv[D];
+  const bool valid = key < N;
+  if (valid) {
+    const uint16_t* kr = k + ((size_t)bh * N + key) * D;
+#pragma unroll
+    for (int c8 = 0; c8 < D / 8; ++c8) {
+      uint4 raw = *reinterpret_cast<const uint4*>(kr + c8 * 8);
+      const uint16_t* h = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) kv[c8 * 8 + i] = widen<BF16>(h[i]);
+    }
+    if (mu != nullptr) {
+#pragma unroll
+      for (int c = 0; c < D; ++c) kv[c] = kv[c] - mu[(size_t)bh * D + c];
+    }
+  }
+  const float* qm = qbar + (size_t)bh * nqb * D;
+  float* out = bias + (size_t)bh * nqb * Np + key;
+  int b0 = 0;
+  for (; b0 + QBG <= nqb; b0 += QBG) {   // full groups: QBG independent chains
+    float acc[QBG];
+#pragma unroll
+    for (int i = 0; i < QBG; ++i) acc[i] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < D; ++c)
+#pragma unroll
+      for (int i = 0; i < QBG; ++i) acc[i] = __builtin_fmaf(qm[(size_t)(b0 + i) * D + c], kv[c], acc[i]);
+#pragma unroll
+    for (int i = 0; i < QBG; ++i) out[(size_t)(b0 + i) * Np] = valid ? acc[i] : 0.0f;
+  }
+  for (; b0 < nqb; ++b0) {               // the remaining blocks, one chain each
+    float acc = 0.0f;
+#pragma unroll
+    for (int c = 0; c < D; ++c) acc = __builtin_fmaf(qm[(size_t)b0 * D + c], kv[c], acc);
+    out[(size_t)b0 * Np] = valid ? acc : 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Row quantizer for Q and K (blocks along D).  One lane owns 8 consecutive
 // channels (a 16-byte load); the 4 (MXFP4) or 2 (NV16) lanes of a block
 // reduce their absolute maxima with cross-lane swaps.  A lane writes its 8
-// codes as one 32-bit word.  Role K subtracts mu and stores each token at
-// its permuted position inside its 64-token group.
+// codes as one 32-bit word.  A mean, when given, is subtracted first: row t
+// of head bh uses mu[(bh * nmb + (t >> mshift)) * D + c] (role K: one mean
+// per head; role Q with smoothing: one per QB-row block).  Role K stores each
+// token at its permuted position inside its group.
 // ---------------------------------------------------------------------------
 // Stored row of K token t.  MXFP4 (32x32x64 block-scaled MFMA): inside each
 // 64-token group, offset o = 32h + 16t' + 4g + r goes to 32t' + 8g + 4h + r.
@@ -93,8 +185,9 @@ __device__ __forceinline__ int k_stored_pos(int t) {
 
 template <int D, bool BF16, int FMT, bool IS_K>
 __global__ __launch_bounds__(256) void quant_rows_kernel(const uint16_t* __restrict__ x, const float* __restrict__ mu,
-                                                         uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
-                                                         int N, int Nout, long long total_units) {
+                                                         int mshift, int nmb, uint8_t* __restrict__ codes,
+                                                         uint8_t* __restrict__ scales, int N, int Nout,
+                                                         long long total_units) {
   constexpr int NB = (FMT == kFmtMX) ? 32 : 16;     // block size
   constexpr int LPB = NB / 8;                       // lanes per block
   constexpr int UPR = D / 8;                        // units (lanes) per row
@@ -109,8 +202,8 @@ __global__ __launch_bounds__(256) void quant_rows_kernel(const uint16_t* __restr
     float v[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = widen<BF16>(hv[i]);
-    if (IS_K && mu != nullptr) {
-      const float* m = mu + bh * D + cu * 8;
+    if (mu != nullptr) {
+      const float* m = mu + ((size_t)bh * nmb + (t >> mshift)) * D + cu * 8;
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] = v[i] - m[i];
     }
@@ -262,13 +355,13 @@ hipError_t launch_kmean(const void* k, double* part, float* mu, int BH, int N, i
 }
 
 template <int D, bool BF16, int FMT, bool IS_K>
-static hipError_t launch_rows_t(const void* x, const float* mu, void* codes, void* scales, int BH, int N, int Nout,
-                                hipStream_t st) {
+static hipError_t launch_rows_t(const void* x, const float* mu, int mshift, int nmb, void* codes, void* scales, int BH,
+                                int N, int Nout, hipStream_t st) {
   const long long units = (long long)BH * N * (D / 8);
   long long blocks = (units + 255) / 256;
   if (blocks > 65536) blocks = 65536;
   hipLaunchKernelGGL((quant_rows_kernel<D, BF16, FMT, IS_K>), dim3((unsigned)blocks), dim3(256), 0, st,
-                     (const uint16_t*)x, mu, (uint8_t*)codes, (uint8_t*)scales, N, Nout, units);
+                     (const uint16_t*)x, mu, mshift, nmb, (uint8_t*)codes, (uint8_t*)scales, N, Nout, units);
   if (IS_K && Nout > N) {
     hipLaunchKernelGGL((k_tail_kernel<D, FMT>), dim3(1, BH), dim3(256), 0, st, (uint8_t*)codes, (uint8_t*)scales, N, Nout);
   }
@@ -276,20 +369,48 @@ static hipError_t launch_rows_t(const void* x, const float* mu, void* codes, voi
 }
 
 template <int D, int FMT, bool IS_K>
-static hipError_t launch_rows_d(const void* x, const float* mu, void* codes, void* scales, int BH, int N, int Nout,
-                                bool bf16, hipStream_t st) {
-  return bf16 ? launch_rows_t<D, true, FMT, IS_K>(x, mu, codes, scales, BH, N, Nout, st)
-              : launch_rows_t<D, false, FMT, IS_K>(x, mu, codes, scales, BH, N, Nout, st);
+static hipError_t launch_rows_d(const void* x, const float* mu, int mshift, int nmb, void* codes, void* scales, int BH,
+                                int N, int Nout, bool bf16, hipStream_t st) {
+  return bf16 ? launch_rows_t<D, true, FMT, IS_K>(x, mu, mshift, nmb, codes, scales, BH, N, Nout, st)
+              : launch_rows_t<D, false, FMT, IS_K>(x, mu, mshift, nmb, codes, scales, BH, N, Nout, st);
 }
 
+// mu: role K one mean per head (or null); role Q with smoothing one per QB-row block (or null).
 hipError_t launch_quant_rows(const void* x, const float* mu, void* codes, void* scales, int BH, int N, int Nout, int D,
                              int fmt, bool is_k, bool bf16, hipStream_t st) {
-#define SAGE_ROWS(DD, FF)                                                                              \
-  return is_k ? launch_rows_d<DD, FF, true>(x, mu, codes, scales, BH, N, Nout, bf16, st)              \
-              : launch_rows_d<DD, FF, false>(x, mu, codes, scales, BH, N, Nout, bf16, st)
+  const int mshift = is_k ? 30 : 7, nmb = is_k ? 1 : (N + QB - 1) / QB;
+  static_assert(QB == (1 << 7), "query smoothing blocks are 128 rows");
+#define SAGE_ROWS(DD, FF)                                                                                   \
+  return is_k ? launch_rows_d<DD, FF, true>(x, mu, mshift, nmb, codes, scales, BH, N, Nout, bf16, st)      \
+              : launch_rows_d<DD, FF, false>(x, mu, mshift, nmb, codes, scales, BH, N, Nout, bf16, st)
   if (D == 128) { if (fmt == kFmtMX) { SAGE_ROWS(128, kFmtMX); } else { SAGE_ROWS(128, kFmtNV16); } }
   else { if (fmt == kFmtMX) { SAGE_ROWS(64, kFmtMX); } else { SAGE_ROWS(64, kFmtNV16); } }
 #undef SAGE_ROWS
+}
+
+int qmean_blocks(int N) { return (N + QB - 1) / QB; }
+
+hipError_t launch_qmean(const void* q, float* qbar, int BH, int N, int D, bool bf16, hipStream_t st) {
+  const dim3 grid((unsigned)qmean_blocks(N), (unsigned)BH);
+#define SAGE_QM(DD, BB) hipLaunchKernelGGL((qmean_kernel<DD, BB>), grid, dim3(KM_THREADS), 0, st, (const uint16_t*)q, \
+                                           qbar, N, qmean_blocks(N))
+  if (D == 128) { if (bf16) { SAGE_QM(128, true); } else { SAGE_QM(128, false); } }
+  else { if (bf16) { SAGE_QM(64, true); } else { SAGE_QM(64, false); } }
+#undef SAGE_QM
+  return hipGetLastError();
+}
+
+// bias [BH, nqb, Np] fp32; Np is a multiple of 128
+hipError_t launch_qk_bias(const void* k, const float* mu, const float* qbar, float* bias, int BH, int N, int Np, int D,
+                          bool bf16, hipStream_t st) {
+  const dim3 grid((unsigned)(Np / 128), (unsigned)BH);
+  const int nqb = qmean_blocks(N);
+#define SAGE_QB(DD, BB) hipLaunchKernelGGL((qk_bias_kernel<DD, BB>), grid, dim3(128), 0, st, (const uint16_t*)k, mu, \
+                                           qbar, bias, N, Np, nqb)
+  if (D == 128) { if (bf16) { SAGE_QB(128, true); } else { SAGE_QB(128, false); } }
+  else { if (bf16) { SAGE_QB(64, true); } else { SAGE_QB(64, false); } }
+#undef SAGE_QB
+  return hipGetLastError();
 }
 
 template <int D, bool BF16, int FMT>

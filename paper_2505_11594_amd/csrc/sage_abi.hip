@@ -14,9 +14,13 @@ hipError_t launch_quant_rows(const void* x, const float* mu, void* codes, void* 
                              int fmt, bool is_k, bool bf16, hipStream_t st);
 hipError_t launch_quant_v(const void* v, void* codes, void* scales, int BH, int N, int Np, int D, int fmt, bool bf16,
                           hipStream_t st);
+hipError_t launch_qmean(const void* q, float* qbar, int BH, int N, int D, bool bf16, hipStream_t st);
+int qmean_blocks(int N);
+hipError_t launch_qk_bias(const void* k, const float* mu, const float* qbar, float* bias, int BH, int N, int Np, int D,
+                          bool bf16, hipStream_t st);
 hipError_t launch_attn_fp4_mx(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                              const void* vs, void* o, int BH, int N, int Np, int D, int bkv, bool causal, int out,
-                              float c2, float log6, hipStream_t st);
+                              const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
+                              bool causal, int out, float c2, float log6, hipStream_t st);
 hipError_t launch_attn_nv16(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
                             const void* vs, void* o, int BH, int N, int Np, int D, int bkv, bool causal, int out,
                             float c2, float logR, hipStream_t st);
@@ -44,8 +48,12 @@ int check_shape(int B, int H, int N, int D, unsigned fmt) {
   if ((long long)B * H > (1LL << 30)) return SAGE_ERR_INVALID_ARG;
   if (N > (1 << 30) - 128) return SAGE_ERR_INVALID_ARG;
   if ((long long)B * H * (long long)pad128(N) * D > kMaxElems) return SAGE_ERR_INVALID_ARG;
-  if (fmt & SAGE_SMOOTH_Q) return SAGE_ERR_UNSUPPORTED;
   return SAGE_OK;
+}
+
+// smoothing Q in the attention: the MXFP4 kernel only
+inline bool smooth_q_supported(unsigned fmt) {
+  return !(fmt & SAGE_SMOOTH_Q) || fmt_of(fmt) == SAGE_FMT_MXFP4;
 }
 
 void sizes(int role, int B, int H, int N, int D, unsigned fmt, size_t* cb, size_t* sb) {
@@ -67,7 +75,7 @@ size_t kmean_ws_bytes(int B, int H, int N, int D) {
 }
 
 struct AttnWs {
-  size_t qc, qs, kc, ks, vc, vs, mu, part, total;
+  size_t qc, qs, kc, ks, vc, vs, mu, part, qbar, bias, total;
 };
 
 AttnWs attn_ws_layout(int B, int H, int N, int D, unsigned fmt) {
@@ -81,6 +89,9 @@ AttnWs attn_ws_layout(int B, int H, int N, int D, unsigned fmt) {
   w.vc = off; off += up256(c); w.vs = off; off += up256(s);
   w.mu = off; off += up256((size_t)B * H * D * sizeof(float));
   w.part = off; off += up256(kmean_ws_bytes(B, H, N, D));
+  const size_t nqb = (fmt & SAGE_SMOOTH_Q) ? (size_t)sage::qmean_blocks(N) : 0;
+  w.qbar = off; off += up256((size_t)B * H * nqb * D * sizeof(float));
+  w.bias = off; off += up256((size_t)B * H * nqb * pad128(N) * sizeof(float));
   w.total = off;
   return w;
 }
@@ -93,7 +104,12 @@ int quant_impl(const void* x, int role, int B, int H, int N, int D, unsigned fmt
   const int BH = B * H, f = fmt_of(fmt);
   hipError_t e = hipSuccess;
   if (role == SAGE_ROLE_Q) {
-    e = sage::launch_quant_rows(x, nullptr, codes, scales, BH, N, N, D, f, false, bf16, st);
+    const bool smooth = (fmt & SAGE_SMOOTH_Q) != 0;     // kmean receives the block means
+    if (smooth) {
+      e = sage::launch_qmean(x, kmean, BH, N, D, bf16, st);
+      if (e != hipSuccess) return SAGE_ERR_HIP;
+    }
+    e = sage::launch_quant_rows(x, smooth ? kmean : nullptr, codes, scales, BH, N, N, D, f, false, bf16, st);
   } else if (role == SAGE_ROLE_K) {
     const bool smooth = !(fmt & SAGE_NO_SMOOTH_K);
     if (smooth) {
@@ -123,13 +139,14 @@ inline float log2_of_2688() { return (float)std::log2(448.0 * 6.0); }
 inline int out_kind(unsigned fmt) { return (fmt & SAGE_OUT_F32) ? 0 : ((fmt & SAGE_IN_BF16) ? 1 : 2); }
 
 int attn_prequant_impl(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc, const void* vs,
-                       void* o, int B, int H, int N, int D, int causal, unsigned fmt, hipStream_t st) {
+                       const float* qkb, void* o, int B, int H, int N, int D, int causal, unsigned fmt,
+                       hipStream_t st) {
   const int bkv = (fmt & SAGE_BKV64) ? 64 : 128;
   if (fmt_of(fmt) == SAGE_FMT_NV16_E4M3)
     return hip_status(sage::launch_attn_nv16(qc, qs, kc, ks, vc, vs, o, B * H, N, pad128(N), D, bkv, causal != 0,
                                              out_kind(fmt), softmax_c2(D), log2_of_2688(), st));
-  return hip_status(sage::launch_attn_fp4_mx(qc, qs, kc, ks, vc, vs, o, B * H, N, pad128(N), D, bkv, causal != 0,
-                                             out_kind(fmt), softmax_c2(D), log2_of_6(), st));
+  return hip_status(sage::launch_attn_fp4_mx(qc, qs, kc, ks, vc, vs, qkb, o, B * H, N, pad128(N), D, bkv,
+                                             causal != 0, out_kind(fmt), softmax_c2(D), log2_of_6(), st));
 }
 
 int attn_ws_impl(const void* q, const void* k, const void* v, void* o, int B, int H, int N, int D, int causal,
@@ -137,12 +154,18 @@ int attn_ws_impl(const void* q, const void* k, const void* v, void* o, int B, in
   const AttnWs w = attn_ws_layout(B, H, N, D, fmt);
   uint8_t* base = static_cast<uint8_t*>(ws);
   float* mu = reinterpret_cast<float*>(base + w.mu);
-  int rc = quant_impl(q, SAGE_ROLE_Q, B, H, N, D, fmt, base + w.qc, base + w.qs, nullptr, nullptr, st);
+  const bool smooth_q = (fmt & SAGE_SMOOTH_Q) != 0, smooth_k = !(fmt & SAGE_NO_SMOOTH_K);
+  float* qbar = smooth_q ? reinterpret_cast<float*>(base + w.qbar) : nullptr;
+  float* bias = smooth_q ? reinterpret_cast<float*>(base + w.bias) : nullptr;
+  int rc = quant_impl(q, SAGE_ROLE_Q, B, H, N, D, fmt, base + w.qc, base + w.qs, qbar, nullptr, st);
   if (rc == SAGE_OK) rc = quant_impl(k, SAGE_ROLE_K, B, H, N, D, fmt, base + w.kc, base + w.ks, mu, base + w.part, st);
   if (rc == SAGE_OK) rc = quant_impl(v, SAGE_ROLE_V, B, H, N, D, fmt, base + w.vc, base + w.vs, nullptr, nullptr, st);
+  if (rc == SAGE_OK && smooth_q)   // GEMV(qbar_i, K'^T) of every query block, over K' = K - mean(K)
+    rc = hip_status(sage::launch_qk_bias(k, smooth_k ? mu : nullptr, qbar, bias, B * H, N, pad128(N), D,
+                                         (fmt & SAGE_IN_BF16) != 0, st));
   if (rc == SAGE_OK)
-    rc = attn_prequant_impl(base + w.qc, base + w.qs, base + w.kc, base + w.ks, base + w.vc, base + w.vs, o, B, H, N, D,
-                            causal, fmt, st);
+    rc = attn_prequant_impl(base + w.qc, base + w.qs, base + w.kc, base + w.ks, base + w.vc, base + w.vs, bias, o, B,
+                            H, N, D, causal, fmt, st);
   return rc;
 }
 
@@ -172,9 +195,12 @@ int sage_quant_fp4(const void* x, int role, int B, int H, int N, int D, unsigned
   if (!x || !codes || !scales) return SAGE_ERR_INVALID_ARG;
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4)) return SAGE_ERR_INVALID_ARG;
   const bool smooth = role == SAGE_ROLE_K && !(fmt & SAGE_NO_SMOOTH_K);
+  const bool smooth_q = role == SAGE_ROLE_Q && (fmt & SAGE_SMOOTH_Q);
   if (smooth) {
     if (!kmean || !aligned(kmean, 4) || !workspace || !aligned(workspace, 8)) return SAGE_ERR_INVALID_ARG;
     if (workspace_bytes < kmean_ws_bytes(B, H, N, D)) return SAGE_ERR_WORKSPACE;
+  } else if (smooth_q) {
+    if (!kmean || !aligned(kmean, 4)) return SAGE_ERR_INVALID_ARG;
   } else if (kmean) {
     return SAGE_ERR_INVALID_ARG;
   }
@@ -182,7 +208,7 @@ int sage_quant_fp4(const void* x, int role, int B, int H, int N, int D, unsigned
 }
 
 size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt) {
-  if (check_shape(B, H, N, D, fmt) != SAGE_OK) return 0;
+  if (check_shape(B, H, N, D, fmt) != SAGE_OK || !smooth_q_supported(fmt)) return 0;
   return attn_ws_layout(B, H, N, D, fmt).total;
 }
 
@@ -190,6 +216,7 @@ int sage_attn_fp4_fwd_ws(const void* q, const void* k, const void* v, void* o, i
                          unsigned fmt, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   int rc = attn_args(q, k, v, o, B, H, N, D, causal, fmt);
   if (rc != SAGE_OK) return rc;
+  if (!smooth_q_supported(fmt)) return SAGE_ERR_UNSUPPORTED;
   if (!workspace || !aligned(workspace, 256)) return SAGE_ERR_INVALID_ARG;
   if (workspace_bytes < attn_ws_layout(B, H, N, D, fmt).total) return SAGE_ERR_WORKSPACE;
   return attn_ws_impl(q, k, v, o, B, H, N, D, causal, fmt, workspace, stream);
@@ -199,6 +226,7 @@ int sage_attn_fp4_fwd(const void* q, const void* k, const void* v, void* o, int 
                       unsigned fmt, hipStream_t stream) {
   int rc = attn_args(q, k, v, o, B, H, N, D, causal, fmt);
   if (rc != SAGE_OK) return rc;
+  if (!smooth_q_supported(fmt)) return SAGE_ERR_UNSUPPORTED;
   const size_t bytes = attn_ws_layout(B, H, N, D, fmt).total;
   void* ws = nullptr;
   if (hipMallocAsync(&ws, bytes, stream) != hipSuccess) return SAGE_ERR_HIP;
@@ -216,8 +244,9 @@ int sage_attn_fp4_fwd_prequant(const void* q_codes, const void* q_scales, const 
   if (!aligned(q_codes, 16) || !aligned(k_codes, 16) || !aligned(vt_codes, 16) || !aligned(o, 16)) return SAGE_ERR_INVALID_ARG;
   if (!aligned(q_scales, 4) || !aligned(k_scales, 4) || !aligned(vt_scales, 4)) return SAGE_ERR_INVALID_ARG;
   if (causal != 0 && causal != 1) return SAGE_ERR_INVALID_ARG;
-  return attn_prequant_impl(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, o, B, H, N, D, causal, fmt,
-                            stream);
+  if (fmt & SAGE_SMOOTH_Q) return SAGE_ERR_UNSUPPORTED;   // the GEMV bias is not an input of this entry point
+  return attn_prequant_impl(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, nullptr, o, B, H, N, D, causal,
+                            fmt, stream);
 }
 
 int sage_attn_bf16_fwd(const void* q, const void* k, const void* v, void* o, int B, int H, int N, int D, int causal,

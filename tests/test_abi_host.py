@@ -56,7 +56,23 @@ def test_attn_invalid_args_rejected_on_host(L, bad):
 
 
 def test_attn_unsupported(L):
-    assert _attn(L, fmt=bd.SAGE_SMOOTH_Q) == bd.SAGE_ERR_UNSUPPORTED
+    # smoothing Q runs in the MXFP4 kernel only, and needs the GEMV bias that prequantized inputs lack
+    assert _attn(L, fmt=bd.SAGE_FMT_NV16_E4M3 | bd.SAGE_SMOOTH_Q) == bd.SAGE_ERR_UNSUPPORTED
+    assert L.sage_attn_fp4_fwd_prequant(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 128, 0,
+                                        bd.SAGE_SMOOTH_Q, None) == bd.SAGE_ERR_UNSUPPORTED
+    assert L.sage_attn_fp4_workspace_size(1, 1, 128, 128, bd.SAGE_FMT_NV16_E4M3 | bd.SAGE_SMOOTH_Q) == 0
+
+
+def test_smooth_q_workspace_and_quant_arguments(L):
+    B, H, N, D = 2, 3, 300, 128
+    nqb, Np = 3, 384
+    extra = L.sage_attn_fp4_workspace_size(B, H, N, D, bd.SAGE_SMOOTH_Q) - L.sage_attn_fp4_workspace_size(B, H, N, D, 0)
+    # block means [B,H,nqb,D] and the GEMV bias [B,H,nqb,Np], each rounded up to 256 bytes
+    assert extra >= B * H * nqb * (D + Np) * 4 and extra < B * H * nqb * (D + Np) * 4 + 512
+    # role Q with smoothing Q needs the mean output; role Q without it must not get one
+    assert L.sage_quant_fp4(FAKE, 0, 1, 1, 128, 128, bd.SAGE_SMOOTH_Q, FAKE, FAKE, None, None, 0,
+                            None) == bd.SAGE_ERR_INVALID_ARG
+    assert L.sage_quant_fp4(FAKE, 0, 1, 1, 128, 128, 0, FAKE, FAKE, FAKE, None, 0, None) == bd.SAGE_ERR_INVALID_ARG
 
 
 def test_quant_sizes_and_validation(L):
