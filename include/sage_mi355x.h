@@ -41,7 +41,7 @@ typedef enum {
 #define SAGE_IN_BF16        0x4u
 #define SAGE_OUT_F32        0x8u  /* o is fp32; otherwise o has the input dtype           */
 #define SAGE_NO_SMOOTH_K    0x10u /* ablation: skip K <- K - mean(K) (Algorithm 1)         */
-#define SAGE_SMOOTH_Q       0x20u /* smoothing Q (Algorithm 1), see below; MXFP4 attention  */
+#define SAGE_SMOOTH_Q       0x20u /* smoothing Q (Algorithm 1), see below                   */
 #define SAGE_BKV64          0x40u /* KV tile of 64 tokens instead of 128                   */
 #define SAGE_FMT_ALL_BITS   0x7Fu
 
@@ -110,8 +110,8 @@ int sage_quant_fp4(const void* x, int role, int B, int H, int N, int D, unsigned
 
 /* Workspace bytes for sage_attn_fp4_fwd_ws (quantized Q, K, V, the mean and
  * its partial sums; with SAGE_SMOOTH_Q also the query-block means and the
- * GEMV term, B*H*ceil(N/128)*(D + Np)*4 bytes).  0 for invalid or unsupported
- * arguments.  Host only. */
+ * GEMV term, B*H*ceil(N/128)*(D + Np)*4 bytes).  0 for invalid arguments.
+ * Host only. */
 size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt);
 
 /*
@@ -125,7 +125,7 @@ size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt);
  * granularity the MFMA cannot take) dequantizes exactly to bf16 and runs on
  * bf16 MFMA.
  * With SAGE_SMOOTH_Q the scores get the smoothing-Q GEMV term described above
- * (MXFP4 only: SAGE_ERR_UNSUPPORTED with SAGE_FMT_NV16_E4M3).
+ * (both formats).
  * Softmax scale is 1/sqrt(D).  causal = 1 keeps key j for query i iff j <= i.
  *  q, k, v  : 16-bit [B,H,N,D], 16-byte aligned
  *  o        : [B,H,N,D] fp32 (SAGE_OUT_F32) or input dtype, 16-byte aligned

@@ -93,17 +93,21 @@ struct Nv16Stage {
   }
 };
 
-template <int D, int BKV, bool CAUSAL, int OUT>   // OUT: 0 = fp32, 1 = bf16, 2 = fp16
+// OUT: 0 = fp32, 1 = bf16, 2 = fp16.  SQ: smoothing Q -- S += qkb[bh, query
+// block, key] (Algorithm 1's GEMV of the block mean with K'; one row of Np
+// floats per 128-query block, this workgroup's query tile).
+template <int D, int BKV, bool CAUSAL, int OUT, bool SQ>
 __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
     const uint8_t* __restrict__ qc, const uint8_t* __restrict__ qs, const uint8_t* __restrict__ kc,
     const uint8_t* __restrict__ ks, const uint8_t* __restrict__ vc, const uint8_t* __restrict__ vs,
-    void* __restrict__ o, int BH, int N, int Np, int nqt, float c2, float logR) {
+    const float* __restrict__ qkb, void* __restrict__ o, int BH, int N, int Np, int nqt, float c2, float logR) {
   using T = Bf16TileT<D, BKV>;
   constexpr int NSUB = BKV / 32;   // 32-key subtiles = P blocks per lane
   constexpr int NKS = D / 16;      // QK K-steps
   constexpr int NPK = BKV / 16;    // PV K-steps
   constexpr int NDB = D / 32;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2][T::BYTES];
+  constexpr int BIAS_OFF = T::BYTES, LBYTES = T::BYTES + (SQ ? BKV * 4 : 0);   // bias of the tile's keys
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2][LBYTES];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 31, hi = lane >> 5;
 
@@ -150,8 +154,19 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   float m = -INFINITY, mc_old = -INFINITY, f_old = 0.0f, lsum_acc = 0.0f;
 
   Nv16Stage<D, BKV> stg;
+  // smoothing Q: threads tid < BKV/4 stage 4 bias entries of the next tile
+  const float* brow = SQ ? qkb + ((size_t)bh * nqt + qt) * Np : nullptr;
+  v4f bst = v4f{0.f, 0.f, 0.f, 0.f};
+  auto bias_load = [&](int kb) {
+    if (SQ && tid < BKV / 4) bst = *reinterpret_cast<const v4f*>(brow + kb + 4 * tid);
+  };
+  auto bias_store = [&](uint8_t* L) {
+    if (SQ && tid < BKV / 4) *reinterpret_cast<v4f*>(L + BIAS_OFF + 16 * tid) = bst;
+  };
   stg.load(kc, ks, vc, vs, bh, Np, 0, tid);
+  bias_load(0);
   stg.store(lds[0], tid);
+  bias_store(lds[0]);
   __syncthreads();
 
   auto tile = [&](auto BUF_, int j) {
@@ -159,7 +174,10 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
     const uint8_t* L = lds[buf];
     const int kb = j * BKV;
     const bool more = j + 1 < ntiles;
-    if (more) stg.load(kc, ks, vc, vs, bh, Np, kb + BKV, tid);
+    if (more) {
+      stg.load(kc, ks, vc, vs, bh, Np, kb + BKV, tid);
+      bias_load(kb + BKV);
+    }
     if (!CAUSAL || kb <= qw + 31) {
       v16f sacc[NSUB];
 #pragma unroll
@@ -173,13 +191,30 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
         }
         sacc[t] = acc;
       }
+      if constexpr (SQ) {
+        // S = fl32(S + bias); element (t, v) is key kb + 32 t + 16 hi + v
+#pragma unroll
+        for (int t = 0; t < NSUB; ++t) {
+          const float* bp = reinterpret_cast<const float*>(L + BIAS_OFF) + 32 * t + 16 * hi;
+#pragma unroll
+          for (int w4 = 0; w4 < 4; ++w4) {
+            const v4f b = *reinterpret_cast<const v4f*>(bp + 4 * w4);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sacc[t][4 * w4 + r] = sacc[t][4 * w4 + r] + b[r];
+          }
+        }
+      }
       if ((kb + BKV > N) || (CAUSAL && kb + BKV - 1 > qw)) {
+        // element (t, v) is key kb + 16 hi + c with c = 32 t + v, kept iff c < rem; the
+        // sign bit of c - rem turns -inf into the bound +inf for kept keys (bit
+        // arithmetic, so no per-element lane masks are formed)
+        const int rem = (CAUSAL ? min(N, qi + 1) : N) - kb - 16 * hi;
 #pragma unroll
         for (int t = 0; t < NSUB; ++t)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            const int key = kb + 32 * t + 16 * hi + v;
-            if (!(key < N && (!CAUSAL || key <= qi))) sacc[t][v] = -INFINITY;
+            const float bound = __uint_as_float(0xFF800000u ^ ((uint32_t)(32 * t + v - rem) & 0x80000000u));
+            sacc[t][v] = __builtin_fminf(sacc[t][v], bound);
           }
       }
       float bm[NSUB];
@@ -248,7 +283,10 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
       mc_old = mc;
       f_old = f;
     }
-    if (more) stg.store(lds[buf ^ 1], tid);
+    if (more) {
+      stg.store(lds[buf ^ 1], tid);
+      bias_store(lds[buf ^ 1]);
+    }
     __syncthreads();
   };
   for (int j = 0; j < ntiles; j += 2) {
@@ -280,30 +318,41 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   }
 }
 
-template <int D, int BKV, bool CAUSAL, int OUT>
+template <int D, int BKV, bool CAUSAL, int OUT, bool SQ>
 static hipError_t launch_nv16_t(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                                const void* vs, void* o, int BH, int N, int Np, float c2, float logR, hipStream_t st) {
+                                const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2, float logR,
+                                hipStream_t st) {
   const int nqt = (N + NQ - 1) / NQ;
-  hipLaunchKernelGGL((attn_nv16_kernel<D, BKV, CAUSAL, OUT>), dim3((unsigned)(nqt * BH)), dim3(256), 0, st,
+  hipLaunchKernelGGL((attn_nv16_kernel<D, BKV, CAUSAL, OUT, SQ>), dim3((unsigned)(nqt * BH)), dim3(256), 0, st,
                      (const uint8_t*)qc, (const uint8_t*)qs, (const uint8_t*)kc, (const uint8_t*)ks, (const uint8_t*)vc,
-                     (const uint8_t*)vs, o, BH, N, Np, nqt, c2, logR);
+                     (const uint8_t*)vs, qkb, o, BH, N, Np, nqt, c2, logR);
   return hipGetLastError();
 }
 
-template <int D, int BKV, bool CAUSAL>
+template <int D, int BKV, bool CAUSAL, bool SQ>
 static hipError_t launch_nv16_o(int out, const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                                const void* vs, void* o, int BH, int N, int Np, float c2, float logR, hipStream_t st) {
-  if (out == 0) return launch_nv16_t<D, BKV, CAUSAL, 0>(qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, logR, st);
-  if (out == 1) return launch_nv16_t<D, BKV, CAUSAL, 1>(qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, logR, st);
-  return launch_nv16_t<D, BKV, CAUSAL, 2>(qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, logR, st);
+                                const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2, float logR,
+                                hipStream_t st) {
+  if (out == 0) return launch_nv16_t<D, BKV, CAUSAL, 0, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st);
+  if (out == 1) return launch_nv16_t<D, BKV, CAUSAL, 1, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st);
+  return launch_nv16_t<D, BKV, CAUSAL, 2, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st);
 }
 
+template <int D, int BKV, bool CAUSAL>
+static hipError_t launch_nv16_s(int out, const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
+                                const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2, float logR,
+                                hipStream_t st) {
+  return qkb ? launch_nv16_o<D, BKV, CAUSAL, true>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st)
+             : launch_nv16_o<D, BKV, CAUSAL, false>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st);
+}
+
+// qkb: smoothing-Q bias [BH, ceil(N/128), Np] fp32, or null without smoothing Q.
 hipError_t launch_attn_nv16(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                            const void* vs, void* o, int BH, int N, int Np, int D, int bkv, bool causal, int out,
-                            float c2, float logR, hipStream_t st) {
-#define SAGE_N(DD, BB)                                                                                 \
-  return causal ? launch_nv16_o<DD, BB, true>(out, qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, logR, st) \
-                : launch_nv16_o<DD, BB, false>(out, qc, qs, kc, ks, vc, vs, o, BH, N, Np, c2, logR, st)
+                            const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
+                            bool causal, int out, float c2, float logR, hipStream_t st) {
+#define SAGE_N(DD, BB)                                                                                      \
+  return causal ? launch_nv16_s<DD, BB, true>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st) \
+                : launch_nv16_s<DD, BB, false>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st)
   if (D == 128) { if (bkv == 128) { SAGE_N(128, 128); } else { SAGE_N(128, 64); } }
   else { if (bkv == 128) { SAGE_N(64, 128); } else { SAGE_N(64, 64); } }
 #undef SAGE_N

@@ -22,8 +22,8 @@ hipError_t launch_attn_fp4_mx(const void* qc, const void* qs, const void* kc, co
                               const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
                               bool causal, int out, float c2, float log6, hipStream_t st);
 hipError_t launch_attn_nv16(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                            const void* vs, void* o, int BH, int N, int Np, int D, int bkv, bool causal, int out,
-                            float c2, float logR, hipStream_t st);
+                            const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
+                            bool causal, int out, float c2, float logR, hipStream_t st);
 hipError_t launch_attn_bf16(const void* q, const void* k, const void* vt, void* o, int BH, int N, int Np, int D,
                             bool causal, bool out_f32, float c2, hipStream_t st);
 hipError_t launch_transpose_v_bf16(const void* v, void* vt, int BH, int N, int Np, int D, hipStream_t st);
@@ -51,10 +51,8 @@ int check_shape(int B, int H, int N, int D, unsigned fmt) {
   return SAGE_OK;
 }
 
-// smoothing Q in the attention: the MXFP4 kernel only
-inline bool smooth_q_supported(unsigned fmt) {
-  return !(fmt & SAGE_SMOOTH_Q) || fmt_of(fmt) == SAGE_FMT_MXFP4;
-}
+// smoothing Q in the attention: both formats
+inline bool smooth_q_supported(unsigned) { return true; }
 
 void sizes(int role, int B, int H, int N, int D, unsigned fmt, size_t* cb, size_t* sb) {
   const size_t BH = (size_t)B * H;
@@ -143,8 +141,8 @@ int attn_prequant_impl(const void* qc, const void* qs, const void* kc, const voi
                        hipStream_t st) {
   const int bkv = (fmt & SAGE_BKV64) ? 64 : 128;
   if (fmt_of(fmt) == SAGE_FMT_NV16_E4M3)
-    return hip_status(sage::launch_attn_nv16(qc, qs, kc, ks, vc, vs, o, B * H, N, pad128(N), D, bkv, causal != 0,
-                                             out_kind(fmt), softmax_c2(D), log2_of_2688(), st));
+    return hip_status(sage::launch_attn_nv16(qc, qs, kc, ks, vc, vs, qkb, o, B * H, N, pad128(N), D, bkv,
+                                             causal != 0, out_kind(fmt), softmax_c2(D), log2_of_2688(), st));
   return hip_status(sage::launch_attn_fp4_mx(qc, qs, kc, ks, vc, vs, qkb, o, B * H, N, pad128(N), D, bkv,
                                              causal != 0, out_kind(fmt), softmax_c2(D), log2_of_6(), st));
 }

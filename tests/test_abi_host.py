@@ -56,11 +56,10 @@ def test_attn_invalid_args_rejected_on_host(L, bad):
 
 
 def test_attn_unsupported(L):
-    # smoothing Q runs in the MXFP4 kernel only, and needs the GEMV bias that prequantized inputs lack
-    assert _attn(L, fmt=bd.SAGE_FMT_NV16_E4M3 | bd.SAGE_SMOOTH_Q) == bd.SAGE_ERR_UNSUPPORTED
-    assert L.sage_attn_fp4_fwd_prequant(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 128, 0,
-                                        bd.SAGE_SMOOTH_Q, None) == bd.SAGE_ERR_UNSUPPORTED
-    assert L.sage_attn_fp4_workspace_size(1, 1, 128, 128, bd.SAGE_FMT_NV16_E4M3 | bd.SAGE_SMOOTH_Q) == 0
+    # smoothing Q needs the GEMV term, which prequantized inputs lack
+    for f in (0, bd.SAGE_FMT_NV16_E4M3):
+        assert L.sage_attn_fp4_fwd_prequant(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 128, 0,
+                                            f | bd.SAGE_SMOOTH_Q, None) == bd.SAGE_ERR_UNSUPPORTED
 
 
 def test_smooth_q_workspace_and_quant_arguments(L):

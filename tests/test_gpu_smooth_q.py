@@ -1,7 +1,8 @@
 """GPU parity of smoothing Q (Algorithm 1: phi(Q_i - mean(Q_i)) over blocks of
 128 query rows, plus GEMV(mean(Q_i), K'^T) added to the scores) against the
-oracle: bit-exact codes, scales and block means; attention within the same bar
-as without smoothing (2e-3 + the oracle's per-row tie bound)."""
+oracle, in both formats: bit-exact codes, scales and block means; attention
+within the same bar as without smoothing (2e-3 + the oracle's per-row tie
+bound)."""
 import numpy as np
 import pytest
 
@@ -42,24 +43,25 @@ def test_quant_q_smooth_bit_exact(fmt, shape, in_dtype):
     assert int((c != oc).sum()) == 0 and int((s != os_).sum()) == 0
 
 
-def gpu_attn_sq(q, k, v, in_dtype, causal, bkv, extra=0):
+def gpu_attn_sq(q, k, v, in_dtype, causal, bkv, extra=0, fmt=0):
     torch = torch_dev()
-    f = bd.SAGE_FMT_MXFP4 | bd.SAGE_SMOOTH_Q | extra | (bd.SAGE_BKV64 if bkv == 64 else 0)
+    f = fmt | bd.SAGE_SMOOTH_Q | extra | (bd.SAGE_BKV64 if bkv == 64 else 0)
     o = bd.sage_attn_fp4_fwd(to_dev(q, in_dtype), to_dev(k, in_dtype), to_dev(v, in_dtype), causal=causal, fmt=f)
     torch.cuda.synchronize()
     return o
 
 
+@pytest.mark.parametrize("fmt", [0, 1])
 @pytest.mark.parametrize("N", [1, 64, 100, 257, 640])
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("bkv", [64, 128])
-def test_attn_smooth_q_edge_shapes(N, D, causal, bkv):
-    say("attn smooth-Q edge N=%d D=%d causal=%d bkv=%d" % (N, D, causal, bkv))
+def test_attn_smooth_q_edge_shapes(fmt, N, D, causal, bkv):
+    say("attn smooth-Q edge fmt=%d N=%d D=%d causal=%d bkv=%d" % (fmt, N, D, causal, bkv))
     in_dtype = 1 if (N + D) % 2 else 0
     q, k, v = q_bias_inputs(1, 2, N, D, in_dtype, seed=500 + N)
-    o = gpu_attn_sq(q, k, v, in_dtype, causal, bkv)
-    ref, tie, _ = oracle.attn(q, k, v, in_dtype, causal, oracle.FMT_MX, bkv, flags=oracle.SMOOTH_Q)
+    o = gpu_attn_sq(q, k, v, in_dtype, causal, bkv, fmt=fmt)
+    ref, tie, _ = oracle.attn(q, k, v, in_dtype, causal, fmt, bkv, flags=oracle.SMOOTH_Q)
     check(o.cpu().numpy().reshape(-1, D), ref, tie, "smooth-Q edge")
 
 
@@ -70,18 +72,19 @@ def test_attn_smooth_q_without_smoothing_k():
     check(o.cpu().numpy().reshape(-1, 128), ref, tie, "smooth-Q, no smooth-K")
 
 
-@pytest.mark.parametrize("ci", [1, 3])
-def test_attn_smooth_q_full_size_sampled_rows(ci):
-    """Full-size workloads (non-causal and causal) with smoothing Q; the oracle
-    computes a seeded sample of rows."""
+@pytest.mark.parametrize("ci,fmt", [(1, 0), (3, 0), (4, 1)])
+def test_attn_smooth_q_full_size_sampled_rows(ci, fmt):
+    """Full-size workloads (non-causal, causal, and the D=64 long sequence in the
+    16-element E4M3 format) with smoothing Q; the oracle computes a seeded
+    sample of rows."""
     w = wl.CONFIGS[ci]
-    say("attn smooth-Q config", ci, w.name)
+    say("attn smooth-Q config", ci, w.name, "fmt", fmt)
     q, k, v = wl.generate(w)
-    o = gpu_attn_sq(q, k, v, w.in_dtype, w.causal, w.bkv)
+    o = gpu_attn_sq(q, k, v, w.in_dtype, w.causal, w.bkv, fmt=fmt)
     BH = w.B * w.H
     heads = sorted({0, BH - 1} | set(np.random.default_rng(ci + 50).choice(BH, min(BH, 4), replace=False).tolist()))
     rows = wl.sample_rows(w, per_head_tiles=3, tile=128, rows_per_tile=8, heads=heads, seed=ci + 50)
-    ref, tie, cnt = oracle.attn(q, k, v, w.in_dtype, w.causal, oracle.FMT_MX, w.bkv, rows=rows, flags=oracle.SMOOTH_Q)
+    ref, tie, cnt = oracle.attn(q, k, v, w.in_dtype, w.causal, fmt, w.bkv, rows=rows, flags=oracle.SMOOTH_Q)
     got = o_rows(o, rows, w.D)
     check(got, ref, tie, w.name + " smooth-Q")
     ex = oracle.exact_attn(q, k, v, w.in_dtype, w.causal, rows=rows)
@@ -105,8 +108,13 @@ def test_attn_smooth_q_raises_accuracy_on_q_bias():
     assert a["l1"] < b["l1"] and a["cossim"] > b["cossim"]
 
 
-def test_attn_smooth_q_nv16_is_unsupported():
+def test_attn_smooth_q_prequant_is_unsupported():
+    torch = torch_dev()
     q, k, v = q_bias_inputs(1, 1, 128, 64, 1, seed=530)
+    qq = bd.sage_quant_fp4(to_dev(q, 1), bd.SAGE_ROLE_Q, bd.SAGE_SMOOTH_Q)
+    kq = bd.sage_quant_fp4(to_dev(k, 1), bd.SAGE_ROLE_K)
+    vq = bd.sage_quant_fp4(to_dev(v, 1), bd.SAGE_ROLE_V)
+    torch.cuda.synchronize()
     with pytest.raises(bd.SageError) as ex:
-        bd.sage_attn_fp4_fwd(to_dev(q, 1), to_dev(k, 1), to_dev(v, 1), fmt=bd.SAGE_FMT_NV16_E4M3 | bd.SAGE_SMOOTH_Q)
+        bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (1, 1, 128, 64), fmt=bd.SAGE_SMOOTH_Q)
     assert ex.value.status == bd.SAGE_ERR_UNSUPPORTED
