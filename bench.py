@@ -292,7 +292,26 @@ def main():
             log("bf16 kernel unavailable:", ex)
 
     others = None
+    smooth_q = None
     if not args.no_configs:
+        # the same step with smoothing Q (query-block means, their GEMV with K', the bias added to S)
+        fmt_sq = bd.SAGE_FMT_MXFP4 | bd.SAGE_SMOOTH_Q
+        ws_sq = torch.empty(bd.attn_fp4_workspace_size(B, H, N, D, fmt_sq | bd.SAGE_IN_BF16 | bd.SAGE_OUT_F32),
+                            dtype=torch.uint8, device=dev)
+        step_sq = lambda: bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=fmt_sq, out_f32=True, out=o,
+                                               workspace=ws_sq)
+        step_sq()
+        torch.cuda.synchronize()
+        n_sq = max(3, min(args.steps, 10))
+        e0.record()
+        for _ in range(n_sq):
+            step_sq()
+        e1.record()
+        torch.cuda.synchronize()
+        t_sq = e0.elapsed_time(e1) / 1e3 / n_sq
+        smooth_q = {"step_ms": t_sq * 1e3, "tops": ops / t_sq / 1e12}
+        log("step with smoothing Q %.3f ms = %.1f TOPS" % (t_sq * 1e3, ops / t_sq / 1e12))
+        del ws_sq
         others = other_configs(torch, bd, wl, args.steps)
 
     cpu = None
@@ -322,6 +341,7 @@ def main():
         "quantize": {"ms": t_quant * 1e3, "algorithmic_GBs": quant_bytes / t_quant / 1e9,
                      "frac_of_hbm_peak": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS},
         "bf16_kernel": bf16,
+        "smooth_q_step": smooth_q,
         "other_configs": others,
         "cpu_baseline": cpu,
     }
