@@ -133,6 +133,29 @@ def issue_rates(torch):
                       "cycles_per_iteration": res, "derived": summary}), flush=True)
 
 
+def accuracy_vs_exact(torch, q, k, v, o, w, nrows=512, seed=7):
+    """CosSim, relative L1 and RMSE of the FP4 output against fp64 softmax(QK^T/sqrt(D))V
+    (the paper's accuracy metrics), on a seeded sample of query rows of every head; the
+    reference is plain torch fp64 on the GPU."""
+    B, H, N, D = w.B, w.H, w.N, w.D
+    g = torch.Generator().manual_seed(seed)
+    rows = torch.randint(0, N, (nrows,), generator=g).to(q.device)
+    ref, got = [], []
+    for bh in range(B * H):
+        b, h = divmod(bh, H)
+        qs = q[b, h].index_select(0, rows).double()
+        s = (qs @ k[b, h].double().T) / float(np.sqrt(D))
+        if w.causal:
+            s = s.masked_fill(torch.arange(N, device=q.device)[None, :] > rows[:, None], float("-inf"))
+        ref.append(torch.softmax(s, dim=1) @ v[b, h].double())
+        got.append(o[b, h].index_select(0, rows).double())
+    a, c = torch.cat(ref).flatten(), torch.cat(got).flatten()
+    return {"cossim": float((a * c).sum() / (a.norm() * c.norm())),
+            "l1": float((a - c).abs().sum() / a.abs().sum()),
+            "rmse": float(((a - c) ** 2).mean().sqrt()),
+            "rows": "%d random query rows per head, all %d heads" % (nrows, B * H)}
+
+
 def other_configs(torch, bd, wl, steps):
     """Attention kernel alone (quantized operands resident) on the other workloads: the small
     non-causal D=128 case, the causal case and the D=64 long-sequence case in both formats."""
@@ -243,6 +266,9 @@ def main():
     t_step = (time.perf_counter() - t0) / args.steps
     log("step %.3f ms" % (t_step * 1e3))
 
+    acc = accuracy_vs_exact(torch, qd, kd, vd, o, w)
+    log("accuracy vs exact attention: cossim %.5f, l1 %.4f, rmse %.3g" % (acc["cossim"], acc["l1"], acc["rmse"]))
+
     # the attention kernel alone, timed with HIP events on the launch stream
     qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q)
     kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K)
@@ -338,6 +364,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
                      "frac": attn_tflops / PEAK_FP4_TFLOPS, "traffic": traffic_from_counters(1),
                      "kernel": "attn_fp4_mx_kernel<128,128,false,0>", "kernel_ms": t_attn * 1e3},
+        "accuracy_vs_exact": acc,
         "quantize": {"ms": t_quant * 1e3, "algorithmic_GBs": quant_bytes / t_quant / 1e9,
                      "frac_of_hbm_peak": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS},
         "bf16_kernel": bf16,
