@@ -109,18 +109,24 @@ __global__ __launch_bounds__(KM_THREADS) void qmean_kernel(const uint16_t* __res
 // GEMV of smoothing Q: bias[bh, b, k] = qbar[bh, b, :] . K'[bh, k, :] with
 // K' = fl32(K - mu) (K itself without smoothing K), as a chain of fp32 fused
 // multiply-adds in order of the channel from 0; keys k >= N get 0.  One
-// thread per key keeps K' in registers and runs QBG independent chains (query
-// blocks) at a time; the block means are wave-uniform scalar loads.
+// thread per key keeps K' in registers; the workgroup stages the means of QBG
+// query blocks at a time in LDS as [channel][block] (double-buffered), so a
+// thread reads the QBG values of one channel with two broadcast 16-byte LDS
+// reads and runs QBG independent chains.
 constexpr int QBG = 8;
+constexpr int QB_THREADS = 256;
 
 template <int D, bool BF16>
-__global__ __launch_bounds__(128) void qk_bias_kernel(const uint16_t* __restrict__ k, const float* __restrict__ mu,
-                                                      const float* __restrict__ qbar, float* __restrict__ bias, int N,
-                                                      int Np, int nqb) {
-  const int bh = blockIdx.y;
-  const int key = blockIdx.x * 128 + threadIdx.x;   // < Np: the grid covers Np / 128 blocks exactly
-  float kv[D];
+__global__ __launch_bounds__(QB_THREADS) void qk_bias_kernel(const uint16_t* __restrict__ k, const float* __restrict__ mu,
+                                                             const float* __restrict__ qbar, float* __restrict__ bias,
+                                                             int N, int Np, int nqb) {
+  static_assert(D * QBG == 4 * QB_THREADS || D * QBG == 2 * QB_THREADS, "one or two staged means per thread");
+  constexpr int PER_T = D * QBG / QB_THREADS;      // means staged per thread per group
+  __shared__ __attribute__((aligned(16))) float qs[2][D][QBG];
+  const int bh = blockIdx.y, tid = threadIdx.x;
+  const int key = blockIdx.x * QB_THREADS + tid;   // the grid covers Np (a multiple of 128) rounded up
   const bool valid = key < N;
+  float kv[D];
   if (valid) {
     const uint16_t* kr = k + ((size_t)bh * N + key) * D;
 #pragma unroll
@@ -134,26 +140,48 @@ __global__ __launch_bounds__(128) void qk_bias_kernel(const uint16_t* __restrict
 #pragma unroll
       for (int c = 0; c < D; ++c) kv[c] = kv[c] - mu[(size_t)bh * D + c];
     }
+  } else {
+#pragma unroll
+    for (int c = 0; c < D; ++c) kv[c] = 0.0f;
   }
   const float* qm = qbar + (size_t)bh * nqb * D;
-  float* out = bias + (size_t)bh * nqb * Np + key;
-  int b0 = 0;
-  for (; b0 + QBG <= nqb; b0 += QBG) {   // full groups: QBG independent chains
+  // stage the means of blocks [b0, b0 + QBG) (zero past nqb), transposed to [channel][block]
+  auto stage = [&](int b0, int buf) {
+#pragma unroll
+    for (int e = 0; e < PER_T; ++e) {
+      const int idx = tid * PER_T + e, i = idx / D, c = idx % D;   // block i, channel c
+      qs[buf][c][i] = (b0 + i < nqb) ? qm[(size_t)(b0 + i) * D + c] : 0.0f;
+    }
+  };
+  const int ngroups = (nqb + QBG - 1) / QBG;
+  stage(0, 0);
+  __syncthreads();
+  for (int gi = 0; gi < ngroups; ++gi) {
+    const int b0 = gi * QBG, buf = gi & 1;
+    if (gi + 1 < ngroups) stage(b0 + QBG, buf ^ 1);   // the other buffer was last read before the barrier below
     float acc[QBG];
 #pragma unroll
     for (int i = 0; i < QBG; ++i) acc[i] = 0.0f;
 #pragma unroll
-    for (int c = 0; c < D; ++c)
+    for (int c = 0; c < D; ++c) {
+      const v4f m0 = *reinterpret_cast<const v4f*>(&qs[buf][c][0]);
+      const v4f m1 = *reinterpret_cast<const v4f*>(&qs[buf][c][4]);
 #pragma unroll
-      for (int i = 0; i < QBG; ++i) acc[i] = __builtin_fmaf(qm[(size_t)(b0 + i) * D + c], kv[c], acc[i]);
+      for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(m0[i], kv[c], acc[i]);
 #pragma unroll
-    for (int i = 0; i < QBG; ++i) out[(size_t)(b0 + i) * Np] = valid ? acc[i] : 0.0f;
-  }
-  for (; b0 < nqb; ++b0) {               // the remaining blocks, one chain each
-    float acc = 0.0f;
+      for (int i = 0; i < 4; ++i) acc[4 + i] = __builtin_fmaf(m1[i], kv[c], acc[4 + i]);
+    }
+    // materialize every chain here: otherwise the compiler sinks each chain into
+    // its guarded store below and keeps all the staged means it reads live
 #pragma unroll
-    for (int c = 0; c < D; ++c) acc = __builtin_fmaf(qm[(size_t)b0 * D + c], kv[c], acc);
-    out[(size_t)b0 * Np] = valid ? acc : 0.0f;
+    for (int i = 0; i < QBG; ++i) asm volatile("" : "+v"(acc[i]));
+    if (key < Np) {
+      float* out = bias + ((size_t)bh * nqb + b0) * Np + key;
+#pragma unroll
+      for (int i = 0; i < QBG; ++i)
+        if (b0 + i < nqb) out[(size_t)i * Np] = valid ? acc[i] : 0.0f;
+    }
+    __syncthreads();
   }
 }
 
@@ -403,10 +431,10 @@ hipError_t launch_qmean(const void* q, float* qbar, int BH, int N, int D, bool b
 // bias [BH, nqb, Np] fp32; Np is a multiple of 128
 hipError_t launch_qk_bias(const void* k, const float* mu, const float* qbar, float* bias, int BH, int N, int Np, int D,
                           bool bf16, hipStream_t st) {
-  const dim3 grid((unsigned)(Np / 128), (unsigned)BH);
+  const dim3 grid((unsigned)((Np + QB_THREADS - 1) / QB_THREADS), (unsigned)BH);
   const int nqb = qmean_blocks(N);
-#define SAGE_QB(DD, BB) hipLaunchKernelGGL((qk_bias_kernel<DD, BB>), grid, dim3(128), 0, st, (const uint16_t*)k, mu, \
-                                           qbar, bias, N, Np, nqb)
+#define SAGE_QB(DD, BB) hipLaunchKernelGGL((qk_bias_kernel<DD, BB>), grid, dim3(QB_THREADS), 0, st, (const uint16_t*)k, \
+                                           mu, qbar, bias, N, Np, nqb)
   if (D == 128) { if (bf16) { SAGE_QB(128, true); } else { SAGE_QB(128, false); } }
   else { if (bf16) { SAGE_QB(64, true); } else { SAGE_QB(64, false); } }
 #undef SAGE_QB
