@@ -23,7 +23,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 FMT_MX, FMT_NV16, FMT_NONE = 0, 1, 2
 IN_FP16, IN_BF16 = 0, 1
 ROLE_Q, ROLE_K, ROLE_V = 0, 1, 2
-NO_SMOOTH_K, DIRECT_P, R_LITERAL, SMOOTH_Q = 1, 2, 4, 8
+NO_SMOOTH_K, DIRECT_P, R_LITERAL, SMOOTH_Q, OCP_SCALE = 1, 2, 4, 8, 16
 
 _lib = None
 
@@ -55,12 +55,16 @@ def lib():
         L.orc_e4m3_decode.argtypes = [ctypes.c_uint8]
         L.orc_e8m0_exponent.restype = ctypes.c_int
         L.orc_e8m0_exponent.argtypes = [ctypes.c_float]
+        L.orc_e8m0_exponent_floor.restype = ctypes.c_int
+        L.orc_e8m0_exponent_floor.argtypes = [ctypes.c_float]
         L.orc_e8m0_decode.restype = ctypes.c_float
         L.orc_e8m0_decode.argtypes = [ctypes.c_uint8]
         L.orc_widen.restype = ctypes.c_float
         L.orc_widen.argtypes = [ctypes.c_uint16, ctypes.c_int]
         L.orc_phi_block.restype = ctypes.c_uint8
         L.orc_phi_block.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+        L.orc_phi_block_ex.restype = ctypes.c_uint8
+        L.orc_phi_block_ex.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_uint, ctypes.c_void_p]
         L.orc_kmean.restype = ctypes.c_long
         L.orc_kmean.argtypes = [ctypes.c_void_p, ctypes.c_int] + [ctypes.c_int] * 4 + [ctypes.c_void_p]
         L.orc_quant.restype = ctypes.c_long
@@ -126,6 +130,11 @@ def e8m0_exponent(amax: float) -> int:
     return int(lib().orc_e8m0_exponent(float(amax)))
 
 
+def e8m0_exponent_floor(amax: float) -> int:
+    """The alternative E8M0 rule of the OCP_SCALE ablation: floor(log2 amax) - 2."""
+    return int(lib().orc_e8m0_exponent_floor(float(amax)))
+
+
 def e8m0_decode(b: int) -> float:
     return float(lib().orc_e8m0_decode(int(b)))
 
@@ -134,11 +143,12 @@ def widen(bits: int, in_dtype: int) -> float:
     return float(lib().orc_widen(int(bits), int(in_dtype)))
 
 
-def phi_block(x: np.ndarray, fmt: int):
-    """phi on one block: returns (codes uint8[n], scale byte)."""
+def phi_block(x: np.ndarray, fmt: int, flags: int = 0):
+    """phi on one block: returns (codes uint8[n], scale byte).  flags may hold
+    OCP_SCALE (the floor rule for E8M0 scales)."""
     x = np.ascontiguousarray(x, dtype=np.float32)
     codes = np.zeros(x.size, dtype=np.uint8)
-    sb = lib().orc_phi_block(_ptr(x), x.size, fmt, _ptr(codes))
+    sb = lib().orc_phi_block_ex(_ptr(x), x.size, fmt, flags, _ptr(codes))
     return codes, int(sb)
 
 

@@ -56,6 +56,9 @@
 #define ORC_SMOOTH_Q 8u      /* smoothing Q (Algorithm 1): quantize Q_i - mean(Q_i)
                                 over each block of B_q rows and add the GEMV
                                 mean(Q_i) . K_j^T to S                          */
+#define ORC_OCP_SCALE 16u    /* ablation (MX only): E8M0 block scales by the floor
+                                rule 2^(floor(log2 amax) - 2) for Q, K, V and the
+                                second level of P, values above 6 s clip to 6    */
 
 /* ------------------------------------------------------------------------ */
 /* 16-bit input widening (exact)                                             */
@@ -149,6 +152,21 @@ int orc_e8m0_exponent(float amax) {
 }
 float orc_e8m0_decode(uint8_t b) { return ldexpf(1.0f, (int)b - 127); }
 
+/* The alternative E8M0 rule (ablation ORC_OCP_SCALE): 2^e with e =          */
+/* floor(log2 amax) - 2, the exponent of amax less that of the largest FP4    */
+/* value's binade (6 = 1.5 * 2^2).  Block values in (6, 8) 2^e exceed the FP4 */
+/* range and saturate to 6; in exchange the scale is half the default one    */
+/* for blocks whose max lies in (6, 8) 2^e.  amax = 0 gives -127.             */
+int orc_e8m0_exponent_floor(float amax) {
+  if (!(amax > 0.0f)) return -127;
+  int E;
+  frexp((double)amax, &E);                      /* amax in [2^(E-1), 2^E) */
+  int e = (E - 1) - 2;
+  if (e < -127) e = -127;
+  if (e > 127) e = 127;
+  return e;
+}
+
 /* ------------------------------------------------------------------------ */
 /* phi on one block of n values (Sec. 3.1, Eq. microscaling).                */
 /* codes: n bytes, one code per byte.  Returns the scale byte.               */
@@ -173,6 +191,15 @@ uint8_t orc_phi_block(const float* x, int n, int fmt, uint8_t* codes) {
     for (int k = 0; k < n; ++k) { volatile float y = x[k] * r; codes[k] = orc_e2m1_encode(y); }
     return sb;
   }
+}
+/* phi with the attention flags: ORC_OCP_SCALE selects the floor rule for MX */
+uint8_t orc_phi_block_ex(const float* x, int n, int fmt, unsigned flags, uint8_t* codes) {
+  if (fmt != ORC_FMT_MX || !(flags & ORC_OCP_SCALE)) return orc_phi_block(x, n, fmt, codes);
+  float amax = 0.0f;
+  for (int k = 0; k < n; ++k) { float a = fabsf(x[k]); if (a > amax) amax = a; }
+  int e = orc_e8m0_exponent_floor(amax);
+  for (int k = 0; k < n; ++k) codes[k] = orc_e2m1_encode(ldexpf(x[k], -e));
+  return (uint8_t)(e + 127);
 }
 static float scale_value(uint8_t sb, int fmt) {
   return fmt == ORC_FMT_MX ? orc_e8m0_decode(sb) : orc_e4m3_decode(sb);
@@ -408,7 +435,7 @@ static void build_head(attn_job_t* J, long bh) {
       if (h->kf) h->kf[(long)t * D + c] = kv;
     }
     for (int blk = 0; blk < D / n; ++blk) {
-      uint8_t sb = orc_phi_block(work + blk * n, n, fmt, codes + (long)t * D + blk * n);
+      uint8_t sb = orc_phi_block_ex(work + blk * n, n, fmt, J->flags, codes + (long)t * D + blk * n);
       h->ks[(long)t * (D / n) + blk] = scale_value(sb, fmt);
     }
     for (int c = 0; c < D; ++c) { int c2; two_code(orc_e2m1_decode(codes[(long)t * D + c]), &c2); h->kc2[(long)t * D + c] = (int8_t)c2; }
@@ -425,7 +452,7 @@ static void build_head(attn_job_t* J, long bh) {
         int t = t0 + kk;
         work[kk] = t < N ? orc_widen(vb[(long)t * D + c], J->in_dtype) : 0.0f;
       }
-      uint8_t sb = orc_phi_block(work, n, fmt, cb);
+      uint8_t sb = orc_phi_block_ex(work, n, fmt, J->flags, cb);
       float s = scale_value(sb, fmt);
       h->vs[(long)c * (Np / n) + t0 / n] = s;
       for (int kk = 0; kk < n; ++kk) {
@@ -571,10 +598,10 @@ int orc_p_tile(const float* S, int bkv, float m_old, int D, int fmt, unsigned fl
       for (int kk = b0; kk < b0 + n; ++kk) if (S[kk] > bm) bm = S[kk];
       int e;
       if (bm == -INFINITY) e = -126;
-      else if (direct || (flags & ORC_R_LITERAL)) {
+      else if (direct || (flags & (ORC_R_LITERAL | ORC_OCP_SCALE))) {
         float am = 0.0f;
         for (int kk = b0; kk < b0 + n; ++kk) if (p2[kk] > am) am = p2[kk];
-        e = orc_e8m0_exponent(am);
+        e = (flags & ORC_OCP_SCALE) ? orc_e8m0_exponent_floor(am) : orc_e8m0_exponent(am);
       } else {
         /* blockmax(P~2) = 6 2^{c2 (bm - t)}; smallest e with 6 2^e >= it */
         volatile float dd = bm - t;
@@ -672,7 +699,7 @@ static void attn_row(attn_job_t* J, long bh, int i, float* out, float* tol_out, 
   if (fmt != ORC_FMT_NONE) {
     uint8_t cb[32];
     for (int blk = 0; blk < D / n; ++blk) {
-      uint8_t sb = orc_phi_block(qf + blk * n, n, fmt, cb);
+      uint8_t sb = orc_phi_block_ex(qf + blk * n, n, fmt, J->flags, cb);
       qs[blk] = scale_value(sb, fmt);
       for (int kk = 0; kk < n; ++kk) { int c2; two_code(orc_e2m1_decode(cb[kk]), &c2); qc2[blk * n + kk] = c2; }
     }

@@ -1,0 +1,170 @@
+"""Accuracy ablations of microscaled-FP4 attention on the five synthetic
+workloads, printed as Markdown.
+
+    python tests/ablation_table.py            # oracle only (CPU)
+    python tests/ablation_table.py --gpu      # plus the HIP kernels' own outputs
+
+Each workload is drawn by its seeded generator at its own N and D, with two
+heads (one batch) in place of the full B x H, and a seeded sample of query
+rows per head; every variant is measured against exact fp64 attention on the
+same rows with the paper's metrics (CosSim, relative L1, RMSE over the
+flattened output).  Variants:
+
+- Table 1(a): MXFP4 against NVFP4-style E4M3 scales;
+- Table 1(b): direct against two-level quantization of P~;
+- the smoothing ablation: smoothing K off, smoothing Q on;
+- reading C9: the literal first-level constant 448*6 with E8M0 scales;
+- reading C3: the floor rule for E8M0 scales.
+
+With --gpu the variants the HIP path implements (both formats, smoothing K
+off, smoothing Q on) are also run through the C ABI on the same inputs, and
+their metrics are printed beside the oracle's.
+
+A first table follows Fig. 3: over tiles of exact (smoothed) scores of the
+4096-token workload, the distribution of P~, the range and the number of distinct E4M3
+scale values that direct and two-level quantization use, and the mean error
+of the scales and of the reconstructed P~.
+
+This is a test-side script: it calls the oracle, which the product path never
+does.
+"""
+from __future__ import annotations
+
+import argparse
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, os.path.dirname(_HERE))
+
+import oracle  # noqa: E402
+from paper_2505_11594_amd import workloads as wl  # noqa: E402
+
+MX, NV = oracle.FMT_MX, oracle.FMT_NV16
+VARIANTS = [
+    # label, oracle fmt, oracle flags, ABI flags (None: not a kernel variant)
+    ("MXFP4 (default)", MX, 0, 0),
+    ("NVFP4 E4M3 scales", NV, 0, 1),
+    ("MXFP4, direct P", MX, oracle.DIRECT_P, None),
+    ("NVFP4, direct P", NV, oracle.DIRECT_P, None),
+    ("MXFP4, no smoothing K", MX, oracle.NO_SMOOTH_K, 0x10),
+    ("NVFP4, no smoothing K", NV, oracle.NO_SMOOTH_K, 0x11),
+    ("MXFP4, smoothing Q", MX, oracle.SMOOTH_Q, 0x20),
+    ("NVFP4, smoothing Q", NV, oracle.SMOOTH_Q, 0x21),
+    ("MXFP4, R = 448*6 (C9)", MX, oracle.R_LITERAL, None),
+    ("MXFP4, floor-rule scales (C3)", MX, oracle.OCP_SCALE, None),
+]
+
+
+def gpu_out(q, k, v, w, abi_flags):
+    import torch
+    from paper_2505_11594_amd import binding as bd
+    dt = torch.bfloat16 if w.in_dtype == 1 else torch.float16
+    dev = [torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(dt).to("cuda") for x in (q, k, v)]
+    f = abi_flags | (bd.SAGE_BKV64 if w.bkv == 64 else 0)
+    o = bd.sage_attn_fp4_fwd(*dev, causal=w.causal, fmt=f, out_f32=True)
+    torch.cuda.synchronize()
+    return o.cpu().numpy().reshape(-1, w.D)
+
+
+def fmt_m(m):
+    return "%.4f%% | %.4f | %.4g" % (100 * m["cossim"], m["l1"], m["rmse"])
+
+
+def accuracy_tables(heads: int, rows_per_head: int, use_gpu: bool):
+    print("## Accuracy against exact attention\n")
+    for w in wl.CONFIGS:
+        H = min(w.H, heads)
+        q, k, v = wl.generate(w, B=1, H=H)
+        rng = np.random.default_rng(w.seed + 1)
+        rows = np.sort(np.concatenate([h * w.N + rng.choice(w.N, min(w.N, rows_per_head), replace=False)
+                                       for h in range(H)])).astype(np.int64)
+        t0 = time.time()
+        ex = oracle.exact_attn(q, k, v, w.in_dtype, w.causal, rows=rows)
+        print("### %s (N=%d, D=%d%s; %d heads, %d rows)\n" % (w.name, w.N, w.D, ", causal" if w.causal else "",
+                                                             H, rows.size))
+        hdr = "| variant | CosSim | L1 | RMSE |" + (" GPU CosSim | GPU L1 | GPU RMSE |" if use_gpu else "")
+        print(hdr)
+        print("|---|---|---|---|" + ("---|---|---|" if use_gpu else ""))
+        for label, fmt, flags, abi in VARIANTS:
+            out, _, _ = oracle.attn(q, k, v, w.in_dtype, w.causal, fmt, w.bkv, rows=rows, flags=flags)
+            line = "| %s | %s |" % (label, fmt_m(oracle.metrics(ex, out)))
+            if use_gpu:
+                if abi is None:
+                    line += " — | — | — |"
+                else:
+                    g = gpu_out(q, k, v, w, abi)[rows]
+                    line += " %s |" % fmt_m(oracle.metrics(ex, g))
+            print(line, flush=True)
+        print("\n(%.1f s)\n" % (time.time() - t0))
+
+
+def fig3_table(ntiles: int):
+    """Fig. 3 on the exact smoothed scores S = Q K'^T of one head of the
+    4096-token workload (tiles of 64 keys at random rows, with the row's
+    final max as the running max)."""
+    w = wl.CONFIGS[1]
+    q, k, v = wl.generate(w, B=1, H=1)
+    qf = wl.from_bits(q, w.in_dtype)[0, 0].astype(np.float64)
+    kf = wl.from_bits(k, w.in_dtype)[0, 0].astype(np.float64)
+    kf = kf - kf.mean(axis=0)
+    S = (qf @ kf.T).astype(np.float32)                       # [N, N]
+    D = w.D
+    c2 = 1.0 / (math.log(2.0) * math.sqrt(D))
+    res = {}
+    for label, flags in (("direct", oracle.DIRECT_P), ("two-level", 0)):
+        rng = np.random.default_rng(5)
+        pts, sv, serr, perr, nsub = [], [], [], [], 0
+        for _ in range(ntiles):
+            i = int(rng.integers(0, w.N))
+            j0 = int(rng.integers(0, w.N // 64)) * 64
+            Srow = S[i, j0:j0 + 64]
+            m = float(S[i].max())
+            r = oracle.p_tile(Srow, m, D, NV, flags=flags)
+            pt = np.exp2(c2 * (Srow.astype(np.float64) - m))
+            pts.append(pt)
+            for b in range(64 // 16):
+                blk = slice(16 * b, 16 * b + 16)
+                s_q = oracle.e4m3_decode(int(r["sbytes"][b]))
+                s_exact = (pt[blk] / r["s1"]).max() / 6.0
+                sv.append(int(r["sbytes"][b]))
+                nsub += s_exact < 2.0 ** -6                    # below the smallest normal E4M3 value
+                serr.append(abs(s_q - s_exact) / s_exact if s_exact > 0 else 0.0)
+                deq = np.array([oracle.e2m1_decode(int(c)) for c in r["codes"][blk]]) * s_q * r["s1"]
+                perr.append(np.abs(deq - pt[blk]).sum())
+        pts = np.concatenate(pts)
+        vals = np.array([oracle.e4m3_decode(b) for b in sv])
+        res[label] = dict(pt=pts, smin=float(vals[vals > 0].min()) if (vals > 0).any() else 0.0,
+                          smax=float(vals.max()), ncodes=len(set(sv)), serr=float(np.mean(serr)),
+                          perr=float(np.sum(perr) / pts.sum()), sub=nsub / len(sv))
+    pt = res["direct"]["pt"]
+    print("## Fig. 3: P~ and its scales (NVFP4-style E4M3; %s, one head, %d tiles of 64 keys)\n" % (w.name, ntiles))
+    qs = np.quantile(pt, [0.5, 0.9, 0.99, 1.0])
+    print("P~ quantiles (0.5, 0.9, 0.99, max): %s\n" % ", ".join("%.3g" % x for x in qs))
+    print("| P~ quantization | s_P range (nonzero) | distinct E4M3 scale codes | scales below the smallest normal "
+          "E4M3 | mean rel. error of s_P | relative L1 error of P~ |")
+    print("|---|---|---|---|---|---|")
+    for label in ("direct", "two-level"):
+        r = res[label]
+        print("| %s | [%.3g, %.3g] | %d | %.3f | %.4f | %.4f |" % (label, r["smin"], r["smax"], r["ncodes"], r["sub"],
+                                                                  r["serr"], r["perr"]))
+    print()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpu", action="store_true", help="also run the HIP kernels on the same inputs")
+    ap.add_argument("--heads", type=int, default=2)
+    ap.add_argument("--rows", type=int, default=256, help="query rows sampled per head")
+    ap.add_argument("--fig3-tiles", type=int, default=400)
+    a = ap.parse_args()
+    fig3_table(a.fig3_tiles)
+    accuracy_tables(a.heads, a.rows, a.gpu)
+
+
+if __name__ == "__main__":
+    main()
