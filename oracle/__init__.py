@@ -18,22 +18,26 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "sage_oracle.c")
+_SRC_I8 = os.path.join(_HERE, "sage_oracle_int8.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 FMT_MX, FMT_NV16, FMT_NONE = 0, 1, 2
 IN_FP16, IN_BF16 = 0, 1
 ROLE_Q, ROLE_K, ROLE_V = 0, 1, 2
 NO_SMOOTH_K, DIRECT_P, R_LITERAL, SMOOTH_Q, OCP_SCALE = 1, 2, 4, 8, 16
+# 8-bit attention (Algorithm 2) flags: NO_SMOOTH_K, and
+I8_STATIC_P, I8_IDENTITY = 32, 64
 
 _lib = None
 
 
 def build(force: bool = False) -> str:
     """Compile sage_oracle.c into liboracle.so (gcc, no fast-math, no FP contraction)."""
-    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+    newest = max(os.path.getmtime(_SRC), os.path.getmtime(_SRC_I8))
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < newest:
         tmp = _LIB + ".tmp%d" % os.getpid()
         cmd = ["gcc", "-O2", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
-               "-pthread", "-o", tmp, _SRC, "-lm"]
+               "-pthread", "-o", tmp, _SRC, _SRC_I8, "-lm"]
         subprocess.run(cmd, check=True)
         os.replace(tmp, _LIB)
     return _LIB
@@ -89,6 +93,14 @@ def lib():
                                   ctypes.c_uint] + [ctypes.c_void_p] * 9)
         L.orc_fp4mm.restype = ctypes.c_long
         L.orc_fp4mm.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_int] * 4 + [ctypes.c_void_p]
+        L.orc_psi_block.restype = ctypes.c_float
+        L.orc_psi_block.argtypes = [ctypes.c_void_p, ctypes.c_long, ctypes.c_void_p]
+        L.orc_quant_int8.restype = ctypes.c_long
+        L.orc_quant_int8.argtypes = ([ctypes.c_void_p, ctypes.c_int, ctypes.c_int] + [ctypes.c_int] * 6 +
+                                     [ctypes.c_void_p] * 3)
+        L.orc_attn_int8.restype = ctypes.c_int
+        L.orc_attn_int8.argtypes = ([ctypes.c_void_p] * 3 + [ctypes.c_int] * 8 + [ctypes.c_uint] +
+                                    [ctypes.c_void_p, ctypes.c_int64] + [ctypes.c_void_p] * 4 + [ctypes.c_int])
         _lib = L
     return _lib
 
@@ -282,3 +294,49 @@ def metrics(o_ref: np.ndarray, o: np.ndarray) -> dict:
     l1 = float(np.abs(a - b).sum() / np.abs(a).sum())
     rmse = float(np.sqrt(((a - b) ** 2).mean()))
     return dict(cossim=cos, l1=l1, rmse=rmse)
+
+
+# ---------------------------------------------------------------- Algorithm 2
+def psi_block(x: np.ndarray):
+    """Per-block INT8 quantization psi (Eq. psi): returns (codes int8[n], scale)."""
+    x = np.ascontiguousarray(x, dtype=np.float32).ravel()
+    codes = np.zeros(x.size, dtype=np.int8)
+    s = lib().orc_psi_block(_ptr(x), x.size, _ptr(codes))
+    return codes, float(np.float32(s))
+
+
+def quant_int8(x_bits: np.ndarray, in_dtype: int, role: int, blk: int, smooth_k: bool = True):
+    """psi over blocks of blk rows (role K: of K - mean(K) unless smooth_k is
+    False).  Returns (codes int8 [B,H,N,D], scales fp32 [B,H,ceil(N/blk)],
+    mu fp32 [B,H,D] or None)."""
+    B, H, N, D = x_bits.shape
+    x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
+    codes = np.zeros((B, H, N, D), dtype=np.int8)
+    scales = np.zeros((B, H, (N + blk - 1) // blk), dtype=np.float32)
+    mu = np.zeros((B, H, D), dtype=np.float32)
+    sm = role == ROLE_K and smooth_k
+    lib().orc_quant_int8(_ptr(x_bits), in_dtype, role, B, H, N, D, blk, int(sm), _ptr(codes), _ptr(scales),
+                         _ptr(mu))
+    return codes, scales, (mu if sm else None)
+
+
+def attn_int8(q_bits, k_bits, v_bits, in_dtype: int, causal: bool, bkv: int, rows=None, flags: int = 0,
+              bq: int = 128, nthreads: int | None = None):
+    """Algorithm 2 (the 8-bit attention forward) on the listed rows.
+
+    Returns (out [nrows, D] fp32, lse [nrows] fp32, tie_tol [nrows] fp32, counters dict)."""
+    B, H, N, D = q_bits.shape
+    arrs = [np.ascontiguousarray(a, dtype=np.uint16) for a in (q_bits, k_bits, v_bits)]
+    if rows is None:
+        rows = np.arange(B * H * N, dtype=np.int64)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.zeros((rows.size, D), dtype=np.float32)
+    lse = np.zeros(rows.size, dtype=np.float32)
+    tol = np.zeros(rows.size, dtype=np.float32)
+    cnt = np.zeros(2, dtype=np.int64)
+    rc = lib().orc_attn_int8(*[_ptr(a) for a in arrs], in_dtype, B, H, N, D, int(bool(causal)), bq, bkv, flags,
+                             _ptr(rows), rows.size, _ptr(out), _ptr(lse), _ptr(tol), _ptr(cnt),
+                             nthreads or default_threads())
+    if rc != 0:
+        raise ValueError("orc_attn_int8: invalid arguments")
+    return out, lse, tol, dict(tie_codes=int(cnt[0]), skipped_tiles=int(cnt[1]))

@@ -1,0 +1,242 @@
+"""Pins for the oracle of the 8-bit attention forward (Algorithm 2), no GPU.
+
+Each test checks the oracle against something independent of its code:
+closed forms of psi (Eq. psi), its rounding bound, textbook softmax attention
+and log-sum-exp (identity mode), the exact log-sum-exp of the quantized
+scores, an error bound derived from the P rounding alone, closed forms of
+the whole forward (Q = 0, one dominant key), invariance to permuting key
+blocks, and the paper's claims (per-token P beats a static 1/127 scale;
+smoothing K helps when K has a channel bias).
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2505_11594_amd import workloads as wl
+
+from test_oracle_attn import textbook_attention
+
+LN2 = math.log(2.0)
+
+
+# ------------------------------------------------------------------ psi
+def test_psi_closed_form_integers_and_ties():
+    """Block max 127 2^e: the scale is exactly 2^e, integer multiples k 2^e
+    map to k, and (k + 1/2) 2^e to the even neighbour."""
+    rng = np.random.default_rng(300)
+    for e in (-20, -3, 0, 5, 17):
+        ks = rng.integers(-126, 127, 200)
+        x = np.concatenate([[127.0 * 2.0 ** e], ks * 2.0 ** e]).astype(np.float32)
+        codes, s = oracle.psi_block(x)
+        assert s == 2.0 ** e
+        assert codes[0] == 127 and np.array_equal(codes[1:], ks)
+        half = rng.integers(-126, 126, 200)
+        y = np.concatenate([[-127.0 * 2.0 ** e], (half + 0.5) * 2.0 ** e]).astype(np.float32)
+        codes, s = oracle.psi_block(y)
+        even = np.where(half % 2 == 0, half, half + 1)
+        assert codes[0] == -127 and np.array_equal(codes[1:], even)
+
+
+def test_psi_rounding_bound_random_blocks():
+    rng = np.random.default_rng(301)
+    for trial in range(300):
+        n = int(rng.integers(1, 5000))
+        x = (rng.standard_normal(n) * 2.0 ** rng.integers(-12, 12)).astype(np.float32)
+        if trial % 4 == 0:
+            x[rng.integers(0, n)] *= np.float32(50.0)
+        codes, s = oracle.psi_block(x)
+        amax = float(np.abs(x).max())
+        assert abs(s * 127.0 - amax) <= amax * 2.0 ** -23
+        assert np.abs(codes.astype(np.int32)).max() <= 127
+        # x * fl32(1/s) carries two roundings of relative 2^-24 on a value <= 127
+        err = np.abs(codes.astype(np.float64) * s - x.astype(np.float64))
+        assert np.all(err <= s * (0.5 + 2.0 ** -15))
+        assert abs(int(codes[np.argmax(np.abs(x))])) == 127
+    codes, s = oracle.psi_block(np.zeros(64, dtype=np.float32))
+    assert s == 0.0 and not codes.any()
+
+
+@pytest.mark.parametrize("role,blk", [(oracle.ROLE_Q, 128), (oracle.ROLE_K, 64), (oracle.ROLE_K, 128),
+                                      (oracle.ROLE_V, 64)])
+def test_quant_int8_blocks_of_rows(role, blk):
+    """One scale per block of blk rows (the last holds the rest); role K
+    quantizes K - mean(K)."""
+    B, H, N, D = 1, 2, 300, 64
+    _, k, _ = wl.make_inputs(B, H, N, D, wl.IN_BF16, seed=302, k_bias_var=4.0)
+    codes, scales, mu = oracle.quant_int8(k, wl.IN_BF16, role, blk)
+    x = wl.from_bits(k, 1).astype(np.float32)
+    if role == oracle.ROLE_K:
+        mu_ref, _ = oracle.kmean(k, wl.IN_BF16)
+        assert np.array_equal(mu, mu_ref)
+        x = (x - mu[:, :, None, :]).astype(np.float32)
+    nb = (N + blk - 1) // blk
+    assert scales.shape == (B, H, nb)
+    for h in range(H):
+        for b in range(nb):
+            xb = x[0, h, b * blk:(b + 1) * blk]
+            amax = float(np.abs(xb).max())
+            s = float(scales[0, h, b])
+            assert abs(s * 127.0 - amax) <= amax * 2.0 ** -23
+            err = np.abs(codes[0, h, b * blk:(b + 1) * blk].astype(np.float64) * s - xb)
+            assert np.all(err <= s * (0.5 + 2.0 ** -15))
+
+
+# ------------------------------------------------------------------ machinery
+def lse_textbook(qf, kf, causal):
+    S = qf.astype(np.float64) @ kf.astype(np.float64).T / math.sqrt(qf.shape[1])
+    if causal:
+        S = np.where(np.tril(np.ones_like(S, dtype=bool)), S, -np.inf)
+    mx = S.max(axis=1, keepdims=True)
+    return (mx[:, 0] + np.log(np.exp(S - mx).sum(axis=1)))
+
+
+@pytest.mark.parametrize("N,bkv,causal", [(200, 64, False), (256, 128, True), (129, 64, True), (1, 64, False)])
+def test_identity_mode_is_textbook_attention_and_lse(N, bkv, causal):
+    D = 64
+    q, k, v = wl.make_inputs(1, 2, N, D, wl.IN_BF16, seed=310 + N, k_bias_var=1.0)
+    out, lse, _, _ = oracle.attn_int8(q, k, v, wl.IN_BF16, causal, bkv, flags=oracle.I8_IDENTITY)
+    out = out.reshape(2, N, D)
+    lse = lse.reshape(2, N)
+    for h in range(2):
+        qf, kf, vf = (wl.from_bits(x[0, h], 1) for x in (q, k, v))
+        ref = textbook_attention(qf, kf, vf, causal)
+        assert np.abs(out[h] - ref).max() <= 2e-6 * np.abs(ref).max()
+        # softmax is invariant to the K mean; L is not, by q . mean(K) / sqrt(D)
+        mu = kf.astype(np.float64).mean(axis=0)
+        lref = lse_textbook(qf, kf, causal) - qf.astype(np.float64) @ mu / math.sqrt(D)
+        assert np.abs(lse[h] - lref).max() <= 1e-5 * (1 + np.abs(lref).max())
+
+
+# ------------------------------------------------------------------ quantized forward
+def dequant_scores(q, k, causal, bq, bkv, smooth=True):
+    """fp64 S/sqrt(D) from the oracle's own (pinned) codes and scales, per head."""
+    B, H, N, D = q.shape
+    qc, qs, _ = oracle.quant_int8(q, wl.IN_BF16, oracle.ROLE_Q, bq)
+    kc, ks, _ = oracle.quant_int8(k, wl.IN_BF16, oracle.ROLE_K, bkv, smooth_k=smooth)
+    out = []
+    for h in range(H):
+        qd = qc[0, h].astype(np.float64) * np.repeat(qs[0, h].astype(np.float64), bq)[:N, None]
+        kd = kc[0, h].astype(np.float64) * np.repeat(ks[0, h].astype(np.float64), bkv)[:N, None]
+        S = qd @ kd.T / math.sqrt(D)
+        if causal:
+            S = np.where(np.tril(np.ones_like(S, dtype=bool)), S, -np.inf)
+        out.append(S)
+    return out
+
+
+@pytest.mark.parametrize("N,bkv,causal", [(300, 64, False), (384, 128, True)])
+def test_lse_is_the_exact_logsumexp_of_the_quantized_scores(N, bkv, causal):
+    """L depends on the running max and the unquantized row sums only."""
+    D = 128
+    q, k, v = wl.make_inputs(1, 2, N, D, wl.IN_BF16, seed=320, k_bias_var=1.0, outlier_frac=0.02)
+    _, lse, _, _ = oracle.attn_int8(q, k, v, wl.IN_BF16, causal, bkv)
+    lse = lse.reshape(2, N)
+    for h, S in enumerate(dequant_scores(q, k, causal, 128, bkv)):
+        mx = S.max(axis=1, keepdims=True)
+        ref = mx[:, 0] + np.log(np.exp(S - mx).sum(axis=1))
+        # fp32 roundings of the log2-domain scores (|u| ulps) and of log2(l)
+        slack = 1e-6 * (1 + np.abs(ref)) + 4 * np.abs(S[np.isfinite(S)]).max() * 2.0 ** -23
+        assert np.all(np.abs(lse[h] - ref) <= slack)
+
+
+@pytest.mark.parametrize("N,bkv,causal", [(300, 64, False), (256, 128, True)])
+def test_output_within_the_p_rounding_bound(N, bkv, causal):
+    """Against exact softmax of the dequantized scores applied to the
+    dequantized V, the only error beyond fp32 rounding is P^'s rounding to
+    integers: at most s_P / 2 per element, with s_P = 2^{u(t_j) - m}/127
+    relative to the final max, so |dO_d| <= sum_j s_P,j / 2 sum_{k in j}
+    |V_kd| / l."""
+    D = 64
+    bq = 128
+    q, k, v = wl.make_inputs(1, 2, N, D, wl.IN_BF16, seed=330 + N, k_bias_var=1.0)
+    out, _, _, _ = oracle.attn_int8(q, k, v, wl.IN_BF16, causal, bkv)
+    out = out.reshape(2, N, D)
+    vc, vs, _ = oracle.quant_int8(v, wl.IN_BF16, oracle.ROLE_V, bkv)
+    for h, S in enumerate(dequant_scores(q, k, causal, bq, bkv)):
+        vd = vc[0, h].astype(np.float64) * np.repeat(vs[0, h].astype(np.float64), bkv)[:N, None]
+        mx = S.max(axis=1, keepdims=True)
+        P = np.exp(S - mx)
+        l = P.sum(axis=1, keepdims=True)
+        ref = P @ vd / l
+        bound = np.zeros_like(ref)
+        for j0 in range(0, N, bkv):
+            t = S[:, j0:j0 + bkv].max(axis=1, keepdims=True)
+            sp = np.where(np.isfinite(t), np.exp(t - mx), 0.0) / 127.0
+            bound += sp / 2 * np.abs(vd[j0:j0 + bkv]).sum(axis=0)[None, :] * (np.isfinite(t))
+        bound = bound / l + 1e-5 * np.abs(ref).max()
+        assert np.all(np.abs(out[h] - ref) <= bound)
+
+
+def test_q_zero_gives_the_mean_of_v_and_log_n():
+    """Q = 0: every score is 0, P^ = 127 with s_P = 1/127, so O is the mean of
+    the dequantized V over the visible keys and L = ln(#keys)."""
+    N, D, bkv = 200, 64, 64
+    _, k, v = wl.make_inputs(1, 1, N, D, wl.IN_BF16, seed=340)
+    q = np.zeros_like(k)
+    vc, vs, _ = oracle.quant_int8(v, wl.IN_BF16, oracle.ROLE_V, bkv)
+    vd = vc[0, 0].astype(np.float64) * np.repeat(vs[0, 0].astype(np.float64), bkv)[:N, None]
+    for causal in (False, True):
+        out, lse, _, _ = oracle.attn_int8(q, k, v, wl.IN_BF16, causal, bkv)
+        cnt = np.arange(1, N + 1) if causal else np.full(N, N)
+        ref = (np.cumsum(vd, axis=0) / cnt[:, None]) if causal else np.broadcast_to(vd.mean(axis=0), (N, D))
+        assert np.abs(out - ref).max() <= 1e-5 * np.abs(vd).max()
+        assert np.abs(lse - np.log(cnt)).max() <= 1e-5 * np.log(N)
+
+
+def test_one_dominant_key_returns_its_value_row():
+    """A key whose score exceeds every other by more than 31 sqrt(D) makes
+    every other P^ round to 0 and their unquantized P~ (which l sums) smaller
+    than e^-31 each, so O is that key's dequantized V row."""
+    N, D, bkv = 128, 64, 64
+    rng = np.random.default_rng(350)
+    qf = np.zeros((1, 1, N, D), dtype=np.float32)
+    kf = (rng.standard_normal((1, 1, N, D)) * 0.05).astype(np.float32)
+    qf[0, 0, :, 3] = 8.0
+    kf[0, 0, 77, 3] = 32.0            # S = 256 for key 77, |S| < 2 elsewhere
+    q, k = wl.to_bits(qf, 1), wl.to_bits(kf, 1)
+    _, _, v = wl.make_inputs(1, 1, N, D, wl.IN_BF16, seed=351)
+    out, _, _, _ = oracle.attn_int8(q, k, v, wl.IN_BF16, False, bkv, flags=oracle.NO_SMOOTH_K)
+    vc, vs, _ = oracle.quant_int8(v, wl.IN_BF16, oracle.ROLE_V, bkv)
+    row = vc[0, 0, 77].astype(np.float64) * float(vs[0, 0, 77 // bkv])
+    assert np.abs(out - row[None, :]).max() <= 1e-6 * np.abs(row).max()
+
+
+def test_permuting_key_blocks_with_their_values():
+    """Moving whole KV blocks keeps every block's scales and codes, so only
+    the fp32 accumulation order across tiles changes."""
+    N, D, bkv = 512, 64, 64
+    q, k, v = wl.make_inputs(1, 1, N, D, wl.IN_BF16, seed=360, k_bias_var=1.0)
+    base, lb, _, _ = oracle.attn_int8(q, k, v, wl.IN_BF16, False, bkv)
+    perm = np.concatenate([b * bkv + np.arange(bkv) for b in np.random.default_rng(361).permutation(N // bkv)])
+    o2, l2, _, _ = oracle.attn_int8(q, k[:, :, perm], v[:, :, perm], wl.IN_BF16, False, bkv)
+    assert np.abs(o2 - base).max() <= 4e-6 * np.abs(base).max()
+    assert np.abs(l2 - lb).max() <= 1e-6 * (1 + np.abs(lb).max())
+
+
+# ------------------------------------------------------------------ the paper's claims
+def _acc(flags, seed, k_bias_var=0.0, outlier_frac=0.0, N=512, D=128, bkv=64):
+    q, k, v = wl.make_inputs(1, 2, N, D, wl.IN_BF16, seed=seed, k_bias_var=k_bias_var, outlier_frac=outlier_frac)
+    rows = np.arange(0, 2 * N, 2, dtype=np.int64)
+    ex = oracle.exact_attn(q, k, v, wl.IN_BF16, False, rows=rows)
+    out, _, _, _ = oracle.attn_int8(q, k, v, wl.IN_BF16, False, bkv, rows=rows, flags=flags)
+    return oracle.metrics(ex, out)
+
+
+@pytest.mark.parametrize("seed,kbias", [(370, 0.0), (372, 1.0)])
+def test_per_token_p_beats_the_static_scale(seed, kbias):
+    """Sec. 4.1: a static 1/127 scale for P~ is inaccurate; per-token scales
+    that reuse the row maxima are more accurate.  (With 2% of Q, K rows
+    scaled x20 the error of the per-block Q, K codes dominates and the two
+    P variants tie.)"""
+    a = _acc(0, seed, k_bias_var=kbias)
+    b = _acc(oracle.I8_STATIC_P, seed, k_bias_var=kbias)
+    assert a["l1"] < b["l1"] and a["rmse"] < b["rmse"] and a["cossim"] > b["cossim"]
+
+
+def test_smoothing_k_helps_int8_with_a_key_bias():
+    a = _acc(0, 380, k_bias_var=4.0)
+    b = _acc(oracle.NO_SMOOTH_K, 380, k_bias_var=4.0)
+    assert a["l1"] < b["l1"] and a["cossim"] > b["cossim"]
+    assert a["cossim"] > 0.99      # 8-bit attention is far more accurate than FP4 on the same data
