@@ -1,6 +1,7 @@
 /*
  * sage_mi355x.h -- C ABI of the MI355X (gfx950) microscaled-FP4 attention
- * forward of SageAttention3 (arXiv 2505.11594).
+ * forward of SageAttention3 (arXiv 2505.11594), and of the paper's 8-bit
+ * attention forward (SageBwd, Algorithm 2).
  *
  * Every function returns an int status (sage_status).  Arguments are checked
  * on the host before any HIP call, so invalid calls fail without touching the
@@ -164,6 +165,84 @@ int sage_attn_fp4_fwd_prequant(const void* q_codes, const void* q_scales,
  */
 int sage_attn_bf16_fwd(const void* q, const void* k, const void* v, void* o,
                        int B, int H, int N, int D, int causal, unsigned flags, hipStream_t stream);
+
+/* ======================================================================== */
+/* 8-bit attention forward of SageBwd (Algorithm 2, Sec. 4.1).             */
+/*                                                                          */
+/* Accepted flags: SAGE_IN_BF16, SAGE_OUT_F32, SAGE_NO_SMOOTH_K, and       */
+/* SAGE_BKV64 (the KV tile is 64 tokens whether it is set or not); any     */
+/* other bit is SAGE_ERR_INVALID_ARG.  D must be 64 or 128; N >= 1.          */
+/*                                                                          */
+/* psi (Eq. psi): one fp32 scale s = max|X|/127 per block of rows -- 128    */
+/* query rows for Q (the last block holds the rest), 64 rows for K and V --  */
+/* and int8 codes round(x * fl32(1/s)), nearest, ties to even; an all-zero  */
+/* block has s = 0 and zero codes.  K is first smoothed, K' = fl32(K -       */
+/* kmean), unless SAGE_NO_SMOOTH_K.  Physical layout (Np = N rounded up to  */
+/* 128):                                                                    */
+/*   Q^  int8 [B,H,N,D],  s_Q fp32 [B,H,ceil(N/128)]                        */
+/*   K^  int8 [B,H,Np,D], s_K fp32 [B,H,Np/64]  (rows >= N are zero)         */
+/*   V^T int8 [B,H,D,Np], s_V fp32 [B,H,Np/64]  V transposed; inside every  */
+/*       32-token group, position 16h + 4g + r (h in {0,1}; g, r in 0..3)   */
+/*       holds token 8g + 4h + r (the order in which the int8 MFMA receives */
+/*       P from the accumulator of S^T); tokens >= N are zero.              */
+/* ======================================================================== */
+
+/* Byte sizes of the codes and scales buffers for one role.  Host only. */
+int sage_quant_int8_sizes(int role, int B, int H, int N, int D, unsigned flags,
+                          size_t* codes_bytes, size_t* scales_bytes);
+
+/*
+ * sage_quant_int8 -- psi for one role (layouts above).
+ *  x        : 16-bit input [B,H,N,D], 16-byte aligned
+ *  codes    : output, sage_quant_int8_sizes() bytes, 16-byte aligned
+ *  scales   : output fp32, sage_quant_int8_sizes() bytes, 4-byte aligned
+ *  kmean    : role K with smoothing: output fp32 [B,H,D] (the exact mean,
+ *             as for sage_quant_fp4); otherwise must be NULL
+ *  workspace: role K with smoothing: at least
+ *             sage_quant_workspace_size(SAGE_ROLE_K, B, H, N, D, 0) bytes,
+ *             8-byte aligned; otherwise may be NULL
+ */
+int sage_quant_int8(const void* x, int role, int B, int H, int N, int D, unsigned flags,
+                    void* codes, float* scales, float* kmean,
+                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes for sage_attn_int8_fwd_ws (quantized Q, K, V, their
+ * scales, the mean and its partial sums); 0 for invalid arguments.  Host
+ * only. */
+size_t sage_attn_int8_workspace_size(int B, int H, int N, int D, unsigned flags);
+
+/*
+ * sage_attn_int8_fwd -- Algorithm 2: smoothing K, psi(Q), psi(K), psi(V),
+ * S = MM(Q^, K^) s_Q s_K on int8 MFMA (exact int32 products), online softmax
+ * over 64-key tiles with the running max m, per-token quantization of P~
+ * reusing the maxima (s_P = rowmax_tile(P~)/127, P^ = rint(P~/s_P)),
+ * O = diag(e^{m_old - m_new}) O + MM(P^, V^) s_P s_V on int8 MFMA, O = O/l.
+ * Softmax scale 1/sqrt(D); causal = 1 keeps key j for query i iff j <= i.
+ *  q, k, v : 16-bit [B,H,N,D], 16-byte aligned
+ *  o       : [B,H,N,D] fp32 (SAGE_OUT_F32) or input dtype, 16-byte aligned
+ *  lse     : fp32 [B,H,N] or NULL: L = m + log(l), the natural-log
+ *            log-sum-exp of the scaled scores S/sqrt(D) of each query row
+ *            (the value the backward pass of Algorithm 3 consumes)
+ * The internal workspace comes from hipMallocAsync on `stream` and is freed
+ * with hipFreeAsync on the same stream.
+ */
+int sage_attn_int8_fwd(const void* q, const void* k, const void* v, void* o, float* lse,
+                       int B, int H, int N, int D, int causal, unsigned flags, hipStream_t stream);
+
+/* Same, with a caller-provided workspace of at least
+ * sage_attn_int8_workspace_size() bytes (256-byte aligned). */
+int sage_attn_int8_fwd_ws(const void* q, const void* k, const void* v, void* o, float* lse,
+                          int B, int H, int N, int D, int causal, unsigned flags,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* The 8-bit attention kernel alone, on tensors produced by sage_quant_int8
+ * (layouts above; kmean is not needed, the smoothing is inside K^).  flags:
+ * SAGE_OUT_F32 and SAGE_IN_BF16 (the dtype of a 16-bit o). */
+int sage_attn_int8_fwd_prequant(const void* q_codes, const float* q_scales,
+                                const void* k_codes, const float* k_scales,
+                                const void* vt_codes, const float* vt_scales,
+                                void* o, float* lse, int B, int H, int N, int D, int causal,
+                                unsigned flags, hipStream_t stream);
 
 /* Human-readable status name; never NULL. */
 const char* sage_status_string(int status);

@@ -49,11 +49,20 @@ def lib():
         L.sage_attn_fp4_fwd_ws.argtypes = [vp, vp, vp, vp, i, i, i, i, i, u, vp, sz, vp]
         L.sage_attn_fp4_fwd_prequant.argtypes = [vp] * 7 + [i, i, i, i, i, u, vp]
         L.sage_attn_bf16_fwd.argtypes = [vp, vp, vp, vp, i, i, i, i, i, u, vp]
+        L.sage_quant_int8_sizes.argtypes = [i, i, i, i, i, u, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+        L.sage_quant_int8.argtypes = [vp, i, i, i, i, i, u, vp, vp, vp, vp, sz, vp]
+        L.sage_attn_int8_workspace_size.argtypes = [i, i, i, i, u]
+        L.sage_attn_int8_workspace_size.restype = sz
+        L.sage_attn_int8_fwd.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, u, vp]
+        L.sage_attn_int8_fwd_ws.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, u, vp, sz, vp]
+        L.sage_attn_int8_fwd_prequant.argtypes = [vp] * 8 + [i, i, i, i, i, u, vp]
         L.sage_status_string.argtypes = [i]
         L.sage_status_string.restype = ctypes.c_char_p
         L.sage_version.restype = ctypes.c_char_p
         for name in ("sage_quant_sizes", "sage_quant_fp4", "sage_attn_fp4_fwd", "sage_attn_fp4_fwd_ws",
-                     "sage_attn_fp4_fwd_prequant", "sage_attn_bf16_fwd"):
+                     "sage_attn_fp4_fwd_prequant", "sage_attn_bf16_fwd", "sage_quant_int8_sizes",
+                     "sage_quant_int8", "sage_attn_int8_fwd", "sage_attn_int8_fwd_ws",
+                     "sage_attn_int8_fwd_prequant"):
             getattr(L, name).restype = i
         _lib = L
     return _lib
@@ -174,6 +183,80 @@ def sage_attn_bf16_fwd(q, k, v, causal: bool = False, out_f32: bool = True, out=
     rc = lib().sage_attn_bf16_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, H, N, D, int(bool(causal)), flags, _stream())
     _check("sage_attn_bf16_fwd", rc)
     return o
+
+
+# ---------------------------------------------------------------- 8-bit attention
+def quant_int8_sizes(role: int, B: int, H: int, N: int, D: int, flags: int = 0):
+    c, s = ctypes.c_size_t(), ctypes.c_size_t()
+    _check("sage_quant_int8_sizes",
+           lib().sage_quant_int8_sizes(role, B, H, N, D, flags, ctypes.byref(c), ctypes.byref(s)))
+    return c.value, s.value
+
+
+def sage_quant_int8(x, role: int, flags: int = 0):
+    """psi for one role; returns (codes int8, scales fp32, mean fp32 or None) on the device
+    (role K with smoothing K: the channel mean [B,H,D])."""
+    import torch
+    B, H, N, D = _shape(x)
+    flags = flags | _in_flag(x)
+    cb, sb = quant_int8_sizes(role, B, H, N, D, flags)
+    codes = torch.empty(cb, dtype=torch.int8, device=x.device)
+    scales = torch.empty(sb // 4, dtype=torch.float32, device=x.device)
+    kmean, ws = None, None
+    if role == SAGE_ROLE_K and not (flags & SAGE_NO_SMOOTH_K):
+        kmean = torch.empty((B, H, D), dtype=torch.float32, device=x.device)
+        wsb = int(lib().sage_quant_workspace_size(role, B, H, N, D, 0))
+        ws = torch.empty(max(wsb, 8), dtype=torch.uint8, device=x.device)
+    _check("sage_quant_int8", lib().sage_quant_int8(_ptr(x), role, B, H, N, D, flags, _ptr(codes), _ptr(scales),
+                                                    _ptr(kmean), _ptr(ws), ws.numel() if ws is not None else 0,
+                                                    _stream()))
+    return codes, scales, kmean
+
+
+def attn_int8_workspace_size(B: int, H: int, N: int, D: int, flags: int = 0) -> int:
+    return int(lib().sage_attn_int8_workspace_size(B, H, N, D, flags))
+
+
+def sage_attn_int8_fwd(q, k, v, causal: bool = False, flags: int = 0, out_f32: bool = True, lse: bool = True,
+                       out=None, lse_out=None, workspace=None):
+    """Algorithm 2's 8-bit attention forward.  Returns (O, L) with L = m + log l
+    [B,H,N] fp32 (None when ``lse`` is False).  With ``workspace`` (uint8, at
+    least attn_int8_workspace_size bytes) no allocation happens inside."""
+    import torch
+    B, H, N, D = _shape(q)
+    if _shape(k) != (B, H, N, D) or _shape(v) != (B, H, N, D):
+        raise ValueError("q, k, v must have the same shape")
+    flags = flags | _in_flag(q) | (SAGE_OUT_F32 if out_f32 else 0)
+    o = _out(q, out_f32) if out is None else out
+    L = None
+    if lse:
+        L = torch.empty((B, H, N), dtype=torch.float32, device=q.device) if lse_out is None else lse_out
+    if workspace is None:
+        rc = lib().sage_attn_int8_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(L), B, H, N, D, int(bool(causal)),
+                                      flags, _stream())
+        _check("sage_attn_int8_fwd", rc)
+    else:
+        rc = lib().sage_attn_int8_fwd_ws(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(L), B, H, N, D, int(bool(causal)),
+                                         flags, _ptr(workspace), workspace.numel(), _stream())
+        _check("sage_attn_int8_fwd_ws", rc)
+    return o, L
+
+
+def sage_attn_int8_fwd_prequant(qq, kq, vq, shape, causal: bool = False, in_bf16: bool = True,
+                                out_f32: bool = True, lse: bool = True):
+    """The 8-bit attention kernel alone on (codes, scales) pairs from sage_quant_int8."""
+    import torch
+    B, H, N, D = shape
+    flags = (SAGE_IN_BF16 if in_bf16 else SAGE_IN_FP16) | (SAGE_OUT_F32 if out_f32 else 0)
+    dev = qq[0].device
+    out = torch.empty(shape, dtype=torch.float32 if out_f32 else (torch.bfloat16 if in_bf16 else torch.float16),
+                      device=dev)
+    L = torch.empty((B, H, N), dtype=torch.float32, device=dev) if lse else None
+    rc = lib().sage_attn_int8_fwd_prequant(_ptr(qq[0]), _ptr(qq[1]), _ptr(kq[0]), _ptr(kq[1]), _ptr(vq[0]),
+                                           _ptr(vq[1]), _ptr(out), _ptr(L), B, H, N, D, int(bool(causal)), flags,
+                                           _stream())
+    _check("sage_attn_int8_fwd_prequant", rc)
+    return out, L
 
 
 def version() -> str:

@@ -27,6 +27,11 @@ hipError_t launch_attn_nv16(const void* qc, const void* qs, const void* kc, cons
 hipError_t launch_attn_bf16(const void* q, const void* k, const void* vt, void* o, int BH, int N, int Np, int D,
                             bool causal, bool out_f32, float c2, hipStream_t st);
 hipError_t launch_transpose_v_bf16(const void* v, void* vt, int BH, int N, int Np, int D, hipStream_t st);
+hipError_t launch_quant_i8(const void* x, const float* mu, void* codes, float* scales, int BH, int N, int Nout,
+                           int D, int R, int role, bool bf16, hipStream_t st);
+hipError_t launch_attn_int8(const void* qc, const float* qs, const void* kc, const float* ks, const void* vc,
+                            const float* vs, void* o, float* lse, int BH, int N, int Np, int D, bool causal, int out,
+                            float c2, float log127, hipStream_t st);
 }  // namespace sage
 
 namespace {
@@ -167,6 +172,102 @@ int attn_ws_impl(const void* q, const void* k, const void* v, void* o, int B, in
   return rc;
 }
 
+// ---- 8-bit attention (Algorithm 2) ----------------------------------------
+constexpr unsigned kI8Flags = SAGE_IN_BF16 | SAGE_OUT_F32 | SAGE_NO_SMOOTH_K | SAGE_BKV64;
+constexpr int kI8Bq = 128, kI8Bkv = 64;
+
+int check_i8(int B, int H, int N, int D, unsigned flags) {
+  if (flags & ~kI8Flags) return SAGE_ERR_INVALID_ARG;
+  return check_shape(B, H, N, D, flags & (SAGE_IN_BF16 | SAGE_OUT_F32));
+}
+
+void sizes_i8(int role, int B, int H, int N, int D, size_t* cb, size_t* sb) {
+  const size_t BH = (size_t)B * H, Np = pad128(N);
+  if (role == SAGE_ROLE_Q) {
+    *cb = BH * N * D;
+    *sb = BH * ((N + kI8Bq - 1) / kI8Bq) * sizeof(float);
+  } else {
+    *cb = BH * Np * D;
+    *sb = BH * (Np / kI8Bkv) * sizeof(float);
+  }
+}
+
+struct I8Ws {
+  size_t qc, qs, kc, ks, vc, vs, mu, part, total;
+};
+
+I8Ws i8_ws_layout(int B, int H, int N, int D) {
+  I8Ws w;
+  size_t c, s, off = 0;
+  sizes_i8(SAGE_ROLE_Q, B, H, N, D, &c, &s);
+  w.qc = off; off += up256(c); w.qs = off; off += up256(s);
+  sizes_i8(SAGE_ROLE_K, B, H, N, D, &c, &s);
+  w.kc = off; off += up256(c); w.ks = off; off += up256(s);
+  sizes_i8(SAGE_ROLE_V, B, H, N, D, &c, &s);
+  w.vc = off; off += up256(c); w.vs = off; off += up256(s);
+  w.mu = off; off += up256((size_t)B * H * D * sizeof(float));
+  w.part = off; off += up256(kmean_ws_bytes(B, H, N, D));
+  w.total = off;
+  return w;
+}
+
+int quant_i8_impl(const void* x, int role, int B, int H, int N, int D, unsigned flags, void* codes, float* scales,
+                  float* kmean, void* ws, hipStream_t st) {
+  const bool bf16 = (flags & SAGE_IN_BF16) != 0;
+  const int BH = B * H;
+  hipError_t e = hipSuccess;
+  if (role == SAGE_ROLE_Q) {
+    e = sage::launch_quant_i8(x, nullptr, codes, scales, BH, N, N, D, kI8Bq, 0, bf16, st);
+  } else if (role == SAGE_ROLE_K) {
+    const bool smooth = !(flags & SAGE_NO_SMOOTH_K);
+    if (smooth) {
+      e = sage::launch_kmean(x, static_cast<double*>(ws), kmean, BH, N, D, bf16, st);
+      if (e != hipSuccess) return SAGE_ERR_HIP;
+    }
+    e = sage::launch_quant_i8(x, smooth ? kmean : nullptr, codes, scales, BH, N, pad128(N), D, kI8Bkv, 1, bf16, st);
+  } else {
+    e = sage::launch_quant_i8(x, nullptr, codes, scales, BH, N, pad128(N), D, kI8Bkv, 2, bf16, st);
+  }
+  return hip_status(e);
+}
+
+inline float log2_of_127() { return (float)std::log2(127.0); }
+
+int attn_i8_prequant_impl(const void* qc, const float* qs, const void* kc, const float* ks, const void* vc,
+                          const float* vs, void* o, float* lse, int B, int H, int N, int D, int causal,
+                          unsigned flags, hipStream_t st) {
+  return hip_status(sage::launch_attn_int8(qc, qs, kc, ks, vc, vs, o, lse, B * H, N, pad128(N), D, causal != 0,
+                                           out_kind(flags), softmax_c2(D), log2_of_127(), st));
+}
+
+int attn_i8_ws_impl(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int N, int D,
+                    int causal, unsigned flags, void* ws, hipStream_t st) {
+  const I8Ws w = i8_ws_layout(B, H, N, D);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  float* qs = reinterpret_cast<float*>(base + w.qs);
+  float* ks = reinterpret_cast<float*>(base + w.ks);
+  float* vs = reinterpret_cast<float*>(base + w.vs);
+  float* mu = reinterpret_cast<float*>(base + w.mu);
+  int rc = quant_i8_impl(q, SAGE_ROLE_Q, B, H, N, D, flags, base + w.qc, qs, nullptr, nullptr, st);
+  if (rc == SAGE_OK) rc = quant_i8_impl(k, SAGE_ROLE_K, B, H, N, D, flags, base + w.kc, ks, mu, base + w.part, st);
+  if (rc == SAGE_OK) rc = quant_i8_impl(v, SAGE_ROLE_V, B, H, N, D, flags, base + w.vc, vs, nullptr, nullptr, st);
+  if (rc == SAGE_OK)
+    rc = attn_i8_prequant_impl(base + w.qc, qs, base + w.kc, ks, base + w.vc, vs, o, lse, B, H, N, D, causal, flags,
+                               st);
+  return rc;
+}
+
+int attn_i8_args(const void* q, const void* k, const void* v, const void* o, const float* lse, int B, int H, int N,
+                 int D, int causal, unsigned flags) {
+  int rc = check_i8(B, H, N, D, flags);
+  if (rc != SAGE_OK) return rc;
+  if (!q || !k || !v || !o) return SAGE_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return SAGE_ERR_INVALID_ARG;
+  if (lse && !aligned(lse, 4)) return SAGE_ERR_INVALID_ARG;
+  if (causal != 0 && causal != 1) return SAGE_ERR_INVALID_ARG;
+  return SAGE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -264,6 +365,76 @@ int sage_attn_bf16_fwd(const void* q, const void* k, const void* v, void* o, int
   rc = hip_status(e);
   if (hipFreeAsync(vt, stream) != hipSuccess && rc == SAGE_OK) rc = SAGE_ERR_HIP;
   return rc;
+}
+
+int sage_quant_int8_sizes(int role, int B, int H, int N, int D, unsigned flags, size_t* codes_bytes,
+                          size_t* scales_bytes) {
+  if (!codes_bytes || !scales_bytes) return SAGE_ERR_INVALID_ARG;
+  if (role != SAGE_ROLE_Q && role != SAGE_ROLE_K && role != SAGE_ROLE_V) return SAGE_ERR_INVALID_ARG;
+  const int rc = check_i8(B, H, N, D, flags);
+  if (rc != SAGE_OK) return rc;
+  sizes_i8(role, B, H, N, D, codes_bytes, scales_bytes);
+  return SAGE_OK;
+}
+
+int sage_quant_int8(const void* x, int role, int B, int H, int N, int D, unsigned flags, void* codes, float* scales,
+                    float* kmean, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (role != SAGE_ROLE_Q && role != SAGE_ROLE_K && role != SAGE_ROLE_V) return SAGE_ERR_INVALID_ARG;
+  int rc = check_i8(B, H, N, D, flags);
+  if (rc != SAGE_OK) return rc;
+  if (!x || !codes || !scales) return SAGE_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4)) return SAGE_ERR_INVALID_ARG;
+  const bool smooth = role == SAGE_ROLE_K && !(flags & SAGE_NO_SMOOTH_K);
+  if (smooth) {
+    if (!kmean || !aligned(kmean, 4) || !workspace || !aligned(workspace, 8)) return SAGE_ERR_INVALID_ARG;
+    if (workspace_bytes < kmean_ws_bytes(B, H, N, D)) return SAGE_ERR_WORKSPACE;
+  } else if (kmean) {
+    return SAGE_ERR_INVALID_ARG;
+  }
+  return quant_i8_impl(x, role, B, H, N, D, flags, codes, scales, kmean, workspace, stream);
+}
+
+size_t sage_attn_int8_workspace_size(int B, int H, int N, int D, unsigned flags) {
+  if (check_i8(B, H, N, D, flags) != SAGE_OK) return 0;
+  return i8_ws_layout(B, H, N, D).total;
+}
+
+int sage_attn_int8_fwd_ws(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int N,
+                          int D, int causal, unsigned flags, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+  int rc = attn_i8_args(q, k, v, o, lse, B, H, N, D, causal, flags);
+  if (rc != SAGE_OK) return rc;
+  if (!workspace || !aligned(workspace, 256)) return SAGE_ERR_INVALID_ARG;
+  if (workspace_bytes < i8_ws_layout(B, H, N, D).total) return SAGE_ERR_WORKSPACE;
+  return attn_i8_ws_impl(q, k, v, o, lse, B, H, N, D, causal, flags, workspace, stream);
+}
+
+int sage_attn_int8_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int N, int D,
+                       int causal, unsigned flags, hipStream_t stream) {
+  int rc = attn_i8_args(q, k, v, o, lse, B, H, N, D, causal, flags);
+  if (rc != SAGE_OK) return rc;
+  const size_t bytes = i8_ws_layout(B, H, N, D).total;
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess) return SAGE_ERR_HIP;
+  rc = attn_i8_ws_impl(q, k, v, o, lse, B, H, N, D, causal, flags, ws, stream);
+  if (hipFreeAsync(ws, stream) != hipSuccess && rc == SAGE_OK) rc = SAGE_ERR_HIP;
+  return rc;
+}
+
+int sage_attn_int8_fwd_prequant(const void* q_codes, const float* q_scales, const void* k_codes,
+                                const float* k_scales, const void* vt_codes, const float* vt_scales, void* o,
+                                float* lse, int B, int H, int N, int D, int causal, unsigned flags,
+                                hipStream_t stream) {
+  int rc = check_i8(B, H, N, D, flags);
+  if (rc != SAGE_OK) return rc;
+  if (!q_codes || !q_scales || !k_codes || !k_scales || !vt_codes || !vt_scales || !o) return SAGE_ERR_INVALID_ARG;
+  if (!aligned(q_codes, 16) || !aligned(k_codes, 16) || !aligned(vt_codes, 16) || !aligned(o, 16))
+    return SAGE_ERR_INVALID_ARG;
+  if (!aligned(q_scales, 4) || !aligned(k_scales, 4) || !aligned(vt_scales, 4)) return SAGE_ERR_INVALID_ARG;
+  if (lse && !aligned(lse, 4)) return SAGE_ERR_INVALID_ARG;
+  if (causal != 0 && causal != 1) return SAGE_ERR_INVALID_ARG;
+  return attn_i8_prequant_impl(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, o, lse, B, H, N, D, causal,
+                               flags, stream);
 }
 
 const char* sage_status_string(int status) {

@@ -115,6 +115,40 @@ def test_prequant_and_bf16_validation(L):
                                 None) == bd.SAGE_ERR_INVALID_ARG
 
 
+def test_int8_sizes_and_validation(L):
+    B, H, N, D = 2, 3, 300, 128
+    assert bd.quant_int8_sizes(bd.SAGE_ROLE_Q, B, H, N, D) == (B * H * N * D, B * H * 3 * 4)
+    assert bd.quant_int8_sizes(bd.SAGE_ROLE_K, B, H, N, D) == (B * H * 384 * D, B * H * 6 * 4)
+    assert bd.quant_int8_sizes(bd.SAGE_ROLE_V, B, H, N, D) == (B * H * D * 384, B * H * 6 * 4)
+    # only the 16-bit dtype, fp32 output, no-smoothing-K and KV-tile bits are accepted
+    for f in (bd.SAGE_FMT_NV16_E4M3, bd.SAGE_SMOOTH_Q, 0x80):
+        with pytest.raises(bd.SageError):
+            bd.quant_int8_sizes(bd.SAGE_ROLE_Q, 1, 1, 128, 128, f)
+        assert L.sage_attn_int8_workspace_size(1, 1, 128, 128, f) == 0
+        assert L.sage_attn_int8_fwd(FAKE, FAKE, FAKE, FAKE, None, 1, 1, 128, 128, 0, f, None) == bd.SAGE_ERR_INVALID_ARG
+    ws = bd.attn_int8_workspace_size(1, 2, 1000, 128, bd.SAGE_BKV64)
+    assert ws >= 2 * (1000 + 2 * 1024) * 128
+    assert L.sage_attn_int8_fwd_ws(FAKE, FAKE, FAKE, FAKE, None, 1, 2, 1000, 128, 0, 0, FAKE, ws - 1,
+                                   None) == bd.SAGE_ERR_WORKSPACE
+    # shapes, pointers, alignment, causal
+    for bad in (dict(D=96), dict(N=0), dict(causal=2), dict(q=None), dict(o=FAKE + 4), dict(lse=FAKE + 2)):
+        a = dict(q=FAKE, o=FAKE, lse=None, D=128, N=128, causal=0)
+        a.update(bad)
+        rc = L.sage_attn_int8_fwd(a["q"], FAKE, FAKE, a["o"], a["lse"], 1, 1, a["N"], a["D"], a["causal"], 0, None)
+        assert rc == bd.SAGE_ERR_INVALID_ARG, bad
+    # role K with smoothing needs kmean and a large enough workspace; other roles take no kmean
+    assert L.sage_quant_int8(FAKE, 1, 1, 1, 128, 128, 0, FAKE, FAKE, None, FAKE, 1 << 20,
+                             None) == bd.SAGE_ERR_INVALID_ARG
+    assert L.sage_quant_int8(FAKE, 1, 1, 1, 1000, 128, 0, FAKE, FAKE, FAKE, FAKE, 8, None) == bd.SAGE_ERR_WORKSPACE
+    assert L.sage_quant_int8(FAKE, 2, 1, 1, 128, 128, 0, FAKE, FAKE, FAKE, None, 0, None) == bd.SAGE_ERR_INVALID_ARG
+    assert L.sage_quant_int8(FAKE, 0, 1, 1, 128, 128, 0, FAKE, FAKE + 2, None, None, 0,
+                             None) == bd.SAGE_ERR_INVALID_ARG
+    pre = [FAKE] * 6 + [FAKE, None, 1, 1, 128, 128, 0, 0, None]
+    bad = list(pre)
+    bad[1] = FAKE + 2
+    assert L.sage_attn_int8_fwd_prequant(*bad) == bd.SAGE_ERR_INVALID_ARG
+
+
 def test_product_path_does_not_import_oracle():
     import paper_2505_11594_amd
     pkg = os.path.dirname(paper_2505_11594_amd.__file__)
