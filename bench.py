@@ -10,7 +10,9 @@ rows scaled by 20 (seeded synthetic data), MXFP4.
 Throughput is attention TOPS = 4 B H N^2 D / t.  The JSON line also carries
 the attention kernel's own rate (HIP events around repeated launches of the
 kernel alone on the same stream) as a fraction of the MXFP4 dense MFMA peak,
-the bf16-MFMA comparison kernel's rate when available, and the CPU oracle
+the bf16-MFMA comparison kernel's rate when available, the 8-bit attention
+forward of Algorithm 2 (its whole step and its INT8-MFMA kernel alone, with
+its accuracy against exact attention) on the same inputs, and the CPU oracle
 timed on a bounded sample of query rows on the host cores.
 """
 from __future__ import annotations
@@ -30,6 +32,7 @@ sys.path.insert(0, ROOT)
 METRIC = "FP4 attention fwd TOPS at D=128,N=32768; % of MI355X MXFP4 MFMA peak"
 PEAK_FP4_TFLOPS = 10100.0      # MI355X dense MXFP4 MFMA, published
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+PEAK_INT8_TOPS = 5000.0        # MI355X dense int8 MFMA, published
 PEAK_HBM_GBS = 8000.0
 COUNTERS = os.path.join(ROOT, "profiles", "attn_fp4_mx_counters.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2505_11594_amd", "csrc", "attn_fp4.hip")
@@ -134,7 +137,7 @@ def issue_rates(torch):
 
 
 def accuracy_vs_exact(torch, q, k, v, o, w, nrows=512, seed=7):
-    """CosSim, relative L1 and RMSE of the FP4 output against fp64 softmax(QK^T/sqrt(D))V
+    """CosSim, relative L1 and RMSE of an attention output against fp64 softmax(QK^T/sqrt(D))V
     (the paper's accuracy metrics), on a seeded sample of query rows of every head; the
     reference is plain torch fp64 on the GPU."""
     B, H, N, D = w.B, w.H, w.N, w.D
@@ -194,6 +197,47 @@ def other_configs(torch, bd, wl, steps):
     return res
 
 
+def int8_forward(torch, bd, w, qd, kd, vd, o, steps):
+    """Algorithm 2 on the bench inputs: the whole step (k-mean, INT8 quantization
+    of Q, K, V, the INT8 attention kernel with L) and the kernel alone, both
+    timed with HIP events on the launch stream, and its accuracy."""
+    B, H, N, D = w.B, w.H, w.N, w.D
+    flags = (bd.SAGE_IN_BF16 if w.in_dtype == 1 else 0) | bd.SAGE_OUT_F32
+    ws = torch.empty(bd.attn_int8_workspace_size(B, H, N, D, flags), dtype=torch.uint8, device=qd.device)
+    L = torch.empty((B, H, N), dtype=torch.float32, device=qd.device)
+    step = lambda: bd.sage_attn_int8_fwd(qd, kd, vd, causal=w.causal, out=o, lse_out=L, workspace=ws)
+    step()
+    torch.cuda.synchronize()
+    acc = accuracy_vs_exact(torch, qd, kd, vd, o, w)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n = max(3, min(steps, 10))
+    e0.record()
+    for _ in range(n):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    t_step = e0.elapsed_time(e1) / 1e3 / n
+    qq = bd.sage_quant_int8(qd, bd.SAGE_ROLE_Q)
+    kq = bd.sage_quant_int8(kd, bd.SAGE_ROLE_K)
+    vq = bd.sage_quant_int8(vd, bd.SAGE_ROLE_V)
+    run = lambda: bd.sage_attn_int8_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal)
+    run()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(n):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    t_k = e0.elapsed_time(e1) / 1e3 / n
+    tops = w.ops / t_k / 1e12
+    log("int8 forward: step %.3f ms = %.1f TOPS; kernel %.3f ms = %.1f TOPS (%.1f%% of the int8 peak); cossim %.5f"
+        % (t_step * 1e3, w.ops / t_step / 1e12, t_k * 1e3, tops, 100 * tops / PEAK_INT8_TOPS, acc["cossim"]))
+    del ws, qq, kq, vq
+    return {"step_ms": t_step * 1e3, "step_tops": w.ops / t_step / 1e12, "kernel": "attn_int8_kernel<128,128,false,0>",
+            "kernel_ms": t_k * 1e3, "kernel_tops": tops, "peak": PEAK_INT8_TOPS, "frac_of_int8_peak": tops / PEAK_INT8_TOPS,
+            "kv_tile": 128, "accuracy_vs_exact": acc}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,8 +246,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the attention-kernel timings of the other workloads")
-    ap.add_argument("--mode", choices=["full", "attn", "copy", "rates"], default="full",
-                    help="attn: only the attention kernel (for counter runs); "
+    ap.add_argument("--no-int8", action="store_true", help="skip the 8-bit attention forward")
+    ap.add_argument("--mode", choices=["full", "attn", "attn_int8", "copy", "rates"], default="full",
+                    help="attn: only the attention kernel (for counter runs); attn_int8: only the 8-bit one; "
                          "copy: a plain 1 GiB device copy (calibrates FETCH_SIZE / WRITE_SIZE); "
                          "rates: instruction issue-rate microbenchmarks behind the VALU co-bound")
     args = ap.parse_args()
@@ -245,6 +290,16 @@ def main():
 
     def step():
         bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=bd.SAGE_FMT_MXFP4, out_f32=True, out=o, workspace=ws)
+
+    if args.mode == "attn_int8":
+        qq = bd.sage_quant_int8(qd, bd.SAGE_ROLE_Q)
+        kq = bd.sage_quant_int8(kd, bd.SAGE_ROLE_K)
+        vq = bd.sage_quant_int8(vd, bd.SAGE_ROLE_V)
+        for _ in range(args.warmup + args.steps):
+            bd.sage_attn_int8_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal)
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "attn_int8", "launches": args.warmup + args.steps, "ops_per_launch": ops}))
+        return
 
     if args.mode == "attn":
         qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q)
@@ -340,6 +395,10 @@ def main():
         del ws_sq
         others = other_configs(torch, bd, wl, args.steps)
 
+    int8 = None
+    if not args.no_int8:
+        int8 = int8_forward(torch, bd, w, qd, kd, vd, o, args.steps)
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
@@ -369,6 +428,7 @@ def main():
                      "frac_of_hbm_peak": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS},
         "bf16_kernel": bf16,
         "smooth_q_step": smooth_q,
+        "int8_fwd": int8,
         "other_configs": others,
         "cpu_baseline": cpu,
     }

@@ -169,19 +169,21 @@ int sage_attn_bf16_fwd(const void* q, const void* k, const void* v, void* o,
 /* ======================================================================== */
 /* 8-bit attention forward of SageBwd (Algorithm 2, Sec. 4.1).             */
 /*                                                                          */
-/* Accepted flags: SAGE_IN_BF16, SAGE_OUT_F32, SAGE_NO_SMOOTH_K, and       */
-/* SAGE_BKV64 (the KV tile is 64 tokens whether it is set or not); any     */
-/* other bit is SAGE_ERR_INVALID_ARG.  D must be 64 or 128; N >= 1.          */
+/* Accepted flags: SAGE_IN_BF16, SAGE_OUT_F32, SAGE_NO_SMOOTH_K and        */
+/* SAGE_BKV64; any other bit is SAGE_ERR_INVALID_ARG.  The KV tile, which   */
+/* is also the block of psi(K) and psi(V), is bkv = 128 tokens, or 64 with  */
+/* SAGE_BKV64 (the flag must then be passed to every call that touches the  */
+/* quantized tensors).  D must be 64 or 128; N >= 1.                         */
 /*                                                                          */
 /* psi (Eq. psi): one fp32 scale s = max|X|/127 per block of rows -- 128    */
-/* query rows for Q (the last block holds the rest), 64 rows for K and V --  */
+/* query rows for Q (the last block holds the rest), bkv rows for K and V -- */
 /* and int8 codes round(x * fl32(1/s)), nearest, ties to even; an all-zero  */
 /* block has s = 0 and zero codes.  K is first smoothed, K' = fl32(K -       */
 /* kmean), unless SAGE_NO_SMOOTH_K.  Physical layout (Np = N rounded up to  */
 /* 128):                                                                    */
 /*   Q^  int8 [B,H,N,D],  s_Q fp32 [B,H,ceil(N/128)]                        */
-/*   K^  int8 [B,H,Np,D], s_K fp32 [B,H,Np/64]  (rows >= N are zero)         */
-/*   V^T int8 [B,H,D,Np], s_V fp32 [B,H,Np/64]  V transposed; inside every  */
+/*   K^  int8 [B,H,Np,D], s_K fp32 [B,H,Np/bkv] (rows >= N are zero)        */
+/*   V^T int8 [B,H,D,Np], s_V fp32 [B,H,Np/bkv] V transposed; inside every  */
 /*       32-token group, position 16h + 4g + r (h in {0,1}; g, r in 0..3)   */
 /*       holds token 8g + 4h + r (the order in which the int8 MFMA receives */
 /*       P from the accumulator of S^T); tokens >= N are zero.              */
@@ -214,7 +216,7 @@ size_t sage_attn_int8_workspace_size(int B, int H, int N, int D, unsigned flags)
 /*
  * sage_attn_int8_fwd -- Algorithm 2: smoothing K, psi(Q), psi(K), psi(V),
  * S = MM(Q^, K^) s_Q s_K on int8 MFMA (exact int32 products), online softmax
- * over 64-key tiles with the running max m, per-token quantization of P~
+ * over bkv-key tiles with the running max m, per-token quantization of P~
  * reusing the maxima (s_P = rowmax_tile(P~)/127, P^ = rint(P~/s_P)),
  * O = diag(e^{m_old - m_new}) O + MM(P^, V^) s_P s_V on int8 MFMA, O = O/l.
  * Softmax scale 1/sqrt(D); causal = 1 keeps key j for query i iff j <= i.
@@ -237,7 +239,8 @@ int sage_attn_int8_fwd_ws(const void* q, const void* k, const void* v, void* o, 
 
 /* The 8-bit attention kernel alone, on tensors produced by sage_quant_int8
  * (layouts above; kmean is not needed, the smoothing is inside K^).  flags:
- * SAGE_OUT_F32 and SAGE_IN_BF16 (the dtype of a 16-bit o). */
+ * SAGE_OUT_F32, SAGE_IN_BF16 (the dtype of a 16-bit o) and SAGE_BKV64 (as
+ * given to sage_quant_int8). */
 int sage_attn_int8_fwd_prequant(const void* q_codes, const float* q_scales,
                                 const void* k_codes, const float* k_scales,
                                 const void* vt_codes, const float* vt_scales,

@@ -243,11 +243,12 @@ def sage_attn_int8_fwd(q, k, v, causal: bool = False, flags: int = 0, out_f32: b
 
 
 def sage_attn_int8_fwd_prequant(qq, kq, vq, shape, causal: bool = False, in_bf16: bool = True,
-                                out_f32: bool = True, lse: bool = True):
-    """The 8-bit attention kernel alone on (codes, scales) pairs from sage_quant_int8."""
+                                out_f32: bool = True, lse: bool = True, flags: int = 0):
+    """The 8-bit attention kernel alone on (codes, scales) pairs from sage_quant_int8
+    (flags: SAGE_BKV64 as given to sage_quant_int8)."""
     import torch
     B, H, N, D = shape
-    flags = (SAGE_IN_BF16 if in_bf16 else SAGE_IN_FP16) | (SAGE_OUT_F32 if out_f32 else 0)
+    flags = flags | (SAGE_IN_BF16 if in_bf16 else SAGE_IN_FP16) | (SAGE_OUT_F32 if out_f32 else 0)
     dev = qq[0].device
     out = torch.empty(shape, dtype=torch.float32 if out_f32 else (torch.bfloat16 if in_bf16 else torch.float16),
                       device=dev)

@@ -1,6 +1,6 @@
 // 8-bit attention forward of SageBwd (Algorithm 2) for gfx950: per-block INT8
 // Q, K, V (psi, Sec. 4.1), S = MM(Q^, K^) s_Q s_K on int8 MFMA, online
-// softmax over 64-key tiles, per-token INT8 quantization of P~ that reuses
+// softmax over KV tiles (128 or 64 keys), per-token INT8 quantization of P~ that reuses
 // the row maxima (s_P = rowmax(P~)/127), O += MM(P^, V^) s_P s_V on int8
 // MFMA, and the outputs O = O/l and L = m + log l.
 //
@@ -29,10 +29,14 @@
 // s_P s_V after O is rescaled by alpha = 2^{m_old - m_new} (skipped when the
 // whole wave has alpha = 1).
 //
-// Data movement as in the FP4 kernel: KV tiles go from HBM straight into LDS
-// in MFMA-operand order (one 1 KiB block per 64-lane operand read), with the
-// tile's two scales; three stages and one barrier per tile; the S^T products
-// of tile j+1 are issued between the row max of tile j and its exponentials.
+// Data movement: KV tiles go from HBM straight into LDS in MFMA-operand order
+// (one 1 KiB block per 64-lane operand read), with the tile's two scales; two
+// stages and one barrier per tile: after the barrier of tile j its loads
+// have landed and every wave is done with tile j-1, whose stage the loads of
+// tile j+1 then overwrite.  S^T is computed at the top of each tile.  (Issuing
+// tile j+1's S^T under tile j's softmax, as the FP4 kernel does, measured
+// slower here: the second set of int32 scores costs the register room of a
+// third wave per SIMD at 64-key tiles and does not fit at 128.)
 #include "sage_common.h"
 
 typedef int v16i __attribute__((ext_vector_type(16)));
@@ -78,7 +82,7 @@ __global__ __launch_bounds__(256, 2) void attn_int8_kernel(
     void* __restrict__ o, float* __restrict__ lse, int BH, int N, int Np, int nqt, float c2, float log127) {
   using T = I8Stage<D, BKV>;
   constexpr int NSUB = T::NSUB, NKS = T::NKS, NDB = T::NDB;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[3][T::BYTES];
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2][T::BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -170,30 +174,24 @@ __global__ __launch_bounds__(256, 2) void attn_int8_kernel(
     }
   };
 
-  issue(0, 0);
-  if (ntiles > 1) issue(1, 1);
-  i8_wait_loads();
-  __syncthreads();
-  v16i sbuf[2][NSUB];
-  if (!CAUSAL || 0 <= qw + 31) qk(lds[0], sbuf[0]);
-
-  auto tile = [&](auto P_, int j, int stage) {
-    constexpr int P = decltype(P_)::value;     // sbuf[P] holds this tile's S^T, sbuf[P ^ 1] gets the next
+  auto tile = [&](int j, int stage) {
     const uint8_t* L = lds[stage];
     const int kb = j * BKV;
-    // kb < N always holds here; as a run-time test it keeps the compiler from
-    // merging the two tiles of a loop iteration into one schedule, which
-    // does not fit the register budget
+    // kb < N always holds here; kept as a run-time test, it keeps the causal
+    // variant inside the register budget (the compiler otherwise hoists work
+    // across the tile boundary)
     const bool active = (!CAUSAL || kb <= qw + 31) && kb < N;
     float sf[NSUB][16];
     float ct = 0.f, bias = 0.f, alpha = 1.f, sP = 0.f;
     float ps[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     if (active) {
+      v16i sacc[NSUB];
+      qk(L, sacc);
       const float sK = *reinterpret_cast<const float*>(L + T::SC_OFF);
 #pragma unroll
       for (int u = 0; u < NSUB; ++u)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) sf[u][v] = (float)sbuf[P][u][v];   // exact: |acc| < 2^24
+        for (int v = 0; v < 16; ++v) sf[u][v] = (float)sacc[u][v];   // exact: |acc| < 2^24
       const bool need_mask = (kb + BKV > N) || (CAUSAL && kb + BKV - 1 > qw);
       if (need_mask) {
         // element (u, v) is key kb + 32u + 8(v >> 2) + 4hi + (v & 3); kept iff
@@ -236,13 +234,6 @@ __global__ __launch_bounds__(256, 2) void attn_int8_kernel(
       }
     }
 
-    if (j + 1 < ntiles) {
-      i8_wait_loads();
-      __syncthreads();
-      const int nstage = stage == 2 ? 0 : stage + 1;
-      if (j + 2 < ntiles) issue(j + 2, nstage == 2 ? 0 : nstage + 1);
-      if (!CAUSAL || kb + BKV <= qw + 31) qk(lds[nstage], sbuf[P ^ 1]);
-    }
     if (active) {
       // P^ = rint(127 2^{u - t}) per element; the unquantized P~/s_P is summed
       v4i pw[NSUB];
@@ -279,14 +270,12 @@ __global__ __launch_bounds__(256, 2) void attn_int8_kernel(
     }
   };
 
-  int stage = 0;
-  for (int j = 0; j < ntiles; j += 2) {
-    tile(ic<0>{}, j, stage);
-    stage = stage == 2 ? 0 : stage + 1;
-    if (j + 1 < ntiles) {
-      tile(ic<1>{}, j + 1, stage);
-      stage = stage == 2 ? 0 : stage + 1;
-    }
+  issue(0, 0);
+  for (int j = 0; j < ntiles; ++j) {
+    i8_wait_loads();
+    __syncthreads();
+    if (j + 1 < ntiles) issue(j + 1, (j + 1) & 1);
+    tile(j, j & 1);
   }
 
   // ---- epilogue: O = O^T / l stored row-major; L = ln 2 (m + log2 l) ----
@@ -316,36 +305,37 @@ __global__ __launch_bounds__(256, 2) void attn_int8_kernel(
   }
 }
 
-template <int D, bool CAUSAL, int OUT>
+template <int D, int BKV, bool CAUSAL, int OUT>
 static hipError_t launch_i8_t(const void* qc, const float* qs, const void* kc, const float* ks, const void* vc,
                               const float* vs, void* o, float* lse, int BH, int N, int Np, float c2, float log127,
                               hipStream_t st) {
   const int nqt = (N + I8_AQ - 1) / I8_AQ;
-  hipLaunchKernelGGL((attn_int8_kernel<D, 64, CAUSAL, OUT>), dim3((unsigned)(nqt * BH)), dim3(256), 0, st,
+  hipLaunchKernelGGL((attn_int8_kernel<D, BKV, CAUSAL, OUT>), dim3((unsigned)(nqt * BH)), dim3(256), 0, st,
                      (const int8_t*)qc, qs, (const int8_t*)kc, ks, (const int8_t*)vc, vs, o, lse, BH, N, Np, nqt, c2,
                      log127);
   return hipGetLastError();
 }
 
-template <int D, bool CAUSAL>
+template <int D, int BKV, bool CAUSAL>
 static hipError_t launch_i8_o(int out, const void* qc, const float* qs, const void* kc, const float* ks,
                               const void* vc, const float* vs, void* o, float* lse, int BH, int N, int Np, float c2,
                               float log127, hipStream_t st) {
-  if (out == 0) return launch_i8_t<D, CAUSAL, 0>(qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st);
-  if (out == 1) return launch_i8_t<D, CAUSAL, 1>(qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st);
-  return launch_i8_t<D, CAUSAL, 2>(qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st);
+  if (out == 0) return launch_i8_t<D, BKV, CAUSAL, 0>(qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st);
+  if (out == 1) return launch_i8_t<D, BKV, CAUSAL, 1>(qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st);
+  return launch_i8_t<D, BKV, CAUSAL, 2>(qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st);
 }
 
-// KV tile and K, V scale blocks of 64 tokens; Q blocks of 128 rows.
-// qs [BH, ceil(N/128)], ks and vs [BH, Np/64]; lse may be null.
+// KV tile (and K, V scale blocks) of bkv = 64 or 128 tokens; Q blocks of 128
+// rows.  qs [BH, ceil(N/128)], ks and vs [BH, Np/bkv]; lse may be null.
 hipError_t launch_attn_int8(const void* qc, const float* qs, const void* kc, const float* ks, const void* vc,
-                            const float* vs, void* o, float* lse, int BH, int N, int Np, int D, bool causal, int out,
-                            float c2, float log127, hipStream_t st) {
-  if (D == 128)
-    return causal ? launch_i8_o<128, true>(out, qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st)
-                  : launch_i8_o<128, false>(out, qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st);
-  return causal ? launch_i8_o<64, true>(out, qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st)
-                : launch_i8_o<64, false>(out, qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st);
+                            const float* vs, void* o, float* lse, int BH, int N, int Np, int D, int bkv, bool causal,
+                            int out, float c2, float log127, hipStream_t st) {
+#define SAGE_I8(DD, BB)                                                                                      \
+  return causal ? launch_i8_o<DD, BB, true>(out, qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st) \
+                : launch_i8_o<DD, BB, false>(out, qc, qs, kc, ks, vc, vs, o, lse, BH, N, Np, c2, log127, st)
+  if (D == 128) { if (bkv == 128) { SAGE_I8(128, 128); } else { SAGE_I8(128, 64); } }
+  else { if (bkv == 128) { SAGE_I8(64, 128); } else { SAGE_I8(64, 64); } }
+#undef SAGE_I8
 }
 
 }  // namespace sage

@@ -30,8 +30,8 @@ hipError_t launch_transpose_v_bf16(const void* v, void* vt, int BH, int N, int N
 hipError_t launch_quant_i8(const void* x, const float* mu, void* codes, float* scales, int BH, int N, int Nout,
                            int D, int R, int role, bool bf16, hipStream_t st);
 hipError_t launch_attn_int8(const void* qc, const float* qs, const void* kc, const float* ks, const void* vc,
-                            const float* vs, void* o, float* lse, int BH, int N, int Np, int D, bool causal, int out,
-                            float c2, float log127, hipStream_t st);
+                            const float* vs, void* o, float* lse, int BH, int N, int Np, int D, int bkv, bool causal,
+                            int out, float c2, float log127, hipStream_t st);
 }  // namespace sage
 
 namespace {
@@ -174,21 +174,22 @@ int attn_ws_impl(const void* q, const void* k, const void* v, void* o, int B, in
 
 // ---- 8-bit attention (Algorithm 2) ----------------------------------------
 constexpr unsigned kI8Flags = SAGE_IN_BF16 | SAGE_OUT_F32 | SAGE_NO_SMOOTH_K | SAGE_BKV64;
-constexpr int kI8Bq = 128, kI8Bkv = 64;
+constexpr int kI8Bq = 128;
+inline int i8_bkv(unsigned flags) { return (flags & SAGE_BKV64) ? 64 : 128; }   // KV tile = K, V scale block
 
 int check_i8(int B, int H, int N, int D, unsigned flags) {
   if (flags & ~kI8Flags) return SAGE_ERR_INVALID_ARG;
   return check_shape(B, H, N, D, flags & (SAGE_IN_BF16 | SAGE_OUT_F32));
 }
 
-void sizes_i8(int role, int B, int H, int N, int D, size_t* cb, size_t* sb) {
+void sizes_i8(int role, int B, int H, int N, int D, unsigned flags, size_t* cb, size_t* sb) {
   const size_t BH = (size_t)B * H, Np = pad128(N);
   if (role == SAGE_ROLE_Q) {
     *cb = BH * N * D;
     *sb = BH * ((N + kI8Bq - 1) / kI8Bq) * sizeof(float);
   } else {
     *cb = BH * Np * D;
-    *sb = BH * (Np / kI8Bkv) * sizeof(float);
+    *sb = BH * (Np / i8_bkv(flags)) * sizeof(float);
   }
 }
 
@@ -196,14 +197,14 @@ struct I8Ws {
   size_t qc, qs, kc, ks, vc, vs, mu, part, total;
 };
 
-I8Ws i8_ws_layout(int B, int H, int N, int D) {
+I8Ws i8_ws_layout(int B, int H, int N, int D, unsigned flags) {
   I8Ws w;
   size_t c, s, off = 0;
-  sizes_i8(SAGE_ROLE_Q, B, H, N, D, &c, &s);
+  sizes_i8(SAGE_ROLE_Q, B, H, N, D, flags, &c, &s);
   w.qc = off; off += up256(c); w.qs = off; off += up256(s);
-  sizes_i8(SAGE_ROLE_K, B, H, N, D, &c, &s);
+  sizes_i8(SAGE_ROLE_K, B, H, N, D, flags, &c, &s);
   w.kc = off; off += up256(c); w.ks = off; off += up256(s);
-  sizes_i8(SAGE_ROLE_V, B, H, N, D, &c, &s);
+  sizes_i8(SAGE_ROLE_V, B, H, N, D, flags, &c, &s);
   w.vc = off; off += up256(c); w.vs = off; off += up256(s);
   w.mu = off; off += up256((size_t)B * H * D * sizeof(float));
   w.part = off; off += up256(kmean_ws_bytes(B, H, N, D));
@@ -224,9 +225,10 @@ int quant_i8_impl(const void* x, int role, int B, int H, int N, int D, unsigned 
       e = sage::launch_kmean(x, static_cast<double*>(ws), kmean, BH, N, D, bf16, st);
       if (e != hipSuccess) return SAGE_ERR_HIP;
     }
-    e = sage::launch_quant_i8(x, smooth ? kmean : nullptr, codes, scales, BH, N, pad128(N), D, kI8Bkv, 1, bf16, st);
+    e = sage::launch_quant_i8(x, smooth ? kmean : nullptr, codes, scales, BH, N, pad128(N), D, i8_bkv(flags), 1,
+                              bf16, st);
   } else {
-    e = sage::launch_quant_i8(x, nullptr, codes, scales, BH, N, pad128(N), D, kI8Bkv, 2, bf16, st);
+    e = sage::launch_quant_i8(x, nullptr, codes, scales, BH, N, pad128(N), D, i8_bkv(flags), 2, bf16, st);
   }
   return hip_status(e);
 }
@@ -236,13 +238,13 @@ inline float log2_of_127() { return (float)std::log2(127.0); }
 int attn_i8_prequant_impl(const void* qc, const float* qs, const void* kc, const float* ks, const void* vc,
                           const float* vs, void* o, float* lse, int B, int H, int N, int D, int causal,
                           unsigned flags, hipStream_t st) {
-  return hip_status(sage::launch_attn_int8(qc, qs, kc, ks, vc, vs, o, lse, B * H, N, pad128(N), D, causal != 0,
-                                           out_kind(flags), softmax_c2(D), log2_of_127(), st));
+  return hip_status(sage::launch_attn_int8(qc, qs, kc, ks, vc, vs, o, lse, B * H, N, pad128(N), D, i8_bkv(flags),
+                                           causal != 0, out_kind(flags), softmax_c2(D), log2_of_127(), st));
 }
 
 int attn_i8_ws_impl(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int N, int D,
                     int causal, unsigned flags, void* ws, hipStream_t st) {
-  const I8Ws w = i8_ws_layout(B, H, N, D);
+  const I8Ws w = i8_ws_layout(B, H, N, D, flags);
   uint8_t* base = static_cast<uint8_t*>(ws);
   float* qs = reinterpret_cast<float*>(base + w.qs);
   float* ks = reinterpret_cast<float*>(base + w.ks);
@@ -373,7 +375,7 @@ int sage_quant_int8_sizes(int role, int B, int H, int N, int D, unsigned flags, 
   if (role != SAGE_ROLE_Q && role != SAGE_ROLE_K && role != SAGE_ROLE_V) return SAGE_ERR_INVALID_ARG;
   const int rc = check_i8(B, H, N, D, flags);
   if (rc != SAGE_OK) return rc;
-  sizes_i8(role, B, H, N, D, codes_bytes, scales_bytes);
+  sizes_i8(role, B, H, N, D, flags, codes_bytes, scales_bytes);
   return SAGE_OK;
 }
 
@@ -396,7 +398,7 @@ int sage_quant_int8(const void* x, int role, int B, int H, int N, int D, unsigne
 
 size_t sage_attn_int8_workspace_size(int B, int H, int N, int D, unsigned flags) {
   if (check_i8(B, H, N, D, flags) != SAGE_OK) return 0;
-  return i8_ws_layout(B, H, N, D).total;
+  return i8_ws_layout(B, H, N, D, flags).total;
 }
 
 int sage_attn_int8_fwd_ws(const void* q, const void* k, const void* v, void* o, float* lse, int B, int H, int N,
@@ -405,7 +407,7 @@ int sage_attn_int8_fwd_ws(const void* q, const void* k, const void* v, void* o, 
   int rc = attn_i8_args(q, k, v, o, lse, B, H, N, D, causal, flags);
   if (rc != SAGE_OK) return rc;
   if (!workspace || !aligned(workspace, 256)) return SAGE_ERR_INVALID_ARG;
-  if (workspace_bytes < i8_ws_layout(B, H, N, D).total) return SAGE_ERR_WORKSPACE;
+  if (workspace_bytes < i8_ws_layout(B, H, N, D, flags).total) return SAGE_ERR_WORKSPACE;
   return attn_i8_ws_impl(q, k, v, o, lse, B, H, N, D, causal, flags, workspace, stream);
 }
 
@@ -413,7 +415,7 @@ int sage_attn_int8_fwd(const void* q, const void* k, const void* v, void* o, flo
                        int causal, unsigned flags, hipStream_t stream) {
   int rc = attn_i8_args(q, k, v, o, lse, B, H, N, D, causal, flags);
   if (rc != SAGE_OK) return rc;
-  const size_t bytes = i8_ws_layout(B, H, N, D).total;
+  const size_t bytes = i8_ws_layout(B, H, N, D, flags).total;
   void* ws = nullptr;
   if (hipMallocAsync(&ws, bytes, stream) != hipSuccess) return SAGE_ERR_HIP;
   rc = attn_i8_ws_impl(q, k, v, o, lse, B, H, N, D, causal, flags, ws, stream);

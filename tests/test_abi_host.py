@@ -118,8 +118,10 @@ def test_prequant_and_bf16_validation(L):
 def test_int8_sizes_and_validation(L):
     B, H, N, D = 2, 3, 300, 128
     assert bd.quant_int8_sizes(bd.SAGE_ROLE_Q, B, H, N, D) == (B * H * N * D, B * H * 3 * 4)
-    assert bd.quant_int8_sizes(bd.SAGE_ROLE_K, B, H, N, D) == (B * H * 384 * D, B * H * 6 * 4)
-    assert bd.quant_int8_sizes(bd.SAGE_ROLE_V, B, H, N, D) == (B * H * D * 384, B * H * 6 * 4)
+    assert bd.quant_int8_sizes(bd.SAGE_ROLE_K, B, H, N, D) == (B * H * 384 * D, B * H * 3 * 4)
+    assert bd.quant_int8_sizes(bd.SAGE_ROLE_V, B, H, N, D) == (B * H * D * 384, B * H * 3 * 4)
+    # 64-key tiles: scale blocks of 64 rows
+    assert bd.quant_int8_sizes(bd.SAGE_ROLE_K, B, H, N, D, bd.SAGE_BKV64) == (B * H * 384 * D, B * H * 6 * 4)
     # only the 16-bit dtype, fp32 output, no-smoothing-K and KV-tile bits are accepted
     for f in (bd.SAGE_FMT_NV16_E4M3, bd.SAGE_SMOOTH_Q, 0x80):
         with pytest.raises(bd.SageError):

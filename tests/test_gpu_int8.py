@@ -16,7 +16,11 @@ from test_gpu_attn import check, o_rows
 
 pytestmark = pytest.mark.gpu
 
-BKV = 64
+BKV = 128      # the default KV tile; SAGE_BKV64 selects 64
+
+
+def bkv_flag(bkv):
+    return bd.SAGE_BKV64 if bkv == 64 else 0
 
 
 def v_stored_position(t):
@@ -28,15 +32,15 @@ def v_stored_position(t):
     return (t & ~31) | (h << 4) | (g << 2) | r
 
 
-def logical_i8(codes, scales, role, B, H, N, D):
+def logical_i8(codes, scales, role, B, H, N, D, bkv=BKV):
     """Device buffers -> the oracle's layout, and the padding that must be zero."""
     c = codes.cpu().numpy()
     s = scales.cpu().numpy()
     if role == bd.SAGE_ROLE_Q:
         return c.reshape(B, H, N, D), s.reshape(B, H, -1), np.zeros(0), np.zeros(0)
     Np = pad128(N)
-    nb = (N + BKV - 1) // BKV
-    s = s.reshape(B, H, Np // BKV)
+    nb = (N + bkv - 1) // bkv
+    s = s.reshape(B, H, Np // bkv)
     if role == bd.SAGE_ROLE_K:
         c = c.reshape(B, H, Np, D)
         return c[:, :, :N], s[:, :, :nb], c[:, :, N:], s[:, :, nb:]
@@ -47,8 +51,9 @@ def logical_i8(codes, scales, role, B, H, N, D):
     return logical, s[:, :, :nb], vt[:, :, :, tail], s[:, :, nb:]
 
 
-def gpu_i8(q, k, v, in_dtype, causal, flags=0, out_f32=True):
+def gpu_i8(q, k, v, in_dtype, causal, flags=0, out_f32=True, bkv=BKV):
     torch = torch_dev()
+    flags |= bkv_flag(bkv)
     o, L = bd.sage_attn_int8_fwd(to_dev(q, in_dtype), to_dev(k, in_dtype), to_dev(v, in_dtype), causal=causal,
                                  flags=flags, out_f32=out_f32)
     torch.cuda.synchronize()
@@ -66,16 +71,17 @@ def check_lse(got, ref, label):
                                    (1, 3, 300, 128), (1, 1, 1000, 64)])
 @pytest.mark.parametrize("in_dtype", [0, 1])
 @pytest.mark.parametrize("smooth", [True, False])
-def test_quant_int8_bit_exact(shape, in_dtype, smooth):
+@pytest.mark.parametrize("bkv", [64, 128])
+def test_quant_int8_bit_exact(shape, in_dtype, smooth, bkv):
     B, H, N, D = shape
-    say("quant int8", shape, "dtype", in_dtype, "smooth", smooth)
+    say("quant int8", shape, "dtype", in_dtype, "smooth", smooth, "bkv", bkv)
     q, k, v = wl.make_inputs(B, H, N, D, in_dtype, seed=700 + N + D, k_bias_var=4.0, outlier_frac=0.02)
     torch = torch_dev()
-    for role, x, blk in ((bd.SAGE_ROLE_Q, q, 128), (bd.SAGE_ROLE_K, k, BKV), (bd.SAGE_ROLE_V, v, BKV)):
-        flags = 0 if smooth else bd.SAGE_NO_SMOOTH_K
+    for role, x, blk in ((bd.SAGE_ROLE_Q, q, 128), (bd.SAGE_ROLE_K, k, bkv), (bd.SAGE_ROLE_V, v, bkv)):
+        flags = (0 if smooth else bd.SAGE_NO_SMOOTH_K) | bkv_flag(bkv)
         codes, scales, mu = bd.sage_quant_int8(to_dev(x, in_dtype), role, flags)
         torch.cuda.synchronize()
-        c, s, ctail, stail = logical_i8(codes, scales, role, B, H, N, D)
+        c, s, ctail, stail = logical_i8(codes, scales, role, B, H, N, D, bkv)
         oc, os_, omu = oracle.quant_int8(x, in_dtype, role, blk, smooth_k=smooth)
         assert np.array_equal(c, oc), role
         assert np.array_equal(s.view(np.uint32), os_.view(np.uint32)), role
@@ -93,7 +99,7 @@ def test_quant_int8_zero_blocks():
     k[:] = k[:, :, :1]
     torch = torch_dev()
     for role, x, blk in ((bd.SAGE_ROLE_Q, q, 128), (bd.SAGE_ROLE_K, k, BKV)):
-        codes, scales, _ = bd.sage_quant_int8(to_dev(x, 1), role)
+        codes, scales, _ = bd.sage_quant_int8(to_dev(x, 1), role, bkv_flag(BKV))
         torch.cuda.synchronize()
         c, s, _, _ = logical_i8(codes, scales, role, B, H, N, D)
         oc, os_, _ = oracle.quant_int8(x, 1, role, blk)
@@ -104,12 +110,13 @@ def test_quant_int8_zero_blocks():
 @pytest.mark.parametrize("N", [1, 64, 100, 257, 640])
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("causal", [False, True])
-def test_attn_int8_edge_shapes(N, D, causal):
-    say("attn int8 edge N=%d D=%d causal=%d" % (N, D, causal))
+@pytest.mark.parametrize("bkv", [64, 128])
+def test_attn_int8_edge_shapes(N, D, causal, bkv):
+    say("attn int8 edge N=%d D=%d causal=%d bkv=%d" % (N, D, causal, bkv))
     in_dtype = 1 if (N + D) % 2 else 0
     q, k, v = wl.make_inputs(1, 2, N, D, in_dtype, seed=720 + N, k_bias_var=4.0, outlier_frac=0.02)
-    o, L = gpu_i8(q, k, v, in_dtype, causal)
-    ref, lref, tie, _ = oracle.attn_int8(q, k, v, in_dtype, causal, BKV)
+    o, L = gpu_i8(q, k, v, in_dtype, causal, bkv=bkv)
+    ref, lref, tie, _ = oracle.attn_int8(q, k, v, in_dtype, causal, bkv)
     check(o.cpu().numpy().reshape(-1, D), ref, tie, "int8 edge")
     check_lse(L.cpu().numpy().ravel(), lref, "int8 edge")
 
