@@ -26,7 +26,7 @@ IN_FP16, IN_BF16 = 0, 1
 ROLE_Q, ROLE_K, ROLE_V = 0, 1, 2
 NO_SMOOTH_K, DIRECT_P, R_LITERAL, SMOOTH_Q, OCP_SCALE = 1, 2, 4, 8, 16
 # 8-bit attention (Algorithm 2) flags: NO_SMOOTH_K, and
-I8_STATIC_P, I8_IDENTITY = 32, 64
+I8_STATIC_P, I8_IDENTITY, I8_DP_INT8 = 32, 64, 128
 
 _lib = None
 
@@ -101,6 +101,9 @@ def lib():
         L.orc_attn_int8.restype = ctypes.c_int
         L.orc_attn_int8.argtypes = ([ctypes.c_void_p] * 3 + [ctypes.c_int] * 8 + [ctypes.c_uint] +
                                     [ctypes.c_void_p, ctypes.c_int64] + [ctypes.c_void_p] * 4 + [ctypes.c_int])
+        L.orc_attn_int8_bwd.restype = ctypes.c_int
+        L.orc_attn_int8_bwd.argtypes = ([ctypes.c_void_p] * 6 + [ctypes.c_int] * 8 + [ctypes.c_uint] +
+                                        [ctypes.c_void_p] * 6 + [ctypes.c_int])
         _lib = L
     return _lib
 
@@ -340,3 +343,22 @@ def attn_int8(q_bits, k_bits, v_bits, in_dtype: int, causal: bool, bkv: int, row
     if rc != 0:
         raise ValueError("orc_attn_int8: invalid arguments")
     return out, lse, tol, dict(tie_codes=int(cnt[0]), skipped_tiles=int(cnt[1]))
+
+
+def attn_int8_bwd(q_bits, k_bits, v_bits, do_bits, o, lse, in_dtype: int, causal: bool, bkv: int, flags: int = 0,
+                  bq: int = 128, tolerance: bool = True, nthreads: int | None = None):
+    """Algorithm 3 (the 8-bit attention backward) for every head.  o: the forward's
+    output fp32 [B,H,N,D]; lse: its L fp32 [B,H,N].  Returns (dq, dk, dv) fp32
+    [B,H,N,D] and, with tolerance, the per-element tolerances (tq, tk, tv)."""
+    B, H, N, D = q_bits.shape
+    arrs = [np.ascontiguousarray(a, dtype=np.uint16) for a in (q_bits, k_bits, v_bits, do_bits)]
+    o = np.ascontiguousarray(o, dtype=np.float32).reshape(B, H, N, D)
+    lse = np.ascontiguousarray(lse, dtype=np.float32).reshape(B, H, N)
+    outs = [np.zeros((B, H, N, D), dtype=np.float32) for _ in range(6 if tolerance else 3)]
+    tp = [_ptr(x) for x in outs[3:]] if tolerance else [None] * 3
+    rc = lib().orc_attn_int8_bwd(*[_ptr(a) for a in arrs], _ptr(o), _ptr(lse), in_dtype, B, H, N, D,
+                                 int(bool(causal)), bq, bkv, flags, *[_ptr(x) for x in outs[:3]], *tp,
+                                 nthreads or default_threads())
+    if rc != 0:
+        raise ValueError("orc_attn_int8_bwd: invalid arguments")
+    return tuple(outs[:3]) + ((tuple(outs[3:]),) if tolerance else ())

@@ -1,6 +1,7 @@
 /*
- * sage_oracle_int8.c -- plain, slow CPU oracle for the 8-bit attention
- * forward of SageBwd (arXiv 2505.11594, Algorithm 2).
+ * sage_oracle_int8.c -- plain, slow CPU oracle for the 8-bit attention of
+ * SageBwd (arXiv 2505.11594): the forward (Algorithm 2) and the backward
+ * (Algorithm 3, further below).
  *
  * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
  * benchmark's CPU-baseline leg may load this library.  It shares no source
@@ -339,5 +340,307 @@ int orc_attn_int8(const uint16_t* q, const uint16_t* k, const uint16_t* v, int i
   if (counters) { counters[0] = J.cnt[0]; counters[1] = J.cnt[1]; }
   for (long bh = 0; bh < (long)B * H; ++bh) if (used[bh]) i8_free_head(&J.heads[bh]);
   free(J.heads); free(used);
+  return 0;
+}
+
+/* ======================================================================== */
+/* Backward pass of the 8-bit attention (Algorithm 3).                      */
+/*                                                                          */
+/* Readings (the kernels implement the same):                               */
+/*  - inputs: Q, K, V, dO 16-bit, O fp32 and L fp32 from the forward; Q^,   */
+/*    K^ (and K_m) are psi of the forward's blocks (B_q = 128 rows of Q,    */
+/*    B_kv rows of K' = fl32(K - K_m)); V enters only dP = MM(dO, V^T),     */
+/*    which stays in 16-bit inputs with fp32 accumulation ("keep in FP16"): */
+/*    dP = fl32 of the exact dot product.                                   */
+/*  - D_q = fl32(sum_d dO[q,d] O[q,d]) (exact sum, rounded once).           */
+/*  - scores as in the forward: u = fl32(fl32(acc) c_t) in the log2 domain; */
+/*    P = exp(S/sqrt(D) - L) = exp2(fma(fl32(acc), c_t, -Lb)),             */
+/*    Lb = fl32(L fl32(log2 e)); masked entries have P = 0.                 */
+/*  - psi of P, dO and dS per (B_q x B_kv) block, (B_q x D) block and      */
+/*    (B_q x B_kv) block, as psi of the forward (s = fl32(max|x|/127),      */
+/*    codes rint(fl32(x fl32(1/s)))).  A block with no visible entry is     */
+/*    skipped.                                                              */
+/*  - dS = fl32(P fl32(dP - D)); the softmax scale enters dQ and dK: with   */
+/*    rsd = fl32(1/sqrt(D)),                                                */
+/*      dV_j = fma(fl32(MM(P^T, dO^)), fl32(s_P s_dO), dV_j)                */
+/*      dK_j = fma(fl32(MM(dS^T, Q^)), fl32(fl32(s_dS s_Q) rsd), dK_j)      */
+/*      dQ_i = fma(fl32(MM(dS^, K^)), fl32(fl32(s_dS s_K) rsd), dQ_i)       */
+/*             then + fl32(fl32(rowsum(dS) rsd) K_m) (smoothing K; the     */
+/*             rowsum sequential in fp32 over the block's keys),            */
+/*    accumulated in the order of Algorithm 3 (KV block j outer, query      */
+/*    block i inner).                                                       */
+/*  - tolerance: a code of P^ or dS^ whose pre-rounding value lies within a */
+/*    window of a rounding midpoint may take either neighbour on a GPU      */
+/*    (exp2 to 1 ulp; dP and D summed in another order); each such code     */
+/*    adds the size of its effect to the per-element tolerance of dV, dK,   */
+/*    dQ.  The window: 8 ulp of the value for P^, and for dS^ the bound     */
+/*    |P| (e_dP + e_D) + |dP - D| |P| 2^-21 (e_x = 2^-17 times the sum of   */
+/*    |terms| of x) over s_dS, plus 8 ulp; block scales that move by an ulp */
+/*    shift every code by a relative 2^-22, also inside the window.          */
+/* Flags: ORC_NO_SMOOTH_K, ORC_I8_IDENTITY (no psi anywhere: the exact      */
+/* gradients of softmax attention up to fp32 rounding), ORC_I8_DP_INT8      */
+/* (ablation, Table 1(c): dP = MM(dO^, V^) with per-block INT8 dO and V).    */
+/* ======================================================================== */
+#define ORC_I8_DP_INT8 128u
+
+typedef struct {
+  const uint16_t *q, *k, *v, *dout;
+  const float *o, *lse;
+  int in_dtype, B, H, N, D, causal, bq, bkv;
+  unsigned flags;
+  float *dq, *dk, *dv, *tq, *tk, *tv;
+  long next;
+  pthread_mutex_t mu;
+} i8bwd_t;
+
+static double mid_dist(float y) {
+  /* distance of |y| to the nearest rounding midpoint k + 1/2 */
+  double a = fabs((double)y);
+  return fabs(a - (floor(a) + 0.5));
+}
+
+static void i8_bwd_head(i8bwd_t* J, long bh) {
+  const int N = J->N, D = J->D, bq = J->bq, bkv = J->bkv;
+  const long ND = (long)N * D;
+  const int ident = (J->flags & ORC_I8_IDENTITY) != 0, smooth = !(J->flags & ORC_NO_SMOOTH_K);
+  const int dp8 = (J->flags & ORC_I8_DP_INT8) != 0;
+  const uint16_t *qb = J->q + bh * ND, *kb = J->k + bh * ND, *vb = J->v + bh * ND, *gb = J->dout + bh * ND;
+  const float *ob = J->o + bh * ND, *lb = J->lse + bh * (long)N;
+  float *dq = J->dq + bh * ND, *dk = J->dk + bh * ND, *dv = J->dv + bh * ND;
+  float *tq = J->tq ? J->tq + bh * ND : NULL, *tk = J->tk ? J->tk + bh * ND : NULL, *tv = J->tv ? J->tv + bh * ND : NULL;
+  const int nqb = (N + bq - 1) / bq, nkb = (N + bkv - 1) / bkv;
+  const float c2 = (float)(1.0 / (log(2.0) * sqrt((double)D)));
+  const float rsd = (float)(1.0 / sqrt((double)D));
+  const float log2e = (float)(1.0 / log(2.0));
+
+  float* mu = (float*)calloc(D, sizeof(float));
+  int8_t *qc = (int8_t*)calloc(ND, 1), *kc = (int8_t*)calloc(ND, 1), *gc = (int8_t*)calloc(ND, 1);
+  int8_t *vc8 = (int8_t*)calloc(ND, 1);
+  float *qs = (float*)calloc(nqb, sizeof(float)), *ks = (float*)calloc(nkb, sizeof(float));
+  float *gs = (float*)calloc(nqb, sizeof(float)), *vs8 = (float*)calloc(nkb, sizeof(float));
+  float *qf = (float*)malloc(sizeof(float) * ND), *kf = (float*)malloc(sizeof(float) * ND);
+  float *vf = (float*)malloc(sizeof(float) * ND), *gf = (float*)malloc(sizeof(float) * ND);
+  if (smooth) orc_kmean(kb, J->in_dtype, 1, 1, N, D, mu);
+  for (long e = 0; e < ND; ++e) {
+    qf[e] = orc_widen(qb[e], J->in_dtype);
+    float kv = orc_widen(kb[e], J->in_dtype);
+    if (smooth) { volatile float d = kv - mu[e % D]; kv = d; }
+    kf[e] = kv;
+    vf[e] = orc_widen(vb[e], J->in_dtype);
+    gf[e] = orc_widen(gb[e], J->in_dtype);
+  }
+  if (!ident) {
+    orc_quant_int8(qb, J->in_dtype, ORC_ROLE_Q, 1, 1, N, D, bq, 0, qc, qs, NULL);
+    float* mu2 = (float*)calloc(D, sizeof(float));
+    orc_quant_int8(kb, J->in_dtype, ORC_ROLE_K, 1, 1, N, D, bkv, smooth, kc, ks, mu2);
+    free(mu2);
+    orc_quant_int8(gb, J->in_dtype, ORC_ROLE_Q, 1, 1, N, D, bq, 0, gc, gs, NULL);
+    if (dp8) orc_quant_int8(vb, J->in_dtype, ORC_ROLE_V, 1, 1, N, D, bkv, 0, vc8, vs8, NULL);
+  }
+  /* D_q and Lb_q */
+  float* Dr = (float*)malloc(sizeof(float) * N);
+  float* Lb = (float*)malloc(sizeof(float) * N);
+  double* Dabs = (double*)malloc(sizeof(double) * N);
+  for (int q = 0; q < N; ++q) {
+    double s = 0.0, a = 0.0;
+    for (int c = 0; c < D; ++c) { double t = (double)gf[(long)q * D + c] * (double)ob[(long)q * D + c]; s += t; a += fabs(t); }
+    Dr[q] = (float)s; Dabs[q] = a;
+    volatile float l2 = lb[q] * log2e;
+    Lb[q] = l2;
+  }
+  memset(dq, 0, sizeof(float) * ND); memset(dk, 0, sizeof(float) * ND); memset(dv, 0, sizeof(float) * ND);
+  if (tq) { memset(tq, 0, sizeof(float) * ND); memset(tk, 0, sizeof(float) * ND); memset(tv, 0, sizeof(float) * ND); }
+
+  float* P = (float*)malloc(sizeof(float) * (size_t)bq * bkv);
+  float* dS = (float*)malloc(sizeof(float) * (size_t)bq * bkv);
+  float* Pc = (float*)malloc(sizeof(float) * (size_t)bq * bkv);     /* P^ (identity: P)  */
+  float* Sc = (float*)malloc(sizeof(float) * (size_t)bq * bkv);     /* dS^ (identity: dS) */
+  double* win = (double*)malloc(sizeof(double) * (size_t)bq * bkv);
+  char* vis = (char*)malloc((size_t)bq * bkv);
+  double* acc = (double*)malloc(sizeof(double) * (size_t)(bq > bkv ? bq : bkv) * D);
+
+  for (int j = 0; j < nkb; ++j) {
+    const int k0 = j * bkv, k1 = (k0 + bkv < N) ? k0 + bkv : N, nk = k1 - k0;
+    for (int i = 0; i < nqb; ++i) {
+      const int q0 = i * bq, q1 = (q0 + bq < N) ? q0 + bq : N, nq = q1 - q0;
+      int any = 0;
+      memset(vis, 0, (size_t)bq * bkv);
+      memset(P, 0, sizeof(float) * (size_t)bq * bkv);
+      memset(dS, 0, sizeof(float) * (size_t)bq * bkv);
+      for (int a = 0; a < nq; ++a)
+        for (int b = 0; b < nk; ++b) {
+          const int vv = !(J->causal && k0 + b > q0 + a);
+          vis[a * bkv + b] = (char)vv;
+          any |= vv;
+        }
+      if (!any) continue;
+      const float sQ = ident ? 1.0f : qs[i], sK = ident ? 1.0f : ks[j];
+      volatile float sqk = sQ * sK;
+      volatile float ct = sqk * c2;
+      /* P = exp(S - L) and dS = P (dP - D) */
+      float pmax = 0.0f;
+      for (int a = 0; a < nq; ++a)
+        for (int b = 0; b < nk; ++b) {
+          const int q = q0 + a, k = k0 + b, e = a * bkv + b;
+          if (!vis[e]) { P[e] = 0.0f; dS[e] = 0.0f; continue; }
+          float accf;
+          if (ident) {
+            double s = 0.0;
+            for (int c = 0; c < D; ++c) s += (double)qf[(long)q * D + c] * (double)kf[(long)k * D + c];
+            accf = (float)s;
+          } else {
+            long s = 0;
+            for (int c = 0; c < D; ++c) s += (long)qc[(long)q * D + c] * kc[(long)k * D + c];
+            accf = (float)s;
+          }
+          P[e] = exp2_cr(fmaf(accf, ct, -Lb[q]));
+          if (P[e] > pmax) pmax = P[e];
+        }
+      float dsmax = 0.0f;
+      for (int a = 0; a < nq; ++a)
+        for (int b = 0; b < nk; ++b) {
+          const int q = q0 + a, k = k0 + b, e = a * bkv + b;
+          win[e] = 0.0;
+          if (!vis[e]) continue;
+          double s = 0.0, sa = 0.0;
+          if (dp8) {
+            long si = 0;
+            for (int c = 0; c < D; ++c) si += (long)gc[(long)q * D + c] * vc8[(long)k * D + c];
+            s = (double)(float)si * (double)(float)(gs[i] * vs8[j]);
+            sa = fabs(s);
+          } else {
+            for (int c = 0; c < D; ++c) { double t = (double)gf[(long)q * D + c] * (double)vf[(long)k * D + c]; s += t; sa += fabs(t); }
+          }
+          const float dP = (float)s;
+          volatile float d = dP - Dr[q];
+          volatile float ds = P[e] * d;
+          dS[e] = ds;
+          if (fabsf(ds) > dsmax) dsmax = fabsf(ds);
+          /* error window of dS from the GPU's other summation orders and exp2 */
+          win[e] = fabs((double)P[e]) * (ldexp(sa, -17) + ldexp(Dabs[q], -17)) + fabs((double)d) * fabs((double)P[e]) * ldexp(1.0, -21);
+        }
+      /* psi(P) over the block, psi(dS) over the block */
+      float sP = 1.0f, sdS = 1.0f;
+      if (!ident) {
+        volatile float s1 = pmax / 127.0f; sP = s1;
+        volatile float r1 = pmax > 0.0f ? 1.0f / sP : 0.0f;
+        volatile float s2 = dsmax / 127.0f; sdS = s2;
+        volatile float r2 = dsmax > 0.0f ? 1.0f / sdS : 0.0f;
+        for (int e = 0; e < bq * bkv; ++e) {
+          volatile float y1 = P[e] * r1;
+          volatile float y2 = dS[e] * r2;
+          Pc[e] = rintf(y1);
+          Sc[e] = rintf(y2);
+          if (tq) {
+            /* flag codes near a midpoint; the effect goes into the tolerance */
+            const double w1 = fabs((double)y1) * ldexp(1.0, -20) + ldexp(1.0, -20);
+            const double w2 = win[e] * (double)r2 + fabs((double)y2) * ldexp(1.0, -20) + ldexp(1.0, -20);
+            const int a = e / bkv, b = e % bkv;
+            if (vis[e] && a < nq && b < nk) {
+              const int q = q0 + a, k = k0 + b;
+              if (mid_dist(y1) <= w1) {
+                const double f = (double)sP * gs[i];
+                for (int c = 0; c < D; ++c) tv[(long)k * D + c] += (float)(f * abs(gc[(long)q * D + c]));
+              }
+              if (mid_dist(y2) <= w2) {
+                const double fk = (double)sdS * qs[i] * rsd, fq = (double)sdS * ks[j] * rsd;
+                for (int c = 0; c < D; ++c) {
+                  tk[(long)k * D + c] += (float)(fk * abs(qc[(long)q * D + c]));
+                  tq[(long)q * D + c] += (float)(fq * abs(kc[(long)k * D + c]));
+                }
+              }
+            }
+          }
+        }
+      } else {
+        for (int e = 0; e < bq * bkv; ++e) { Pc[e] = P[e]; Sc[e] = dS[e]; }
+      }
+      /* dV_j += MM(P^T, dO^) s_P s_dO */
+      {
+        volatile float f = sP * (ident ? 1.0f : gs[i]);
+        for (int b = 0; b < nk; ++b)
+          for (int c = 0; c < D; ++c) {
+            double s = 0.0;
+            for (int a = 0; a < nq; ++a)
+              s += (double)Pc[a * bkv + b] * (ident ? (double)gf[(long)(q0 + a) * D + c] : (double)gc[(long)(q0 + a) * D + c]);
+            const long o = (long)(k0 + b) * D + c;
+            dv[o] = fmaf((float)s, f, dv[o]);
+          }
+      }
+      /* dK_j += MM(dS^T, Q^) s_dS s_Q / sqrt(D) */
+      {
+        volatile float f0 = sdS * sQ;
+        volatile float f = f0 * rsd;
+        for (int b = 0; b < nk; ++b)
+          for (int c = 0; c < D; ++c) {
+            double s = 0.0;
+            for (int a = 0; a < nq; ++a)
+              s += (double)Sc[a * bkv + b] * (ident ? (double)qf[(long)(q0 + a) * D + c] : (double)qc[(long)(q0 + a) * D + c]);
+            const long o = (long)(k0 + b) * D + c;
+            dk[o] = fmaf((float)s, f, dk[o]);
+          }
+      }
+      /* dQ_i += MM(dS^, K^) s_dS s_K / sqrt(D) + rowsum(dS) K_m / sqrt(D) */
+      {
+        volatile float f0 = sdS * sK;
+        volatile float f = f0 * rsd;
+        for (int a = 0; a < nq; ++a) {
+          float rs = 0.0f;
+          for (int b = 0; b < nk; ++b) rs += dS[a * bkv + b];
+          volatile float rr = rs * rsd;
+          for (int c = 0; c < D; ++c) {
+            double s = 0.0;
+            for (int b = 0; b < nk; ++b)
+              s += (double)Sc[a * bkv + b] * (ident ? (double)kf[(long)(k0 + b) * D + c] : (double)kc[(long)(k0 + b) * D + c]);
+            const long o = (long)(q0 + a) * D + c;
+            float x = fmaf((float)s, f, dq[o]);
+            if (smooth) x = fmaf(rr, mu[c], x);
+            dq[o] = x;
+          }
+        }
+      }
+    }
+  }
+  free(mu); free(qc); free(kc); free(gc); free(vc8); free(qs); free(ks); free(gs); free(vs8);
+  free(qf); free(kf); free(vf); free(gf); free(Dr); free(Lb); free(Dabs);
+  free(P); free(dS); free(Pc); free(Sc); free(win); free(vis); free(acc);
+}
+
+static void* i8_bwd_worker(void* arg) {
+  i8bwd_t* J = (i8bwd_t*)arg;
+  for (;;) {
+    pthread_mutex_lock(&J->mu);
+    long bh = J->next++;
+    pthread_mutex_unlock(&J->mu);
+    if (bh >= (long)J->B * J->H) break;
+    i8_bwd_head(J, bh);
+  }
+  return NULL;
+}
+
+/* ------------------------------------------------------------------------ */
+/* orc_attn_int8_bwd: Algorithm 3 for every head.                            */
+/*  q, k, v, dout: 16-bit [B,H,N,D]; o fp32 [B,H,N,D]; lse fp32 [B,H,N]     */
+/*  dq, dk, dv: fp32 [B,H,N,D] outputs; tq, tk, tv: per-element tolerances  */
+/*  (same shape) or all NULL.  Returns 0, or -1 for invalid arguments.      */
+/* ------------------------------------------------------------------------ */
+int orc_attn_int8_bwd(const uint16_t* q, const uint16_t* k, const uint16_t* v, const uint16_t* dout,
+                      const float* o, const float* lse, int in_dtype, int B, int H, int N, int D, int causal,
+                      int bq, int bkv, unsigned flags, float* dq, float* dk, float* dv, float* tq, float* tk,
+                      float* tv, int nthreads) {
+  if (B <= 0 || H <= 0 || N <= 0 || D <= 0 || D > 128 || bq <= 0 || bkv <= 0) return -1;
+  if ((tq == NULL) != (tk == NULL) || (tq == NULL) != (tv == NULL)) return -1;
+  i8bwd_t J;
+  memset(&J, 0, sizeof(J));
+  J.q = q; J.k = k; J.v = v; J.dout = dout; J.o = o; J.lse = lse; J.in_dtype = in_dtype;
+  J.B = B; J.H = H; J.N = N; J.D = D; J.causal = causal; J.bq = bq; J.bkv = bkv; J.flags = flags;
+  J.dq = dq; J.dk = dk; J.dv = dv; J.tq = tq; J.tk = tk; J.tv = tv;
+  pthread_mutex_init(&J.mu, NULL);
+  if (nthreads < 1) nthreads = 1;
+  pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)nthreads);
+  for (int t = 0; t < nthreads; ++t) pthread_create(&th[t], NULL, i8_bwd_worker, &J);
+  for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
+  free(th);
+  pthread_mutex_destroy(&J.mu);
   return 0;
 }
