@@ -1,7 +1,7 @@
 /*
  * sage_mi355x.h -- C ABI of the MI355X (gfx950) microscaled-FP4 attention
  * forward of SageAttention3 (arXiv 2505.11594), and of the paper's 8-bit
- * attention forward (SageBwd, Algorithm 2).
+ * attention (SageBwd: the forward of Algorithm 2, the backward of Algorithm 3).
  *
  * Every function returns an int status (sage_status).  Arguments are checked
  * on the host before any HIP call, so invalid calls fail without touching the
@@ -246,6 +246,39 @@ int sage_attn_int8_fwd_prequant(const void* q_codes, const float* q_scales,
                                 const void* vt_codes, const float* vt_scales,
                                 void* o, float* lse, int B, int H, int N, int D, int causal,
                                 unsigned flags, hipStream_t stream);
+
+/*
+ * sage_attn_int8_bwd -- the backward pass of the 8-bit attention (Algorithm
+ * 3): D = rowsum(dO o O); per KV block j and query block i (128 x 128):
+ * S = MM(Q^, K^) s_Q s_K, P = exp(S/sqrt(D) - L), psi(P), psi(dO) (per 128
+ * rows), dV_j += MM(P^T, dO^) s_P s_dO, dP = MM(dO, V^T) in the 16-bit input
+ * type with fp32 accumulation, dS = P o (dP - D), psi(dS), dQ_i +=
+ * MM(dS^, K^) s_dS s_K / sqrt(D) + rowsum(dS) K_m / sqrt(D) (the smoothing
+ * of K), dK_j += MM(dS^T, Q^) s_dS s_Q / sqrt(D).  Q^, K^ and K_m are
+ * recomputed exactly as the forward computes them (psi blocks of 128 rows).
+ *  q, k, v, dout: 16-bit [B,H,N,D] (dO has the input dtype), 16-byte aligned
+ *  o    : the forward's output, fp32 [B,H,N,D], 16-byte aligned
+ *  lse  : the forward's L, fp32 [B,H,N], 4-byte aligned
+ *  dq, dk, dv: outputs, fp32 [B,H,N,D], 16-byte aligned
+ * flags: SAGE_IN_BF16, SAGE_NO_SMOOTH_K (as given to the forward); SAGE_OUT_F32
+ * is accepted and changes nothing (gradients are fp32); SAGE_BKV64 returns
+ * SAGE_ERR_UNSUPPORTED (the backward's KV blocks are 128 keys).  The
+ * internal workspace comes from hipMallocAsync on `stream`.
+ */
+int sage_attn_int8_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
+                       const void* dout, float* dq, float* dk, float* dv,
+                       int B, int H, int N, int D, int causal, unsigned flags, hipStream_t stream);
+
+/* Workspace bytes for sage_attn_int8_bwd_ws; 0 for invalid or unsupported
+ * arguments.  Host only. */
+size_t sage_attn_int8_bwd_workspace_size(int B, int H, int N, int D, unsigned flags);
+
+/* Same as sage_attn_int8_bwd, with a caller-provided workspace of at least
+ * sage_attn_int8_bwd_workspace_size() bytes (256-byte aligned). */
+int sage_attn_int8_bwd_ws(const void* q, const void* k, const void* v, const float* o, const float* lse,
+                          const void* dout, float* dq, float* dk, float* dv,
+                          int B, int H, int N, int D, int causal, unsigned flags,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Human-readable status name; never NULL. */
 const char* sage_status_string(int status);

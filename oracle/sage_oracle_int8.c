@@ -376,7 +376,11 @@ int orc_attn_int8(const uint16_t* q, const uint16_t* k, const uint16_t* v, int i
 /*    dQ.  The window: 8 ulp of the value for P^, and for dS^ the bound     */
 /*    |P| (e_dP + e_D) + |dP - D| |P| 2^-21 (e_x = 2^-17 times the sum of   */
 /*    |terms| of x) over s_dS, plus 8 ulp; block scales that move by an ulp */
-/*    shift every code by a relative 2^-22, also inside the window.          */
+/*    shift every code by a relative 2^-22, also inside the window.  The    */
+/*    same dS error also reaches dQ and dK continuously -- through s_dS     */
+/*    (its bound is the largest element bound over 127: every code's value */
+/*    and the fold factor move with it) and through rowsum(dS) in the       */
+/*    smoothing-K term -- and is added to their tolerance.                  */
 /* Flags: ORC_NO_SMOOTH_K, ORC_I8_IDENTITY (no psi anywhere: the exact      */
 /* gradients of softmax attention up to fp32 rounding), ORC_I8_DP_INT8      */
 /* (ablation, Table 1(c): dP = MM(dO^, V^) with per-block INT8 dO and V).    */
@@ -521,6 +525,9 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
         }
       /* psi(P) over the block, psi(dS) over the block */
       float sP = 1.0f, sdS = 1.0f;
+      double es = 0.0;                        /* bound on the move of s_dS */
+      for (int e = 0; e < bq * bkv; ++e) if (win[e] > es) es = win[e];
+      es /= 127.0;
       if (!ident) {
         volatile float s1 = pmax / 127.0f; sP = s1;
         volatile float r1 = pmax > 0.0f ? 1.0f / sP : 0.0f;
@@ -534,7 +541,8 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
           if (tq) {
             /* flag codes near a midpoint; the effect goes into the tolerance */
             const double w1 = fabs((double)y1) * ldexp(1.0, -20) + ldexp(1.0, -20);
-            const double w2 = win[e] * (double)r2 + fabs((double)y2) * ldexp(1.0, -20) + ldexp(1.0, -20);
+            const double w2 = win[e] * (double)r2 + fabs((double)y2) * (es * (double)r2 + ldexp(1.0, -20)) +
+                              ldexp(1.0, -20);
             const int a = e / bkv, b = e % bkv;
             if (vis[e] && a < nq && b < nk) {
               const int q = q0 + a, k = k0 + b;
@@ -578,6 +586,7 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
               s += (double)Sc[a * bkv + b] * (ident ? (double)qf[(long)(q0 + a) * D + c] : (double)qc[(long)(q0 + a) * D + c]);
             const long o = (long)(k0 + b) * D + c;
             dk[o] = fmaf((float)s, f, dk[o]);
+            if (tk && !ident) tk[o] += (float)(fabs(s) * es * sQ * rsd);
           }
       }
       /* dQ_i += MM(dS^, K^) s_dS s_K / sqrt(D) + rowsum(dS) K_m / sqrt(D) */
@@ -586,7 +595,8 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
         volatile float f = f0 * rsd;
         for (int a = 0; a < nq; ++a) {
           float rs = 0.0f;
-          for (int b = 0; b < nk; ++b) rs += dS[a * bkv + b];
+          double rse = 0.0;                   /* bound on the error of rowsum(dS) */
+          for (int b = 0; b < nk; ++b) { rs += dS[a * bkv + b]; rse += win[a * bkv + b]; }
           volatile float rr = rs * rsd;
           for (int c = 0; c < D; ++c) {
             double s = 0.0;
@@ -596,6 +606,8 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
             float x = fmaf((float)s, f, dq[o]);
             if (smooth) x = fmaf(rr, mu[c], x);
             dq[o] = x;
+            if (tq && !ident)
+              tq[o] += (float)(fabs(s) * es * sK * rsd + (smooth ? rse * rsd * fabs((double)mu[c]) : 0.0));
           }
         }
       }

@@ -56,13 +56,17 @@ def lib():
         L.sage_attn_int8_fwd.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, u, vp]
         L.sage_attn_int8_fwd_ws.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, u, vp, sz, vp]
         L.sage_attn_int8_fwd_prequant.argtypes = [vp] * 8 + [i, i, i, i, i, u, vp]
+        L.sage_attn_int8_bwd.argtypes = [vp] * 9 + [i, i, i, i, i, u, vp]
+        L.sage_attn_int8_bwd_ws.argtypes = [vp] * 9 + [i, i, i, i, i, u, vp, sz, vp]
+        L.sage_attn_int8_bwd_workspace_size.argtypes = [i, i, i, i, u]
+        L.sage_attn_int8_bwd_workspace_size.restype = sz
         L.sage_status_string.argtypes = [i]
         L.sage_status_string.restype = ctypes.c_char_p
         L.sage_version.restype = ctypes.c_char_p
         for name in ("sage_quant_sizes", "sage_quant_fp4", "sage_attn_fp4_fwd", "sage_attn_fp4_fwd_ws",
                      "sage_attn_fp4_fwd_prequant", "sage_attn_bf16_fwd", "sage_quant_int8_sizes",
                      "sage_quant_int8", "sage_attn_int8_fwd", "sage_attn_int8_fwd_ws",
-                     "sage_attn_int8_fwd_prequant"):
+                     "sage_attn_int8_fwd_prequant", "sage_attn_int8_bwd", "sage_attn_int8_bwd_ws"):
             getattr(L, name).restype = i
         _lib = L
     return _lib
@@ -258,6 +262,35 @@ def sage_attn_int8_fwd_prequant(qq, kq, vq, shape, causal: bool = False, in_bf16
                                            _stream())
     _check("sage_attn_int8_fwd_prequant", rc)
     return out, L
+
+
+def attn_int8_bwd_workspace_size(B: int, H: int, N: int, D: int, flags: int = 0) -> int:
+    return int(lib().sage_attn_int8_bwd_workspace_size(B, H, N, D, flags))
+
+
+def sage_attn_int8_bwd(q, k, v, o, lse, dout, causal: bool = False, flags: int = 0, workspace=None, out=None):
+    """Algorithm 3's 8-bit attention backward: returns (dQ, dK, dV) fp32 [B,H,N,D].
+    o, lse: the forward's fp32 output and L.  ``out``: three preallocated fp32
+    tensors; with ``workspace`` nothing is allocated inside."""
+    import torch
+    B, H, N, D = _shape(q)
+    for t in (k, v, dout):
+        if _shape(t) != (B, H, N, D) or t.dtype != q.dtype:
+            raise ValueError("q, k, v, dout must have the same shape and dtype")
+    if _shape(o) != (B, H, N, D) or o.dtype != torch.float32:
+        raise ValueError("o must be the fp32 forward output")
+    if tuple(lse.shape) != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
+        raise ValueError("lse must be fp32 [B,H,N]")
+    flags = flags | _in_flag(q)
+    dq, dk, dv = out if out is not None else [torch.empty((B, H, N, D), dtype=torch.float32, device=q.device)
+                                              for _ in range(3)]
+    ptrs = [_ptr(t) for t in (q, k, v, o, lse, dout, dq, dk, dv)]
+    if workspace is None:
+        _check("sage_attn_int8_bwd", lib().sage_attn_int8_bwd(*ptrs, B, H, N, D, int(bool(causal)), flags, _stream()))
+    else:
+        _check("sage_attn_int8_bwd_ws", lib().sage_attn_int8_bwd_ws(*ptrs, B, H, N, D, int(bool(causal)), flags,
+                                                                  _ptr(workspace), workspace.numel(), _stream()))
+    return dq, dk, dv
 
 
 def version() -> str:

@@ -18,7 +18,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsage_mi355x.so")
 SOURCES = ["sage_abi.hip", "quant.hip", "attn_fp4.hip", "attn_bf16.hip", "attn_nv16.hip", "quant_int8.hip",
-           "attn_int8.hip"]
+           "attn_int8.hip", "attn_int8_bwd.hip"]
 RATES_LIB = os.path.join(HERE, "libsage_rates.so")
 RATES_SOURCES = ["issue_rates.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

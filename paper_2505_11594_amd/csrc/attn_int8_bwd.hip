@@ -1,0 +1,425 @@
+// Backward pass of the 8-bit attention of SageBwd (Algorithm 3) for gfx950.
+//
+// Four of the five products run on v_mfma_i32_32x32x32_i8 with per-block INT8
+// operands (psi, Sec. 4.1): S = MM(Q^, K^) s_Q s_K, dV += MM(P^T, dO^) s_P s_dO,
+// dQ += MM(dS^, K^) s_dS s_K / sqrt(D) and dK += MM(dS^T, Q^) s_dS s_Q / sqrt(D);
+// dP = MM(dO, V^T) stays in 16-bit inputs (v_mfma_f32_32x32x16_bf16 / _f16,
+// fp32 accumulation).  P = exp(S/sqrt(D) - L) uses the forward's L, dS =
+// P (dP - D) with D = rowsum(dO O), and dQ gets rowsum(dS) K_m / sqrt(D) for
+// the smoothing of K.  psi of P and dS is per (128 query x 128 key) block,
+// psi of dO per 128-row block, as the forward's Q^.
+//
+// Two deterministic kernels (no atomics):
+//  - dK/dV: a workgroup owns 128 keys (4 waves x 32) and walks the query
+//    blocks.  S = Q^ K^T puts a key in each lane's column and 16 queries in its
+//    rows, so P^ and dS^ of a 32-query subtile are, as they stand, the B
+//    operands of dV^T = dO^T P^ and dK^T = Q^T dS^ (A = dO^T / Q^T rows with
+//    each 32-query group permuted as V^T in the forward).  The block scales
+//    of P and dS need the block's maxima before any code is formed: a first
+//    pass computes S, P, dP and dS for the maxima (reduced across the waves
+//    through LDS), a second recomputes them -- bit-identically -- and
+//    quantizes.
+//  - dQ: a workgroup owns 128 queries (4 waves x 32) and walks the KV blocks.
+//    S^T = K^ Q^T puts a query in each lane's column; dS of the block stays in
+//    registers while its maximum is reduced across the waves, and dS^ is the B
+//    operand of dQ^T = K^T dS^T (A = K^T rows, permuted the same way).
+// Both run one wave per SIMD (the int32 and fp32 accumulators of two
+// products do not fit two waves' register budget); operands come straight
+// from HBM / L2 into registers.
+#include "sage_common.h"
+
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+
+namespace sage {
+
+constexpr int BW_Q = 128;    // query block (psi(Q), psi(dO), P and dS blocks)
+constexpr int BW_K = 128;    // key block
+constexpr float kBwRoundMagic = 12582912.0f;   // 1.5 * 2^23
+
+template <bool BF16>
+__device__ __forceinline__ v16f mfma16(const v4i a, const v4i b, v16f c) {
+  if constexpr (BF16) return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, a), __builtin_bit_cast(v8bf, b), c, 0, 0, 0);
+  else return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(v8h, a), __builtin_bit_cast(v8h, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ int bw_pack4(float a, float b, float c, float d) {
+  const uint32_t ab = __builtin_amdgcn_perm(__float_as_uint(b), __float_as_uint(a), 0x0C0C0400u);
+  const uint32_t cd = __builtin_amdgcn_perm(__float_as_uint(d), __float_as_uint(c), 0x0C0C0400u);
+  return (int)__builtin_amdgcn_perm(cd, ab, 0x05040100u);
+}
+
+// 16 values -> 16 int8 codes rint(x r) in value order (v = 4g + r -> byte v)
+__device__ __forceinline__ v4i bw_codes(const float (&x)[16], float r) {
+  int w[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+    w[g] = bw_pack4(x[4 * g] * r + kBwRoundMagic, x[4 * g + 1] * r + kBwRoundMagic,
+                    x[4 * g + 2] * r + kBwRoundMagic, x[4 * g + 3] * r + kBwRoundMagic);
+  return v4i{w[0], w[1], w[2], w[3]};
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = __builtin_fmaxf(x, __shfl_xor(x, off, 64));
+  return x;
+}
+
+// ---------------------------------------------------------------------------
+// D_q = sum_d dO[q,d] O[q,d] (fp32) and Lb_q = L_q log2(e), for q < N; rows
+// [N, Np) get 0.  D/8 lanes per row, 8 elements each.
+// ---------------------------------------------------------------------------
+template <int D, bool BF16>
+__global__ __launch_bounds__(256) void i8_bwd_prep_kernel(const uint16_t* __restrict__ dout, const float* __restrict__ o,
+                                                          const float* __restrict__ lse, float* __restrict__ drow,
+                                                          float* __restrict__ lb, int N, int Np, long long rows,
+                                                          float log2e) {
+  constexpr int LPR = D / 8;
+  const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long row = t / LPR;                   // (bh, q) over Np rows per head
+  const int part = (int)(t % LPR);
+  if (row >= rows) return;                         // whole rows: LPR divides the block size
+  const long long bh = row / Np;
+  const int q = (int)(row % Np);
+  float s = 0.0f;
+  if (q < N) {
+    const size_t e = ((size_t)bh * N + q) * D + part * 8;
+    const uint4 g = *reinterpret_cast<const uint4*>(dout + e);
+    const uint16_t* gh = reinterpret_cast<const uint16_t*>(&g);
+    const float4 o0 = *reinterpret_cast<const float4*>(o + e);
+    const float4 o1 = *reinterpret_cast<const float4*>(o + e + 4);
+    const float ov[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s = __builtin_fmaf(widen<BF16>(gh[i]), ov[i], s);
+  }
+#pragma unroll
+  for (int off = LPR / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (part == 0) {
+    drow[row] = s;
+    lb[row] = q < N ? lse[(size_t)bh * N + q] * log2e : 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dK, dV.  qc/kc: Q^, K^ row-major; qt, gt: Q^T, dO^T int8 [BH, D, Np] with
+// each 32-query group permuted; qs, gs: s_Q, s_dO per 128 rows; ks: s_K per
+// 128 keys; v, dout: 16-bit [BH, N, D]; drow, lb: [BH, Np].
+// ---------------------------------------------------------------------------
+template <int D, bool CAUSAL, bool BF16>
+__global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
+    const int8_t* __restrict__ qc, const float* __restrict__ qs, const int8_t* __restrict__ qt,
+    const int8_t* __restrict__ kc, const float* __restrict__ ks, const uint16_t* __restrict__ v,
+    const uint16_t* __restrict__ dout, const int8_t* __restrict__ gt, const float* __restrict__ gs,
+    const float* __restrict__ drow, const float* __restrict__ lb, float* __restrict__ dk, float* __restrict__ dv,
+    int N, int Np, int nqb, float c2, float rsd) {
+  constexpr int NKS = D / 32, NKS16 = D / 16, NDB = D / 32;
+  __shared__ float red[2][2][4];                   // [block parity][P, dS][wave]
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, hi = lane >> 5;
+  const int kblk = blockIdx.x, bh = blockIdx.y;
+  const int kb = kblk * BW_K, kw = kb + 32 * wave, key = kw + col;
+  const float sK = ks[(size_t)bh * (Np / BW_K) + kblk];
+
+  // B operands of this wave's 32 keys: K^ (channels [32s + 16hi, +16)) and V
+  // (16-bit, channels [16s + 8hi, +8))
+  v4i kreg[NKS], vreg[NKS16];
+  {
+    const int8_t* kr = kc + ((size_t)bh * Np + key) * D;
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) kreg[s] = *reinterpret_cast<const v4i*>(kr + 32 * s + 16 * hi);
+    const uint16_t* vr = v + ((size_t)bh * N + key) * D;
+#pragma unroll
+    for (int s = 0; s < NKS16; ++s)
+      vreg[s] = key < N ? *reinterpret_cast<const v4i*>(vr + 16 * s + 8 * hi) : v4i{0, 0, 0, 0};
+  }
+  v16f dva[NDB], dka[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) { dva[db] = v16f{}; dka[db] = v16f{}; }
+
+  const int i0 = CAUSAL ? kb / BW_Q : 0;
+  for (int i = i0; i < nqb; ++i) {
+    const int q0 = i * BW_Q;
+    const float sQ = qs[(size_t)bh * nqb + i];
+    const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);   // see the forward kernel
+    const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && q0 < kb + BW_K - 1);
+
+    // P and dS of one 32-query subtile: element v is query q0 + 32u + 8(v>>2) + 4hi + (v&3)
+    auto subtile = [&](int u, float (&P)[16], float (&dS)[16]) {
+      const int qrow = q0 + 32 * u + col;          // A-operand row of this lane
+      v4i qa[NKS], ga[NKS16];
+      const int8_t* qr = qc + ((size_t)bh * N + qrow) * D;
+      const uint16_t* gr = dout + ((size_t)bh * N + qrow) * D;
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) qa[s] = qrow < N ? *reinterpret_cast<const v4i*>(qr + 32 * s + 16 * hi) : v4i{0, 0, 0, 0};
+#pragma unroll
+      for (int s = 0; s < NKS16; ++s) ga[s] = qrow < N ? *reinterpret_cast<const v4i*>(gr + 16 * s + 8 * hi) : v4i{0, 0, 0, 0};
+      v16i sacc = v16i{};
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(qa[s], kreg[s], sacc, 0, 0, 0);
+      v16f dp = v16f{};
+#pragma unroll
+      for (int s = 0; s < NKS16; ++s) dp = mfma16<BF16>(ga[s], vreg[s], dp);
+      const int qb4 = q0 + 32 * u + 4 * hi;
+      const float* lbr = lb + (size_t)bh * Np + qb4;
+      const float* dr = drow + (size_t)bh * Np + qb4;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 l4 = *reinterpret_cast<const float4*>(lbr + 8 * g);
+        const float4 d4 = *reinterpret_cast<const float4*>(dr + 8 * g);
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dvv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int e = 4 * g + r;
+          float arg = __builtin_fmaf((float)sacc[e], ct, -lv[r]);
+          if (need_mask) {
+            // visible iff q < N, key < N and (causal) key <= q: the three sign bits
+            const int q = qb4 + 8 * g + r;
+            int m = (q - N) & (key - N);
+            if (CAUSAL) m &= ~(q - key);
+            arg = __builtin_fminf(arg, __uint_as_float(0xFF800000u ^ ((uint32_t)m & 0x80000000u)));
+          }
+          const float p = __builtin_amdgcn_exp2f(arg);
+          const float d = dp[e] - dvv[r];
+          P[e] = p;
+          dS[e] = p * d;
+        }
+      }
+    };
+
+    // pass 1: the block maxima of P and |dS|
+    float pm = 0.0f, dm = 0.0f;
+#pragma unroll 1
+    for (int u = 0; u < BW_Q / 32; ++u) {
+      float P[16], dS[16];
+      subtile(u, P, dS);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) { pm = __builtin_fmaxf(pm, P[e]); dm = __builtin_fmaxf(dm, __builtin_fabsf(dS[e])); }
+    }
+    pm = wave_max(pm);
+    dm = wave_max(dm);
+    const int par = i & 1;
+    if (lane == 0) { red[par][0][wave] = pm; red[par][1][wave] = dm; }
+    __syncthreads();
+    pm = __builtin_fmaxf(__builtin_fmaxf(red[par][0][0], red[par][0][1]), __builtin_fmaxf(red[par][0][2], red[par][0][3]));
+    dm = __builtin_fmaxf(__builtin_fmaxf(red[par][1][0], red[par][1][1]), __builtin_fmaxf(red[par][1][2], red[par][1][3]));
+    const float sP = pm / 127.0f, rP = pm > 0.0f ? 1.0f / sP : 0.0f;
+    const float sdS = dm / 127.0f, rdS = dm > 0.0f ? 1.0f / sdS : 0.0f;
+
+    // pass 2: codes and the two int8 products of the block
+    v16i dvi[NDB], dki[NDB];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) { dvi[db] = v16i{}; dki[db] = v16i{}; }
+#pragma unroll 1
+    for (int u = 0; u < BW_Q / 32; ++u) {
+      float P[16], dS[16];
+      subtile(u, P, dS);
+      const v4i pc = bw_codes(P, rP), sc = bw_codes(dS, rdS);
+      const size_t tq = (size_t)q0 + 32 * u + 16 * hi;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const size_t rowo = ((size_t)bh * D + 32 * db + col) * Np + tq;
+        const v4i ga = *reinterpret_cast<const v4i*>(gt + rowo);
+        const v4i qa = *reinterpret_cast<const v4i*>(qt + rowo);
+        dvi[db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ga, pc, dvi[db], 0, 0, 0);
+        dki[db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(qa, sc, dki[db], 0, 0, 0);
+      }
+    }
+    const float fv = sP * gs[(size_t)bh * nqb + i];
+    const float fk = (sdS * sQ) * rsd;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        dva[db][e] = __builtin_fmaf((float)dvi[db][e], fv, dva[db][e]);
+        dka[db][e] = __builtin_fmaf((float)dki[db][e], fk, dka[db][e]);
+      }
+  }
+
+  // dV^T, dK^T: lane holds key kw + col and channels 32db + 8g + 4hi + r
+  if (key < N) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const size_t idx = ((size_t)bh * N + key) * D + 32 * db + 8 * g + 4 * hi;
+        *reinterpret_cast<float4*>(dv + idx) = make_float4(dva[db][4 * g], dva[db][4 * g + 1], dva[db][4 * g + 2], dva[db][4 * g + 3]);
+        *reinterpret_cast<float4*>(dk + idx) = make_float4(dka[db][4 * g], dka[db][4 * g + 1], dka[db][4 * g + 2], dka[db][4 * g + 3]);
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dQ.  kt: K^T int8 [BH, D, Np] with each 32-key group permuted; kmean: K_m
+// [BH, D] or null (no smoothing).
+// ---------------------------------------------------------------------------
+template <int D, bool CAUSAL, bool BF16>
+__global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
+    const int8_t* __restrict__ qc, const float* __restrict__ qs, const int8_t* __restrict__ kc,
+    const float* __restrict__ ks, const int8_t* __restrict__ kt, const uint16_t* __restrict__ v,
+    const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lb,
+    const float* __restrict__ kmean, float* __restrict__ dq, int N, int Np, int nqb, float c2, float rsd) {
+  constexpr int NKS = D / 32, NKS16 = D / 16, NDB = D / 32, NT = BW_K / 32;
+  __shared__ float red[2][4];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, hi = lane >> 5;
+  const int i = blockIdx.x, bh = blockIdx.y;
+  const int q0 = i * BW_Q, qw = q0 + 32 * wave, qi = qw + col;
+  const float sQ = qs[(size_t)bh * nqb + i];
+  const float lbq = lb[(size_t)bh * Np + qi], dq_row = drow[(size_t)bh * Np + qi];
+
+  v4i qreg[NKS], greg[NKS16];
+  {
+    const int8_t* qr = qc + ((size_t)bh * N + qi) * D;
+    const uint16_t* gr = dout + ((size_t)bh * N + qi) * D;
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) qreg[s] = qi < N ? *reinterpret_cast<const v4i*>(qr + 32 * s + 16 * hi) : v4i{0, 0, 0, 0};
+#pragma unroll
+    for (int s = 0; s < NKS16; ++s) greg[s] = qi < N ? *reinterpret_cast<const v4i*>(gr + 16 * s + 8 * hi) : v4i{0, 0, 0, 0};
+  }
+  v16f dqa[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) dqa[db] = v16f{};
+
+  int nkb = (N + BW_K - 1) / BW_K;
+  if (CAUSAL) nkb = min(nkb, min(q0 + BW_Q - 1, N - 1) / BW_K + 1);
+  for (int j = 0; j < nkb; ++j) {
+    const int kb = j * BW_K;
+    const float sK = ks[(size_t)bh * (Np / BW_K) + j];
+    const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);
+    const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && kb + BW_K - 1 > q0);
+    float dS[NT][16];
+    float dm = 0.0f, rs = 0.0f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int krow = kb + 32 * t + col;          // A-operand row of this lane
+      const int8_t* kr = kc + ((size_t)bh * Np + krow) * D;
+      const uint16_t* vr = v + ((size_t)bh * N + krow) * D;
+      v16i sacc = v16i{};
+#pragma unroll
+      for (int s = 0; s < NKS; ++s)
+        sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(*reinterpret_cast<const v4i*>(kr + 32 * s + 16 * hi), qreg[s], sacc, 0, 0, 0);
+      v16f dp = v16f{};
+#pragma unroll
+      for (int s = 0; s < NKS16; ++s)
+        dp = mfma16<BF16>(krow < N ? *reinterpret_cast<const v4i*>(vr + 16 * s + 8 * hi) : v4i{0, 0, 0, 0}, greg[s], dp);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        float arg = __builtin_fmaf((float)sacc[e], ct, -lbq);
+        if (need_mask) {
+          const int k = kb + 32 * t + 8 * (e >> 2) + 4 * hi + (e & 3);
+          int m = (qi - N) & (k - N);
+          if (CAUSAL) m &= ~(qi - k);
+          arg = __builtin_fminf(arg, __uint_as_float(0xFF800000u ^ ((uint32_t)m & 0x80000000u)));
+        }
+        const float p = __builtin_amdgcn_exp2f(arg);
+        const float d = dp[e] - dq_row;
+        const float x = p * d;
+        dS[t][e] = x;
+        rs += x;
+        dm = __builtin_fmaxf(dm, __builtin_fabsf(x));
+      }
+    }
+    dm = wave_max(dm);
+    const int par = j & 1;
+    if (lane == 0) red[par][wave] = dm;
+    __syncthreads();
+    dm = __builtin_fmaxf(__builtin_fmaxf(red[par][0], red[par][1]), __builtin_fmaxf(red[par][2], red[par][3]));
+    const float sdS = dm / 127.0f, rdS = dm > 0.0f ? 1.0f / sdS : 0.0f;
+    v16i dqi[NDB];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) dqi[db] = v16i{};
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const v4i sc = bw_codes(dS[t], rdS);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const v4i ka = *reinterpret_cast<const v4i*>(kt + ((size_t)bh * D + 32 * db + col) * Np + kb + 32 * t + 16 * hi);
+        dqi[db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ka, sc, dqi[db], 0, 0, 0);
+      }
+    }
+    const float fq = (sdS * sK) * rsd;
+    const float rr = (rs + __shfl_xor(rs, 32, 64)) * rsd;   // rowsum(dS) of this lane's query, / sqrt(D)
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float4 km = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (kmean != nullptr) km = *reinterpret_cast<const float4*>(kmean + (size_t)bh * D + 32 * db + 8 * g + 4 * hi);
+        const float kmv[4] = {km.x, km.y, km.z, km.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int e = 4 * g + r;
+          float x = __builtin_fmaf((float)dqi[db][e], fq, dqa[db][e]);
+          if (kmean != nullptr) x = __builtin_fmaf(rr, kmv[r], x);
+          dqa[db][e] = x;
+        }
+      }
+  }
+  if (qi < N) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const size_t idx = ((size_t)bh * N + qi) * D + 32 * db + 8 * g + 4 * hi;
+        *reinterpret_cast<float4*>(dq + idx) = make_float4(dqa[db][4 * g], dqa[db][4 * g + 1], dqa[db][4 * g + 2], dqa[db][4 * g + 3]);
+      }
+  }
+}
+
+hipError_t launch_i8_bwd_prep(const void* dout, const float* o, const float* lse, float* drow, float* lb, int BH,
+                              int N, int Np, int D, bool bf16, hipStream_t st) {
+  const long long rows = (long long)BH * Np;
+  const long long threads = rows * (D / 8);
+  const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
+  const float log2e = 1.44269504088896340736f;
+  const uint16_t* g = static_cast<const uint16_t*>(dout);
+  if (D == 128) {
+    if (bf16) hipLaunchKernelGGL((i8_bwd_prep_kernel<128, true>), grid, block, 0, st, g, o, lse, drow, lb, N, Np, rows, log2e);
+    else hipLaunchKernelGGL((i8_bwd_prep_kernel<128, false>), grid, block, 0, st, g, o, lse, drow, lb, N, Np, rows, log2e);
+  } else {
+    if (bf16) hipLaunchKernelGGL((i8_bwd_prep_kernel<64, true>), grid, block, 0, st, g, o, lse, drow, lb, N, Np, rows, log2e);
+    else hipLaunchKernelGGL((i8_bwd_prep_kernel<64, false>), grid, block, 0, st, g, o, lse, drow, lb, N, Np, rows, log2e);
+  }
+  return hipGetLastError();
+}
+
+template <int D, bool CAUSAL, bool BF16>
+static hipError_t launch_bwd_t(const int8_t* qc, const float* qs, const int8_t* qt, const int8_t* kc, const float* ks,
+                               const int8_t* kt, const uint16_t* v, const uint16_t* dout, const int8_t* gt,
+                               const float* gs, const float* drow, const float* lb, const float* kmean, float* dq,
+                               float* dk, float* dv, int BH, int N, int Np, float c2, float rsd, hipStream_t st) {
+  const int nqb = (N + BW_Q - 1) / BW_Q;
+  hipLaunchKernelGGL((attn_i8_bwd_dkdv_kernel<D, CAUSAL, BF16>), dim3((unsigned)(Np / BW_K), (unsigned)BH), dim3(256), 0,
+                     st, qc, qs, qt, kc, ks, v, dout, gt, gs, drow, lb, dk, dv, N, Np, nqb, c2, rsd);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_i8_bwd_dq_kernel<D, CAUSAL, BF16>), dim3((unsigned)nqb, (unsigned)BH), dim3(256), 0, st, qc,
+                     qs, kc, ks, kt, v, dout, drow, lb, kmean, dq, N, Np, nqb, c2, rsd);
+  return hipGetLastError();
+}
+
+// Q^ [BH, N, D], K^ [BH, Np, D] row-major; Q^T, K^T, dO^T [BH, D, Np] permuted
+// per 32 rows; scales per 128 rows; kmean null without smoothing.
+hipError_t launch_attn_int8_bwd(const void* qc, const float* qs, const void* qt, const void* kc, const float* ks,
+                                const void* kt, const void* v, const void* dout, const void* gt, const float* gs,
+                                const float* drow, const float* lb, const float* kmean, float* dq, float* dk, float* dv,
+                                int BH, int N, int Np, int D, bool causal, bool bf16, float c2, float rsd,
+                                hipStream_t st) {
+  const int8_t *a = (const int8_t*)qc, *b = (const int8_t*)qt, *c = (const int8_t*)kc, *d = (const int8_t*)kt,
+               *g = (const int8_t*)gt;
+  const uint16_t *vv = (const uint16_t*)v, *gg = (const uint16_t*)dout;
+#define SAGE_BW(DD, CC, BB) \
+  return launch_bwd_t<DD, CC, BB>(a, qs, b, c, ks, d, vv, gg, g, gs, drow, lb, kmean, dq, dk, dv, BH, N, Np, c2, rsd, st)
+  if (D == 128) {
+    if (causal) { if (bf16) SAGE_BW(128, true, true); else SAGE_BW(128, true, false); }
+    else { if (bf16) SAGE_BW(128, false, true); else SAGE_BW(128, false, false); }
+  } else {
+    if (causal) { if (bf16) SAGE_BW(64, true, true); else SAGE_BW(64, true, false); }
+    else { if (bf16) SAGE_BW(64, false, true); else SAGE_BW(64, false, false); }
+  }
+#undef SAGE_BW
+}
+
+}  // namespace sage

@@ -1,9 +1,9 @@
-// INT8 per-block quantization psi for the 8-bit attention forward of SageBwd
-// (Algorithm 2; Sec. 4.1, Eq. psi) on gfx950.
+// INT8 per-block quantization psi for the 8-bit attention of SageBwd
+// (Algorithms 2 and 3; Sec. 4.1, Eq. psi) on gfx950.
 //
 // One scale s = max|X| / 127 per block of R consecutive rows with all D
-// channels -- R = 128 query rows for Q (the attention kernel's query tile),
-// the KV tile (64 rows) for K and V -- and codes round(x * fl32(1/s)) to the
+// channels -- R = 128 query rows for Q and dO (the attention kernels' query
+// tile), the KV tile (128 or 64 rows) for K and V -- and codes round(x * fl32(1/s)) to the
 // nearest integer, ties to even; an all-zero block gets s = 0 and zero codes.
 // K is smoothed first: K' = fl32(K - mean_t K) with the exact mean of the
 // FP4 path's k-mean kernels.
@@ -12,6 +12,8 @@
 // zero); V^T [BH, D, Np] transposed, the tokens of every 32-token group
 // stored in the order in which the int8 MFMA of P.V receives P from the
 // accumulator of S^T = K^ Q^T: position 16h + 4g + r holds token 8g + 4h + r.
+// The backward stores Q^, K^ and dO^ transposed the same way (the A operands
+// of dK^T = Q^T dS^, dQ^T = K^T dS^T and dV^T = dO^T P^).
 //
 // One workgroup per block: each thread owns 8 channels of up to 8 rows (one
 // 16-byte load each), the block max is reduced across the wave and through
@@ -37,7 +39,8 @@ __device__ __forceinline__ uint32_t pack_low_bytes(uint32_t a, uint32_t b, uint3
   return __builtin_amdgcn_perm(cd, ab, 0x05040100u);              // [a, b, c, d]
 }
 
-// ROLE: 0 = Q, 1 = K, 2 = V.  Block b of head bh holds rows [b R, b R + R) of
+// ROLE: 0 = Q, 1 = K, 2 = V (or any tensor stored transposed), 3 = K stored
+// transposed (the backward's K^T).  Block b of head bh holds rows [b R, b R + R) of
 // the input (rows >= N are zero); nb = blocks per head; Nout = rows of the
 // Q^ / K^ output (N or Np), Np = columns of V^T.
 template <int D, bool BF16, int ROLE>
@@ -54,7 +57,7 @@ __global__ __launch_bounds__(I8Q_THREADS) void quant_i8_kernel(const uint16_t* _
 
   float m8[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) m8[i] = (ROLE == 1 && mu != nullptr) ? mu[(size_t)bh * D + cg * 8 + i] : 0.0f;
+  for (int i = 0; i < 8; ++i) m8[i] = ((ROLE == 1 || ROLE == 3) && mu != nullptr) ? mu[(size_t)bh * D + cg * 8 + i] : 0.0f;
 
   float v[MAXU][8];
   float amax = 0.0f;
@@ -67,7 +70,7 @@ __global__ __launch_bounds__(I8Q_THREADS) void quant_i8_kernel(const uint16_t* _
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         float a = widen<BF16>(h[i]);
-        if (ROLE == 1) a = a - m8[i];
+        if (ROLE == 1 || ROLE == 3) a = a - m8[i];
         v[u][i] = a;
         amax = __builtin_fmaxf(amax, __builtin_fabsf(a));
       }
@@ -87,7 +90,7 @@ __global__ __launch_bounds__(I8Q_THREADS) void quant_i8_kernel(const uint16_t* _
   const float r = amax > 0.0f ? 1.0f / s : 0.0f;  // a zero block: codes 0
   if (tid == 0) scales[(size_t)bh * nb + b] = s;
 
-  if constexpr (ROLE != 2) {
+  if constexpr (ROLE == 0 || ROLE == 1) {
 #pragma unroll
     for (int u = 0; u < MAXU; ++u) {
       const int row = rsub + u * RSTEP, t = r0 + row;
@@ -121,9 +124,9 @@ __global__ __launch_bounds__(I8Q_THREADS) void quant_i8_kernel(const uint16_t* _
   }
 }
 
-// role: 0 Q (R must be 128, Nout = N), 1 K (Nout = Np), 2 V (Nout = Np, the
-// row length of V^T).  nb = blocks per head: ceil(N / 128) for Q, Np / R
-// for K and V.
+// role: 0 Q (R must be 128, Nout = N), 1 K (Nout = Np), 2 V or any tensor
+// transposed (Nout = Np, the row length of the transposed output), 3 K
+// transposed.  nb = blocks per head: ceil(N / 128) for Q, Np / R otherwise.
 hipError_t launch_quant_i8(const void* x, const float* mu, void* codes, float* scales, int BH, int N, int Nout,
                            int D, int R, int role, bool bf16, hipStream_t st) {
   const int nb = role == 0 ? (N + R - 1) / R : Nout / R;
@@ -136,7 +139,8 @@ hipError_t launch_quant_i8(const void* x, const float* mu, void* codes, float* s
   do {                                        \
     if (role == 0) SAGE_Q8(DD, BB, 0);        \
     else if (role == 1) SAGE_Q8(DD, BB, 1);   \
-    else SAGE_Q8(DD, BB, 2);                  \
+    else if (role == 2) SAGE_Q8(DD, BB, 2);   \
+    else SAGE_Q8(DD, BB, 3);                  \
   } while (0)
   if (D == 128) { if (bf16) SAGE_Q8R(128, true); else SAGE_Q8R(128, false); }
   else { if (bf16) SAGE_Q8R(64, true); else SAGE_Q8R(64, false); }

@@ -32,6 +32,13 @@ hipError_t launch_quant_i8(const void* x, const float* mu, void* codes, float* s
 hipError_t launch_attn_int8(const void* qc, const float* qs, const void* kc, const float* ks, const void* vc,
                             const float* vs, void* o, float* lse, int BH, int N, int Np, int D, int bkv, bool causal,
                             int out, float c2, float log127, hipStream_t st);
+hipError_t launch_i8_bwd_prep(const void* dout, const float* o, const float* lse, float* drow, float* lb, int BH,
+                              int N, int Np, int D, bool bf16, hipStream_t st);
+hipError_t launch_attn_int8_bwd(const void* qc, const float* qs, const void* qt, const void* kc, const float* ks,
+                                const void* kt, const void* v, const void* dout, const void* gt, const float* gs,
+                                const float* drow, const float* lb, const float* kmean, float* dq, float* dk, float* dv,
+                                int BH, int N, int Np, int D, bool causal, bool bf16, float c2, float rsd,
+                                hipStream_t st);
 }  // namespace sage
 
 namespace {
@@ -270,6 +277,77 @@ int attn_i8_args(const void* q, const void* k, const void* v, const void* o, con
   return SAGE_OK;
 }
 
+// ---- 8-bit attention backward (Algorithm 3) -------------------------------
+constexpr unsigned kI8BwdFlags = SAGE_IN_BF16 | SAGE_OUT_F32 | SAGE_NO_SMOOTH_K | SAGE_BKV64;
+
+struct I8BwdWs {
+  size_t qc, qs, qt, kc, ks, kt, mu, part, gt, gs, drow, lb, total;
+};
+
+I8BwdWs i8_bwd_ws_layout(int B, int H, int N, int D) {
+  I8BwdWs w;
+  const size_t BH = (size_t)B * H, Np = pad128(N), nb = Np / 128, off0 = 0;
+  size_t off = off0;
+  w.qc = off; off += up256(BH * N * D);
+  w.qs = off; off += up256(BH * nb * sizeof(float));
+  w.qt = off; off += up256(BH * D * Np);
+  w.kc = off; off += up256(BH * Np * D);
+  w.ks = off; off += up256(BH * nb * sizeof(float));
+  w.kt = off; off += up256(BH * D * Np);
+  w.mu = off; off += up256(BH * D * sizeof(float));
+  w.part = off; off += up256(kmean_ws_bytes(B, H, N, D));
+  w.gt = off; off += up256(BH * D * Np);
+  w.gs = off; off += up256(BH * nb * sizeof(float));
+  w.drow = off; off += up256(BH * Np * sizeof(float));
+  w.lb = off; off += up256(BH * Np * sizeof(float));
+  w.total = off;
+  return w;
+}
+
+int attn_i8_bwd_ws_impl(const void* q, const void* k, const void* v, const float* o, const float* lse,
+                        const void* dout, float* dq, float* dk, float* dv, int B, int H, int N, int D, int causal,
+                        unsigned flags, void* ws, hipStream_t st) {
+  const I8BwdWs w = i8_bwd_ws_layout(B, H, N, D);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  const bool bf16 = (flags & SAGE_IN_BF16) != 0, smooth = !(flags & SAGE_NO_SMOOTH_K);
+  const int BH = B * H, Np = pad128(N);
+  float* qs = reinterpret_cast<float*>(base + w.qs);
+  float* ks = reinterpret_cast<float*>(base + w.ks);
+  float* gs = reinterpret_cast<float*>(base + w.gs);
+  float* mu = reinterpret_cast<float*>(base + w.mu);
+  float* drow = reinterpret_cast<float*>(base + w.drow);
+  float* lb = reinterpret_cast<float*>(base + w.lb);
+  // psi of Q (row-major and transposed), K' (both), dO (transposed): blocks of 128 rows
+  hipError_t e = sage::launch_quant_i8(q, nullptr, base + w.qc, qs, BH, N, N, D, 128, 0, bf16, st);
+  if (e == hipSuccess) e = sage::launch_quant_i8(q, nullptr, base + w.qt, qs, BH, N, Np, D, 128, 2, bf16, st);
+  if (e == hipSuccess && smooth) e = sage::launch_kmean(k, reinterpret_cast<double*>(base + w.part), mu, BH, N, D, bf16, st);
+  const float* mup = smooth ? mu : nullptr;
+  if (e == hipSuccess) e = sage::launch_quant_i8(k, mup, base + w.kc, ks, BH, N, Np, D, 128, 1, bf16, st);
+  if (e == hipSuccess) e = sage::launch_quant_i8(k, mup, base + w.kt, ks, BH, N, Np, D, 128, 3, bf16, st);
+  if (e == hipSuccess) e = sage::launch_quant_i8(dout, nullptr, base + w.gt, gs, BH, N, Np, D, 128, 2, bf16, st);
+  if (e == hipSuccess) e = sage::launch_i8_bwd_prep(dout, o, lse, drow, lb, BH, N, Np, D, bf16, st);
+  if (e == hipSuccess)
+    e = sage::launch_attn_int8_bwd(base + w.qc, qs, base + w.qt, base + w.kc, ks, base + w.kt, v, dout, base + w.gt, gs,
+                                   drow, lb, mup, dq, dk, dv, BH, N, Np, D, causal != 0, bf16, softmax_c2(D),
+                                   (float)(1.0 / std::sqrt((double)D)), st);
+  return hip_status(e);
+}
+
+int attn_i8_bwd_args(const void* q, const void* k, const void* v, const float* o, const float* lse, const void* dout,
+                     const float* dq, const float* dk, const float* dv, int B, int H, int N, int D, int causal,
+                     unsigned flags) {
+  if (flags & ~kI8BwdFlags) return SAGE_ERR_INVALID_ARG;
+  int rc = check_shape(B, H, N, D, flags & SAGE_IN_BF16);
+  if (rc != SAGE_OK) return rc;
+  if (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv) return SAGE_ERR_INVALID_ARG;
+  for (const void* p : {q, k, v, (const void*)o, dout, (const void*)dq, (const void*)dk, (const void*)dv})
+    if (!aligned(p, 16)) return SAGE_ERR_INVALID_ARG;
+  if (!aligned(lse, 4)) return SAGE_ERR_INVALID_ARG;
+  if (causal != 0 && causal != 1) return SAGE_ERR_INVALID_ARG;
+  if (flags & SAGE_BKV64) return SAGE_ERR_UNSUPPORTED;     // the backward's KV blocks are 128 keys
+  return SAGE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -437,6 +515,35 @@ int sage_attn_int8_fwd_prequant(const void* q_codes, const float* q_scales, cons
   if (causal != 0 && causal != 1) return SAGE_ERR_INVALID_ARG;
   return attn_i8_prequant_impl(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, o, lse, B, H, N, D, causal,
                                flags, stream);
+}
+
+size_t sage_attn_int8_bwd_workspace_size(int B, int H, int N, int D, unsigned flags) {
+  if ((flags & ~kI8BwdFlags) || (flags & SAGE_BKV64) || check_shape(B, H, N, D, flags & SAGE_IN_BF16) != SAGE_OK)
+    return 0;
+  return i8_bwd_ws_layout(B, H, N, D).total;
+}
+
+int sage_attn_int8_bwd_ws(const void* q, const void* k, const void* v, const float* o, const float* lse,
+                          const void* dout, float* dq, float* dk, float* dv, int B, int H, int N, int D, int causal,
+                          unsigned flags, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int rc = attn_i8_bwd_args(q, k, v, o, lse, dout, dq, dk, dv, B, H, N, D, causal, flags);
+  if (rc != SAGE_OK) return rc;
+  if (!workspace || !aligned(workspace, 256)) return SAGE_ERR_INVALID_ARG;
+  if (workspace_bytes < i8_bwd_ws_layout(B, H, N, D).total) return SAGE_ERR_WORKSPACE;
+  return attn_i8_bwd_ws_impl(q, k, v, o, lse, dout, dq, dk, dv, B, H, N, D, causal, flags, workspace, stream);
+}
+
+int sage_attn_int8_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse, const void* dout,
+                       float* dq, float* dk, float* dv, int B, int H, int N, int D, int causal, unsigned flags,
+                       hipStream_t stream) {
+  int rc = attn_i8_bwd_args(q, k, v, o, lse, dout, dq, dk, dv, B, H, N, D, causal, flags);
+  if (rc != SAGE_OK) return rc;
+  const size_t bytes = i8_bwd_ws_layout(B, H, N, D).total;
+  void* ws = nullptr;
+  if (hipMallocAsync(&ws, bytes, stream) != hipSuccess) return SAGE_ERR_HIP;
+  rc = attn_i8_bwd_ws_impl(q, k, v, o, lse, dout, dq, dk, dv, B, H, N, D, causal, flags, ws, stream);
+  if (hipFreeAsync(ws, stream) != hipSuccess && rc == SAGE_OK) rc = SAGE_ERR_HIP;
+  return rc;
 }
 
 const char* sage_status_string(int status) {

@@ -151,6 +151,22 @@ def test_int8_sizes_and_validation(L):
     assert L.sage_attn_int8_fwd_prequant(*bad) == bd.SAGE_ERR_INVALID_ARG
 
 
+def test_int8_bwd_validation(L):
+    args = lambda **kw: [kw.get(n, FAKE) for n in ("q", "k", "v", "o", "lse", "do", "dq", "dk", "dv")]
+    ok = args()
+    assert L.sage_attn_int8_bwd_workspace_size(1, 2, 1000, 128, 0) > 2 * 1000 * 128 * 5
+    assert L.sage_attn_int8_bwd_workspace_size(1, 2, 1000, 128, bd.SAGE_BKV64) == 0
+    assert L.sage_attn_int8_bwd_workspace_size(1, 2, 1000, 96, 0) == 0
+    assert L.sage_attn_int8_bwd(*ok, 1, 1, 128, 128, 0, bd.SAGE_BKV64, None) == bd.SAGE_ERR_UNSUPPORTED
+    for f in (bd.SAGE_FMT_NV16_E4M3, bd.SAGE_SMOOTH_Q, 0x80):
+        assert L.sage_attn_int8_bwd(*ok, 1, 1, 128, 128, 0, f, None) == bd.SAGE_ERR_INVALID_ARG
+    for bad in (dict(q=None), dict(lse=None), dict(dv=None), dict(o=FAKE + 4), dict(do=FAKE + 8), dict(lse=FAKE + 2)):
+        assert L.sage_attn_int8_bwd(*args(**bad), 1, 1, 128, 128, 0, 0, None) == bd.SAGE_ERR_INVALID_ARG, bad
+    assert L.sage_attn_int8_bwd(*ok, 1, 1, 128, 128, 2, 0, None) == bd.SAGE_ERR_INVALID_ARG
+    need = L.sage_attn_int8_bwd_workspace_size(1, 1, 128, 128, 0)
+    assert L.sage_attn_int8_bwd_ws(*ok, 1, 1, 128, 128, 0, 0, FAKE, need - 1, None) == bd.SAGE_ERR_WORKSPACE
+
+
 def test_product_path_does_not_import_oracle():
     import paper_2505_11594_amd
     pkg = os.path.dirname(paper_2505_11594_amd.__file__)

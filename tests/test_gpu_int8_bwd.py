@@ -1,0 +1,99 @@
+"""GPU parity of the 8-bit attention backward (Algorithm 3) against the
+oracle, through the C ABI.  Both sides take the same O and L (the oracle's
+forward); dQ, dK, dV must match within the oracle's per-element tolerance
+(codes of P^ and dS^ whose pre-rounding value lies near a rounding midpoint
+may take either neighbour on the GPU) plus 2e-5 of the tensor's largest
+magnitude for fp32 rounding and summation order."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2505_11594_amd import binding as bd
+from paper_2505_11594_amd import workloads as wl
+
+from _gpu import to_dev, torch_dev, say
+
+pytestmark = pytest.mark.gpu
+
+
+def make_case(B, H, N, D, in_dtype, seed, causal, k_bias_var=1.0, outlier_frac=0.0):
+    q, k, v = wl.make_inputs(B, H, N, D, in_dtype, seed=seed, k_bias_var=k_bias_var, outlier_frac=outlier_frac)
+    rng = np.random.default_rng(seed + 3)
+    do = wl.to_bits(rng.standard_normal((B, H, N, D)).astype(np.float32), in_dtype)
+    o, lse, _, _ = oracle.attn_int8(q, k, v, in_dtype, causal, 128)
+    return q, k, v, do, o.reshape(B, H, N, D), lse.reshape(B, H, N)
+
+
+def gpu_bwd(q, k, v, do, o, lse, in_dtype, causal, flags=0):
+    torch = torch_dev()
+    od = torch.from_numpy(o).to("cuda")
+    ld = torch.from_numpy(lse).to("cuda")
+    r = bd.sage_attn_int8_bwd(to_dev(q, in_dtype), to_dev(k, in_dtype), to_dev(v, in_dtype), od, ld,
+                              to_dev(do, in_dtype), causal=causal, flags=flags)
+    torch.cuda.synchronize()
+    return [x.cpu().numpy() for x in r]
+
+
+def check_grads(got, ref, tol, label):
+    for name, g, r, t in zip(("dQ", "dK", "dV"), got, ref, tol):
+        err = np.abs(g - r)
+        lim = t + 2e-5 * np.abs(r).max()
+        say("%s %s: max err %.3g (max |ref| %.3g), tie elements %d" % (label, name, float(err.max()),
+                                                                     float(np.abs(r).max()), int((t > 0).sum())))
+        assert np.all(err <= lim), "%s %s: %d elements over, worst %.3g" % (label, name, int((err > lim).sum()),
+                                                                           float(err.max()))
+
+
+@pytest.mark.parametrize("N", [1, 100, 257, 640])
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_bwd_edge_shapes(N, D, causal):
+    in_dtype = 1 if (N + D) % 2 else 0
+    say("bwd edge N=%d D=%d causal=%d dtype=%d" % (N, D, causal, in_dtype))
+    q, k, v, do, o, lse = make_case(1, 2, N, D, in_dtype, seed=1100 + N, causal=causal, k_bias_var=4.0,
+                                    outlier_frac=0.02)
+    got = gpu_bwd(q, k, v, do, o, lse, in_dtype, causal)
+    *ref, tol = oracle.attn_int8_bwd(q, k, v, do, o, lse, in_dtype, causal, 128)
+    check_grads(got, ref, tol, "edge")
+
+
+def test_bwd_no_smooth_k():
+    q, k, v, do, o, lse = make_case(1, 2, 300, 128, 1, seed=1110, causal=False, k_bias_var=4.0)
+    got = gpu_bwd(q, k, v, do, o, lse, 1, False, flags=bd.SAGE_NO_SMOOTH_K)
+    *ref, tol = oracle.attn_int8_bwd(q, k, v, do, o, lse, 1, False, 128, flags=oracle.NO_SMOOTH_K)
+    check_grads(got, ref, tol, "no smooth-K")
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_bwd_longer_sequence(causal):
+    q, k, v, do, o, lse = make_case(1, 2, 2048, 128, 1, seed=1120 + causal, causal=causal)
+    got = gpu_bwd(q, k, v, do, o, lse, 1, causal)
+    *ref, tol = oracle.attn_int8_bwd(q, k, v, do, o, lse, 1, causal, 128)
+    check_grads(got, ref, tol, "N=2048")
+
+
+def test_bwd_deterministic_and_workspace_variant():
+    torch = torch_dev()
+    B, H, N, D = 1, 2, 1024, 128
+    q, k, v, do, o, lse = make_case(B, H, N, D, 1, seed=1130, causal=False)
+    a = gpu_bwd(q, k, v, do, o, lse, 1, False)
+    b = gpu_bwd(q, k, v, do, o, lse, 1, False)
+    ws = torch.empty(bd.attn_int8_bwd_workspace_size(B, H, N, D, bd.SAGE_IN_BF16), dtype=torch.uint8, device="cuda")
+    c = bd.sage_attn_int8_bwd(to_dev(q, 1), to_dev(k, 1), to_dev(v, 1), torch.from_numpy(o).cuda(),
+                              torch.from_numpy(lse).cuda(), to_dev(do, 1), workspace=ws)
+    torch.cuda.synchronize()
+    for x, y, z in zip(a, b, c):
+        assert np.array_equal(x, y) and np.array_equal(x, z.cpu().numpy())
+
+
+def test_bwd_zero_do_and_doubling():
+    """Closed forms on the GPU: dO = 0 gives zero gradients; doubling dO
+    doubles every gradient bit for bit."""
+    q, k, v, do, o, lse = make_case(1, 1, 300, 128, 1, seed=1140, causal=True)
+    z = gpu_bwd(q, k, v, np.zeros_like(do), o, lse, 1, True)
+    assert not any(x.any() for x in z)
+    a = gpu_bwd(q, k, v, do, o, lse, 1, True)
+    d2 = wl.to_bits(wl.from_bits(do, 1) * np.float32(2.0), 1)
+    b = gpu_bwd(q, k, v, d2, o, lse, 1, True)
+    for x, y in zip(a, b):
+        assert np.array_equal(2 * x, y)
