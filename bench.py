@@ -12,7 +12,8 @@ the attention kernel's own rate (HIP events around repeated launches of the
 kernel alone on the same stream) as a fraction of the MXFP4 dense MFMA peak,
 the bf16-MFMA comparison kernel's rate when available, the 8-bit attention
 forward of Algorithm 2 (its whole step and its INT8-MFMA kernel alone, with
-its accuracy against exact attention) on the same inputs, and the CPU oracle
+its accuracy against exact attention) and the backward of Algorithm 3 on the
+same inputs, and the CPU oracle
 timed on a bounded sample of query rows on the host cores.
 """
 from __future__ import annotations
@@ -232,10 +233,48 @@ def int8_forward(torch, bd, w, qd, kd, vd, o, steps):
     tops = w.ops / t_k / 1e12
     log("int8 forward: step %.3f ms = %.1f TOPS; kernel %.3f ms = %.1f TOPS (%.1f%% of the int8 peak); cossim %.5f"
         % (t_step * 1e3, w.ops / t_step / 1e12, t_k * 1e3, tops, 100 * tops / PEAK_INT8_TOPS, acc["cossim"]))
+    step()                                       # leave this step's O and L in o, L for the backward
+    torch.cuda.synchronize()
+    int8_forward.lse = L
     del ws, qq, kq, vq
     return {"step_ms": t_step * 1e3, "step_tops": w.ops / t_step / 1e12, "kernel": "attn_int8_kernel<128,128,false,0>",
             "kernel_ms": t_k * 1e3, "kernel_tops": tops, "peak": PEAK_INT8_TOPS, "frac_of_int8_peak": tops / PEAK_INT8_TOPS,
             "kv_tile": 128, "accuracy_vs_exact": acc}
+
+
+def int8_backward(torch, bd, w, qd, kd, vd, o, L, steps):
+    """Algorithm 3 on the bench inputs, from the 8-bit forward's O and L and a
+    seeded dO: the whole step (INT8 psi of Q, K, dO and their transposed
+    copies, D = rowsum(dO O), the dK/dV and dQ kernels) timed with HIP events.
+    Algorithmic work: the five products, 10 B H N^2 D (halved when causal);
+    its floor is four int8 products at the int8 peak plus dO V^T at the
+    16-bit peak."""
+    B, H, N, D = w.B, w.H, w.N, w.D
+    g = torch.Generator(device=qd.device).manual_seed(11)
+    dout = torch.randn((B, H, N, D), generator=g, device=qd.device, dtype=torch.float32).to(qd.dtype)
+    flags = bd.SAGE_IN_BF16 if w.in_dtype == 1 else 0
+    ws = torch.empty(bd.attn_int8_bwd_workspace_size(B, H, N, D, flags), dtype=torch.uint8, device=qd.device)
+    grads = [torch.empty((B, H, N, D), dtype=torch.float32, device=qd.device) for _ in range(3)]
+    run = lambda: bd.sage_attn_int8_bwd(qd, kd, vd, o, L, dout, causal=w.causal, workspace=ws, out=grads)
+    run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n = max(2, min(steps, 3))
+    e0.record()
+    for _ in range(n):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / 1e3 / n
+    ops = 10.0 * B * H * N * N * D * (0.5 if w.causal else 1.0)
+    floor = (0.8 * ops) / (PEAK_INT8_TOPS * 1e12) + (0.2 * ops) / (PEAK_BF16_TFLOPS * 1e12)
+    log("int8 backward: step %.3f ms = %.1f TOPS (%.1f%% of its mixed int8/bf16 peak)" % (t * 1e3, ops / t / 1e12,
+                                                                                      100 * floor / t))
+    del ws, grads, dout
+    return {"step_ms": t * 1e3, "tops": ops / t / 1e12, "ops": ops,
+            "kernels": ["attn_i8_bwd_dkdv_kernel<128,false,true>", "attn_i8_bwd_dq_kernel<128,false,true>"],
+            "frac_of_mixed_peak": floor / t,
+            "peak_note": "8/10 of the work at the int8 peak (5000 TOPS), 2/10 (dO V^T) at the bf16 peak (2500 TFLOP/s)"}
 
 
 def main():
@@ -396,8 +435,10 @@ def main():
         others = other_configs(torch, bd, wl, args.steps)
 
     int8 = None
+    int8_bwd = None
     if not args.no_int8:
         int8 = int8_forward(torch, bd, w, qd, kd, vd, o, args.steps)
+        int8_bwd = int8_backward(torch, bd, w, qd, kd, vd, o, int8_forward.lse, args.steps)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -429,6 +470,7 @@ def main():
         "bf16_kernel": bf16,
         "smooth_q_step": smooth_q,
         "int8_fwd": int8,
+        "int8_bwd": int8_bwd,
         "other_configs": others,
         "cpu_baseline": cpu,
     }
