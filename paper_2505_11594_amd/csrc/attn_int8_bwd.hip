@@ -24,8 +24,11 @@
 //    registers while its maximum is reduced across the waves, and dS^ is the B
 //    operand of dQ^T = K^T dS^T (A = K^T rows, permuted the same way).
 // Both run one wave per SIMD (the int32 and fp32 accumulators of two
-// products do not fit two waves' register budget); operands come straight
-// from HBM / L2 into registers.
+// products do not fit two waves' register budget).  Each workgroup stages the
+// operands its four waves share -- a query block (Q^, dO, L, D and the
+// transposed Q^, dO^) for dK/dV, a KV block (K^, V, K^T) for dQ -- in LDS in
+// MFMA-operand order with global loads that write LDS, one block ahead of
+// the block being computed.
 #include "sage_common.h"
 
 typedef int v16i __attribute__((ext_vector_type(16)));
@@ -100,6 +103,34 @@ __global__ __launch_bounds__(256) void i8_bwd_prep_kernel(const uint16_t* __rest
   }
 }
 
+__device__ __forceinline__ void bw_lds_load16(const void* src, void* dst) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+}
+__device__ __forceinline__ void bw_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
+// vmcnt(n) for the counts used below (n < 16: the low field of the immediate)
+template <int N>
+__device__ __forceinline__ void bw_wait_vm() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
+// LDS of the dK/dV kernel: per query block, in MFMA-operand order (1 KiB per
+// 64-lane operand read, lane l's 16 bytes at 16 l):
+//   A stage (double-buffered): Q^ operand blocks (u, s) -- rows q0 + 32u + col,
+//   channels [32s + 16hi, +16) --, dO operand blocks (u, s16) -- channels
+//   [16s16 + 8hi, +8) --, and the block's Lb and D (128 floats each);
+//   T (single): Q^T and dO^T operand blocks (db, u) -- channel rows 32db +
+//   col, queries [32u + 16hi, +16) of the block.
+template <int D>
+struct BwKvLds {
+  static constexpr int NKS = D / 32, NKS16 = D / 16, NDB = D / 32;
+  static constexpr int NQA = 4 * NKS, NGA = 4 * NKS16, NT = NDB * 4;
+  static constexpr int QA_OFF = 0, GA_OFF = NQA * 1024, LD_OFF = GA_OFF + NGA * 1024, A_BYTES = LD_OFF + 1024;
+  static constexpr int QT_OFF = 0, GT_OFF = NT * 1024, T_BYTES = 2 * NT * 1024;
+  static constexpr int AJ = (NQA + NGA) / 4, TJ = 2 * NT / 4;   // loads per wave
+  static_assert((NQA + NGA) % 4 == 0 && (2 * NT) % 4 == 0, "even split over 4 waves");
+};
+
 // ---------------------------------------------------------------------------
 // dK, dV.  qc/kc: Q^, K^ row-major; qt, gt: Q^T, dO^T int8 [BH, D, Np] with
 // each 32-query group permuted; qs, gs: s_Q, s_dO per 128 rows; ks: s_K per
@@ -112,7 +143,10 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
     const uint16_t* __restrict__ dout, const int8_t* __restrict__ gt, const float* __restrict__ gs,
     const float* __restrict__ drow, const float* __restrict__ lb, float* __restrict__ dk, float* __restrict__ dv,
     int N, int Np, int nqb, float c2, float rsd) {
-  constexpr int NKS = D / 32, NKS16 = D / 16, NDB = D / 32;
+  using T = BwKvLds<D>;
+  constexpr int NKS = T::NKS, NKS16 = T::NKS16, NDB = T::NDB;
+  __shared__ __attribute__((aligned(16))) uint8_t ldsA[2][T::A_BYTES];
+  __shared__ __attribute__((aligned(16))) uint8_t ldsT[T::T_BYTES];
   __shared__ float red[2][2][4];                   // [block parity][P, dS][wave]
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -137,41 +171,76 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
 #pragma unroll
   for (int db = 0; db < NDB; ++db) { dva[db] = v16f{}; dka[db] = v16f{}; }
 
-  const int i0 = CAUSAL ? kb / BW_Q : 0;
-  for (int i = i0; i < nqb; ++i) {
+  // loads of query block i: wave w takes operand blocks w, w + 4, ...; rows
+  // >= N read row N - 1 (those entries are masked)
+  auto issue_A = [&](int i, int buf) {
     const int q0 = i * BW_Q;
+    uint8_t* L = ldsA[buf];
+#pragma unroll
+    for (int k = 0; k < T::AJ; ++k) {
+      const int b = wave + 4 * k;
+      if (b < T::NQA) {
+        const int u = b / NKS, s = b % NKS;
+        const int q = min(q0 + 32 * u + col, N - 1);
+        bw_lds_load16(qc + ((size_t)bh * N + q) * D + 32 * s + 16 * hi, L + T::QA_OFF + b * 1024);
+      } else {
+        const int g = b - T::NQA, u = g / NKS16, s = g % NKS16;
+        const int q = min(q0 + 32 * u + col, N - 1);
+        bw_lds_load16(dout + ((size_t)bh * N + q) * D + 16 * s + 8 * hi, L + T::GA_OFF + g * 1024);
+      }
+    }
+  };
+  auto issue_LD = [&](int i, int buf) {          // Lb and D of block i (wave 0)
+    const int q0 = i * BW_Q;
+    const float* src = (lane < 32 ? lb + (size_t)bh * Np + q0 + 4 * lane : drow + (size_t)bh * Np + q0 + 4 * (lane - 32));
+    bw_lds_load16(src, ldsA[buf] + T::LD_OFF);
+  };
+  auto issue_T = [&](int i) {
+    const int q0 = i * BW_Q;
+#pragma unroll
+    for (int k = 0; k < T::TJ; ++k) {
+      const int b = wave + 4 * k, which = b / T::NT, t = b % T::NT, db = t / 4, u = t % 4;
+      const size_t off = ((size_t)bh * D + 32 * db + col) * Np + q0 + 32 * u + 16 * hi;
+      bw_lds_load16((which ? gt : qt) + off, ldsT + (which ? T::GT_OFF : T::QT_OFF) + t * 1024);
+    }
+  };
+
+  const int i0 = CAUSAL ? kb / BW_Q : 0;
+  if (wave == 0) issue_LD(i0, i0 & 1);
+  issue_A(i0, i0 & 1);
+  for (int i = i0; i < nqb; ++i) {
+    const int q0 = i * BW_Q, a = i & 1;
+    bw_wait_all();                                 // this wave's loads of block i have landed
+    __syncthreads();                               // everyone's; every wave is done with block i - 1
+    if (i + 1 < nqb && wave == 0) issue_LD(i + 1, a ^ 1);
+    issue_T(i);
+    if (i + 1 < nqb) issue_A(i + 1, a ^ 1);
+    const uint8_t* L = ldsA[a];
     const float sQ = qs[(size_t)bh * nqb + i];
     const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);   // see the forward kernel
     const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && q0 < kb + BW_K - 1);
 
     // P and dS of one 32-query subtile: element v is query q0 + 32u + 8(v>>2) + 4hi + (v&3)
     auto subtile = [&](int u, float (&P)[16], float (&dS)[16]) {
-      const int qrow = q0 + 32 * u + col;          // A-operand row of this lane
-      v4i qa[NKS], ga[NKS16];
-      const int8_t* qr = qc + ((size_t)bh * N + qrow) * D;
-      const uint16_t* gr = dout + ((size_t)bh * N + qrow) * D;
-#pragma unroll
-      for (int s = 0; s < NKS; ++s) qa[s] = qrow < N ? *reinterpret_cast<const v4i*>(qr + 32 * s + 16 * hi) : v4i{0, 0, 0, 0};
-#pragma unroll
-      for (int s = 0; s < NKS16; ++s) ga[s] = qrow < N ? *reinterpret_cast<const v4i*>(gr + 16 * s + 8 * hi) : v4i{0, 0, 0, 0};
       v16i sacc = v16i{};
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(qa[s], kreg[s], sacc, 0, 0, 0);
+      for (int s = 0; s < NKS; ++s)
+        sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+            *reinterpret_cast<const v4i*>(L + T::QA_OFF + (u * NKS + s) * 1024 + lane * 16), kreg[s], sacc, 0, 0, 0);
       v16f dp = v16f{};
 #pragma unroll
-      for (int s = 0; s < NKS16; ++s) dp = mfma16<BF16>(ga[s], vreg[s], dp);
+      for (int s = 0; s < NKS16; ++s)
+        dp = mfma16<BF16>(*reinterpret_cast<const v4i*>(L + T::GA_OFF + (u * NKS16 + s) * 1024 + lane * 16), vreg[s], dp);
       const int qb4 = q0 + 32 * u + 4 * hi;
-      const float* lbr = lb + (size_t)bh * Np + qb4;
-      const float* dr = drow + (size_t)bh * Np + qb4;
+      const float* lbr = reinterpret_cast<const float*>(L + T::LD_OFF) + 32 * u + 4 * hi;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const float4 l4 = *reinterpret_cast<const float4*>(lbr + 8 * g);
-        const float4 d4 = *reinterpret_cast<const float4*>(dr + 8 * g);
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dvv[4] = {d4.x, d4.y, d4.z, d4.w};
+        const v4f l4 = *reinterpret_cast<const v4f*>(lbr + 8 * g);
+        const v4f d4 = *reinterpret_cast<const v4f*>(lbr + 128 + 8 * g);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int e = 4 * g + r;
-          float arg = __builtin_fmaf((float)sacc[e], ct, -lv[r]);
+          float arg = __builtin_fmaf((float)sacc[e], ct, -l4[r]);
           if (need_mask) {
             // visible iff q < N, key < N and (causal) key <= q: the three sign bits
             const int q = qb4 + 8 * g + r;
@@ -180,7 +249,7 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
             arg = __builtin_fminf(arg, __uint_as_float(0xFF800000u ^ ((uint32_t)m & 0x80000000u)));
           }
           const float p = __builtin_amdgcn_exp2f(arg);
-          const float d = dp[e] - dvv[r];
+          const float d = dp[e] - d4[r];
           P[e] = p;
           dS[e] = p * d;
         }
@@ -198,11 +267,13 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
     }
     pm = wave_max(pm);
     dm = wave_max(dm);
-    const int par = i & 1;
-    if (lane == 0) { red[par][0][wave] = pm; red[par][1][wave] = dm; }
+    if (lane == 0) { red[a][0][wave] = pm; red[a][1][wave] = dm; }
+    // the T loads of this block were issued before the next block's A loads
+    if (i + 1 < nqb) bw_wait_vm<T::AJ>();
+    else bw_wait_all();
     __syncthreads();
-    pm = __builtin_fmaxf(__builtin_fmaxf(red[par][0][0], red[par][0][1]), __builtin_fmaxf(red[par][0][2], red[par][0][3]));
-    dm = __builtin_fmaxf(__builtin_fmaxf(red[par][1][0], red[par][1][1]), __builtin_fmaxf(red[par][1][2], red[par][1][3]));
+    pm = __builtin_fmaxf(__builtin_fmaxf(red[a][0][0], red[a][0][1]), __builtin_fmaxf(red[a][0][2], red[a][0][3]));
+    dm = __builtin_fmaxf(__builtin_fmaxf(red[a][1][0], red[a][1][1]), __builtin_fmaxf(red[a][1][2], red[a][1][3]));
     const float sP = pm / 127.0f, rP = pm > 0.0f ? 1.0f / sP : 0.0f;
     const float sdS = dm / 127.0f, rdS = dm > 0.0f ? 1.0f / sdS : 0.0f;
 
@@ -215,12 +286,10 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
       float P[16], dS[16];
       subtile(u, P, dS);
       const v4i pc = bw_codes(P, rP), sc = bw_codes(dS, rdS);
-      const size_t tq = (size_t)q0 + 32 * u + 16 * hi;
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        const size_t rowo = ((size_t)bh * D + 32 * db + col) * Np + tq;
-        const v4i ga = *reinterpret_cast<const v4i*>(gt + rowo);
-        const v4i qa = *reinterpret_cast<const v4i*>(qt + rowo);
+        const v4i ga = *reinterpret_cast<const v4i*>(ldsT + T::GT_OFF + (db * 4 + u) * 1024 + lane * 16);
+        const v4i qa = *reinterpret_cast<const v4i*>(ldsT + T::QT_OFF + (db * 4 + u) * 1024 + lane * 16);
         dvi[db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ga, pc, dvi[db], 0, 0, 0);
         dki[db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(qa, sc, dki[db], 0, 0, 0);
       }
@@ -249,6 +318,19 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
   }
 }
 
+// LDS of the dQ kernel: per KV block (double-buffered), in operand order:
+// K^ blocks (t, s) -- key rows kb + 32t + col, channels [32s + 16hi, +16) --,
+// V blocks (t, s16) -- channels [16s16 + 8hi, +8) --, K^T blocks (db, t) --
+// channel rows 32db + col, keys [32t + 16hi, +16) of the block.
+template <int D>
+struct BwQLds {
+  static constexpr int NKS = D / 32, NKS16 = D / 16, NDB = D / 32, NT = BW_K / 32;
+  static constexpr int NKA = NT * NKS, NVA = NT * NKS16, NKT = NDB * NT;
+  static constexpr int KA_OFF = 0, VA_OFF = NKA * 1024, KT_OFF = VA_OFF + NVA * 1024, BYTES = KT_OFF + NKT * 1024;
+  static constexpr int J = (NKA + NVA + NKT) / 4;
+  static_assert((NKA + NVA + NKT) % 4 == 0, "even split over 4 waves");
+};
+
 // ---------------------------------------------------------------------------
 // dQ.  kt: K^T int8 [BH, D, Np] with each 32-key group permuted; kmean: K_m
 // [BH, D] or null (no smoothing).
@@ -259,7 +341,10 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
     const float* __restrict__ ks, const int8_t* __restrict__ kt, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lb,
     const float* __restrict__ kmean, float* __restrict__ dq, int N, int Np, int nqb, float c2, float rsd) {
-  constexpr int NKS = D / 32, NKS16 = D / 16, NDB = D / 32, NT = BW_K / 32;
+  using T = BwQLds<D>;
+  constexpr int NKS = T::NKS, NKS16 = T::NKS16, NDB = T::NDB, NT = T::NT;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2][T::BYTES];
+  __shared__ __attribute__((aligned(16))) float kms[D];
   __shared__ float red[2][4];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -268,6 +353,7 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
   const int q0 = i * BW_Q, qw = q0 + 32 * wave, qi = qw + col;
   const float sQ = qs[(size_t)bh * nqb + i];
   const float lbq = lb[(size_t)bh * Np + qi], dq_row = drow[(size_t)bh * Np + qi];
+  if (tid < D) kms[tid] = kmean != nullptr ? kmean[(size_t)bh * D + tid] : 0.0f;
 
   v4i qreg[NKS], greg[NKS16];
   {
@@ -282,10 +368,37 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
 #pragma unroll
   for (int db = 0; db < NDB; ++db) dqa[db] = v16f{};
 
+  // loads of KV block j: wave w takes operand blocks w, w + 4, ...; V rows
+  // >= N read row N - 1 (those keys are masked)
+  auto issue = [&](int j, int buf) {
+    const int kb = j * BW_K;
+    uint8_t* L = lds[buf];
+#pragma unroll
+    for (int k = 0; k < T::J; ++k) {
+      const int b = wave + 4 * k;
+      if (b < T::NKA) {
+        const int t = b / NKS, s = b % NKS;
+        bw_lds_load16(kc + ((size_t)bh * Np + kb + 32 * t + col) * D + 32 * s + 16 * hi, L + T::KA_OFF + b * 1024);
+      } else if (b < T::NKA + T::NVA) {
+        const int g = b - T::NKA, t = g / NKS16, s = g % NKS16;
+        const int kr = min(kb + 32 * t + col, N - 1);
+        bw_lds_load16(v + ((size_t)bh * N + kr) * D + 16 * s + 8 * hi, L + T::VA_OFF + g * 1024);
+      } else {
+        const int g = b - T::NKA - T::NVA, db = g / NT, t = g % NT;
+        bw_lds_load16(kt + ((size_t)bh * D + 32 * db + col) * Np + kb + 32 * t + 16 * hi, L + T::KT_OFF + g * 1024);
+      }
+    }
+  };
+
   int nkb = (N + BW_K - 1) / BW_K;
   if (CAUSAL) nkb = min(nkb, min(q0 + BW_Q - 1, N - 1) / BW_K + 1);
+  issue(0, 0);
   for (int j = 0; j < nkb; ++j) {
-    const int kb = j * BW_K;
+    const int kb = j * BW_K, buf = j & 1;
+    bw_wait_all();
+    __syncthreads();                               // block j has landed; every wave is done with block j - 1
+    if (j + 1 < nkb) issue(j + 1, buf ^ 1);
+    const uint8_t* L = lds[buf];
     const float sK = ks[(size_t)bh * (Np / BW_K) + j];
     const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);
     const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && kb + BW_K - 1 > q0);
@@ -293,17 +406,15 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
     float dm = 0.0f, rs = 0.0f;
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      const int krow = kb + 32 * t + col;          // A-operand row of this lane
-      const int8_t* kr = kc + ((size_t)bh * Np + krow) * D;
-      const uint16_t* vr = v + ((size_t)bh * N + krow) * D;
       v16i sacc = v16i{};
 #pragma unroll
       for (int s = 0; s < NKS; ++s)
-        sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(*reinterpret_cast<const v4i*>(kr + 32 * s + 16 * hi), qreg[s], sacc, 0, 0, 0);
+        sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+            *reinterpret_cast<const v4i*>(L + T::KA_OFF + (t * NKS + s) * 1024 + lane * 16), qreg[s], sacc, 0, 0, 0);
       v16f dp = v16f{};
 #pragma unroll
       for (int s = 0; s < NKS16; ++s)
-        dp = mfma16<BF16>(krow < N ? *reinterpret_cast<const v4i*>(vr + 16 * s + 8 * hi) : v4i{0, 0, 0, 0}, greg[s], dp);
+        dp = mfma16<BF16>(*reinterpret_cast<const v4i*>(L + T::VA_OFF + (t * NKS16 + s) * 1024 + lane * 16), greg[s], dp);
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         float arg = __builtin_fmaf((float)sacc[e], ct, -lbq);
@@ -322,10 +433,9 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
       }
     }
     dm = wave_max(dm);
-    const int par = j & 1;
-    if (lane == 0) red[par][wave] = dm;
+    if (lane == 0) red[buf][wave] = dm;
     __syncthreads();
-    dm = __builtin_fmaxf(__builtin_fmaxf(red[par][0], red[par][1]), __builtin_fmaxf(red[par][2], red[par][3]));
+    dm = __builtin_fmaxf(__builtin_fmaxf(red[buf][0], red[buf][1]), __builtin_fmaxf(red[buf][2], red[buf][3]));
     const float sdS = dm / 127.0f, rdS = dm > 0.0f ? 1.0f / sdS : 0.0f;
     v16i dqi[NDB];
 #pragma unroll
@@ -334,10 +444,9 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
     for (int t = 0; t < NT; ++t) {
       const v4i sc = bw_codes(dS[t], rdS);
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const v4i ka = *reinterpret_cast<const v4i*>(kt + ((size_t)bh * D + 32 * db + col) * Np + kb + 32 * t + 16 * hi);
-        dqi[db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ka, sc, dqi[db], 0, 0, 0);
-      }
+      for (int db = 0; db < NDB; ++db)
+        dqi[db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+            *reinterpret_cast<const v4i*>(L + T::KT_OFF + (db * NT + t) * 1024 + lane * 16), sc, dqi[db], 0, 0, 0);
     }
     const float fq = (sdS * sK) * rsd;
     const float rr = (rs + __shfl_xor(rs, 32, 64)) * rsd;   // rowsum(dS) of this lane's query, / sqrt(D)
@@ -345,14 +454,12 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        float4 km = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (kmean != nullptr) km = *reinterpret_cast<const float4*>(kmean + (size_t)bh * D + 32 * db + 8 * g + 4 * hi);
-        const float kmv[4] = {km.x, km.y, km.z, km.w};
+        const v4f km = *reinterpret_cast<const v4f*>(kms + 32 * db + 8 * g + 4 * hi);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int e = 4 * g + r;
           float x = __builtin_fmaf((float)dqi[db][e], fq, dqa[db][e]);
-          if (kmean != nullptr) x = __builtin_fmaf(rr, kmv[r], x);
+          if (kmean != nullptr) x = __builtin_fmaf(rr, km[r], x);
           dqa[db][e] = x;
         }
       }
