@@ -31,9 +31,16 @@ class SageError(RuntimeError):
 
 
 def lib():
-    """Load the in-tree HIP library (raises if it has not been built)."""
+    """Load the in-tree HIP library (raises if it has not been built).
+
+    torch is imported first: its wheel carries its own HIP runtime under the
+    same soname as ROCm's, and the runtime loaded first is the one every
+    later library binds to.  Loading this library before torch would map
+    ROCm's runtime next to torch's, and device pointers and streams would
+    cross between the two."""
     global _lib
     if _lib is None:
+        import torch  # noqa: F401  (see above)
         if not os.path.exists(LIB_PATH):
             raise RuntimeError("libsage_mi355x.so is not built; run __graft_entry__.build() "
                                "or python paper_2505_11594_amd/build.py")

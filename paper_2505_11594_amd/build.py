@@ -1,6 +1,8 @@
-"""Build the gfx950 HIP library ``libsage_mi355x.so`` in-tree with hipcc, and
-the separate measurement library ``libsage_rates.so`` (instruction issue-rate
-microbenchmarks used by ``bench.py --mode rates``).
+"""Build the gfx950 HIP library ``libsage_mi355x.so`` in-tree with hipcc, the
+separate measurement library ``libsage_rates.so`` (instruction issue-rate
+microbenchmarks used by ``bench.py --mode rates``) and the hardware-probe
+library ``libsage_probes.so`` (the conversion, exp2 and MFMA-layout semantics
+the kernels rely on, checked by the tests).
 
 Every HIP source is compiled for ``--offload-arch=gfx950`` only.  Packed FP32
 instructions are disabled (``-packed-fp32-ops``) and floating-point
@@ -21,6 +23,8 @@ SOURCES = ["sage_abi.hip", "quant.hip", "attn_fp4.hip", "attn_bf16.hip", "attn_n
            "attn_int8.hip", "attn_int8_bwd.hip"]
 RATES_LIB = os.path.join(HERE, "libsage_rates.so")
 RATES_SOURCES = ["issue_rates.hip"]
+PROBES_LIB = os.path.join(HERE, "libsage_probes.so")
+PROBES_SOURCES = ["probes.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -49,6 +53,7 @@ def _compile(lib: str, sources, verbose: bool) -> str:
 
 def build(verbose: bool = False) -> str:
     _compile(RATES_LIB, RATES_SOURCES, verbose)
+    _compile(PROBES_LIB, PROBES_SOURCES, verbose)
     return _compile(LIB, SOURCES, verbose)
 
 
