@@ -94,7 +94,10 @@ RATE_TESTS = [  # (name, what one loop iteration issues, instructions of the cou
     ("mfma_fp4+exp", "4 FP4 MFMA + 8 v_exp_f32", 4), ("mfma_bf16", "4 v_mfma_f32_32x32x16_bf16", 4),
     ("mfma_bf16+fma", "4 bf16 MFMA + 32 v_fma_f32", 4), ("mfma16_fp4", "8 v_mfma_scale_f32_16x16x128_f8f6f4 (FP4)", 8),
     ("mfma16_fp4+fma", "8 FP4 16x16x128 MFMA + 32 v_fma_f32", 8),
-    ("split", "even SIMD slots: 4 FP4 MFMA; odd slots: 32 v_fma_f32", None)]
+    ("split", "even SIMD slots: 4 FP4 MFMA; odd slots: 32 v_fma_f32", None),
+    ("exp+fma", "8 v_exp_f32 + 32 independent v_fma_f32", 8),
+    ("cvt_fp4+fma", "8 v_cvt_scalef32_pk_fp4_f32 + 32 independent v_fma_f32", 8),
+    ("chain", "8 x (v_fma_f32 -> v_exp_f32 -> v_add_f32) + 4 FP4 packs", 8)]
 
 
 def issue_rates(torch):
@@ -132,7 +135,13 @@ def issue_rates(torch):
             "fma_hidden_under_bf16_mfma": (g("mfma_bf16") + g("fma") - g("mfma_bf16+fma")) / g("fma"),
             "fma_hidden_under_fp4_16x16x128": (g("mfma16_fp4") + g("fma") - g("mfma16_fp4+fma")) / g("fma"),
             # split: half the waves of a SIMD run only MFMAs, the other half only fma
-            "split_vs_serial": g("split") / ((g("mfma_fp4") + g("fma")) / 2)}
+            "split_vs_serial": g("split") / ((g("mfma_fp4") + g("fma")) / 2),
+            # transcendental / pack work against plain VALU work on independent registers
+            "exp_hidden_under_fma": (g("fma") + g("exp") - g("exp+fma")) / g("exp"),
+            "cvt_fp4_hidden_under_fma": (g("fma") + g("cvt_fp4") - g("cvt_fp4+fma")) / g("cvt_fp4"),
+            # the attention kernel's per-score work (fma, exp, add, half a pack), as measured
+            "chain_cycles_per_score": g("chain") / 8,
+            "chain_vs_isolated_rates": g("chain") / (16 * g("fma") / 32 + g("exp") + 4 * g("cvt_fp4") / 8)}
     print(json.dumps({"mode": "rates", "clock_assumed_ghz": 2.4, "iterations": iters,
                       "cycles_per_iteration": res, "derived": summary}), flush=True)
 

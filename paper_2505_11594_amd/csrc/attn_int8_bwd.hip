@@ -15,10 +15,10 @@
 //    rows, so P^ and dS^ of a 32-query subtile are, as they stand, the B
 //    operands of dV^T = dO^T P^ and dK^T = Q^T dS^ (A = dO^T / Q^T rows with
 //    each 32-query group permuted as V^T in the forward).  The block scales
-//    of P and dS need the block's maxima before any code is formed: a first
-//    pass computes S, P, dP and dS for the maxima (reduced across the waves
-//    through LDS), a second recomputes them -- bit-identically -- and
-//    quantizes.
+//    of P and dS need the block's maxima before any code is formed: P and dS
+//    of the whole block stay in registers while the maxima are reduced across
+//    the waves through LDS, then all codes are formed and each channel
+//    block's two products run over the block's four subtiles.
 //  - dQ: a workgroup owns 128 queries (4 waves x 32) and walks the KV blocks.
 //    S^T = K^ Q^T puts a query in each lane's column; dS of the block stays in
 //    registers while its maximum is reduced across the waves, and dS^ is the B
@@ -220,17 +220,20 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
     const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);   // see the forward kernel
     const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && q0 < kb + BW_K - 1);
 
-    // P and dS of one 32-query subtile: element v is query q0 + 32u + 8(v>>2) + 4hi + (v&3)
-    auto subtile = [&](int u, float (&P)[16], float (&dS)[16]) {
-      v16i sacc = v16i{};
+    // S (exact int32) and dP (fp32) of one 32-query subtile
+    auto products = [&](int u, v16i& sacc, v16f& dp) {
+      sacc = v16i{};
 #pragma unroll
       for (int s = 0; s < NKS; ++s)
         sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(
             *reinterpret_cast<const v4i*>(L + T::QA_OFF + (u * NKS + s) * 1024 + lane * 16), kreg[s], sacc, 0, 0, 0);
-      v16f dp = v16f{};
+      dp = v16f{};
 #pragma unroll
       for (int s = 0; s < NKS16; ++s)
         dp = mfma16<BF16>(*reinterpret_cast<const v4i*>(L + T::GA_OFF + (u * NKS16 + s) * 1024 + lane * 16), vreg[s], dp);
+    };
+    // P and dS of the subtile: element v is query q0 + 32u + 8(v>>2) + 4hi + (v&3)
+    auto softmax_grad = [&](int u, const v16i& sacc, const v16f& dp, float (&P)[16], float (&dS)[16]) {
       const int qb4 = q0 + 32 * u + 4 * hi;
       const float* lbr = reinterpret_cast<const float*>(L + T::LD_OFF) + 32 * u + 4 * hi;
 #pragma unroll
@@ -256,14 +259,21 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
       }
     };
 
-    // pass 1: the block maxima of P and |dS|
+    // P and dS of the whole block stay in registers (4 subtiles x 16 values)
+    // while the block maxima of P and |dS| are reduced across the waves; the
+    // products of subtile u + 1 are issued before the softmax work of subtile u
+    float P[BW_Q / 32][16], dS[BW_Q / 32][16];
     float pm = 0.0f, dm = 0.0f;
-#pragma unroll 1
-    for (int u = 0; u < BW_Q / 32; ++u) {
-      float P[16], dS[16];
-      subtile(u, P, dS);
+    v16i sacc[2];
+    v16f dp[2];
+    products(0, sacc[0], dp[0]);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) { pm = __builtin_fmaxf(pm, P[e]); dm = __builtin_fmaxf(dm, __builtin_fabsf(dS[e])); }
+    for (int u = 0; u < BW_Q / 32; ++u) {
+      if (u + 1 < BW_Q / 32) products(u + 1, sacc[(u + 1) & 1], dp[(u + 1) & 1]);
+      softmax_grad(u, sacc[u & 1], dp[u & 1], P[u], dS[u]);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) { pm = __builtin_fmaxf(pm, P[u][e]); dm = __builtin_fmaxf(dm, __builtin_fabsf(dS[u][e])); }
+      __builtin_amdgcn_sched_barrier(0);
     }
     pm = wave_max(pm);
     dm = wave_max(dm);
@@ -277,32 +287,29 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
     const float sP = pm / 127.0f, rP = pm > 0.0f ? 1.0f / sP : 0.0f;
     const float sdS = dm / 127.0f, rdS = dm > 0.0f ? 1.0f / sdS : 0.0f;
 
-    // pass 2: codes and the two int8 products of the block
-    v16i dvi[NDB], dki[NDB];
+    // codes of the block, then per channel block the two int8 products over
+    // its four subtiles (exact int32), folded into fp32 once per block
+    v4i pc[BW_Q / 32], sc[BW_Q / 32];
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) { dvi[db] = v16i{}; dki[db] = v16i{}; }
-#pragma unroll 1
-    for (int u = 0; u < BW_Q / 32; ++u) {
-      float P[16], dS[16];
-      subtile(u, P, dS);
-      const v4i pc = bw_codes(P, rP), sc = bw_codes(dS, rdS);
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const v4i ga = *reinterpret_cast<const v4i*>(ldsT + T::GT_OFF + (db * 4 + u) * 1024 + lane * 16);
-        const v4i qa = *reinterpret_cast<const v4i*>(ldsT + T::QT_OFF + (db * 4 + u) * 1024 + lane * 16);
-        dvi[db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(ga, pc, dvi[db], 0, 0, 0);
-        dki[db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(qa, sc, dki[db], 0, 0, 0);
-      }
-    }
+    for (int u = 0; u < BW_Q / 32; ++u) { pc[u] = bw_codes(P[u], rP); sc[u] = bw_codes(dS[u], rdS); }
     const float fv = sP * gs[(size_t)bh * nqb + i];
     const float fk = (sdS * sQ) * rsd;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+    for (int db = 0; db < NDB; ++db) {
+      v16i dvi = v16i{}, dki = v16i{};
+#pragma unroll
+      for (int u = 0; u < BW_Q / 32; ++u) {
+        const v4i ga = *reinterpret_cast<const v4i*>(ldsT + T::GT_OFF + (db * 4 + u) * 1024 + lane * 16);
+        const v4i qa = *reinterpret_cast<const v4i*>(ldsT + T::QT_OFF + (db * 4 + u) * 1024 + lane * 16);
+        dvi = __builtin_amdgcn_mfma_i32_32x32x32_i8(ga, pc[u], dvi, 0, 0, 0);
+        dki = __builtin_amdgcn_mfma_i32_32x32x32_i8(qa, sc[u], dki, 0, 0, 0);
+      }
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        dva[db][e] = __builtin_fmaf((float)dvi[db][e], fv, dva[db][e]);
-        dka[db][e] = __builtin_fmaf((float)dki[db][e], fk, dka[db][e]);
+        dva[db][e] = __builtin_fmaf((float)dvi[e], fv, dva[db][e]);
+        dka[db][e] = __builtin_fmaf((float)dki[e], fk, dka[db][e]);
       }
+    }
   }
 
   // dV^T, dK^T: lane holds key kw + col and channels 32db + 8g + 4hi + r

@@ -29,15 +29,22 @@ enum Test {
   kMfma16Fp4 = 8,    // 8 v_mfma_scale_f32_16x16x128_f8f6f4 (the same MACs as test 3)
   kMfma16Fp4Fma = 9, // the same + 32 v_fma_f32
   kSplit = 10,       // waves on even SIMD slots: test 3; odd slots: 32 v_fma_f32
-  kNumTests = 11
+  kExpFma = 11,      // 8 v_exp_f32 + 32 v_fma_f32 on independent registers
+  kCvtFma = 12,      // 8 v_cvt_scalef32_pk_fp4_f32 + 32 v_fma_f32 on independent registers
+  kChain = 13,       // the attention kernel's per-score chain: 8 x (v_fma_f32 -> v_exp_f32 -> v_add_f32) + 4 FP4 packs
+  kNumTests = 14
 };
 
 template <int T>
 __global__ __launch_bounds__(64) void rate_kernel(float* out, float seed) {
   const int lane = threadIdx.x;
-  float x[8];
+  float x[8], y[8], z[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) x[i] = seed + 0.001f * (lane + i);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) y[i] = seed - 0.002f * (lane + i);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) z[i] = 0.0f;
   unsigned w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   v16f acc[4] = {};
   v4f acc16[8] = {};
@@ -69,18 +76,34 @@ __global__ __launch_bounds__(64) void rate_kernel(float* out, float seed) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) x[i] = __builtin_fmaf(x[i], 0.999f, 0.0001f);
     }
-    if (T == kExp || T == kMfmaFp4Exp) {
+    if (T == kExpFma || T == kCvtFma) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) y[i] = __builtin_fmaf(y[i], 0.999f, 0.0001f);
+    }
+    if (T == kExp || T == kMfmaFp4Exp || T == kExpFma) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) x[i] = __builtin_amdgcn_exp2f(-x[i]);
     }
-    if (T == kCvtFp4) {
+    if (T == kChain) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i], 0.999f, -0.5f));
+        z[i] += p;
+        x[i] = p;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[i], x[2 * i], x[2 * i + 1], 1.0f, 0);
+    }
+    if (T == kCvtFp4 || T == kCvtFma) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) w[i] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w[i], x[i], x[(i + 1) & 7], 1.0f, 0);
     }
   }
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) s += x[i] + __uint_as_float(w[i] & 0x3fffffffu);
+  for (int i = 0; i < 8; ++i) s += x[i] + y[i] + z[i] + __uint_as_float(w[i] & 0x3fffffffu);
 #pragma unroll
   for (int i = 0; i < 4; ++i) s += acc[i][lane & 15];
 #pragma unroll
@@ -106,6 +129,10 @@ hipError_t launch_test(int test, float* out, int blocks, hipStream_t st) {
     case kMfmaBf16Fma: return launch<kMfmaBf16Fma>(out, blocks, st);
     case kMfma16Fp4: return launch<kMfma16Fp4>(out, blocks, st);
     case kMfma16Fp4Fma: return launch<kMfma16Fp4Fma>(out, blocks, st);
+    case kSplit: return launch<kSplit>(out, blocks, st);
+    case kExpFma: return launch<kExpFma>(out, blocks, st);
+    case kCvtFma: return launch<kCvtFma>(out, blocks, st);
+    case kChain: return launch<kChain>(out, blocks, st);
     default: return launch<kSplit>(out, blocks, st);
   }
 }
