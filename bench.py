@@ -281,7 +281,7 @@ def int8_backward(torch, bd, w, qd, kd, vd, o, L, steps):
                                                                                       100 * floor / t))
     del ws, grads, dout
     return {"step_ms": t * 1e3, "tops": ops / t / 1e12, "ops": ops,
-            "kernels": ["attn_i8_bwd_dkdv_kernel<128,false,true>", "attn_i8_bwd_dq_kernel<128,false,true>"],
+            "kernels": ["attn_i8_bwd_dv_kernel<128,false>", "attn_i8_bwd_dk_kernel<128,false,true>", "attn_i8_bwd_dq_kernel<128,false,true>"],
             "frac_of_mixed_peak": floor / t,
             "peak_note": "8/10 of the work at the int8 peak (5000 TOPS), 2/10 (dO V^T) at the bf16 peak (2500 TFLOP/s)"}
 
@@ -295,8 +295,9 @@ def main():
     ap.add_argument("--no-bf16", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the attention-kernel timings of the other workloads")
     ap.add_argument("--no-int8", action="store_true", help="skip the 8-bit attention forward")
-    ap.add_argument("--mode", choices=["full", "attn", "attn_int8", "copy", "rates"], default="full",
+    ap.add_argument("--mode", choices=["full", "attn", "attn_int8", "attn_int8_bwd", "copy", "rates"], default="full",
                     help="attn: only the attention kernel (for counter runs); attn_int8: only the 8-bit one; "
+                         "attn_int8_bwd: only the 8-bit backward (after one 8-bit forward for O and L); "
                          "copy: a plain 1 GiB device copy (calibrates FETCH_SIZE / WRITE_SIZE); "
                          "rates: instruction issue-rate microbenchmarks behind the VALU co-bound")
     args = ap.parse_args()
@@ -347,6 +348,20 @@ def main():
             bd.sage_attn_int8_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal)
         torch.cuda.synchronize()
         print(json.dumps({"mode": "attn_int8", "launches": args.warmup + args.steps, "ops_per_launch": ops}))
+        return
+
+    if args.mode == "attn_int8_bwd":
+        o8, L8 = bd.sage_attn_int8_fwd(qd, kd, vd, causal=w.causal, out_f32=True)
+        g = torch.Generator(device=dev).manual_seed(11)
+        dout = torch.randn((B, H, N, D), generator=g, device=dev, dtype=torch.float32).to(dt)
+        flags = bd.SAGE_IN_BF16 if w.in_dtype == wl.IN_BF16 else 0
+        wsb = torch.empty(bd.attn_int8_bwd_workspace_size(B, H, N, D, flags), dtype=torch.uint8, device=dev)
+        grads = [torch.empty((B, H, N, D), dtype=torch.float32, device=dev) for _ in range(3)]
+        for _ in range(args.warmup + args.steps):
+            bd.sage_attn_int8_bwd(qd, kd, vd, o8, L8, dout, causal=w.causal, workspace=wsb, out=grads)
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "attn_int8_bwd", "launches": args.warmup + args.steps,
+                          "ops_per_launch": 10.0 * B * H * N * N * D * (0.5 if w.causal else 1.0)}))
         return
 
     if args.mode == "attn":

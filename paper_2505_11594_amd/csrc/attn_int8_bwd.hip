@@ -9,26 +9,27 @@
 // the smoothing of K.  psi of P and dS is per (128 query x 128 key) block,
 // psi of dO per 128-row block, as the forward's Q^.
 //
-// Two deterministic kernels (no atomics):
-//  - dK/dV: a workgroup owns 128 keys (4 waves x 32) and walks the query
+// Three deterministic kernels (no atomics):
+//  - dV and dK: a workgroup owns 128 keys (4 waves x 32) and walks the query
 //    blocks.  S = Q^ K^T puts a key in each lane's column and 16 queries in its
 //    rows, so P^ and dS^ of a 32-query subtile are, as they stand, the B
 //    operands of dV^T = dO^T P^ and dK^T = Q^T dS^ (A = dO^T / Q^T rows with
 //    each 32-query group permuted as V^T in the forward).  The block scales
-//    of P and dS need the block's maxima before any code is formed: P and dS
-//    of the whole block stay in registers while the maxima are reduced across
-//    the waves through LDS, then all codes are formed and each channel
-//    block's two products run over the block's four subtiles.
+//    of P and dS need the block's maxima before any code is formed: the
+//    block's exp2 arguments (dV) or its dS (dK) stay in registers while the
+//    maximum is reduced across the waves through LDS, then all codes are
+//    formed and each channel block's product runs over the four subtiles.
+//    Apart, the two kernels keep their fp32 state within the 256
+//    architectural registers a wave has (together they would not), and dV
+//    needs neither dP nor the 16-bit operands.
 //  - dQ: a workgroup owns 128 queries (4 waves x 32) and walks the KV blocks.
 //    S^T = K^ Q^T puts a query in each lane's column; dS of the block stays in
 //    registers while its maximum is reduced across the waves, and dS^ is the B
 //    operand of dQ^T = K^T dS^T (A = K^T rows, permuted the same way).
-// Both run one wave per SIMD (the int32 and fp32 accumulators of two
-// products do not fit two waves' register budget).  Each workgroup stages the
-// operands its four waves share -- a query block (Q^, dO, L, D and the
-// transposed Q^, dO^) for dK/dV, a KV block (K^, V, K^T) for dQ -- in LDS in
-// MFMA-operand order with global loads that write LDS, one block ahead of
-// the block being computed.
+// Each workgroup stages the operands its four waves share -- a query block
+// (Q^, dO, L, D and a transposed Q^ or dO^) for dV and dK, a KV block (K^, V,
+// K^T) for dQ -- in LDS in MFMA-operand order with global loads that write
+// LDS, one block ahead of the block being computed.
 #include "sage_common.h"
 
 typedef int v16i __attribute__((ext_vector_type(16)));
@@ -114,48 +115,218 @@ __device__ __forceinline__ void bw_wait_vm() {
   __builtin_amdgcn_s_waitcnt(0x0F70 | N);
 }
 
-// LDS of the dK/dV kernel: per query block, in MFMA-operand order (1 KiB per
-// 64-lane operand read, lane l's 16 bytes at 16 l):
-//   A stage (double-buffered): Q^ operand blocks (u, s) -- rows q0 + 32u + col,
-//   channels [32s + 16hi, +16) --, dO operand blocks (u, s16) -- channels
-//   [16s16 + 8hi, +8) --, and the block's Lb and D (128 floats each);
-//   T (single): Q^T and dO^T operand blocks (db, u) -- channel rows 32db +
-//   col, queries [32u + 16hi, +16) of the block.
+// The dV and dK kernels: a workgroup owns 128 keys (4 waves x 32) of one
+// (b,h) and walks the query blocks; S = Q^ K^T puts a key in each lane's
+// column and 16 queries in its rows.  LDS holds the query block's operands in
+// MFMA-operand order (1 KiB per 64-lane operand read, lane l's 16 bytes at
+// 16 l): Q^ operand blocks (u, s) -- rows q0 + 32u + col, channels
+// [32s + 16hi, +16) --, dO operand blocks (u, s16) -- channels [16s16 + 8hi,
+// +8) --, transposed operand blocks (db, u) -- channel rows 32db + col,
+// queries [32u + 16hi, +16) of the block --, and the block's Lb and D (128
+// floats each).  Query rows >= N read row N - 1 (those entries are masked).
+
+// query-block loads shared by the two kernels (wave w takes operand blocks
+// w, w + 4, ...)
 template <int D>
-struct BwKvLds {
-  static constexpr int NKS = D / 32, NKS16 = D / 16, NDB = D / 32;
-  static constexpr int NQA = 4 * NKS, NGA = 4 * NKS16, NT = NDB * 4;
-  static constexpr int QA_OFF = 0, GA_OFF = NQA * 1024, LD_OFF = GA_OFF + NGA * 1024, A_BYTES = LD_OFF + 1024;
-  static constexpr int QT_OFF = 0, GT_OFF = NT * 1024, T_BYTES = 2 * NT * 1024;
-  static constexpr int AJ = (NQA + NGA) / 4, TJ = 2 * NT / 4;   // loads per wave
-  static_assert((NQA + NGA) % 4 == 0 && (2 * NT) % 4 == 0, "even split over 4 waves");
-};
+__device__ __forceinline__ void bw_load_qa(const int8_t* qc, uint8_t* dst, int b, int bh, int N, int q0, int col,
+                                           int hi) {
+  constexpr int NKS = D / 32;
+  const int u = b / NKS, s = b % NKS;
+  const int q = min(q0 + 32 * u + col, N - 1);
+  bw_lds_load16(qc + ((size_t)bh * N + q) * D + 32 * s + 16 * hi, dst);
+}
+template <int D>
+__device__ __forceinline__ void bw_load_t(const int8_t* xt, uint8_t* dst, int t, int bh, int Np, int q0, int col,
+                                          int hi) {
+  const int db = t / 4, u = t % 4;
+  bw_lds_load16(xt + ((size_t)bh * D + 32 * db + col) * Np + q0 + 32 * u + 16 * hi, dst);
+}
+// Lb and D of the query block (one wave: lanes 0-31 Lb, 32-63 D)
+__device__ __forceinline__ void bw_load_ld(const float* lb, const float* drow, uint8_t* dst, int bh, int Np, int q0,
+                                           int lane) {
+  const float* src = lane < 32 ? lb + (size_t)bh * Np + q0 + 4 * lane : drow + (size_t)bh * Np + q0 + 4 * (lane - 32);
+  bw_lds_load16(src, dst);
+}
+
+// visible iff q < N, key < N and (causal) key <= q: the three sign bits,
+// applied to an exp2 argument as min(arg, bound)
+template <bool CAUSAL>
+__device__ __forceinline__ float bw_mask(float arg, int q, int key, int N) {
+  int m = (q - N) & (key - N);
+  if (CAUSAL) m &= ~(q - key);
+  return __builtin_fminf(arg, __uint_as_float(0xFF800000u ^ ((uint32_t)m & 0x80000000u)));
+}
 
 // ---------------------------------------------------------------------------
-// dK, dV.  qc/kc: Q^, K^ row-major; qt, gt: Q^T, dO^T int8 [BH, D, Np] with
-// each 32-query group permuted; qs, gs: s_Q, s_dO per 128 rows; ks: s_K per
-// 128 keys; v, dout: 16-bit [BH, N, D]; drow, lb: [BH, Np].
+// dV.  dV^T = dO^T P^ per query block: S = Q^ K^T, P = exp2(S c_t - Lb), psi
+// of P per (128 x 128) block.  The block maximum of P is exp2 of the block
+// maximum of its argument (exp2 is monotone), so the arguments of the whole
+// block stay in registers while that maximum is reduced across the waves,
+// and each P is formed once, right before its code.  No 16-bit operand
+// takes part.  gt: dO^T int8 [BH, D, Np] permuted per 32 rows.
 // ---------------------------------------------------------------------------
-template <int D, bool CAUSAL, bool BF16>
-__global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
-    const int8_t* __restrict__ qc, const float* __restrict__ qs, const int8_t* __restrict__ qt,
-    const int8_t* __restrict__ kc, const float* __restrict__ ks, const uint16_t* __restrict__ v,
-    const uint16_t* __restrict__ dout, const int8_t* __restrict__ gt, const float* __restrict__ gs,
-    const float* __restrict__ drow, const float* __restrict__ lb, float* __restrict__ dk, float* __restrict__ dv,
-    int N, int Np, int nqb, float c2, float rsd) {
-  using T = BwKvLds<D>;
-  constexpr int NKS = T::NKS, NKS16 = T::NKS16, NDB = T::NDB;
-  __shared__ __attribute__((aligned(16))) uint8_t ldsA[2][T::A_BYTES];
-  __shared__ __attribute__((aligned(16))) uint8_t ldsT[T::T_BYTES];
-  __shared__ float red[2][2][4];                   // [block parity][P, dS][wave]
+template <int D>
+struct BwDvLds {
+  static constexpr int NKS = D / 32, NDB = D / 32;
+  static constexpr int NQA = 4 * NKS, NT = NDB * 4;
+  static constexpr int QA_OFF = 0, GT_OFF = NQA * 1024, LD_OFF = GT_OFF + NT * 1024, BYTES = LD_OFF + 1024;
+  static constexpr int J = (NQA + NT) / 4;
+  static_assert((NQA + NT) % 4 == 0, "even split over 4 waves");
+};
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(256, 2) void attn_i8_bwd_dv_kernel(
+    const int8_t* __restrict__ qc, const float* __restrict__ qs, const int8_t* __restrict__ kc,
+    const float* __restrict__ ks, const int8_t* __restrict__ gt, const float* __restrict__ gs,
+    const float* __restrict__ drow, const float* __restrict__ lb, float* __restrict__ dv, int N, int Np, int nqb,
+    float c2) {
+  using T = BwDvLds<D>;
+  constexpr int NKS = T::NKS, NDB = T::NDB, NU = BW_Q / 32;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2][T::BYTES];
+  __shared__ float red[2][4];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31, hi = lane >> 5;
   const int kblk = blockIdx.x, bh = blockIdx.y;
-  const int kb = kblk * BW_K, kw = kb + 32 * wave, key = kw + col;
+  const int kb = kblk * BW_K, key = kb + 32 * wave + col;
   const float sK = ks[(size_t)bh * (Np / BW_K) + kblk];
 
-  // B operands of this wave's 32 keys: K^ (channels [32s + 16hi, +16)) and V
+  v4i kreg[NKS];   // B operand of S: this lane's key, channels [32s + 16hi, +16)
+  {
+    const int8_t* kr = kc + ((size_t)bh * Np + key) * D;
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) kreg[s] = *reinterpret_cast<const v4i*>(kr + 32 * s + 16 * hi);
+  }
+  v16f dva[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) dva[db] = v16f{};
+
+  auto issue = [&](int i, int buf) {
+    const int q0 = i * BW_Q;
+    uint8_t* L = lds[buf];
+#pragma unroll
+    for (int k = 0; k < T::J; ++k) {
+      const int b = wave + 4 * k;
+      if (b < T::NQA) bw_load_qa<D>(qc, L + T::QA_OFF + b * 1024, b, bh, N, q0, col, hi);
+      else bw_load_t<D>(gt, L + T::GT_OFF + (b - T::NQA) * 1024, b - T::NQA, bh, Np, q0, col, hi);
+    }
+    if (wave == 0) bw_load_ld(lb, drow, L + T::LD_OFF, bh, Np, q0, lane);
+  };
+
+  const int i0 = CAUSAL ? kb / BW_Q : 0;
+  issue(i0, i0 & 1);
+  for (int i = i0; i < nqb; ++i) {
+    const int q0 = i * BW_Q, a = i & 1;
+    bw_wait_all();                                 // this wave's loads of block i have landed
+    __syncthreads();                               // everyone's; every wave is done with block i - 1
+    if (i + 1 < nqb) issue(i + 1, a ^ 1);
+    const uint8_t* L = lds[a];
+    const float sQ = qs[(size_t)bh * nqb + i];
+    const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);   // see the forward kernel
+    const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && q0 < kb + BW_K - 1);
+
+    // exp2 arguments of the block: element v of subtile u is query q0 + 32u + 8(v>>2) + 4hi + (v&3)
+    float arg[NU][16];
+    float am = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      v16i sacc = v16i{};
+#pragma unroll
+      for (int s = 0; s < NKS; ++s)
+        sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+            *reinterpret_cast<const v4i*>(L + T::QA_OFF + (u * NKS + s) * 1024 + lane * 16), kreg[s], sacc, 0, 0, 0);
+      const float* lbr = reinterpret_cast<const float*>(L + T::LD_OFF) + 32 * u + 4 * hi;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const v4f l4 = *reinterpret_cast<const v4f*>(lbr + 8 * g);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int e = 4 * g + r;
+          float x = __builtin_fmaf((float)sacc[e], ct, -l4[r]);
+          if (need_mask) x = bw_mask<CAUSAL>(x, q0 + 32 * u + 4 * hi + 8 * g + r, key, N);
+          arg[u][e] = x;
+          am = __builtin_fmaxf(am, x);
+        }
+      }
+    }
+    am = wave_max(am);
+    if (lane == 0) red[a][wave] = am;
+    __syncthreads();
+    am = __builtin_fmaxf(__builtin_fmaxf(red[a][0], red[a][1]), __builtin_fmaxf(red[a][2], red[a][3]));
+    const float pm = __builtin_amdgcn_exp2f(am);   // max P of the block (0 when it is fully masked)
+    const float sP = pm / 127.0f, rP = pm > 0.0f ? 1.0f / sP : 0.0f;
+
+    v4i pc[NU];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      float P[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) P[e] = __builtin_amdgcn_exp2f(arg[u][e]);
+      pc[u] = bw_codes(P, rP);
+    }
+    const float fv = sP * gs[(size_t)bh * nqb + i];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      v16i dvi = v16i{};
+#pragma unroll
+      for (int u = 0; u < NU; ++u)
+        dvi = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+            *reinterpret_cast<const v4i*>(L + T::GT_OFF + (db * 4 + u) * 1024 + lane * 16), pc[u], dvi, 0, 0, 0);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) dva[db][e] = __builtin_fmaf((float)dvi[e], fv, dva[db][e]);
+    }
+  }
+
+  // dV^T: lane holds key kb + 32 wave + col and channels 32db + 8g + 4hi + r
+  if (key < N) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const size_t idx = ((size_t)bh * N + key) * D + 32 * db + 8 * g + 4 * hi;
+        *reinterpret_cast<float4*>(dv + idx) = make_float4(dva[db][4 * g], dva[db][4 * g + 1], dva[db][4 * g + 2], dva[db][4 * g + 3]);
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dK.  dK^T = Q^T dS^ per query block: S = Q^ K^T and dP = dO V^T of each
+// 32-query subtile, P = exp2(S c_t - Lb), dS = P (dP - D); dS of the whole
+// block stays in registers while its maximum is reduced across the waves,
+// then psi of dS and the product.  The query block's Q^ and dO (double-
+// buffered) and Q^T (single: loaded after the block's first barrier, waited
+// for before its second) are staged in LDS.  qt: Q^T int8 [BH, D, Np]
+// permuted per 32 rows.
+// ---------------------------------------------------------------------------
+template <int D>
+struct BwDkLds {
+  static constexpr int NKS = D / 32, NKS16 = D / 16, NDB = D / 32;
+  static constexpr int NQA = 4 * NKS, NGA = 4 * NKS16, NT = NDB * 4;
+  static constexpr int QA_OFF = 0, GA_OFF = NQA * 1024, LD_OFF = GA_OFF + NGA * 1024, A_BYTES = LD_OFF + 1024;
+  static constexpr int T_BYTES = NT * 1024;
+  static constexpr int AJ = (NQA + NGA) / 4, TJ = NT / 4;   // loads per wave
+  static_assert((NQA + NGA) % 4 == 0 && NT % 4 == 0, "even split over 4 waves");
+};
+
+template <int D, bool CAUSAL, bool BF16>
+__global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
+    const int8_t* __restrict__ qc, const float* __restrict__ qs, const int8_t* __restrict__ qt,
+    const int8_t* __restrict__ kc, const float* __restrict__ ks, const uint16_t* __restrict__ v,
+    const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lb,
+    float* __restrict__ dk, int N, int Np, int nqb, float c2, float rsd) {
+  using T = BwDkLds<D>;
+  constexpr int NKS = T::NKS, NKS16 = T::NKS16, NDB = T::NDB, NU = BW_Q / 32;
+  __shared__ __attribute__((aligned(16))) uint8_t ldsA[2][T::A_BYTES];
+  __shared__ __attribute__((aligned(16))) uint8_t ldsT[T::T_BYTES];
+  __shared__ float red[2][4];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, hi = lane >> 5;
+  const int kblk = blockIdx.x, bh = blockIdx.y;
+  const int kb = kblk * BW_K, key = kb + 32 * wave + col;
+  const float sK = ks[(size_t)bh * (Np / BW_K) + kblk];
+
+  // B operands of this lane's key: K^ (channels [32s + 16hi, +16)) and V
   // (16-bit, channels [16s + 8hi, +8))
   v4i kreg[NKS], vreg[NKS16];
   {
@@ -167,12 +338,10 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
     for (int s = 0; s < NKS16; ++s)
       vreg[s] = key < N ? *reinterpret_cast<const v4i*>(vr + 16 * s + 8 * hi) : v4i{0, 0, 0, 0};
   }
-  v16f dva[NDB], dka[NDB];
+  v16f dka[NDB];
 #pragma unroll
-  for (int db = 0; db < NDB; ++db) { dva[db] = v16f{}; dka[db] = v16f{}; }
+  for (int db = 0; db < NDB; ++db) dka[db] = v16f{};
 
-  // loads of query block i: wave w takes operand blocks w, w + 4, ...; rows
-  // >= N read row N - 1 (those entries are masked)
   auto issue_A = [&](int i, int buf) {
     const int q0 = i * BW_Q;
     uint8_t* L = ldsA[buf];
@@ -180,9 +349,7 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
     for (int k = 0; k < T::AJ; ++k) {
       const int b = wave + 4 * k;
       if (b < T::NQA) {
-        const int u = b / NKS, s = b % NKS;
-        const int q = min(q0 + 32 * u + col, N - 1);
-        bw_lds_load16(qc + ((size_t)bh * N + q) * D + 32 * s + 16 * hi, L + T::QA_OFF + b * 1024);
+        bw_load_qa<D>(qc, L + T::QA_OFF + b * 1024, b, bh, N, q0, col, hi);
       } else {
         const int g = b - T::NQA, u = g / NKS16, s = g % NKS16;
         const int q = min(q0 + 32 * u + col, N - 1);
@@ -190,29 +357,22 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
       }
     }
   };
-  auto issue_LD = [&](int i, int buf) {          // Lb and D of block i (wave 0)
-    const int q0 = i * BW_Q;
-    const float* src = (lane < 32 ? lb + (size_t)bh * Np + q0 + 4 * lane : drow + (size_t)bh * Np + q0 + 4 * (lane - 32));
-    bw_lds_load16(src, ldsA[buf] + T::LD_OFF);
-  };
   auto issue_T = [&](int i) {
-    const int q0 = i * BW_Q;
 #pragma unroll
     for (int k = 0; k < T::TJ; ++k) {
-      const int b = wave + 4 * k, which = b / T::NT, t = b % T::NT, db = t / 4, u = t % 4;
-      const size_t off = ((size_t)bh * D + 32 * db + col) * Np + q0 + 32 * u + 16 * hi;
-      bw_lds_load16((which ? gt : qt) + off, ldsT + (which ? T::GT_OFF : T::QT_OFF) + t * 1024);
+      const int t = wave + 4 * k;
+      bw_load_t<D>(qt, ldsT + t * 1024, t, bh, Np, i * BW_Q, col, hi);
     }
   };
 
   const int i0 = CAUSAL ? kb / BW_Q : 0;
-  if (wave == 0) issue_LD(i0, i0 & 1);
+  if (wave == 0) bw_load_ld(lb, drow, ldsA[i0 & 1] + T::LD_OFF, bh, Np, i0 * BW_Q, lane);
   issue_A(i0, i0 & 1);
   for (int i = i0; i < nqb; ++i) {
     const int q0 = i * BW_Q, a = i & 1;
     bw_wait_all();                                 // this wave's loads of block i have landed
     __syncthreads();                               // everyone's; every wave is done with block i - 1
-    if (i + 1 < nqb && wave == 0) issue_LD(i + 1, a ^ 1);
+    if (i + 1 < nqb && wave == 0) bw_load_ld(lb, drow, ldsA[a ^ 1] + T::LD_OFF, bh, Np, q0 + BW_Q, lane);
     issue_T(i);
     if (i + 1 < nqb) issue_A(i + 1, a ^ 1);
     const uint8_t* L = ldsA[a];
@@ -220,21 +380,20 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
     const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);   // see the forward kernel
     const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && q0 < kb + BW_K - 1);
 
-    // S (exact int32) and dP (fp32) of one 32-query subtile
-    auto products = [&](int u, v16i& sacc, v16f& dp) {
-      sacc = v16i{};
+    // dS of the block: element v of subtile u is query q0 + 32u + 8(v>>2) + 4hi + (v&3)
+    float dS[NU][16];
+    float dm = 0.0f;
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      v16i sacc = v16i{};
 #pragma unroll
       for (int s = 0; s < NKS; ++s)
         sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(
             *reinterpret_cast<const v4i*>(L + T::QA_OFF + (u * NKS + s) * 1024 + lane * 16), kreg[s], sacc, 0, 0, 0);
-      dp = v16f{};
+      v16f dp = v16f{};
 #pragma unroll
       for (int s = 0; s < NKS16; ++s)
         dp = mfma16<BF16>(*reinterpret_cast<const v4i*>(L + T::GA_OFF + (u * NKS16 + s) * 1024 + lane * 16), vreg[s], dp);
-    };
-    // P and dS of the subtile: element v is query q0 + 32u + 8(v>>2) + 4hi + (v&3)
-    auto softmax_grad = [&](int u, const v16i& sacc, const v16f& dp, float (&P)[16], float (&dS)[16]) {
-      const int qb4 = q0 + 32 * u + 4 * hi;
       const float* lbr = reinterpret_cast<const float*>(L + T::LD_OFF) + 32 * u + 4 * hi;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
@@ -243,83 +402,47 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dkdv_kernel(
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int e = 4 * g + r;
-          float arg = __builtin_fmaf((float)sacc[e], ct, -l4[r]);
-          if (need_mask) {
-            // visible iff q < N, key < N and (causal) key <= q: the three sign bits
-            const int q = qb4 + 8 * g + r;
-            int m = (q - N) & (key - N);
-            if (CAUSAL) m &= ~(q - key);
-            arg = __builtin_fminf(arg, __uint_as_float(0xFF800000u ^ ((uint32_t)m & 0x80000000u)));
-          }
-          const float p = __builtin_amdgcn_exp2f(arg);
-          const float d = dp[e] - d4[r];
-          P[e] = p;
-          dS[e] = p * d;
+          float x = __builtin_fmaf((float)sacc[e], ct, -l4[r]);
+          if (need_mask) x = bw_mask<CAUSAL>(x, q0 + 32 * u + 4 * hi + 8 * g + r, key, N);
+          const float p = __builtin_amdgcn_exp2f(x);
+          const float y = p * (dp[e] - d4[r]);
+          dS[u][e] = y;
+          dm = __builtin_fmaxf(dm, __builtin_fabsf(y));
         }
       }
-    };
-
-    // P and dS of the whole block stay in registers (4 subtiles x 16 values)
-    // while the block maxima of P and |dS| are reduced across the waves; the
-    // products of subtile u + 1 are issued before the softmax work of subtile u
-    float P[BW_Q / 32][16], dS[BW_Q / 32][16];
-    float pm = 0.0f, dm = 0.0f;
-    v16i sacc[2];
-    v16f dp[2];
-    products(0, sacc[0], dp[0]);
-#pragma unroll
-    for (int u = 0; u < BW_Q / 32; ++u) {
-      if (u + 1 < BW_Q / 32) products(u + 1, sacc[(u + 1) & 1], dp[(u + 1) & 1]);
-      softmax_grad(u, sacc[u & 1], dp[u & 1], P[u], dS[u]);
-#pragma unroll
-      for (int e = 0; e < 16; ++e) { pm = __builtin_fmaxf(pm, P[u][e]); dm = __builtin_fmaxf(dm, __builtin_fabsf(dS[u][e])); }
-      __builtin_amdgcn_sched_barrier(0);
     }
-    pm = wave_max(pm);
     dm = wave_max(dm);
-    if (lane == 0) { red[a][0][wave] = pm; red[a][1][wave] = dm; }
+    if (lane == 0) red[a][wave] = dm;
     // the T loads of this block were issued before the next block's A loads
     if (i + 1 < nqb) bw_wait_vm<T::AJ>();
     else bw_wait_all();
     __syncthreads();
-    pm = __builtin_fmaxf(__builtin_fmaxf(red[a][0][0], red[a][0][1]), __builtin_fmaxf(red[a][0][2], red[a][0][3]));
-    dm = __builtin_fmaxf(__builtin_fmaxf(red[a][1][0], red[a][1][1]), __builtin_fmaxf(red[a][1][2], red[a][1][3]));
-    const float sP = pm / 127.0f, rP = pm > 0.0f ? 1.0f / sP : 0.0f;
+    dm = __builtin_fmaxf(__builtin_fmaxf(red[a][0], red[a][1]), __builtin_fmaxf(red[a][2], red[a][3]));
     const float sdS = dm / 127.0f, rdS = dm > 0.0f ? 1.0f / sdS : 0.0f;
 
-    // codes of the block, then per channel block the two int8 products over
-    // its four subtiles (exact int32), folded into fp32 once per block
-    v4i pc[BW_Q / 32], sc[BW_Q / 32];
+    v4i sc[NU];
 #pragma unroll
-    for (int u = 0; u < BW_Q / 32; ++u) { pc[u] = bw_codes(P[u], rP); sc[u] = bw_codes(dS[u], rdS); }
-    const float fv = sP * gs[(size_t)bh * nqb + i];
+    for (int u = 0; u < NU; ++u) sc[u] = bw_codes(dS[u], rdS);
     const float fk = (sdS * sQ) * rsd;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
-      v16i dvi = v16i{}, dki = v16i{};
+      v16i dki = v16i{};
 #pragma unroll
-      for (int u = 0; u < BW_Q / 32; ++u) {
-        const v4i ga = *reinterpret_cast<const v4i*>(ldsT + T::GT_OFF + (db * 4 + u) * 1024 + lane * 16);
-        const v4i qa = *reinterpret_cast<const v4i*>(ldsT + T::QT_OFF + (db * 4 + u) * 1024 + lane * 16);
-        dvi = __builtin_amdgcn_mfma_i32_32x32x32_i8(ga, pc[u], dvi, 0, 0, 0);
-        dki = __builtin_amdgcn_mfma_i32_32x32x32_i8(qa, sc[u], dki, 0, 0, 0);
-      }
+      for (int u = 0; u < NU; ++u)
+        dki = __builtin_amdgcn_mfma_i32_32x32x32_i8(*reinterpret_cast<const v4i*>(ldsT + (db * 4 + u) * 1024 + lane * 16),
+                                                    sc[u], dki, 0, 0, 0);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        dva[db][e] = __builtin_fmaf((float)dvi[e], fv, dva[db][e]);
-        dka[db][e] = __builtin_fmaf((float)dki[e], fk, dka[db][e]);
-      }
+      for (int e = 0; e < 16; ++e) dka[db][e] = __builtin_fmaf((float)dki[e], fk, dka[db][e]);
     }
   }
 
-  // dV^T, dK^T: lane holds key kw + col and channels 32db + 8g + 4hi + r
+  // dK^T: lane holds key kb + 32 wave + col and channels 32db + 8g + 4hi + r
   if (key < N) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const size_t idx = ((size_t)bh * N + key) * D + 32 * db + 8 * g + 4 * hi;
-        *reinterpret_cast<float4*>(dv + idx) = make_float4(dva[db][4 * g], dva[db][4 * g + 1], dva[db][4 * g + 2], dva[db][4 * g + 3]);
         *reinterpret_cast<float4*>(dk + idx) = make_float4(dka[db][4 * g], dka[db][4 * g + 1], dka[db][4 * g + 2], dka[db][4 * g + 3]);
       }
   }
@@ -409,22 +532,37 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
     const float sK = ks[(size_t)bh * (Np / BW_K) + j];
     const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);
     const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && kb + BW_K - 1 > q0);
+    // S^T (exact int32) and dP^T (fp32) of one 32-key subtile: the subtile's
+    // twelve A-operand reads are issued together, ahead of its MFMAs
+    auto products = [&](int t, v16i& sacc, v16f& dp) {
+      v4i ka[NKS], va[NKS16];
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) ka[s] = *reinterpret_cast<const v4i*>(L + T::KA_OFF + (t * NKS + s) * 1024 + lane * 16);
+#pragma unroll
+      for (int s = 0; s < NKS16; ++s) va[s] = *reinterpret_cast<const v4i*>(L + T::VA_OFF + (t * NKS16 + s) * 1024 + lane * 16);
+      sacc = v16i{};
+#pragma unroll
+      for (int s = 0; s < NKS; ++s) sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(ka[s], qreg[s], sacc, 0, 0, 0);
+      dp = v16f{};
+#pragma unroll
+      for (int s = 0; s < NKS16; ++s) dp = mfma16<BF16>(va[s], greg[s], dp);
+      __builtin_amdgcn_sched_group_barrier(0x100, NKS + NKS16, 0);   // the LDS reads
+      __builtin_amdgcn_sched_group_barrier(0x008, NKS + NKS16, 0);   // then the MFMAs
+    };
+    // dS of the block stays in registers while its maximum is reduced across
+    // the waves; the products of subtile t + 1 are issued before the softmax
+    // work of subtile t
     float dS[NT][16];
     float dm = 0.0f, rs = 0.0f;
+    v16i sacc[2];
+    v16f dp[2];
+    products(0, sacc[0], dp[0]);
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      v16i sacc = v16i{};
-#pragma unroll
-      for (int s = 0; s < NKS; ++s)
-        sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(
-            *reinterpret_cast<const v4i*>(L + T::KA_OFF + (t * NKS + s) * 1024 + lane * 16), qreg[s], sacc, 0, 0, 0);
-      v16f dp = v16f{};
-#pragma unroll
-      for (int s = 0; s < NKS16; ++s)
-        dp = mfma16<BF16>(*reinterpret_cast<const v4i*>(L + T::VA_OFF + (t * NKS16 + s) * 1024 + lane * 16), greg[s], dp);
+      if (t + 1 < NT) products(t + 1, sacc[(t + 1) & 1], dp[(t + 1) & 1]);
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        float arg = __builtin_fmaf((float)sacc[e], ct, -lbq);
+        float arg = __builtin_fmaf((float)sacc[t & 1][e], ct, -lbq);
         if (need_mask) {
           const int k = kb + 32 * t + 8 * (e >> 2) + 4 * hi + (e & 3);
           int m = (qi - N) & (k - N);
@@ -432,44 +570,45 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
           arg = __builtin_fminf(arg, __uint_as_float(0xFF800000u ^ ((uint32_t)m & 0x80000000u)));
         }
         const float p = __builtin_amdgcn_exp2f(arg);
-        const float d = dp[e] - dq_row;
+        const float d = dp[t & 1][e] - dq_row;
         const float x = p * d;
         dS[t][e] = x;
         rs += x;
         dm = __builtin_fmaxf(dm, __builtin_fabsf(x));
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
     dm = wave_max(dm);
     if (lane == 0) red[buf][wave] = dm;
     __syncthreads();
     dm = __builtin_fmaxf(__builtin_fmaxf(red[buf][0], red[buf][1]), __builtin_fmaxf(red[buf][2], red[buf][3]));
     const float sdS = dm / 127.0f, rdS = dm > 0.0f ? 1.0f / sdS : 0.0f;
-    v16i dqi[NDB];
+    // codes of the block, then per channel block the product over its four
+    // subtiles (exact int32), folded into fp32 once per block
+    v4i sc[NT];
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) dqi[db] = v16i{};
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const v4i sc = bw_codes(dS[t], rdS);
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-        dqi[db] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
-            *reinterpret_cast<const v4i*>(L + T::KT_OFF + (db * NT + t) * 1024 + lane * 16), sc, dqi[db], 0, 0, 0);
-    }
+    for (int t = 0; t < NT; ++t) sc[t] = bw_codes(dS[t], rdS);
     const float fq = (sdS * sK) * rsd;
     const float rr = (rs + __shfl_xor(rs, 32, 64)) * rsd;   // rowsum(dS) of this lane's query, / sqrt(D)
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+    for (int db = 0; db < NDB; ++db) {
+      v16i dqi = v16i{};
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        dqi = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+            *reinterpret_cast<const v4i*>(L + T::KT_OFF + (db * NT + t) * 1024 + lane * 16), sc[t], dqi, 0, 0, 0);
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const v4f km = *reinterpret_cast<const v4f*>(kms + 32 * db + 8 * g + 4 * hi);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int e = 4 * g + r;
-          float x = __builtin_fmaf((float)dqi[db][e], fq, dqa[db][e]);
+          float x = __builtin_fmaf((float)dqi[e], fq, dqa[db][e]);
           if (kmean != nullptr) x = __builtin_fmaf(rr, km[r], x);
           dqa[db][e] = x;
         }
       }
+    }
   }
   if (qi < N) {
 #pragma unroll
@@ -505,9 +644,14 @@ static hipError_t launch_bwd_t(const int8_t* qc, const float* qs, const int8_t* 
                                const float* gs, const float* drow, const float* lb, const float* kmean, float* dq,
                                float* dk, float* dv, int BH, int N, int Np, float c2, float rsd, hipStream_t st) {
   const int nqb = (N + BW_Q - 1) / BW_Q;
-  hipLaunchKernelGGL((attn_i8_bwd_dkdv_kernel<D, CAUSAL, BF16>), dim3((unsigned)(Np / BW_K), (unsigned)BH), dim3(256), 0,
-                     st, qc, qs, qt, kc, ks, v, dout, gt, gs, drow, lb, dk, dv, N, Np, nqb, c2, rsd);
+  const dim3 kgrid((unsigned)(Np / BW_K), (unsigned)BH);
+  hipLaunchKernelGGL((attn_i8_bwd_dv_kernel<D, CAUSAL>), kgrid, dim3(256), 0, st, qc, qs, kc, ks, gt, gs, drow, lb, dv, N,
+                     Np, nqb, c2);
   hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attn_i8_bwd_dk_kernel<D, CAUSAL, BF16>), kgrid, dim3(256), 0, st, qc, qs, qt, kc, ks, v, dout,
+                     drow, lb, dk, N, Np, nqb, c2, rsd);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_i8_bwd_dq_kernel<D, CAUSAL, BF16>), dim3((unsigned)nqb, (unsigned)BH), dim3(256), 0, st, qc,
                      qs, kc, ks, kt, v, dout, drow, lb, kmean, dq, N, Np, nqb, c2, rsd);

@@ -6,7 +6,8 @@ checked against independent CPU definitions.
   (-16, 16), ties included, and with power-of-two scales;
 - v_exp_f32 against the correctly rounded exp2 over the arguments the kernels
   use: its error must stay within the 8-ulp window inside which the oracle
-  treats an FP4 or INT8 code of P as tie-ambiguous;
+  treats an FP4 or INT8 code of P as tie-ambiguous; and it must never decrease
+  its output as its argument grows, on every fp32 in [-130, 0];
 - the register layouts of the FP4 block-scaled, int8 and bf16 32x32 MFMAs
   against numpy products (and, for FP4, the oracle's exact FP4MM).
 """
@@ -79,6 +80,27 @@ def test_exp2_error_within_the_tie_window(P):
     ulp = np.spacing(ref[normal].astype(np.float32)).astype(np.float64)
     err = np.abs(y[normal] - ref[normal]) / ulp
     assert err.max() <= 2.0, err.max()          # the oracle's tie window is 8 ulp
+
+
+def test_exp2_is_monotone_on_every_fp32_in_minus130_0(P):
+    # the 8-bit backward's dV kernel takes the block maximum of P = exp2(arg) as
+    # exp2 of the block maximum of arg: exact when v_exp_f32 never decreases
+    torch = torch_dev()
+    top = int(np.float32(130.0).view(np.int32))            # bit patterns 0 .. |-130| of the magnitude
+    chunk = 1 << 27
+    prev = None
+    for start in range(0, top + 1, chunk):
+        n = min(chunk, top + 1 - start)
+        mag = torch.arange(start, start + n, dtype=torch.int32, device="cuda").view(torch.float32)
+        xd = (-mag).contiguous()                            # -0, then decreasing to -130
+        yd = torch.empty_like(xd)
+        run(P.sage_probe_exp2, dptr(xd), dptr(yd), n)
+        assert bool((yd[1:] <= yd[:-1]).all()), "exp2 increases somewhere in chunk %d" % (start // chunk)
+        if prev is not None:
+            assert float(yd[0]) <= prev
+        prev = float(yd[-1])
+        del mag, xd, yd
+    assert prev == 0.0 or prev < 2.0 ** -126
 
 
 def fp4_case(seed, lo, hi):
