@@ -380,37 +380,59 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
     const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);   // see the forward kernel
     const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && q0 < kb + BW_K - 1);
 
-    // dS of the block: element v of subtile u is query q0 + 32u + 8(v>>2) + 4hi + (v&3)
+    // dS of the block: element v of subtile u is query q0 + 32u + 8(v>>2) + 4hi + (v&3).
+    // The products of subtile u + 1 are interleaved with the softmax work of
+    // subtile u (one MFMA, then eight VALU instructions), so that MFMAs run
+    // under VALU work of the same wave; the masking choice is made per block.
     float dS[NU][16];
     float dm = 0.0f;
-#pragma unroll
-    for (int u = 0; u < NU; ++u) {
-      v16i sacc = v16i{};
+    auto products = [&](int u, v16i& sacc, v16f& dp) {
+      sacc = v16i{};
 #pragma unroll
       for (int s = 0; s < NKS; ++s)
         sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(
             *reinterpret_cast<const v4i*>(L + T::QA_OFF + (u * NKS + s) * 1024 + lane * 16), kreg[s], sacc, 0, 0, 0);
-      v16f dp = v16f{};
+      dp = v16f{};
 #pragma unroll
       for (int s = 0; s < NKS16; ++s)
         dp = mfma16<BF16>(*reinterpret_cast<const v4i*>(L + T::GA_OFF + (u * NKS16 + s) * 1024 + lane * 16), vreg[s], dp);
-      const float* lbr = reinterpret_cast<const float*>(L + T::LD_OFF) + 32 * u + 4 * hi;
+    };
+    auto phase1 = [&](auto MASK_) {
+      constexpr bool MASK = decltype(MASK_)::value != 0;
+      v16i sacc[2];
+      v16f dp[2];
+      products(0, sacc[0], dp[0]);
+      static_for<NU>([&](auto U_) {
+        constexpr int u = decltype(U_)::value;
+        if constexpr (u + 1 < NU) products(u + 1, sacc[(u + 1) & 1], dp[(u + 1) & 1]);
+        const float* lbr = reinterpret_cast<const float*>(L + T::LD_OFF) + 32 * u + 4 * hi;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const v4f l4 = *reinterpret_cast<const v4f*>(lbr + 8 * g);
-        const v4f d4 = *reinterpret_cast<const v4f*>(lbr + 128 + 8 * g);
+        for (int g = 0; g < 4; ++g) {
+          const v4f l4 = *reinterpret_cast<const v4f*>(lbr + 8 * g);
+          const v4f d4 = *reinterpret_cast<const v4f*>(lbr + 128 + 8 * g);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int e = 4 * g + r;
-          float x = __builtin_fmaf((float)sacc[e], ct, -l4[r]);
-          if (need_mask) x = bw_mask<CAUSAL>(x, q0 + 32 * u + 4 * hi + 8 * g + r, key, N);
-          const float p = __builtin_amdgcn_exp2f(x);
-          const float y = p * (dp[e] - d4[r]);
-          dS[u][e] = y;
-          dm = __builtin_fmaxf(dm, __builtin_fabsf(y));
+          for (int r = 0; r < 4; ++r) {
+            const int e = 4 * g + r;
+            float x = __builtin_fmaf((float)sacc[u & 1][e], ct, -l4[r]);
+            if constexpr (MASK) x = bw_mask<CAUSAL>(x, q0 + 32 * u + 4 * hi + 8 * g + r, key, N);
+            const float p = __builtin_amdgcn_exp2f(x);
+            const float y = p * (dp[u & 1][e] - d4[r]);
+            dS[u][e] = y;
+            dm = __builtin_fmaxf(dm, __builtin_fabsf(y));
+          }
         }
-      }
-    }
+        if constexpr (u + 1 < NU) {
+#pragma unroll
+          for (int m = 0; m < NKS + NKS16; ++m) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    };
+    if (need_mask) phase1(ic<1>{});
+    else phase1(ic<0>{});
     dm = wave_max(dm);
     if (lane == 0) red[a][wave] = dm;
     // the T loads of this block were issued before the next block's A loads
@@ -532,52 +554,54 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
     const float sK = ks[(size_t)bh * (Np / BW_K) + j];
     const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);
     const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && kb + BW_K - 1 > q0);
-    // S^T (exact int32) and dP^T (fp32) of one 32-key subtile: the subtile's
-    // twelve A-operand reads are issued together, ahead of its MFMAs
+    // S^T (exact int32) and dP^T (fp32) of one 32-key subtile
     auto products = [&](int t, v16i& sacc, v16f& dp) {
-      v4i ka[NKS], va[NKS16];
-#pragma unroll
-      for (int s = 0; s < NKS; ++s) ka[s] = *reinterpret_cast<const v4i*>(L + T::KA_OFF + (t * NKS + s) * 1024 + lane * 16);
-#pragma unroll
-      for (int s = 0; s < NKS16; ++s) va[s] = *reinterpret_cast<const v4i*>(L + T::VA_OFF + (t * NKS16 + s) * 1024 + lane * 16);
       sacc = v16i{};
 #pragma unroll
-      for (int s = 0; s < NKS; ++s) sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(ka[s], qreg[s], sacc, 0, 0, 0);
+      for (int s = 0; s < NKS; ++s)
+        sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+            *reinterpret_cast<const v4i*>(L + T::KA_OFF + (t * NKS + s) * 1024 + lane * 16), qreg[s], sacc, 0, 0, 0);
       dp = v16f{};
 #pragma unroll
-      for (int s = 0; s < NKS16; ++s) dp = mfma16<BF16>(va[s], greg[s], dp);
-      __builtin_amdgcn_sched_group_barrier(0x100, NKS + NKS16, 0);   // the LDS reads
-      __builtin_amdgcn_sched_group_barrier(0x008, NKS + NKS16, 0);   // then the MFMAs
+      for (int s = 0; s < NKS16; ++s)
+        dp = mfma16<BF16>(*reinterpret_cast<const v4i*>(L + T::VA_OFF + (t * NKS16 + s) * 1024 + lane * 16), greg[s], dp);
     };
     // dS of the block stays in registers while its maximum is reduced across
-    // the waves; the products of subtile t + 1 are issued before the softmax
-    // work of subtile t
+    // the waves.  The products of subtile t + 1 are interleaved with the
+    // softmax work of subtile t (one MFMA, then eight VALU instructions); the
+    // masking choice is made per block.
     float dS[NT][16];
     float dm = 0.0f, rs = 0.0f;
-    v16i sacc[2];
-    v16f dp[2];
-    products(0, sacc[0], dp[0]);
+    auto phase1 = [&](auto MASK_) {
+      constexpr bool MASK = decltype(MASK_)::value != 0;
+      v16i sacc[2];
+      v16f dp[2];
+      products(0, sacc[0], dp[0]);
+      static_for<NT>([&](auto T_) {
+        constexpr int t = decltype(T_)::value;
+        if constexpr (t + 1 < NT) products(t + 1, sacc[(t + 1) & 1], dp[(t + 1) & 1]);
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      if (t + 1 < NT) products(t + 1, sacc[(t + 1) & 1], dp[(t + 1) & 1]);
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float arg = __builtin_fmaf((float)sacc[t & 1][e], ct, -lbq);
-        if (need_mask) {
-          const int k = kb + 32 * t + 8 * (e >> 2) + 4 * hi + (e & 3);
-          int m = (qi - N) & (k - N);
-          if (CAUSAL) m &= ~(qi - k);
-          arg = __builtin_fminf(arg, __uint_as_float(0xFF800000u ^ ((uint32_t)m & 0x80000000u)));
+        for (int e = 0; e < 16; ++e) {
+          float arg = __builtin_fmaf((float)sacc[t & 1][e], ct, -lbq);
+          if constexpr (MASK) arg = bw_mask<CAUSAL>(arg, qi, kb + 32 * t + 8 * (e >> 2) + 4 * hi + (e & 3), N);
+          const float p = __builtin_amdgcn_exp2f(arg);
+          const float x = p * (dp[t & 1][e] - dq_row);
+          dS[t][e] = x;
+          rs += x;
+          dm = __builtin_fmaxf(dm, __builtin_fabsf(x));
         }
-        const float p = __builtin_amdgcn_exp2f(arg);
-        const float d = dp[t & 1][e] - dq_row;
-        const float x = p * d;
-        dS[t][e] = x;
-        rs += x;
-        dm = __builtin_fmaxf(dm, __builtin_fabsf(x));
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
+        if constexpr (t + 1 < NT) {
+#pragma unroll
+          for (int m = 0; m < NKS + NKS16; ++m) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    };
+    if (need_mask) phase1(ic<1>{});
+    else phase1(ic<0>{});
     dm = wave_max(dm);
     if (lane == 0) red[buf][wave] = dm;
     __syncthreads();
