@@ -263,18 +263,31 @@ int sage_attn_int8_fwd_prequant(const void* q_codes, const float* q_scales,
  * flags: SAGE_IN_BF16, SAGE_NO_SMOOTH_K (as given to the forward); SAGE_OUT_F32
  * is accepted and changes nothing (gradients are fp32); SAGE_BKV64 returns
  * SAGE_ERR_UNSUPPORTED (the backward's KV blocks are 128 keys).  The
- * internal workspace comes from hipMallocAsync on `stream`.
+ * internal workspace (sage_attn_int8_bwd_workspace_size bytes) comes from
+ * hipMallocAsync on `stream`.
  */
 int sage_attn_int8_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse,
                        const void* dout, float* dq, float* dk, float* dv,
                        int B, int H, int N, int D, int causal, unsigned flags, hipStream_t stream);
 
-/* Workspace bytes for sage_attn_int8_bwd_ws; 0 for invalid or unsupported
- * arguments.  Host only. */
+/* Recommended workspace bytes for sage_attn_int8_bwd_ws (the size
+ * sage_attn_int8_bwd allocates); 0 for invalid or unsupported arguments.
+ * Beyond the minimum it holds the stored dS^ state of up to B*H heads
+ * (sage_attn_int8_bwd_min_workspace_size explains it), capped at 64 GiB of
+ * that state: about N^2 + 4 N^2 / 128 bytes per head.  Host only. */
 size_t sage_attn_int8_bwd_workspace_size(int B, int H, int N, int D, unsigned flags);
 
+/* Smallest workspace sage_attn_int8_bwd_ws accepts; 0 for invalid or
+ * unsupported arguments.  Host only.  With it the dQ kernel recomputes S, dP
+ * and dS; every head whose stored dS^ state (its codes, s_dS per block pair
+ * and per-pair row sums of dS, which the dK kernel writes) also fits lets the
+ * dQ kernel read them back instead, heads processed in groups of that many.
+ * The result does not depend on the workspace size beyond rounding order of
+ * the row-sum term of the smoothing of K. */
+size_t sage_attn_int8_bwd_min_workspace_size(int B, int H, int N, int D, unsigned flags);
+
 /* Same as sage_attn_int8_bwd, with a caller-provided workspace of at least
- * sage_attn_int8_bwd_workspace_size() bytes (256-byte aligned). */
+ * sage_attn_int8_bwd_min_workspace_size() bytes (256-byte aligned). */
 int sage_attn_int8_bwd_ws(const void* q, const void* k, const void* v, const float* o, const float* lse,
                           const void* dout, float* dq, float* dk, float* dv,
                           int B, int H, int N, int D, int causal, unsigned flags,

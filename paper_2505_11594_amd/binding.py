@@ -67,6 +67,8 @@ def lib():
         L.sage_attn_int8_bwd_ws.argtypes = [vp] * 9 + [i, i, i, i, i, u, vp, sz, vp]
         L.sage_attn_int8_bwd_workspace_size.argtypes = [i, i, i, i, u]
         L.sage_attn_int8_bwd_workspace_size.restype = sz
+        L.sage_attn_int8_bwd_min_workspace_size.argtypes = [i, i, i, i, u]
+        L.sage_attn_int8_bwd_min_workspace_size.restype = sz
         L.sage_status_string.argtypes = [i]
         L.sage_status_string.restype = ctypes.c_char_p
         L.sage_version.restype = ctypes.c_char_p
@@ -273,6 +275,10 @@ def sage_attn_int8_fwd_prequant(qq, kq, vq, shape, causal: bool = False, in_bf16
 
 def attn_int8_bwd_workspace_size(B: int, H: int, N: int, D: int, flags: int = 0) -> int:
     return int(lib().sage_attn_int8_bwd_workspace_size(B, H, N, D, flags))
+
+
+def attn_int8_bwd_min_workspace_size(B: int, H: int, N: int, D: int, flags: int = 0) -> int:
+    return int(lib().sage_attn_int8_bwd_min_workspace_size(B, H, N, D, flags))
 
 
 def sage_attn_int8_bwd(q, k, v, o, lse, dout, causal: bool = False, flags: int = 0, workspace=None, out=None):

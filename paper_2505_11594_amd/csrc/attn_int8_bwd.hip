@@ -63,6 +63,16 @@ __device__ __forceinline__ v4i bw_codes(const float (&x)[16], float r) {
   return v4i{w[0], w[1], w[2], w[3]};
 }
 
+// 4 x 4 byte transpose inside each quad of lanes: lane 4m + j returns the
+// bytes j of lanes 4m, 4m + 1, 4m + 2, 4m + 3 (in that order, low byte first).
+__device__ __forceinline__ uint32_t quad_byte_transpose(uint32_t w, int lane) {
+  const int j = lane & 3;
+  const uint32_t p1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w, 0xB1, 0xF, 0xF, true);    // quad_perm [1,0,3,2]
+  const uint32_t x1 = __builtin_amdgcn_perm(p1, w, (j & 1) ? 0x03070105u : 0x06020400u);
+  const uint32_t p2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x1, 0x4E, 0xF, 0xF, true);   // quad_perm [2,3,0,1]
+  return __builtin_amdgcn_perm(p2, x1, (j & 2) ? 0x03020706u : 0x05040100u);
+}
+
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) x = __builtin_fmaxf(x, __shfl_xor(x, off, 64));
@@ -308,21 +318,36 @@ struct BwDkLds {
   static_assert((NQA + NGA) % 4 == 0 && NT % 4 == 0, "even split over 4 waves");
 };
 
-template <int D, bool CAUSAL, bool BF16>
+// STORE_DS: also write, for every (query block, KV block) pair, the dS^ codes
+// in the operand order of the dQ kernel's product (query-block-major, 16
+// operand blocks of 1 KiB: (query group w, key subtile t) -- lane l holds
+// query 32w + l%32 and the 16 keys at positions [16 (l/32), +16) of subtile t,
+// position 16h + 4g + r holding key 8g + 4h + r), s_dS of the pair, and the
+// pair's row sums of the unquantized dS (one per query, [KV block][query]).
+// The codes go through LDS (bytes in place), the row sums through a per-wave
+// transpose; both leave with whole 16-byte vector stores.  Heads are
+// bh0 + blockIdx.y; the stored arrays are indexed by blockIdx.y.
+template <int D, bool CAUSAL, bool BF16, bool STORE_DS>
 __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
     const int8_t* __restrict__ qc, const float* __restrict__ qs, const int8_t* __restrict__ qt,
     const int8_t* __restrict__ kc, const float* __restrict__ ks, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lb,
-    float* __restrict__ dk, int N, int Np, int nqb, float c2, float rsd) {
+    float* __restrict__ dk, int8_t* __restrict__ dsc, float* __restrict__ dss, float* __restrict__ drs, int N, int Np,
+    int nqb, int bh0, float c2, float rsd) {
   using T = BwDkLds<D>;
   constexpr int NKS = T::NKS, NKS16 = T::NKS16, NDB = T::NDB, NU = BW_Q / 32;
+  constexpr int RS_STRIDE = 36;                    // floats per staged row (16-byte aligned, staggered banks)
   __shared__ __attribute__((aligned(16))) uint8_t ldsA[2][T::A_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t ldsT[T::T_BYTES];
+  __shared__ __attribute__((aligned(16))) uint8_t dsl[STORE_DS ? 16 * 1024 : 16];
+  __shared__ __attribute__((aligned(16))) float rsl[STORE_DS ? 4 * 32 * RS_STRIDE : 4];
+  __shared__ float red2[STORE_DS ? 4 * BW_Q : 1];
   __shared__ float red[2][4];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31, hi = lane >> 5;
-  const int kblk = blockIdx.x, bh = blockIdx.y;
+  const int kblk = blockIdx.x, lbh = blockIdx.y, bh = bh0 + lbh;
+  const int nkb = Np / BW_K;
   const int kb = kblk * BW_K, key = kb + 32 * wave + col;
   const float sK = ks[(size_t)bh * (Np / BW_K) + kblk];
 
@@ -445,6 +470,37 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
     v4i sc[NU];
 #pragma unroll
     for (int u = 0; u < NU; ++u) sc[u] = bw_codes(dS[u], rdS);
+    if constexpr (STORE_DS) {
+      // codes: byte e = 4g + r of sc[u] is query 32u + 8g + 4hi + r and key
+      // 32 wave + col; after the quad transpose this lane holds query
+      // 32u + 8g + 4hi + (col & 3) for keys 4 (col >> 2) + [0, 4)
+#pragma unroll
+      for (int u = 0; u < NU; ++u)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const uint32_t t = quad_byte_transpose((uint32_t)sc[u][g], lane);
+          const int m = col >> 2, lq = 8 * g + 4 * hi + (col & 3) + 32 * (m & 1);
+          *reinterpret_cast<uint32_t*>(dsl + (u * 4 + wave) * 1024 + lq * 16 + 4 * (m >> 1)) = t;
+        }
+      // row sums of dS over this wave's 32 keys: stage [query][key], sum each row
+      float* rw = rsl + wave * 32 * RS_STRIDE;
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) rw[(8 * (e >> 2) + 4 * hi + (e & 3)) * RS_STRIDE + col] = dS[u][e];
+        __builtin_amdgcn_wave_barrier();
+        const float* rr = rw + col * RS_STRIDE + 16 * hi;   // row: query 32u + col, keys [16hi, +16)
+        float x = 0.0f;
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4) {
+          const v4f y = *reinterpret_cast<const v4f*>(rr + 4 * c4);
+          x = ((x + y[0]) + y[1]) + (y[2] + y[3]);
+        }
+        x += __shfl_xor(x, 32, 64);
+        if (hi == 0) red2[wave * BW_Q + 32 * u + col] = x;
+        __builtin_amdgcn_wave_barrier();
+      }
+    }
     const float fk = (sdS * sQ) * rsd;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
@@ -455,6 +511,21 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
                                                     sc[u], dki, 0, 0, 0);
 #pragma unroll
       for (int e = 0; e < 16; ++e) dka[db][e] = __builtin_fmaf((float)dki[e], fk, dka[db][e]);
+    }
+    if constexpr (STORE_DS) {
+      __syncthreads();                             // every wave's codes and row sums are staged
+      const size_t pair = ((size_t)lbh * nqb + i) * nkb + kblk;
+#pragma unroll
+      for (int b4 = 0; b4 < 4; ++b4) {
+        const int b = wave * 4 + b4;
+        *reinterpret_cast<v4i*>(dsc + (pair * 16 + b) * 1024 + lane * 16) =
+            *reinterpret_cast<const v4i*>(dsl + b * 1024 + lane * 16);
+      }
+      if (tid < BW_Q) {
+        const float x = (red2[tid] + red2[BW_Q + tid]) + (red2[2 * BW_Q + tid] + red2[3 * BW_Q + tid]);
+        drs[((size_t)lbh * nkb + kblk) * Np + q0 + tid] = x;
+      }
+      if (tid == 0) dss[pair] = sdS;
     }
   }
 
@@ -645,6 +716,106 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// dQ from the stored dS^ of the dK kernel: per (query block, KV block) pair
+// dQ^T += (K^T dS^T) s_dS s_K / sqrt(D) + rowsum(dS) K_m / sqrt(D), with the
+// pair's codes, s_dS and row sums read back instead of recomputing S, dP and
+// dS.  A workgroup owns 128 queries (4 waves x 32); each KV block's K^T
+// operand blocks and the pair's 16 dS^ operand blocks are staged in LDS one
+// block ahead.  Heads are bh0 + blockIdx.y; the stored arrays are indexed by
+// blockIdx.y.
+// ---------------------------------------------------------------------------
+template <int D>
+struct BwQdsLds {
+  static constexpr int NDB = D / 32, NT = BW_K / 32;
+  static constexpr int NKT = NDB * NT, NDS = (BW_Q / 32) * NT;
+  static constexpr int KT_OFF = 0, DS_OFF = NKT * 1024, BYTES = DS_OFF + NDS * 1024;
+  static constexpr int J = (NKT + NDS) / 4;
+  static_assert((NKT + NDS) % 4 == 0, "even split over 4 waves");
+};
+
+template <int D, bool CAUSAL>
+__global__ __launch_bounds__(256, 2) void attn_i8_bwd_dq_ds_kernel(
+    const float* __restrict__ ks, const int8_t* __restrict__ kt, const int8_t* __restrict__ dsc,
+    const float* __restrict__ dss, const float* __restrict__ drs, const float* __restrict__ kmean,
+    float* __restrict__ dq, int N, int Np, int nqb, int bh0, float rsd) {
+  using T = BwQdsLds<D>;
+  constexpr int NDB = T::NDB, NT = T::NT;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2][T::BYTES];
+  __shared__ __attribute__((aligned(16))) float kms[D];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, hi = lane >> 5;
+  const int i = blockIdx.x, lbh = blockIdx.y, bh = bh0 + lbh;
+  const int nkbt = Np / BW_K;
+  const int q0 = i * BW_Q, qi = q0 + 32 * wave + col;
+  if (tid < D) kms[tid] = kmean != nullptr ? kmean[(size_t)bh * D + tid] : 0.0f;
+  v16f dqa[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) dqa[db] = v16f{};
+
+  auto issue = [&](int j, int buf) {
+    const int kb = j * BW_K;
+    uint8_t* L = lds[buf];
+    const int8_t* dpair = dsc + (((size_t)lbh * nqb + i) * nkbt + j) * (size_t)(T::NDS * 1024);
+#pragma unroll
+    for (int k = 0; k < T::J; ++k) {
+      const int b = wave + 4 * k;
+      if (b < T::NKT) {
+        const int db = b / NT, t = b % NT;
+        bw_lds_load16(kt + ((size_t)bh * D + 32 * db + col) * Np + kb + 32 * t + 16 * hi, L + T::KT_OFF + b * 1024);
+      } else {
+        const int d = b - T::NKT;
+        bw_lds_load16(dpair + d * 1024 + lane * 16, L + T::DS_OFF + d * 1024);
+      }
+    }
+  };
+
+  int nkb = nkbt;
+  if (CAUSAL) nkb = min(nkb, min(q0 + BW_Q - 1, N - 1) / BW_K + 1);
+  issue(0, 0);
+  for (int j = 0; j < nkb; ++j) {
+    const int buf = j & 1;
+    bw_wait_all();
+    __syncthreads();                               // block j has landed; every wave is done with block j - 1
+    if (j + 1 < nkb) issue(j + 1, buf ^ 1);
+    const uint8_t* L = lds[buf];
+    const float sK = ks[(size_t)bh * nkbt + j];
+    const float sdS = dss[((size_t)lbh * nqb + i) * nkbt + j];
+    const float fq = (sdS * sK) * rsd;
+    const float rr = drs[((size_t)lbh * nkbt + j) * Np + qi] * rsd;   // rowsum(dS) of this lane's query, / sqrt(D)
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      v16i dqi = v16i{};
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        dqi = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+            *reinterpret_cast<const v4i*>(L + T::KT_OFF + (db * NT + t) * 1024 + lane * 16),
+            *reinterpret_cast<const v4i*>(L + T::DS_OFF + (wave * NT + t) * 1024 + lane * 16), dqi, 0, 0, 0);
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const v4f km = *reinterpret_cast<const v4f*>(kms + 32 * db + 8 * g + 4 * hi);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int e = 4 * g + r;
+          float x = __builtin_fmaf((float)dqi[e], fq, dqa[db][e]);
+          if (kmean != nullptr) x = __builtin_fmaf(rr, km[r], x);
+          dqa[db][e] = x;
+        }
+      }
+    }
+  }
+  if (qi < N) {
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const size_t idx = ((size_t)bh * N + qi) * D + 32 * db + 8 * g + 4 * hi;
+        *reinterpret_cast<float4*>(dq + idx) = make_float4(dqa[db][4 * g], dqa[db][4 * g + 1], dqa[db][4 * g + 2], dqa[db][4 * g + 3]);
+      }
+  }
+}
+
 hipError_t launch_i8_bwd_prep(const void* dout, const float* o, const float* lse, float* drow, float* lb, int BH,
                               int N, int Np, int D, bool bf16, hipStream_t st) {
   const long long rows = (long long)BH * Np;
@@ -666,34 +837,62 @@ template <int D, bool CAUSAL, bool BF16>
 static hipError_t launch_bwd_t(const int8_t* qc, const float* qs, const int8_t* qt, const int8_t* kc, const float* ks,
                                const int8_t* kt, const uint16_t* v, const uint16_t* dout, const int8_t* gt,
                                const float* gs, const float* drow, const float* lb, const float* kmean, float* dq,
-                               float* dk, float* dv, int BH, int N, int Np, float c2, float rsd, hipStream_t st) {
-  const int nqb = (N + BW_Q - 1) / BW_Q;
-  const dim3 kgrid((unsigned)(Np / BW_K), (unsigned)BH);
-  hipLaunchKernelGGL((attn_i8_bwd_dv_kernel<D, CAUSAL>), kgrid, dim3(256), 0, st, qc, qs, kc, ks, gt, gs, drow, lb, dv, N,
-                     Np, nqb, c2);
+                               float* dk, float* dv, int8_t* dsc, float* dss, float* drs, int G, int BH, int N, int Np,
+                               float c2, float rsd, hipStream_t st) {
+  const int nqb = (N + BW_Q - 1) / BW_Q, nkb = Np / BW_K;
+  hipLaunchKernelGGL((attn_i8_bwd_dv_kernel<D, CAUSAL>), dim3((unsigned)nkb, (unsigned)BH), dim3(256), 0, st, qc, qs,
+                     kc, ks, gt, gs, drow, lb, dv, N, Np, nqb, c2);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_i8_bwd_dk_kernel<D, CAUSAL, BF16>), kgrid, dim3(256), 0, st, qc, qs, qt, kc, ks, v, dout,
-                     drow, lb, dk, N, Np, nqb, c2, rsd);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_i8_bwd_dq_kernel<D, CAUSAL, BF16>), dim3((unsigned)nqb, (unsigned)BH), dim3(256), 0, st, qc,
-                     qs, kc, ks, kt, v, dout, drow, lb, kmean, dq, N, Np, nqb, c2, rsd);
-  return hipGetLastError();
+  if (G <= 0) {                                    // no room to store dS^: dQ recomputes it
+    hipLaunchKernelGGL((attn_i8_bwd_dk_kernel<D, CAUSAL, BF16, false>), dim3((unsigned)nkb, (unsigned)BH), dim3(256), 0,
+                       st, qc, qs, qt, kc, ks, v, dout, drow, lb, dk, nullptr, nullptr, nullptr, N, Np, nqb, 0, c2, rsd);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_i8_bwd_dq_kernel<D, CAUSAL, BF16>), dim3((unsigned)nqb, (unsigned)BH), dim3(256), 0, st,
+                       qc, qs, kc, ks, kt, v, dout, drow, lb, kmean, dq, N, Np, nqb, c2, rsd);
+    return hipGetLastError();
+  }
+  for (int h0 = 0; h0 < BH; h0 += G) {             // groups of G heads share the stored dS^
+    const int g = min(G, BH - h0);
+    hipLaunchKernelGGL((attn_i8_bwd_dk_kernel<D, CAUSAL, BF16, true>), dim3((unsigned)nkb, (unsigned)g), dim3(256), 0,
+                       st, qc, qs, qt, kc, ks, v, dout, drow, lb, dk, dsc, dss, drs, N, Np, nqb, h0, c2, rsd);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((attn_i8_bwd_dq_ds_kernel<D, CAUSAL>), dim3((unsigned)nqb, (unsigned)g), dim3(256), 0, st, ks, kt,
+                       dsc, dss, drs, kmean, dq, N, Np, nqb, h0, rsd);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// Bytes of stored dS^ state per head: codes (16 KiB per (query block, KV
+// block) pair), s_dS per pair, and row sums [KV block][Np] fp32.
+size_t i8_bwd_ds_bytes_per_head(int N) {
+  const size_t Np = (size_t)((N + 127) / 128) * 128, nb = Np / 128;
+  return nb * nb * 16384 + nb * nb * sizeof(float) + nb * Np * sizeof(float);
 }
 
 // Q^ [BH, N, D], K^ [BH, Np, D] row-major; Q^T, K^T, dO^T [BH, D, Np] permuted
-// per 32 rows; scales per 128 rows; kmean null without smoothing.
+// per 32 rows; scales per 128 rows; kmean null without smoothing.  dsc, dss,
+// drs: the stored dS^ state of G heads (i8_bwd_ds_bytes_per_head each, in
+// that order), or G = 0 to recompute dS^ in the dQ kernel.
 hipError_t launch_attn_int8_bwd(const void* qc, const float* qs, const void* qt, const void* kc, const float* ks,
                                 const void* kt, const void* v, const void* dout, const void* gt, const float* gs,
                                 const float* drow, const float* lb, const float* kmean, float* dq, float* dk, float* dv,
-                                int BH, int N, int Np, int D, bool causal, bool bf16, float c2, float rsd,
-                                hipStream_t st) {
+                                void* ds_state, int G, int BH, int N, int Np, int D, bool causal, bool bf16, float c2,
+                                float rsd, hipStream_t st) {
   const int8_t *a = (const int8_t*)qc, *b = (const int8_t*)qt, *c = (const int8_t*)kc, *d = (const int8_t*)kt,
                *g = (const int8_t*)gt;
   const uint16_t *vv = (const uint16_t*)v, *gg = (const uint16_t*)dout;
-#define SAGE_BW(DD, CC, BB) \
-  return launch_bwd_t<DD, CC, BB>(a, qs, b, c, ks, d, vv, gg, g, gs, drow, lb, kmean, dq, dk, dv, BH, N, Np, c2, rsd, st)
+  const size_t nb = (size_t)Np / 128;
+  int8_t* dsc = static_cast<int8_t*>(ds_state);
+  float* dss = G > 0 ? reinterpret_cast<float*>(dsc + (size_t)G * nb * nb * 16384) : nullptr;
+  float* drs = G > 0 ? dss + (size_t)G * nb * nb : nullptr;
+#define SAGE_BW(DD, CC, BB)                                                                                          \
+  return launch_bwd_t<DD, CC, BB>(a, qs, b, c, ks, d, vv, gg, g, gs, drow, lb, kmean, dq, dk, dv, dsc, dss, drs, G, BH, \
+                                  N, Np, c2, rsd, st)
   if (D == 128) {
     if (causal) { if (bf16) SAGE_BW(128, true, true); else SAGE_BW(128, true, false); }
     else { if (bf16) SAGE_BW(128, false, true); else SAGE_BW(128, false, false); }

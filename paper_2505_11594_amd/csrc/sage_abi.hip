@@ -1,5 +1,6 @@
 // C ABI of the gfx950 microscaled-FP4 attention library.  Argument checks run
 // on the host before any HIP call; kernels are enqueued on the caller's stream.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -37,8 +38,9 @@ hipError_t launch_i8_bwd_prep(const void* dout, const float* o, const float* lse
 hipError_t launch_attn_int8_bwd(const void* qc, const float* qs, const void* qt, const void* kc, const float* ks,
                                 const void* kt, const void* v, const void* dout, const void* gt, const float* gs,
                                 const float* drow, const float* lb, const float* kmean, float* dq, float* dk, float* dv,
-                                int BH, int N, int Np, int D, bool causal, bool bf16, float c2, float rsd,
-                                hipStream_t st);
+                                void* ds_state, int G, int BH, int N, int Np, int D, bool causal, bool bf16, float c2,
+                                float rsd, hipStream_t st);
+size_t i8_bwd_ds_bytes_per_head(int N);
 }  // namespace sage
 
 namespace {
@@ -280,8 +282,13 @@ int attn_i8_args(const void* q, const void* k, const void* v, const void* o, con
 // ---- 8-bit attention backward (Algorithm 3) -------------------------------
 constexpr unsigned kI8BwdFlags = SAGE_IN_BF16 | SAGE_OUT_F32 | SAGE_NO_SMOOTH_K | SAGE_BKV64;
 
+// Stored dS^ state of the backward (the dK kernel writes it, the dQ kernel
+// reads it back instead of recomputing S, dP and dS) is capped at this many
+// bytes in the recommended workspace: heads are processed in groups that fit.
+constexpr size_t kI8BwdDsCap = size_t(64) << 30;
+
 struct I8BwdWs {
-  size_t qc, qs, qt, kc, ks, kt, mu, part, gt, gs, drow, lb, total;
+  size_t qc, qs, qt, kc, ks, kt, mu, part, gt, gs, drow, lb, ds, total;   // total: without the dS^ state
 };
 
 I8BwdWs i8_bwd_ws_layout(int B, int H, int N, int D) {
@@ -300,14 +307,31 @@ I8BwdWs i8_bwd_ws_layout(int B, int H, int N, int D) {
   w.gs = off; off += up256(BH * nb * sizeof(float));
   w.drow = off; off += up256(BH * Np * sizeof(float));
   w.lb = off; off += up256(BH * Np * sizeof(float));
+  w.ds = off;
   w.total = off;
   return w;
 }
 
+// heads whose dS^ state fits in `bytes` of workspace (0: the dQ kernel recomputes dS^)
+int i8_bwd_ds_heads(int B, int H, int N, int D, size_t bytes) {
+  const I8BwdWs w = i8_bwd_ws_layout(B, H, N, D);
+  if (bytes <= w.ds) return 0;
+  const size_t fit = (bytes - w.ds) / sage::i8_bwd_ds_bytes_per_head(N);
+  return (int)std::min<size_t>(fit, (size_t)B * H);
+}
+
+size_t i8_bwd_recommended_bytes(int B, int H, int N, int D) {
+  const I8BwdWs w = i8_bwd_ws_layout(B, H, N, D);
+  const size_t per = sage::i8_bwd_ds_bytes_per_head(N);
+  const size_t heads = std::min<size_t>((size_t)B * H, kI8BwdDsCap / per);
+  return w.ds + heads * per;
+}
+
 int attn_i8_bwd_ws_impl(const void* q, const void* k, const void* v, const float* o, const float* lse,
                         const void* dout, float* dq, float* dk, float* dv, int B, int H, int N, int D, int causal,
-                        unsigned flags, void* ws, hipStream_t st) {
+                        unsigned flags, void* ws, size_t ws_bytes, hipStream_t st) {
   const I8BwdWs w = i8_bwd_ws_layout(B, H, N, D);
+  const int G = i8_bwd_ds_heads(B, H, N, D, ws_bytes);
   uint8_t* base = static_cast<uint8_t*>(ws);
   const bool bf16 = (flags & SAGE_IN_BF16) != 0, smooth = !(flags & SAGE_NO_SMOOTH_K);
   const int BH = B * H, Np = pad128(N);
@@ -328,8 +352,8 @@ int attn_i8_bwd_ws_impl(const void* q, const void* k, const void* v, const float
   if (e == hipSuccess) e = sage::launch_i8_bwd_prep(dout, o, lse, drow, lb, BH, N, Np, D, bf16, st);
   if (e == hipSuccess)
     e = sage::launch_attn_int8_bwd(base + w.qc, qs, base + w.qt, base + w.kc, ks, base + w.kt, v, dout, base + w.gt, gs,
-                                   drow, lb, mup, dq, dk, dv, BH, N, Np, D, causal != 0, bf16, softmax_c2(D),
-                                   (float)(1.0 / std::sqrt((double)D)), st);
+                                   drow, lb, mup, dq, dk, dv, base + w.ds, G, BH, N, Np, D, causal != 0, bf16,
+                                   softmax_c2(D), (float)(1.0 / std::sqrt((double)D)), st);
   return hip_status(e);
 }
 
@@ -520,6 +544,12 @@ int sage_attn_int8_fwd_prequant(const void* q_codes, const float* q_scales, cons
 size_t sage_attn_int8_bwd_workspace_size(int B, int H, int N, int D, unsigned flags) {
   if ((flags & ~kI8BwdFlags) || (flags & SAGE_BKV64) || check_shape(B, H, N, D, flags & SAGE_IN_BF16) != SAGE_OK)
     return 0;
+  return i8_bwd_recommended_bytes(B, H, N, D);
+}
+
+size_t sage_attn_int8_bwd_min_workspace_size(int B, int H, int N, int D, unsigned flags) {
+  if ((flags & ~kI8BwdFlags) || (flags & SAGE_BKV64) || check_shape(B, H, N, D, flags & SAGE_IN_BF16) != SAGE_OK)
+    return 0;
   return i8_bwd_ws_layout(B, H, N, D).total;
 }
 
@@ -530,7 +560,8 @@ int sage_attn_int8_bwd_ws(const void* q, const void* k, const void* v, const flo
   if (rc != SAGE_OK) return rc;
   if (!workspace || !aligned(workspace, 256)) return SAGE_ERR_INVALID_ARG;
   if (workspace_bytes < i8_bwd_ws_layout(B, H, N, D).total) return SAGE_ERR_WORKSPACE;
-  return attn_i8_bwd_ws_impl(q, k, v, o, lse, dout, dq, dk, dv, B, H, N, D, causal, flags, workspace, stream);
+  return attn_i8_bwd_ws_impl(q, k, v, o, lse, dout, dq, dk, dv, B, H, N, D, causal, flags, workspace, workspace_bytes,
+                             stream);
 }
 
 int sage_attn_int8_bwd(const void* q, const void* k, const void* v, const float* o, const float* lse, const void* dout,
@@ -538,10 +569,10 @@ int sage_attn_int8_bwd(const void* q, const void* k, const void* v, const float*
                        hipStream_t stream) {
   int rc = attn_i8_bwd_args(q, k, v, o, lse, dout, dq, dk, dv, B, H, N, D, causal, flags);
   if (rc != SAGE_OK) return rc;
-  const size_t bytes = i8_bwd_ws_layout(B, H, N, D).total;
+  const size_t bytes = i8_bwd_recommended_bytes(B, H, N, D);
   void* ws = nullptr;
   if (hipMallocAsync(&ws, bytes, stream) != hipSuccess) return SAGE_ERR_HIP;
-  rc = attn_i8_bwd_ws_impl(q, k, v, o, lse, dout, dq, dk, dv, B, H, N, D, causal, flags, ws, stream);
+  rc = attn_i8_bwd_ws_impl(q, k, v, o, lse, dout, dq, dk, dv, B, H, N, D, causal, flags, ws, bytes, stream);
   if (hipFreeAsync(ws, stream) != hipSuccess && rc == SAGE_OK) rc = SAGE_ERR_HIP;
   return rc;
 }

@@ -163,8 +163,21 @@ def test_int8_bwd_validation(L):
     for bad in (dict(q=None), dict(lse=None), dict(dv=None), dict(o=FAKE + 4), dict(do=FAKE + 8), dict(lse=FAKE + 2)):
         assert L.sage_attn_int8_bwd(*args(**bad), 1, 1, 128, 128, 0, 0, None) == bd.SAGE_ERR_INVALID_ARG, bad
     assert L.sage_attn_int8_bwd(*ok, 1, 1, 128, 128, 2, 0, None) == bd.SAGE_ERR_INVALID_ARG
-    need = L.sage_attn_int8_bwd_workspace_size(1, 1, 128, 128, 0)
+    need = L.sage_attn_int8_bwd_min_workspace_size(1, 1, 128, 128, 0)
     assert L.sage_attn_int8_bwd_ws(*ok, 1, 1, 128, 128, 0, 0, FAKE, need - 1, None) == bd.SAGE_ERR_WORKSPACE
+    # the recommended size adds the stored dS^ state of every head: codes of
+    # every (query block, KV block) pair, one s_dS per pair, row sums per pair
+    for B, H, N, D in ((1, 2, 1000, 128), (2, 3, 300, 64), (1, 1, 1, 128)):
+        lo = L.sage_attn_int8_bwd_min_workspace_size(B, H, N, D, 0)
+        hi = L.sage_attn_int8_bwd_workspace_size(B, H, N, D, 0)
+        nb = (N + 127) // 128
+        assert 0 < lo < hi and hi - lo == B * H * (nb * nb * (16384 + 4) + nb * nb * 128 * 4)
+    assert L.sage_attn_int8_bwd_min_workspace_size(1, 2, 1000, 96, 0) == 0
+    assert L.sage_attn_int8_bwd_min_workspace_size(1, 2, 1000, 128, bd.SAGE_BKV64) == 0
+    # the stored state is capped at 64 GiB: at 32 heads of 65536 tokens only 15 heads fit
+    per = 512 * 512 * (16384 + 4) + 512 * 65536 * 4
+    lo = L.sage_attn_int8_bwd_min_workspace_size(1, 32, 65536, 128, 0)
+    assert L.sage_attn_int8_bwd_workspace_size(1, 32, 65536, 128, 0) - lo == ((64 << 30) // per) * per
 
 
 def test_product_path_does_not_import_oracle():

@@ -97,3 +97,36 @@ def test_bwd_zero_do_and_doubling():
     b = gpu_bwd(q, k, v, d2, o, lse, 1, True)
     for x, y in zip(a, b):
         assert np.array_equal(2 * x, y)
+
+
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_bwd_workspace_selects_stored_or_recomputed_ds(D, causal):
+    """The minimum workspace makes the dQ kernel recompute S, dP and dS; each
+    head's worth of workspace beyond it lets the dK kernel store dS^ for the
+    dQ kernel, heads in groups of that many.  dK and dV are the same bits on
+    every path, dQ the same bits on every stored path, and all of them match
+    the oracle."""
+    torch = torch_dev()
+    B, H, N = 1, 3, 300
+    say("bwd workspace paths D=%d causal=%d" % (D, causal))
+    q, k, v, do, o, lse = make_case(B, H, N, D, 1, seed=1150 + D + causal, causal=causal, k_bias_var=4.0)
+    lo = bd.attn_int8_bwd_min_workspace_size(B, H, N, D, bd.SAGE_IN_BF16)
+    hi = bd.attn_int8_bwd_workspace_size(B, H, N, D, bd.SAGE_IN_BF16)
+    assert 0 < lo < hi and (hi - lo) % (B * H) == 0
+    per_head = (hi - lo) // (B * H)
+    *ref, tol = oracle.attn_int8_bwd(q, k, v, do, o, lse, 1, causal, 128)
+    args = [to_dev(q, 1), to_dev(k, 1), to_dev(v, 1), torch.from_numpy(o).cuda(), torch.from_numpy(lse).cuda(),
+            to_dev(do, 1)]
+    runs = {}
+    for heads in (0, 1, 2, 3):
+        ws = torch.empty(lo + heads * per_head, dtype=torch.uint8, device="cuda")
+        r = bd.sage_attn_int8_bwd(*args, causal=causal, workspace=ws)
+        torch.cuda.synchronize()
+        runs[heads] = [x.cpu().numpy() for x in r]
+        check_grads(runs[heads], ref, tol, "heads stored %d" % heads)
+    for heads in (1, 2, 3):
+        assert np.array_equal(runs[heads][1], runs[0][1]) and np.array_equal(runs[heads][2], runs[0][2])
+        assert np.array_equal(runs[heads][0], runs[1][0])
+    with pytest.raises(RuntimeError):
+        bd.sage_attn_int8_bwd(*args, causal=causal, workspace=torch.empty(lo - 256, dtype=torch.uint8, device="cuda"))
