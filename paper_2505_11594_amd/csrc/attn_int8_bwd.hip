@@ -73,6 +73,22 @@ __device__ __forceinline__ uint32_t quad_byte_transpose(uint32_t w, int lane) {
   return __builtin_amdgcn_perm(p2, x1, (j & 2) ? 0x03020706u : 0x05040100u);
 }
 
+// One step of a butterfly reduction over lanes: each lane keeps one half of
+// its 2H values (the upper half where `upper`), adds the partner lane's other
+// half to it, the partner given by a DPP control (CTRL >= 0) or lane ^ 16.
+template <int H, int CTRL>
+__device__ __forceinline__ void bw_fold(float (&x)[16], bool upper) {
+#pragma unroll
+  for (int i = 0; i < H; ++i) {
+    const float send = upper ? x[i] : x[i + H];
+    const float keep = upper ? x[i + H] : x[i];
+    float recv;
+    if constexpr (CTRL < 0) recv = __shfl_xor(send, 16, 64);
+    else recv = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(send), CTRL, 0xF, 0xF, true));
+    x[i] = keep + recv;
+  }
+}
+
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) x = __builtin_fmaxf(x, __shfl_xor(x, off, 64));
@@ -324,8 +340,9 @@ struct BwDkLds {
 // query 32w + l%32 and the 16 keys at positions [16 (l/32), +16) of subtile t,
 // position 16h + 4g + r holding key 8g + 4h + r), s_dS of the pair, and the
 // pair's row sums of the unquantized dS (one per query, [KV block][query]).
-// The codes go through LDS (bytes in place), the row sums through a per-wave
-// transpose; both leave with whole 16-byte vector stores.  Heads are
+// The codes go through LDS (a byte transpose inside each quad of lanes, then
+// dword writes in place) and leave with whole 16-byte vector stores; the row
+// sums are reduced across lanes in registers.  Heads are
 // bh0 + blockIdx.y; the stored arrays are indexed by blockIdx.y.
 template <int D, bool CAUSAL, bool BF16, bool STORE_DS>
 __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
@@ -336,11 +353,9 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
     int nqb, int bh0, float c2, float rsd) {
   using T = BwDkLds<D>;
   constexpr int NKS = T::NKS, NKS16 = T::NKS16, NDB = T::NDB, NU = BW_Q / 32;
-  constexpr int RS_STRIDE = 36;                    // floats per staged row (16-byte aligned, staggered banks)
   __shared__ __attribute__((aligned(16))) uint8_t ldsA[2][T::A_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t ldsT[T::T_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t dsl[STORE_DS ? 16 * 1024 : 16];
-  __shared__ __attribute__((aligned(16))) float rsl[STORE_DS ? 4 * 32 * RS_STRIDE : 4];
   __shared__ float red2[STORE_DS ? 4 * BW_Q : 1];
   __shared__ float red[2][4];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -482,23 +497,23 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
           const int m = col >> 2, lq = 8 * g + 4 * hi + (col & 3) + 32 * (m & 1);
           *reinterpret_cast<uint32_t*>(dsl + (u * 4 + wave) * 1024 + lq * 16 + 4 * (m >> 1)) = t;
         }
-      // row sums of dS over this wave's 32 keys: stage [query][key], sum each row
-      float* rw = rsl + wave * 32 * RS_STRIDE;
+      // row sums of dS over this wave's 32 keys: a butterfly over the 32 lanes
+      // that share hi (partners lane ^ 16, row rotation by 8, half-row mirror,
+      // quad swaps), after which lanes 2e and 2e + 1 hold the sum of element e
 #pragma unroll
       for (int u = 0; u < NU; ++u) {
+        float x[16];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) rw[(8 * (e >> 2) + 4 * hi + (e & 3)) * RS_STRIDE + col] = dS[u][e];
-        __builtin_amdgcn_wave_barrier();
-        const float* rr = rw + col * RS_STRIDE + 16 * hi;   // row: query 32u + col, keys [16hi, +16)
-        float x = 0.0f;
-#pragma unroll
-        for (int c4 = 0; c4 < 4; ++c4) {
-          const v4f y = *reinterpret_cast<const v4f*>(rr + 4 * c4);
-          x = ((x + y[0]) + y[1]) + (y[2] + y[3]);
+        for (int e = 0; e < 16; ++e) x[e] = dS[u][e];
+        bw_fold<8, -1>(x, (col & 16) != 0);
+        bw_fold<4, 0x128>(x, (col & 8) != 0);      // row_ror:8
+        bw_fold<2, 0x141>(x, (col & 4) != 0);      // row_half_mirror
+        bw_fold<1, 0x4E>(x, (col & 2) != 0);       // quad_perm [2,3,0,1]
+        const float sum = x[0] + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x[0]), 0xB1, 0xF, 0xF, true));
+        if ((col & 1) == 0) {
+          const int e = col >> 1;
+          red2[wave * BW_Q + 32 * u + 8 * (e >> 2) + 4 * hi + (e & 3)] = sum;
         }
-        x += __shfl_xor(x, 32, 64);
-        if (hi == 0) red2[wave * BW_Q + 32 * u + col] = x;
-        __builtin_amdgcn_wave_barrier();
       }
     }
     const float fk = (sdS * sQ) * rsd;
