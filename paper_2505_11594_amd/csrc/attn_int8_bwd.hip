@@ -319,19 +319,26 @@ __global__ __launch_bounds__(256, 2) void attn_i8_bwd_dv_kernel(
 // dK.  dK^T = Q^T dS^ per query block: S = Q^ K^T and dP = dO V^T of each
 // 32-query subtile, P = exp2(S c_t - Lb), dS = P (dP - D); dS of the whole
 // block stays in registers while its maximum is reduced across the waves,
-// then psi of dS and the product.  The query block's Q^ and dO (double-
-// buffered) and Q^T (single: loaded after the block's first barrier, waited
-// for before its second) are staged in LDS.  qt: Q^T int8 [BH, D, Np]
-// permuted per 32 rows.
+// then psi of dS and the product.  Eight waves, two per 32-key group: wave
+// (kg, qh) forms S, dP and dS of subtiles 2qh and 2qh + 1 for its keys, the
+// waves swap their dS^ codes through LDS, and each wave then runs the product
+// over all four subtiles for half of the channel blocks -- the int32 block
+// products stay whole, and each wave holds half the fp32 accumulators, which
+// lets two waves share a SIMD.  The query block's Q^ and dO (double-buffered)
+// and Q^T (single: loaded after the block's first barrier, waited for before
+// its second) are staged in LDS.  qt: Q^T int8 [BH, D, Np] permuted per 32
+// rows.
 // ---------------------------------------------------------------------------
+constexpr int BW_DK_WAVES = 8;
+
 template <int D>
 struct BwDkLds {
   static constexpr int NKS = D / 32, NKS16 = D / 16, NDB = D / 32;
   static constexpr int NQA = 4 * NKS, NGA = 4 * NKS16, NT = NDB * 4;
   static constexpr int QA_OFF = 0, GA_OFF = NQA * 1024, LD_OFF = GA_OFF + NGA * 1024, A_BYTES = LD_OFF + 1024;
   static constexpr int T_BYTES = NT * 1024;
-  static constexpr int AJ = (NQA + NGA) / 4, TJ = NT / 4;   // loads per wave
-  static_assert((NQA + NGA) % 4 == 0 && NT % 4 == 0, "even split over 4 waves");
+  static constexpr int AJ = (NQA + NGA) / BW_DK_WAVES, TJ = NT / BW_DK_WAVES;   // loads per wave
+  static_assert((NQA + NGA) % BW_DK_WAVES == 0 && NT % BW_DK_WAVES == 0, "even split over the waves");
 };
 
 // STORE_DS: also write, for every (query block, KV block) pair, the dS^ codes
@@ -345,25 +352,27 @@ struct BwDkLds {
 // sums are reduced across lanes in registers.  Heads are
 // bh0 + blockIdx.y; the stored arrays are indexed by blockIdx.y.
 template <int D, bool CAUSAL, bool BF16, bool STORE_DS>
-__global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
+__global__ __launch_bounds__(64 * BW_DK_WAVES, 1) void attn_i8_bwd_dk_kernel(
     const int8_t* __restrict__ qc, const float* __restrict__ qs, const int8_t* __restrict__ qt,
     const int8_t* __restrict__ kc, const float* __restrict__ ks, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dout, const float* __restrict__ drow, const float* __restrict__ lb,
     float* __restrict__ dk, int8_t* __restrict__ dsc, float* __restrict__ dss, float* __restrict__ drs, int N, int Np,
     int nqb, int bh0, float c2, float rsd) {
   using T = BwDkLds<D>;
-  constexpr int NKS = T::NKS, NKS16 = T::NKS16, NDB = T::NDB, NU = BW_Q / 32;
+  constexpr int NKS = T::NKS, NKS16 = T::NKS16, NDB = T::NDB, NU = BW_Q / 32, NH = NDB / 2;
   __shared__ __attribute__((aligned(16))) uint8_t ldsA[2][T::A_BYTES];
   __shared__ __attribute__((aligned(16))) uint8_t ldsT[T::T_BYTES];
+  __shared__ __attribute__((aligned(16))) uint8_t cx[4 * NU * 1024];   // dS^ codes: (key group, subtile) blocks
   __shared__ __attribute__((aligned(16))) uint8_t dsl[STORE_DS ? 16 * 1024 : 16];
   __shared__ float red2[STORE_DS ? 4 * BW_Q : 1];
-  __shared__ float red[2][4];
+  __shared__ float red[2][BW_DK_WAVES];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kg = wave & 3, qh = wave >> 2;          // key group; query half (subtiles 2qh, 2qh + 1); channel half
   const int col = lane & 31, hi = lane >> 5;
   const int kblk = blockIdx.x, lbh = blockIdx.y, bh = bh0 + lbh;
   const int nkb = Np / BW_K;
-  const int kb = kblk * BW_K, key = kb + 32 * wave + col;
+  const int kb = kblk * BW_K, key = kb + 32 * kg + col;
   const float sK = ks[(size_t)bh * (Np / BW_K) + kblk];
 
   // B operands of this lane's key: K^ (channels [32s + 16hi, +16)) and V
@@ -378,16 +387,16 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
     for (int s = 0; s < NKS16; ++s)
       vreg[s] = key < N ? *reinterpret_cast<const v4i*>(vr + 16 * s + 8 * hi) : v4i{0, 0, 0, 0};
   }
-  v16f dka[NDB];
+  v16f dka[NH];                                      // channel blocks qh NH + h
 #pragma unroll
-  for (int db = 0; db < NDB; ++db) dka[db] = v16f{};
+  for (int h = 0; h < NH; ++h) dka[h] = v16f{};
 
   auto issue_A = [&](int i, int buf) {
     const int q0 = i * BW_Q;
     uint8_t* L = ldsA[buf];
 #pragma unroll
     for (int k = 0; k < T::AJ; ++k) {
-      const int b = wave + 4 * k;
+      const int b = wave + BW_DK_WAVES * k;
       if (b < T::NQA) {
         bw_load_qa<D>(qc, L + T::QA_OFF + b * 1024, b, bh, N, q0, col, hi);
       } else {
@@ -400,7 +409,7 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
   auto issue_T = [&](int i) {
 #pragma unroll
     for (int k = 0; k < T::TJ; ++k) {
-      const int t = wave + 4 * k;
+      const int t = wave + BW_DK_WAVES * k;
       bw_load_t<D>(qt, ldsT + t * 1024, t, bh, Np, i * BW_Q, col, hi);
     }
   };
@@ -420,31 +429,24 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
     const float ct = __builtin_fmaxf(sQ * sK * c2, 1.17549435e-38f);   // see the forward kernel
     const bool need_mask = (q0 + BW_Q > N) || (kb + BW_K > N) || (CAUSAL && q0 < kb + BW_K - 1);
 
-    // dS of the block: element v of subtile u is query q0 + 32u + 8(v>>2) + 4hi + (v&3).
-    // The products of subtile u + 1 are interleaved with the softmax work of
-    // subtile u (one MFMA, then eight VALU instructions), so that MFMAs run
-    // under VALU work of the same wave; the masking choice is made per block.
-    float dS[NU][16];
+    // dS of this wave's two subtiles u = 2qh + uu: element v is query
+    // q0 + 32u + 8(v>>2) + 4hi + (v&3); the masking choice is made per block
+    float dS[2][16];
     float dm = 0.0f;
-    auto products = [&](int u, v16i& sacc, v16f& dp) {
-      sacc = v16i{};
-#pragma unroll
-      for (int s = 0; s < NKS; ++s)
-        sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(
-            *reinterpret_cast<const v4i*>(L + T::QA_OFF + (u * NKS + s) * 1024 + lane * 16), kreg[s], sacc, 0, 0, 0);
-      dp = v16f{};
-#pragma unroll
-      for (int s = 0; s < NKS16; ++s)
-        dp = mfma16<BF16>(*reinterpret_cast<const v4i*>(L + T::GA_OFF + (u * NKS16 + s) * 1024 + lane * 16), vreg[s], dp);
-    };
     auto phase1 = [&](auto MASK_) {
       constexpr bool MASK = decltype(MASK_)::value != 0;
-      v16i sacc[2];
-      v16f dp[2];
-      products(0, sacc[0], dp[0]);
-      static_for<NU>([&](auto U_) {
-        constexpr int u = decltype(U_)::value;
-        if constexpr (u + 1 < NU) products(u + 1, sacc[(u + 1) & 1], dp[(u + 1) & 1]);
+#pragma unroll
+      for (int uu = 0; uu < 2; ++uu) {
+        const int u = 2 * qh + uu;
+        v16i sacc = v16i{};
+#pragma unroll
+        for (int s = 0; s < NKS; ++s)
+          sacc = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+              *reinterpret_cast<const v4i*>(L + T::QA_OFF + (u * NKS + s) * 1024 + lane * 16), kreg[s], sacc, 0, 0, 0);
+        v16f dp = v16f{};
+#pragma unroll
+        for (int s = 0; s < NKS16; ++s)
+          dp = mfma16<BF16>(*reinterpret_cast<const v4i*>(L + T::GA_OFF + (u * NKS16 + s) * 1024 + lane * 16), vreg[s], dp);
         const float* lbr = reinterpret_cast<const float*>(L + T::LD_OFF) + 32 * u + 4 * hi;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
@@ -453,23 +455,15 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int e = 4 * g + r;
-            float x = __builtin_fmaf((float)sacc[u & 1][e], ct, -l4[r]);
+            float x = __builtin_fmaf((float)sacc[e], ct, -l4[r]);
             if constexpr (MASK) x = bw_mask<CAUSAL>(x, q0 + 32 * u + 4 * hi + 8 * g + r, key, N);
             const float p = __builtin_amdgcn_exp2f(x);
-            const float y = p * (dp[u & 1][e] - d4[r]);
-            dS[u][e] = y;
+            const float y = p * (dp[e] - d4[r]);
+            dS[uu][e] = y;
             dm = __builtin_fmaxf(dm, __builtin_fabsf(y));
           }
         }
-        if constexpr (u + 1 < NU) {
-#pragma unroll
-          for (int m = 0; m < NKS + NKS16; ++m) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
-          }
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      });
+      }
     };
     if (need_mask) phase1(ic<1>{});
     else phase1(ic<0>{});
@@ -479,32 +473,33 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
     if (i + 1 < nqb) bw_wait_vm<T::AJ>();
     else bw_wait_all();
     __syncthreads();
-    dm = __builtin_fmaxf(__builtin_fmaxf(red[a][0], red[a][1]), __builtin_fmaxf(red[a][2], red[a][3]));
+    dm = 0.0f;
+#pragma unroll
+    for (int w = 0; w < BW_DK_WAVES; ++w) dm = __builtin_fmaxf(dm, red[a][w]);
     const float sdS = dm / 127.0f, rdS = dm > 0.0f ? 1.0f / sdS : 0.0f;
 
-    v4i sc[NU];
 #pragma unroll
-    for (int u = 0; u < NU; ++u) sc[u] = bw_codes(dS[u], rdS);
-    if constexpr (STORE_DS) {
-      // codes: byte e = 4g + r of sc[u] is query 32u + 8g + 4hi + r and key
-      // 32 wave + col; after the quad transpose this lane holds query
-      // 32u + 8g + 4hi + (col & 3) for keys 4 (col >> 2) + [0, 4)
-#pragma unroll
-      for (int u = 0; u < NU; ++u)
+    for (int uu = 0; uu < 2; ++uu) {
+      const int u = 2 * qh + uu;
+      const v4i sc = bw_codes(dS[uu], rdS);
+      *reinterpret_cast<v4i*>(cx + (kg * NU + u) * 1024 + lane * 16) = sc;
+      if constexpr (STORE_DS) {
+        // codes: byte e = 4g + r of sc is query 32u + 8g + 4hi + r and key
+        // 32 kg + col; after the quad transpose this lane holds query
+        // 32u + 8g + 4hi + (col & 3) for keys 4 (col >> 2) + [0, 4)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const uint32_t t = quad_byte_transpose((uint32_t)sc[u][g], lane);
+          const uint32_t t = quad_byte_transpose((uint32_t)sc[g], lane);
           const int m = col >> 2, lq = 8 * g + 4 * hi + (col & 3) + 32 * (m & 1);
-          *reinterpret_cast<uint32_t*>(dsl + (u * 4 + wave) * 1024 + lq * 16 + 4 * (m >> 1)) = t;
+          *reinterpret_cast<uint32_t*>(dsl + (u * 4 + kg) * 1024 + lq * 16 + 4 * (m >> 1)) = t;
         }
-      // row sums of dS over this wave's 32 keys: a butterfly over the 32 lanes
-      // that share hi (partners lane ^ 16, row rotation by 8, half-row mirror,
-      // quad swaps), after which lanes 2e and 2e + 1 hold the sum of element e
-#pragma unroll
-      for (int u = 0; u < NU; ++u) {
+        // row sums of dS over this wave's 32 keys: a butterfly over the 32
+        // lanes that share hi (partners lane ^ 16, row rotation by 8, half-row
+        // mirror, quad swaps), after which lanes 2e and 2e + 1 hold the sum of
+        // element e
         float x[16];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) x[e] = dS[u][e];
+        for (int e = 0; e < 16; ++e) x[e] = dS[uu][e];
         bw_fold<8, -1>(x, (col & 16) != 0);
         bw_fold<4, 0x128>(x, (col & 8) != 0);      // row_ror:8
         bw_fold<2, 0x141>(x, (col & 4) != 0);      // row_half_mirror
@@ -512,27 +507,31 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
         const float sum = x[0] + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x[0]), 0xB1, 0xF, 0xF, true));
         if ((col & 1) == 0) {
           const int e = col >> 1;
-          red2[wave * BW_Q + 32 * u + 8 * (e >> 2) + 4 * hi + (e & 3)] = sum;
+          red2[kg * BW_Q + 32 * u + 8 * (e >> 2) + 4 * hi + (e & 3)] = sum;
         }
       }
     }
+    __syncthreads();                               // every wave's codes (and, storing dS^, its staging) are in LDS
+    v4i cs[NU];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) cs[u] = *reinterpret_cast<const v4i*>(cx + (kg * NU + u) * 1024 + lane * 16);
     const float fk = (sdS * sQ) * rsd;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
+    for (int h = 0; h < NH; ++h) {
+      const int db = qh * NH + h;
       v16i dki = v16i{};
 #pragma unroll
       for (int u = 0; u < NU; ++u)
         dki = __builtin_amdgcn_mfma_i32_32x32x32_i8(*reinterpret_cast<const v4i*>(ldsT + (db * 4 + u) * 1024 + lane * 16),
-                                                    sc[u], dki, 0, 0, 0);
+                                                    cs[u], dki, 0, 0, 0);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) dka[db][e] = __builtin_fmaf((float)dki[e], fk, dka[db][e]);
+      for (int e = 0; e < 16; ++e) dka[h][e] = __builtin_fmaf((float)dki[e], fk, dka[h][e]);
     }
     if constexpr (STORE_DS) {
-      __syncthreads();                             // every wave's codes and row sums are staged
       const size_t pair = ((size_t)lbh * nqb + i) * nkb + kblk;
 #pragma unroll
-      for (int b4 = 0; b4 < 4; ++b4) {
-        const int b = wave * 4 + b4;
+      for (int b2 = 0; b2 < 16 / BW_DK_WAVES; ++b2) {
+        const int b = wave * (16 / BW_DK_WAVES) + b2;
         *reinterpret_cast<v4i*>(dsc + (pair * 16 + b) * 1024 + lane * 16) =
             *reinterpret_cast<const v4i*>(dsl + b * 1024 + lane * 16);
       }
@@ -544,14 +543,14 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dk_kernel(
     }
   }
 
-  // dK^T: lane holds key kb + 32 wave + col and channels 32db + 8g + 4hi + r
+  // dK^T: lane holds key kb + 32 kg + col and channels 32db + 8g + 4hi + r
   if (key < N) {
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+    for (int h = 0; h < NH; ++h)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const size_t idx = ((size_t)bh * N + key) * D + 32 * db + 8 * g + 4 * hi;
-        *reinterpret_cast<float4*>(dk + idx) = make_float4(dka[db][4 * g], dka[db][4 * g + 1], dka[db][4 * g + 2], dka[db][4 * g + 3]);
+        const size_t idx = ((size_t)bh * N + key) * D + 32 * (qh * NH + h) + 8 * g + 4 * hi;
+        *reinterpret_cast<float4*>(dk + idx) = make_float4(dka[h][4 * g], dka[h][4 * g + 1], dka[h][4 * g + 2], dka[h][4 * g + 3]);
       }
   }
 }
@@ -860,7 +859,8 @@ static hipError_t launch_bwd_t(const int8_t* qc, const float* qs, const int8_t* 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (G <= 0) {                                    // no room to store dS^: dQ recomputes it
-    hipLaunchKernelGGL((attn_i8_bwd_dk_kernel<D, CAUSAL, BF16, false>), dim3((unsigned)nkb, (unsigned)BH), dim3(256), 0,
+    hipLaunchKernelGGL((attn_i8_bwd_dk_kernel<D, CAUSAL, BF16, false>), dim3((unsigned)nkb, (unsigned)BH),
+                       dim3(64 * BW_DK_WAVES), 0,
                        st, qc, qs, qt, kc, ks, v, dout, drow, lb, dk, nullptr, nullptr, nullptr, N, Np, nqb, 0, c2, rsd);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -870,7 +870,8 @@ static hipError_t launch_bwd_t(const int8_t* qc, const float* qs, const int8_t* 
   }
   for (int h0 = 0; h0 < BH; h0 += G) {             // groups of G heads share the stored dS^
     const int g = min(G, BH - h0);
-    hipLaunchKernelGGL((attn_i8_bwd_dk_kernel<D, CAUSAL, BF16, true>), dim3((unsigned)nkb, (unsigned)g), dim3(256), 0,
+    hipLaunchKernelGGL((attn_i8_bwd_dk_kernel<D, CAUSAL, BF16, true>), dim3((unsigned)nkb, (unsigned)g),
+                       dim3(64 * BW_DK_WAVES), 0,
                        st, qc, qs, qt, kc, ks, v, dout, drow, lb, dk, dsc, dss, drs, N, Np, nqb, h0, c2, rsd);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
