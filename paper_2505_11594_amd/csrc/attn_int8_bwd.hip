@@ -735,21 +735,22 @@ __global__ __launch_bounds__(256, 1) void attn_i8_bwd_dq_kernel(
 // dQ^T += (K^T dS^T) s_dS s_K / sqrt(D) + rowsum(dS) K_m / sqrt(D), with the
 // pair's codes, s_dS and row sums read back instead of recomputing S, dP and
 // dS.  A workgroup owns 128 queries (4 waves x 32); each KV block's K^T
-// operand blocks and the pair's 16 dS^ operand blocks are staged in LDS one
-// block ahead.  Heads are bh0 + blockIdx.y; the stored arrays are indexed by
-// blockIdx.y.
+// operand blocks are staged in LDS one block ahead, and each wave loads its
+// own four dS^ operand blocks (1 KiB each, contiguous) straight into
+// registers one block ahead.  Heads are bh0 + blockIdx.y; the stored arrays
+// are indexed by blockIdx.y.
 // ---------------------------------------------------------------------------
 template <int D>
 struct BwQdsLds {
   static constexpr int NDB = D / 32, NT = BW_K / 32;
-  static constexpr int NKT = NDB * NT, NDS = (BW_Q / 32) * NT;
-  static constexpr int KT_OFF = 0, DS_OFF = NKT * 1024, BYTES = DS_OFF + NDS * 1024;
-  static constexpr int J = (NKT + NDS) / 4;
-  static_assert((NKT + NDS) % 4 == 0, "even split over 4 waves");
+  static constexpr int NKT = NDB * NT;
+  static constexpr int BYTES = NKT * 1024;
+  static constexpr int J = NKT / 4;
+  static_assert(NKT % 4 == 0, "even split over 4 waves");
 };
 
 template <int D, bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void attn_i8_bwd_dq_ds_kernel(
+__global__ __launch_bounds__(256, 3) void attn_i8_bwd_dq_ds_kernel(
     const float* __restrict__ ks, const int8_t* __restrict__ kt, const int8_t* __restrict__ dsc,
     const float* __restrict__ dss, const float* __restrict__ drs, const float* __restrict__ kmean,
     float* __restrict__ dq, int N, int Np, int nqb, int bh0, float rsd) {
@@ -771,28 +772,33 @@ __global__ __launch_bounds__(256, 2) void attn_i8_bwd_dq_ds_kernel(
   auto issue = [&](int j, int buf) {
     const int kb = j * BW_K;
     uint8_t* L = lds[buf];
-    const int8_t* dpair = dsc + (((size_t)lbh * nqb + i) * nkbt + j) * (size_t)(T::NDS * 1024);
 #pragma unroll
     for (int k = 0; k < T::J; ++k) {
-      const int b = wave + 4 * k;
-      if (b < T::NKT) {
-        const int db = b / NT, t = b % NT;
-        bw_lds_load16(kt + ((size_t)bh * D + 32 * db + col) * Np + kb + 32 * t + 16 * hi, L + T::KT_OFF + b * 1024);
-      } else {
-        const int d = b - T::NKT;
-        bw_lds_load16(dpair + d * 1024 + lane * 16, L + T::DS_OFF + d * 1024);
-      }
+      const int b = wave + 4 * k, db = b / NT, t = b % NT;
+      bw_lds_load16(kt + ((size_t)bh * D + 32 * db + col) * Np + kb + 32 * t + 16 * hi, L + b * 1024);
     }
+  };
+  // this wave's dS^ operand blocks (query group `wave`, key subtiles 0..NT-1) of pair (i, j)
+  auto load_ds = [&](int j, v4i (&d)[NT]) {
+    const int8_t* p = dsc + ((((size_t)lbh * nqb + i) * nkbt + j) * (size_t)((BW_Q / 32) * NT) + wave * NT) * 1024 +
+                      lane * 16;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) d[t] = *reinterpret_cast<const v4i*>(p + t * 1024);
   };
 
   int nkb = nkbt;
   if (CAUSAL) nkb = min(nkb, min(q0 + BW_Q - 1, N - 1) / BW_K + 1);
+  v4i dcur[NT], dnext[NT];
   issue(0, 0);
+  load_ds(0, dcur);
   for (int j = 0; j < nkb; ++j) {
     const int buf = j & 1;
     bw_wait_all();
     __syncthreads();                               // block j has landed; every wave is done with block j - 1
-    if (j + 1 < nkb) issue(j + 1, buf ^ 1);
+    if (j + 1 < nkb) {
+      issue(j + 1, buf ^ 1);
+      load_ds(j + 1, dnext);
+    }
     const uint8_t* L = lds[buf];
     const float sK = ks[(size_t)bh * nkbt + j];
     const float sdS = dss[((size_t)lbh * nqb + i) * nkbt + j];
@@ -803,9 +809,8 @@ __global__ __launch_bounds__(256, 2) void attn_i8_bwd_dq_ds_kernel(
       v16i dqi = v16i{};
 #pragma unroll
       for (int t = 0; t < NT; ++t)
-        dqi = __builtin_amdgcn_mfma_i32_32x32x32_i8(
-            *reinterpret_cast<const v4i*>(L + T::KT_OFF + (db * NT + t) * 1024 + lane * 16),
-            *reinterpret_cast<const v4i*>(L + T::DS_OFF + (wave * NT + t) * 1024 + lane * 16), dqi, 0, 0, 0);
+        dqi = __builtin_amdgcn_mfma_i32_32x32x32_i8(*reinterpret_cast<const v4i*>(L + (db * NT + t) * 1024 + lane * 16),
+                                                    dcur[t], dqi, 0, 0, 0);
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const v4f km = *reinterpret_cast<const v4f*>(kms + 32 * db + 8 * g + 4 * hi);
@@ -818,6 +823,8 @@ __global__ __launch_bounds__(256, 2) void attn_i8_bwd_dq_ds_kernel(
         }
       }
     }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) dcur[t] = dnext[t];
   }
   if (qi < N) {
 #pragma unroll
