@@ -23,8 +23,8 @@
 // fl32(fl32(s_Q s_K) log2(e)/sqrt(D)), acc the exact int32 product: the tile
 // max is taken on fl32(acc) (the rounding is monotone, so it is the max of
 // u), P^ = rint(127 2^{u - t}) = rint(exp2(fma(acc, c_t, log2 127 - t)))
-// with the rounding done by one add of 1.5 * 2^23 (the code is the low byte
-// of the sum), and the unquantized P~ = s_P P^ is summed into l.  Each tile's
+// with the rounding done by v_cvt_pk_u8_f32 (nearest even, packed a byte at
+// a time), and the unquantized P~ = s_P P^ is summed into l.  Each tile's
 // int32 P.V product is folded into the fp32 O with one fused multiply-add by
 // s_P s_V after O is rescaled by alpha = 2^{m_old - m_new} (skipped when the
 // whole wave has alpha = 1).
@@ -44,7 +44,6 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 namespace sage {
 
 constexpr int I8_AQ = 128;   // queries per workgroup (4 waves x 32)
-constexpr float kI8RoundMagic = 12582912.0f;   // 1.5 * 2^23
 
 __device__ __forceinline__ void i8_lds_load16(const void* src, void* dst) {
   __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
@@ -54,11 +53,13 @@ __device__ __forceinline__ void i8_lds_load4(const void* src, void* dst) {
 }
 __device__ __forceinline__ void i8_wait_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
 
-// low bytes of four rounded values, packed (element 0 in the low byte)
-__device__ __forceinline__ int i8_pack4(float a, float b, float c, float d) {
-  const uint32_t ab = __builtin_amdgcn_perm(__float_as_uint(b), __float_as_uint(a), 0x0C0C0400u);
-  const uint32_t cd = __builtin_amdgcn_perm(__float_as_uint(d), __float_as_uint(c), 0x0C0C0400u);
-  return (int)__builtin_amdgcn_perm(cd, ab, 0x05040100u);
+// rint of four values in [0, 255], packed (element 0 in the low byte):
+// v_cvt_pk_u8_f32 rounds to nearest even and clamps to [0, 255]
+__device__ __forceinline__ int i8_codes4(float a, float b, float c, float d) {
+  uint32_t w = __builtin_amdgcn_cvt_pk_u8_f32(a, 0, 0u);
+  w = __builtin_amdgcn_cvt_pk_u8_f32(b, 1, w);
+  w = __builtin_amdgcn_cvt_pk_u8_f32(c, 2, w);
+  return (int)__builtin_amdgcn_cvt_pk_u8_f32(d, 3, w);
 }
 
 template <int D, int BKV>
@@ -248,7 +249,7 @@ __global__ __launch_bounds__(256, 2) void attn_int8_kernel(
             p[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sf[u][4 * g + r], ct, bias));
             ps[r] += p[r];
           }
-          w[g] = i8_pack4(p[0] + kI8RoundMagic, p[1] + kI8RoundMagic, p[2] + kI8RoundMagic, p[3] + kI8RoundMagic);
+          w[g] = i8_codes4(p[0], p[1], p[2], p[3]);
         }
         pw[u] = v4i{w[0], w[1], w[2], w[3]};
       }

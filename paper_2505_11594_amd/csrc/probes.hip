@@ -4,6 +4,7 @@
 //   - v_cvt_scalef32_pk_fp4_f32: FP4 E2M1 rounding (nearest even), saturation
 //     at +-6, the sign of zero, and division by the power-of-two scale;
 //   - v_exp_f32: its error against the correctly rounded exp2;
+//   - v_cvt_pk_u8_f32: its rounding (nearest even) and clamping to [0, 255];
 //   - the register layouts of v_mfma_scale_f32_32x32x64_f8f6f4 (FP4 operands,
 //     E8M0 scales), v_mfma_i32_32x32x32_i8 and v_mfma_f32_32x32x16_bf16: lane
 //     l supplies row / column l%32 and a contiguous run of the reduction index
@@ -30,6 +31,11 @@ __global__ __launch_bounds__(256) void cvt_fp4_kernel(const float* __restrict__ 
   const uint32_t b = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, x[2 * p], x[2 * p + 1], scale, 0) & 0xFFu;
   codes[2 * p] = (uint8_t)(b & 0xF);
   codes[2 * p + 1] = (uint8_t)(b >> 4);
+}
+
+__global__ __launch_bounds__(256) void cvt_u8_kernel(const float* __restrict__ x, uint8_t* __restrict__ y, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] = (uint8_t)(__builtin_amdgcn_cvt_pk_u8_f32(x[i], 0, 0u) & 0xFFu);
 }
 
 __global__ __launch_bounds__(256) void exp2_kernel(const float* __restrict__ x, float* __restrict__ y, int n) {
@@ -105,6 +111,13 @@ int sage_probe_cvt_fp4(const float* x, uint8_t* codes, int n, float scale, hipSt
   if (!x || !codes || n < 2 || (n & 1)) return 1;
   const int np = n / 2;
   hipLaunchKernelGGL(cvt_fp4_kernel, dim3((unsigned)((np + 255) / 256)), dim3(256), 0, stream, x, codes, np, scale);
+  return st(hipGetLastError());
+}
+
+// y: n bytes, the byte v_cvt_pk_u8_f32 makes of x[i]
+int sage_probe_cvt_u8(const float* x, uint8_t* y, int n, hipStream_t stream) {
+  if (!x || !y || n < 1) return 1;
+  hipLaunchKernelGGL(cvt_u8_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, x, y, n);
   return st(hipGetLastError());
 }
 

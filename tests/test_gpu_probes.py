@@ -8,6 +8,7 @@ checked against independent CPU definitions.
   use: its error must stay within the 8-ulp window inside which the oracle
   treats an FP4 or INT8 code of P as tie-ambiguous; and it must never decrease
   its output as its argument grows, on every fp32 in [-130, 0];
+- v_cvt_pk_u8_f32 against rint with clamping to [0, 255];
 - the register layouts of the FP4 block-scaled, int8 and bf16 32x32 MFMAs
   against numpy products (and, for FP4, the oracle's exact FP4MM).
 """
@@ -35,6 +36,7 @@ def P():
     vp = ctypes.c_void_p
     L.sage_probe_cvt_fp4.argtypes = [vp, vp, ctypes.c_int, ctypes.c_float, vp]
     L.sage_probe_exp2.argtypes = [vp, vp, ctypes.c_int, vp]
+    L.sage_probe_cvt_u8.argtypes = [vp, vp, ctypes.c_int, vp]
     L.sage_probe_mfma_fp4.argtypes = [vp] * 6
     L.sage_probe_mfma_i8.argtypes = [vp] * 4
     L.sage_probe_mfma_bf16.argtypes = [vp] * 4
@@ -101,6 +103,19 @@ def test_exp2_is_monotone_on_every_fp32_in_minus130_0(P):
         prev = float(yd[-1])
         del mag, xd, yd
     assert prev == 0.0 or prev < 2.0 ** -126
+
+
+def test_cvt_pk_u8_rounds_to_nearest_even_and_clamps(P):
+    # the 8-bit forward forms its P codes rint(127 2^{u-t}) with this convert
+    torch = torch_dev()
+    x = np.arange(-64, 4160, dtype=np.float64) / 16.0                  # -4 .. 260 in steps of 1/16, ties included
+    x = np.concatenate([x, [0.49999997, 0.50000006, 126.49999, 126.5, 127.5, 254.5, 255.49998, 1e6, -1e6, -0.0]])
+    x = x.astype(np.float32)
+    xd = torch.from_numpy(x).cuda()
+    yd = torch.empty(x.size, dtype=torch.uint8, device="cuda")
+    run(P.sage_probe_cvt_u8, dptr(xd), dptr(yd), x.size)
+    want = np.clip(np.rint(x.astype(np.float64)), 0, 255).astype(np.uint8)   # numpy rint: nearest even
+    assert np.array_equal(yd.cpu().numpy(), want)
 
 
 def fp4_case(seed, lo, hi):
