@@ -89,6 +89,20 @@ __device__ __forceinline__ void bw_fold(float (&x)[16], bool upper) {
   }
 }
 
+// 16 values in [0, 127 (1 + 2^-20)] -> 16 codes rint(x r): v_cvt_pk_u8_f32
+// rounds to nearest even (the same integer as the magic-number add above)
+__device__ __forceinline__ v4i bw_codes_u(const float (&x)[16], float r) {
+  int w[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    uint32_t t = __builtin_amdgcn_cvt_pk_u8_f32(x[4 * g] * r, 0, 0u);
+    t = __builtin_amdgcn_cvt_pk_u8_f32(x[4 * g + 1] * r, 1, t);
+    t = __builtin_amdgcn_cvt_pk_u8_f32(x[4 * g + 2] * r, 2, t);
+    w[g] = (int)__builtin_amdgcn_cvt_pk_u8_f32(x[4 * g + 3] * r, 3, t);
+  }
+  return v4i{w[0], w[1], w[2], w[3]};
+}
+
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) x = __builtin_fmaxf(x, __shfl_xor(x, off, 64));
@@ -288,7 +302,7 @@ __global__ __launch_bounds__(256, 2) void attn_i8_bwd_dv_kernel(
       float P[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) P[e] = __builtin_amdgcn_exp2f(arg[u][e]);
-      pc[u] = bw_codes(P, rP);
+      pc[u] = bw_codes_u(P, rP);
     }
     const float fv = sP * gs[(size_t)bh * nqb + i];
 #pragma unroll
