@@ -59,14 +59,25 @@ __global__ __launch_bounds__(KM_THREADS) void kmean_partial_kernel(const uint16_
   }
 }
 
-// Pass 2: mu = fl32(fl64(sum) / N).
+// Pass 2: mu = fl32(fl64(sum) / N).  One workgroup per (b,h): 256 / D
+// threads per channel sum strided chunks, then one of them adds the partial
+// sums (exact in fp64, so the order does not matter).
 template <int D>
-__global__ void kmean_final_kernel(const double* __restrict__ part, float* __restrict__ mu, int N, int nchunk) {
-  const int bh = blockIdx.x, c = threadIdx.x;
-  if (c >= D) return;
+__global__ __launch_bounds__(256) void kmean_final_kernel(const double* __restrict__ part, float* __restrict__ mu,
+                                                          int N, int nchunk) {
+  constexpr int TPC = 256 / D;
+  const int bh = blockIdx.x, tid = threadIdx.x, c = tid % D, k = tid / D;
   double s = 0.0;
-  for (int j = 0; j < nchunk; ++j) s += part[((size_t)bh * nchunk + j) * D + c];
-  mu[(size_t)bh * D + c] = (float)(s / (double)N);
+  for (int j = k; j < nchunk; j += TPC) s += part[((size_t)bh * nchunk + j) * D + c];
+  __shared__ double red[256];
+  red[tid] = s;
+  __syncthreads();
+  if (k == 0) {
+    double t = 0.0;
+#pragma unroll
+    for (int i = 0; i < TPC; ++i) t += red[i * D + c];
+    mu[(size_t)bh * D + c] = (float)(t / (double)N);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -294,9 +305,6 @@ template <int D, bool BF16, int FMT>
 __global__ __launch_bounds__(256) void quant_v_kernel(const uint16_t* __restrict__ v, uint8_t* __restrict__ codes,
                                                       uint8_t* __restrict__ scales, int N, int Np) {
   constexpr int NB = (FMT == kFmtMX) ? 32 : 16;
-  constexpr int TPC = 256 / D;               // threads per channel: 2 (D=128) or 4 (D=64)
-  constexpr int BPT = VT / NB / TPC;         // token blocks per thread
-  static_assert(BPT >= 1, "tile shape");
   // all lanes of a wave read one row (consecutive channels): no padding needed
   __shared__ uint16_t tile[VT][D];
   // Workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous
@@ -321,45 +329,63 @@ __global__ __launch_bounds__(256) void quant_v_kernel(const uint16_t* __restrict
     *reinterpret_cast<uint4*>(&tile[r][cu * 8]) = raw;
   }
   __syncthreads();
-  const int c = tid % D, part = tid / D;
-  uint8_t* crow = codes + ((size_t)bh * D + c) * (Np / 2);
-  uint8_t* srow = scales + ((size_t)bh * D + c) * (Np / NB);
+  // each thread quantizes CPT adjacent channels of BPT token blocks (one
+  // 32-bit LDS read per token for two channels)
+  constexpr int CPT = (D == 128) ? 2 : 1;
+  constexpr int TPG = 256 / (D / CPT);       // threads per channel group
+  constexpr int BPT = VT / NB / TPG;         // token blocks per thread
+  static_assert(BPT >= 1 && TPG * (D / CPT) == 256, "tile shape");
+  const int c0 = (tid % (D / CPT)) * CPT, part = tid / (D / CPT);
 #pragma unroll
   for (int bb = 0; bb < BPT; ++bb) {
     const int blk = part * BPT + bb;         // token block inside the tile
     if (t0 + blk * NB >= Np) break;          // the last tile may end at Np (a multiple of 128)
-    float x[NB];
-    float am = 0.0f;
+    float x[CPT][NB];
+    float am[CPT];
+#pragma unroll
+    for (int k = 0; k < CPT; ++k) am[k] = 0.0f;
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       const int r = blk * NB + j;
-      x[j] = (t0 + r < N) ? widen<BF16>(tile[r][c]) : 0.0f;
-      am = __builtin_fmaxf(am, __builtin_fabsf(x[j]));
+      const bool in = t0 + r < N;
+      if constexpr (CPT == 2) {
+        const uint32_t two = *reinterpret_cast<const uint32_t*>(&tile[r][c0]);
+        x[0][j] = in ? widen<BF16>((uint16_t)(two & 0xFFFFu)) : 0.0f;
+        x[1][j] = in ? widen<BF16>((uint16_t)(two >> 16)) : 0.0f;
+      } else {
+        x[0][j] = in ? widen<BF16>(tile[r][c0]) : 0.0f;
+      }
+#pragma unroll
+      for (int k = 0; k < CPT; ++k) am[k] = __builtin_fmaxf(am[k], __builtin_fabsf(x[k][j]));
     }
-    uint32_t sbyte;
-    if (FMT == kFmtMX) {
-      const int e = e8m0_exponent(am);
-      sbyte = (uint32_t)(e + 127);
 #pragma unroll
-      for (int j = 0; j < NB; ++j) x[j] = __builtin_ldexpf(x[j], -e);
-    } else {
-      sbyte = e4m3_encode(am / 6.0f);
-      const float s = e4m3_decode(sbyte);
-      const float r = (s == 0.0f) ? 0.0f : 1.0f / s;
+    for (int k = 0; k < CPT; ++k) {
+      uint32_t sbyte;
+      if (FMT == kFmtMX) {
+        const int e = e8m0_exponent(am[k]);
+        sbyte = (uint32_t)(e + 127);
 #pragma unroll
-      for (int j = 0; j < NB; ++j) x[j] = (s == 0.0f) ? 0.0f : x[j] * r;
+        for (int j = 0; j < NB; ++j) x[k][j] = __builtin_ldexpf(x[k][j], -e);
+      } else {
+        sbyte = e4m3_encode(am[k] / 6.0f);
+        const float s = e4m3_decode(sbyte);
+        const float r = (s == 0.0f) ? 0.0f : 1.0f / s;
+#pragma unroll
+        for (int j = 0; j < NB; ++j) x[k][j] = (s == 0.0f) ? 0.0f : x[k][j] * r;
+      }
+      uint32_t w[NB / 8];
+#pragma unroll
+      for (int q = 0; q < NB / 8; ++q) {
+        w[q] = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) w[q] |= cvt_fp4x2(x[k][8 * q + 2 * i], x[k][8 * q + 2 * i + 1]) << (8 * i);
+      }
+      const int c = c0 + k;
+      uint8_t* dst = codes + ((size_t)bh * D + c) * (Np / 2) + (t0 + blk * NB) / 2;
+      if (NB == 32) *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+      else *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
+      scales[((size_t)bh * D + c) * (Np / NB) + (t0 + blk * NB) / NB] = (uint8_t)sbyte;
     }
-    uint32_t w[NB / 8];
-#pragma unroll
-    for (int q = 0; q < NB / 8; ++q) {
-      w[q] = 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) w[q] |= cvt_fp4x2(x[8 * q + 2 * i], x[8 * q + 2 * i + 1]) << (8 * i);
-    }
-    uint8_t* dst = crow + (t0 + blk * NB) / 2;
-    if (NB == 32) *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
-    else *reinterpret_cast<uint2*>(dst) = make_uint2(w[0], w[1]);
-    srow[(t0 + blk * NB) / NB] = (uint8_t)sbyte;
   }
 }
 
@@ -373,7 +399,7 @@ static hipError_t launch_kmean_t(const void* k, double* part, float* mu, int BH,
   const int nchunk = kmean_chunks(N);
   hipLaunchKernelGGL((kmean_partial_kernel<D, BF16>), dim3(nchunk, BH), dim3(KM_THREADS), 0, st,
                      (const uint16_t*)k, part, N, nchunk);
-  hipLaunchKernelGGL((kmean_final_kernel<D>), dim3(BH), dim3(D), 0, st, (const double*)part, mu, N, nchunk);
+  hipLaunchKernelGGL((kmean_final_kernel<D>), dim3(BH), dim3(256), 0, st, (const double*)part, mu, N, nchunk);
   return hipGetLastError();
 }
 
