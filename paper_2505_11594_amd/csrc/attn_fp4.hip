@@ -244,27 +244,27 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
           for (int v = 0; v < 16; ++v) {
             const int c = 64 * (u >> 1) + 16 * (u & 1) + v;
             const float bound = __uint_as_float(0xFF800000u ^ ((uint32_t)(c - rem) & 0x80000000u));
-            sacc[u][v] = __builtin_fminf(sacc[u][v], bound);
+            sacc[u][v] = smin(sacc[u][v], bound);
           }
       }
       // ---- tile row max (raw scores); block max is lane-local ----------
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
-        // a serial chain: the compiler fuses it into v_max3
+        // a serial chain: the compiler fuses it into v_maximum3
         float x = sacc[2 * g][0];
 #pragma unroll
-        for (int v = 1; v < 16; ++v) x = __builtin_fmaxf(x, sacc[2 * g][v]);
+        for (int v = 1; v < 16; ++v) x = smax(x, sacc[2 * g][v]);
 #pragma unroll
-        for (int v = 0; v < 16; ++v) x = __builtin_fmaxf(x, sacc[2 * g + 1][v]);
+        for (int v = 0; v < 16; ++v) x = smax(x, sacc[2 * g + 1][v]);
         bm[g] = x;
       }
       float tl = bm[0];
 #pragma unroll
-      for (int g = 1; g < NG; ++g) tl = __builtin_fmaxf(tl, bm[g]);
+      for (int g = 1; g < NG; ++g) tl = smax(tl, bm[g]);
       // row max over the two lane halves that share a query
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(tl), __float_as_uint(tl), false, false);
-      t = __builtin_fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-      m_new = __builtin_fmaxf(m, t);
+      t = smax(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+      m_new = smax(m, t);
       const float tc = t * c2;
       mc = m_new * c2;
       const float delta = tc - mc;                       // c2 (t - m_new) <= 0

@@ -204,23 +204,23 @@ __global__ __launch_bounds__(256, 2) void attn_int8_kernel(
           for (int v = 0; v < 16; ++v) {
             const int c = 32 * u + 8 * (v >> 2) + (v & 3);
             const float bound = __uint_as_float(0xFF800000u ^ ((uint32_t)(c - rem) & 0x80000000u));
-            sf[u][v] = __builtin_fminf(sf[u][v], bound);
+            sf[u][v] = smin(sf[u][v], bound);
           }
       }
       float x = sf[0][0];
 #pragma unroll
       for (int u = 0; u < NSUB; ++u)
 #pragma unroll
-        for (int v = (u == 0 ? 1 : 0); v < 16; ++v) x = __builtin_fmaxf(x, sf[u][v]);
+        for (int v = (u == 0 ? 1 : 0); v < 16; ++v) x = smax(x, sf[u][v]);
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-      const float amax = __builtin_fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+      const float amax = smax(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
       const float sqk = sQ * sK;
       // an all-zero Q or K block gives c_t = 0; the smallest normal fp32 in its
       // place keeps -inf scores at -inf and changes no P^ and no l (every
       // |u| is then below 2^-105, under half an ulp of log2 127)
       ct = __builtin_fmaxf(sqk * c2, 1.17549435e-38f);
       const float t = amax * ct;                       // tile max of u
-      const float m_new = __builtin_fmaxf(m, t);
+      const float m_new = smax(m, t);
       alpha = __builtin_amdgcn_exp2f(m - m_new);       // 0 on the first tile (m = -inf)
       const float rho = __builtin_amdgcn_exp2f(t - m_new);
       sP = rho / 127.0f;                               // correctly rounded, as the oracle

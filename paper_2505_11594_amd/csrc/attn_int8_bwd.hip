@@ -194,7 +194,7 @@ template <bool CAUSAL>
 __device__ __forceinline__ float bw_mask(float arg, int q, int key, int N) {
   int m = (q - N) & (key - N);
   if (CAUSAL) m &= ~(q - key);
-  return __builtin_fminf(arg, __uint_as_float(0xFF800000u ^ ((uint32_t)m & 0x80000000u)));
+  return smin(arg, __uint_as_float(0xFF800000u ^ ((uint32_t)m & 0x80000000u)));
 }
 
 // ---------------------------------------------------------------------------

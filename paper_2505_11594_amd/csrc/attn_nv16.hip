@@ -214,7 +214,7 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const float bound = __uint_as_float(0xFF800000u ^ ((uint32_t)(32 * t + v - rem) & 0x80000000u));
-            sacc[t][v] = __builtin_fminf(sacc[t][v], bound);
+            sacc[t][v] = smin(sacc[t][v], bound);
           }
       }
       float bm[NSUB];

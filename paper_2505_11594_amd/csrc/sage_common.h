@@ -95,4 +95,10 @@ __device__ __forceinline__ uint32_t cvt_fp4x2(float a, float b) {
 
 __device__ __forceinline__ float fmax3(float a, float b, float c) { return __builtin_fmaxf(a, __builtin_fmaxf(b, c)); }
 
+// Maximum / minimum of two scores or bounds (finite or +-inf, never NaN): the
+// IEEE maximum and minimum, which unlike fmaxf / fminf need no NaN-quieting of
+// their operands (v_maximum3_f32, v_minimum3_f32).
+__device__ __forceinline__ float smax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float smin(float a, float b) { return __builtin_elementwise_minimum(a, b); }
+
 }  // namespace sage
