@@ -151,16 +151,17 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
   auto issue = [&](int j, int stage) {
     const int kb = j * BKV;
     uint8_t* L = lds[stage];
-    const uint8_t* kt = kbase + (size_t)kb * (D / 2);
-    const uint8_t* vt = vbase + kb / 2;
+    // a head's base in SGPRs plus a 32-bit lane offset that carries the tile
+    // offset (one 32-bit add per load, no 64-bit address arithmetic)
+    const uint32_t kto = (uint32_t)kb * (D / 2), vto = (uint32_t)kb / 2;
 #pragma unroll
     for (int i = 0; i < KJ; ++i)
       if (T::NKB % 4 == 0 || wave + 4 * i < T::NKB)
-        lds_load16(kt + ko[i], L + T::KC_OFF + (wave + 4 * i) * 1024);
+        lds_load16(kbase + (ko[i] + kto), L + T::KC_OFF + (wave + 4 * i) * 1024);
 #pragma unroll
     for (int i = 0; i < VJ; ++i)
       if (T::NVB % 4 == 0 || wave + 4 * i < T::NVB)
-        lds_load16(vt + vo[i], L + T::VC_OFF + (wave + 4 * i) * 1024);
+        lds_load16(vbase + (vo[i] + vto), L + T::VC_OFF + (wave + 4 * i) * 1024);
     if (ks_job) {
       if (ks_lane)
         lds_load4(ksbase + (size_t)kb * (D / 32) + so, L + T::KS_OFF + wave * 256);
@@ -292,6 +293,8 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
         const int tt = 2 * g + half;
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
+          // the four converts write all four bytes, so the word starts from the
+          // bits of the first value rather than from a zero
           uint32_t word = 0;
           static_for<4>([&](auto I_) {
             constexpr int i = decltype(I_)::value;
@@ -299,6 +302,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
             const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[tt][8 * q + 2 * i + 1], c2, bias));
             ps[(2 * half + q) & 3] += p0;
             ps[(2 * half + q) & 3] += p1;
+            if constexpr (i == 0) word = __float_as_uint(p0);
             word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, p0, p1, escale, i);
           });
           w[2 * half + q] = word;

@@ -258,7 +258,9 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
             const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v + 1], c2, bias));
             ps[i & 1] += p0;
             ps[i & 1] += p1;
-            const uint32_t code = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, p0 * r, p1 * r, 1.0f, 0);
+            // byte 0 gets the two codes; the other bytes are never read
+            const float y0 = p0 * r;
+            const uint32_t code = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(__float_as_uint(y0), y0, p1 * r, 1.0f, 0);
             const auto dq = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(code, 1.0f, 0);
             typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
             const v2bf pb = {(__bf16)(dq[0] * s2k), (__bf16)(dq[1] * s2k)};

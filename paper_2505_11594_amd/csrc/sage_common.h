@@ -90,7 +90,7 @@ __device__ __forceinline__ float e4m3_decode(uint32_t b) {
 // Inputs here are already scaled, so the scale is 1.0.  Returns the byte with
 // a in the low nibble and b in the high nibble.
 __device__ __forceinline__ uint32_t cvt_fp4x2(float a, float b) {
-  return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, a, b, 1.0f, 0) & 0xFFu;
+  return __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(__float_as_uint(a), a, b, 1.0f, 0) & 0xFFu;   // byte 0 only
 }
 
 __device__ __forceinline__ float fmax3(float a, float b, float c) { return __builtin_fmaxf(a, __builtin_fmaxf(b, c)); }
