@@ -186,8 +186,9 @@ def other_configs(torch, bd, wl, steps):
             fmt = bd.SAGE_FMT_MXFP4 if f == wl.FMT_MX else bd.SAGE_FMT_NV16_E4M3
             qq, kq, vq = (bd.sage_quant_fp4(x, r, fmt) for x, r in ((qd, bd.SAGE_ROLE_Q), (kd, bd.SAGE_ROLE_K),
                                                                     (vd, bd.SAGE_ROLE_V)))
+            fk = fmt | (bd.bkv_flag(w.bkv) if f == wl.FMT_MX else 0)
             run = lambda: bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (w.B, w.H, w.N, w.D), causal=w.causal,
-                                                         fmt=fmt, out=o)
+                                                         fmt=fk, out=o)
             run()
             torch.cuda.synchronize()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -332,13 +333,15 @@ def main():
     dev = torch.device("cuda:0")
     to_dev = lambda a: torch.from_numpy(a.view(np.int16)).view(dt).to(dev)
     qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)
-    fmt = bd.SAGE_FMT_MXFP4 | (bd.SAGE_IN_BF16 if w.in_dtype == wl.IN_BF16 else 0) | bd.SAGE_OUT_F32
+    tile = bd.bkv_flag(w.bkv)
+    fmt = bd.SAGE_FMT_MXFP4 | tile | (bd.SAGE_IN_BF16 if w.in_dtype == wl.IN_BF16 else 0) | bd.SAGE_OUT_F32
     ws = torch.empty(bd.attn_fp4_workspace_size(B, H, N, D, fmt), dtype=torch.uint8, device=dev)
     o = torch.empty((B, H, N, D), dtype=torch.float32, device=dev)
     ops = w.ops
 
     def step():
-        bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=bd.SAGE_FMT_MXFP4, out_f32=True, out=o, workspace=ws)
+        bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=bd.SAGE_FMT_MXFP4 | tile, out_f32=True, out=o,
+                             workspace=ws)
 
     if args.mode == "attn_int8":
         qq = bd.sage_quant_int8(qd, bd.SAGE_ROLE_Q)
@@ -369,7 +372,7 @@ def main():
         kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K)
         vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V)
         for _ in range(args.warmup + args.steps):
-            bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, out=o)
+            bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, fmt=tile, out=o)
         torch.cuda.synchronize()
         print(json.dumps({"mode": "attn", "launches": args.warmup + args.steps, "ops_per_launch": ops}))
         return
@@ -393,7 +396,7 @@ def main():
     vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V)
 
     def attn_only():
-        bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, out=o)
+        bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, fmt=tile, out=o)
 
     for _ in range(2):
         attn_only()
@@ -439,7 +442,7 @@ def main():
     smooth_q = None
     if not args.no_configs:
         # the same step with smoothing Q (query-block means, their GEMV with K', the bias added to S)
-        fmt_sq = bd.SAGE_FMT_MXFP4 | bd.SAGE_SMOOTH_Q
+        fmt_sq = bd.SAGE_FMT_MXFP4 | tile | bd.SAGE_SMOOTH_Q
         ws_sq = torch.empty(bd.attn_fp4_workspace_size(B, H, N, D, fmt_sq | bd.SAGE_IN_BF16 | bd.SAGE_OUT_F32),
                             dtype=torch.uint8, device=dev)
         step_sq = lambda: bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=fmt_sq, out_f32=True, out=o,
@@ -487,7 +490,8 @@ def main():
                    "step": "kmean + quantize Q/K/V + FP4 attention (sage_attn_fp4_fwd_ws)"},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
                      "frac": attn_tflops / PEAK_FP4_TFLOPS, "traffic": traffic_from_counters(1),
-                     "kernel": "attn_fp4_mx_kernel<128,128,false,0>", "kernel_ms": t_attn * 1e3},
+                     "kernel": ("attn_fp4_mx256_kernel<128,false,0,false>" if w.bkv == 256 else
+                                "attn_fp4_mx_kernel<%d,%d,false,0,false>" % (D, w.bkv)), "kernel_ms": t_attn * 1e3},
         "accuracy_vs_exact": acc,
         "quantize": {"ms": t_quant * 1e3, "algorithmic_GBs": quant_bytes / t_quant / 1e9,
                      "frac_of_hbm_peak": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS},

@@ -44,7 +44,8 @@ typedef enum {
 #define SAGE_NO_SMOOTH_K    0x10u /* ablation: skip K <- K - mean(K) (Algorithm 1)         */
 #define SAGE_SMOOTH_Q       0x20u /* smoothing Q (Algorithm 1), see below                   */
 #define SAGE_BKV64          0x40u /* KV tile of 64 tokens instead of 128                   */
-#define SAGE_FMT_ALL_BITS   0x7Fu
+#define SAGE_BKV256         0x80u /* KV tile of 256 tokens (MXFP4 attention only)          */
+#define SAGE_FMT_ALL_BITS   0xFFu
 
 /* ---- quantization roles ------------------------------------------------ */
 #define SAGE_ROLE_Q 0
@@ -127,6 +128,10 @@ size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt);
  * bf16 MFMA.
  * With SAGE_SMOOTH_Q the scores get the smoothing-Q GEMV term described above
  * (both formats).
+ * KV tiles (the granularity of s_P1) are 128 keys; SAGE_BKV64 takes 64,
+ * SAGE_BKV256 takes 256 (MXFP4 only: SAGE_ERR_UNSUPPORTED with NV16; both
+ * tile flags together are SAGE_ERR_INVALID_ARG).  The tile changes only the
+ * rounding of P (per-tile row maxima), not the quantized layouts.
  * Softmax scale is 1/sqrt(D).  causal = 1 keeps key j for query i iff j <= i.
  *  q, k, v  : 16-bit [B,H,N,D], 16-byte aligned
  *  o        : [B,H,N,D] fp32 (SAGE_OUT_F32) or input dtype, 16-byte aligned

@@ -19,6 +19,12 @@ SAGE_OUT_F32 = 0x8
 SAGE_NO_SMOOTH_K = 0x10
 SAGE_SMOOTH_Q = 0x20
 SAGE_BKV64 = 0x40
+SAGE_BKV256 = 0x80
+
+
+def bkv_flag(bkv: int) -> int:
+    """The fmt bit that selects a KV tile of ``bkv`` keys (64, 128 or 256)."""
+    return {64: SAGE_BKV64, 128: 0, 256: SAGE_BKV256}[bkv]
 SAGE_ROLE_Q, SAGE_ROLE_K, SAGE_ROLE_V = 0, 1, 2
 
 _lib = None

@@ -372,6 +372,310 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// 256-key tiles.  The per-tile work -- the accumulator rescale (one multiply
+// per O element), the tile's softmax scalars and its block scales -- is spread
+// over twice the keys; the tile's S (128 VGPRs) takes the place of the
+// double-buffered S of the 128-key kernel, so S is computed at the top of each
+// tile and two LDS stages (load tile j + 1 while tile j runs, one barrier per
+// tile) keep two workgroups per CU.  Same per-lane layouts as above, with
+// four 64-key groups per tile.  Np is a multiple of 128: when the last tile
+// reaches past Np its upper 128 keys are loaded from its lower half (finite
+// values, masked as keys >= N).
+// ---------------------------------------------------------------------------
+template <int D, bool SQ>
+struct Fp4Stage256 {
+  static constexpr int BKV = 256;
+  static constexpr int NSUB = BKV / 32, NKS = D / 64, NDB = D / 32, NG = BKV / 64;
+  static constexpr int NKB = NSUB * NKS, NVB = NDB * NG;
+  static constexpr int KC_OFF = 0;
+  static constexpr int VC_OFF = KC_OFF + NKB * 1024;
+  static constexpr int KS_OFF = VC_OFF + NVB * 1024;     // K^ scales: BKV rows x D/32 bytes
+  static constexpr int KS_BYTES = BKV * (D / 32);
+  static constexpr int VS_OFF = KS_OFF + KS_BYTES;       // V^T scales: 8 bytes (the tile's 8 blocks) per dim row
+  static constexpr int BIAS_OFF = VS_OFF + D * 8;
+  static constexpr int BYTES = BIAS_OFF + (SQ ? BKV * 4 : 0);
+  static constexpr int NKSJ = KS_BYTES / 4 / 64, NVSJ = D * 2 / 64;   // dword-load jobs of 64 lanes
+  static constexpr int SJ = (NKSJ + NVSJ) / 4;                        // per wave
+  static_assert((NKSJ + NVSJ) % 4 == 0 && NKB % 4 == 0 && NVB % 4 == 0, "even split over 4 waves");
+};
+
+template <int D, bool CAUSAL, int OUT, bool SQ>
+__global__ __launch_bounds__(256, 2) void attn_fp4_mx256_kernel(
+    const uint8_t* __restrict__ qc, const uint8_t* __restrict__ qs, const uint8_t* __restrict__ kc,
+    const uint8_t* __restrict__ ks, const uint8_t* __restrict__ vc, const uint8_t* __restrict__ vs,
+    const float* __restrict__ qkb, void* __restrict__ o, int BH, int N, int Np, int nqt, float c2, float log6) {
+  using T = Fp4Stage256<D, SQ>;
+  constexpr int BKV = T::BKV, NSUB = T::NSUB, NKS = T::NKS, NDB = T::NDB, NG = T::NG;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2][T::BYTES];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 31, hi = lane >> 5;
+  const int total = nqt * BH;
+  int lin = blockIdx.x;
+  if ((total & 7) == 0) lin = (blockIdx.x & 7) * (total >> 3) + (blockIdx.x >> 3);
+  const long long bh = lin / nqt;
+  int qt = lin % nqt;
+  if (CAUSAL) qt = nqt - 1 - qt;
+  const int q0 = qt * AQ;
+  const int qw = q0 + wave * 32;
+  const int qi = qw + col;
+
+  v4i qreg[NKS];
+  uint32_t qsc = 0;
+  if (qi < N) {
+    const uint8_t* qrow = qc + ((size_t)bh * N + qi) * (D / 2);
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) qreg[s] = *reinterpret_cast<const v4i*>(qrow + (2 * s + hi) * 16);
+    const uint8_t* srow = qs + ((size_t)bh * N + qi) * (D / 32);
+    qsc = (D == 128) ? *reinterpret_cast<const uint32_t*>(srow) : (uint32_t)*reinterpret_cast<const uint16_t*>(srow);
+  } else {
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) qreg[s] = v4i{0, 0, 0, 0};
+  }
+  qsc >>= 8 * hi;
+
+  int ntiles = (N + BKV - 1) / BKV;
+  if (CAUSAL) ntiles = min(ntiles, min(q0 + AQ - 1, N - 1) / BKV + 1);
+
+  constexpr int KJ = T::NKB / 4, VJ = T::NVB / 4;
+  const uint8_t* kbase = kc + (size_t)bh * Np * (D / 2);
+  const uint8_t* vbase = vc + (size_t)bh * D * (Np / 2);
+  const uint8_t* ksbase = ks + (size_t)bh * Np * (D / 32);
+  const uint8_t* vsbase = vs + (size_t)bh * D * (Np / 32);
+  uint32_t ko[KJ], vo[VJ], so[T::SJ];
+#pragma unroll
+  for (int i = 0; i < KJ; ++i) {
+    const int b = wave + 4 * i, t = b / NKS, s = b % NKS;
+    ko[i] = (32 * t + col) * (D / 2) + 32 * s + 16 * hi;
+  }
+#pragma unroll
+  for (int i = 0; i < VJ; ++i) {
+    const int b = wave + 4 * i, db = b / NG, g = b % NG;
+    vo[i] = (32 * db + col) * (Np / 2) + 32 * g + 16 * hi;
+  }
+#pragma unroll
+  for (int i = 0; i < T::SJ; ++i) {
+    const int jb = wave + 4 * i;
+    if (jb < T::NKSJ) {
+      so[i] = (64 * jb + lane) * 4;                        // K^ scale dword of the tile
+    } else {
+      const int d = 64 * (jb - T::NKSJ) + lane;            // V^T scale dword d: dim row d / 2, half d & 1
+      so[i] = (d >> 1) * (Np / 32) + 4 * (d & 1);
+    }
+  }
+  const float* brow = SQ ? qkb + ((size_t)bh * nqt + qt) * Np : nullptr;
+  auto issue = [&](int j, int stage) {
+    const int kb = j * BKV;
+    const bool short_tail = kb + BKV > Np;                 // keys [kb + 128, kb + 256) lie past Np
+    uint8_t* L = lds[stage];
+    const uint32_t kto = (uint32_t)kb * (D / 2), vto = (uint32_t)kb / 2;
+#pragma unroll
+    for (int i = 0; i < KJ; ++i) {
+      const int b = wave + 4 * i, t = b / NKS;
+      const uint32_t back = (short_tail && t >= NSUB / 2) ? 128u * (D / 2) : 0u;
+      lds_load16(kbase + (ko[i] + kto - back), L + T::KC_OFF + b * 1024);
+    }
+#pragma unroll
+    for (int i = 0; i < VJ; ++i) {
+      const int b = wave + 4 * i, g = b % NG;
+      const uint32_t back = (short_tail && g >= NG / 2) ? 64u : 0u;
+      lds_load16(vbase + (vo[i] + vto - back), L + T::VC_OFF + b * 1024);
+    }
+#pragma unroll
+    for (int i = 0; i < T::SJ; ++i) {
+      const int jb = wave + 4 * i;
+      if (jb < T::NKSJ) {
+        const uint32_t back = (short_tail && 64 * jb * 4 >= T::KS_BYTES / 2) ? (uint32_t)(T::KS_BYTES / 2) : 0u;
+        lds_load4(ksbase + (size_t)kb * (D / 32) + so[i] - back, L + T::KS_OFF + jb * 256);
+      } else {
+        const uint32_t back = (short_tail && (lane & 1)) ? 4u : 0u;
+        lds_load4(vsbase + kb / 32 + so[i] - back, L + T::VS_OFF + (jb - T::NKSJ) * 256);
+      }
+    }
+    if constexpr (SQ) {
+      if (wave == 0) lds_load16(brow + min(kb + 4 * lane, Np - 4), L + T::BIAS_OFF);
+    }
+  };
+
+  v16f oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) oacc[db] = v16f{};
+  float m = -INFINITY, mc_old = -INFINITY, f_old = 0.0f, lsum_acc = 0.0f;
+
+  issue(0, 0);
+  for (int j = 0; j < ntiles; ++j) {
+    const int stage = j & 1;
+    wait_loads();                                          // this wave's loads of tile j have landed
+    __syncthreads();                                       // everyone's; every wave is past tile j - 1
+    if (j + 1 < ntiles) issue(j + 1, stage ^ 1);
+    const uint8_t* L = lds[stage];
+    const int kb = j * BKV;
+    if (CAUSAL && kb > qw + 31) continue;                  // the whole tile is above this wave's diagonal
+
+    // S^T = K^ . Q^T for the tile
+    v16f sacc[NSUB];
+#pragma unroll
+    for (int t = 0; t < NSUB; ++t) {
+      uint32_t ksc;
+      if constexpr (D == 128) ksc = *reinterpret_cast<const uint32_t*>(L + T::KS_OFF + (32 * t + col) * 4) >> (8 * hi);
+      else ksc = L[T::KS_OFF + (32 * t + col) * 2 + hi];
+      v16f acc = v16f{};
+      static_for<NKS>([&](auto S_) {
+        constexpr int s = decltype(S_)::value;
+        const v4i a = *reinterpret_cast<const v4i*>(L + T::KC_OFF + (t * NKS + s) * 1024 + lane * 16);
+        acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(qreg[s]), acc, 4, 4, 2 * s, (int)ksc,
+                                                              2 * s, (int)qsc);
+      });
+      sacc[t] = acc;
+    }
+    if constexpr (SQ) {
+#pragma unroll
+      for (int u = 0; u < NSUB; ++u) {
+        const float* bp = reinterpret_cast<const float*>(L + T::BIAS_OFF) + 64 * (u >> 1) + 32 * hi + 16 * (u & 1);
+#pragma unroll
+        for (int w4 = 0; w4 < 4; ++w4) {
+          const v4f b = *reinterpret_cast<const v4f*>(bp + 4 * w4);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sacc[u][4 * w4 + r] = sacc[u][4 * w4 + r] + b[r];
+        }
+      }
+    }
+    const bool need_mask = (kb + BKV > N) || (CAUSAL && kb + BKV - 1 > qw);
+    if (need_mask) {
+      const int rem = (CAUSAL ? min(N, qi + 1) : N) - kb - 32 * hi;
+#pragma unroll
+      for (int u = 0; u < NSUB; ++u)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int c = 64 * (u >> 1) + 16 * (u & 1) + v;
+          const float bound = __uint_as_float(0xFF800000u ^ ((uint32_t)(c - rem) & 0x80000000u));
+          sacc[u][v] = smin(sacc[u][v], bound);
+        }
+    }
+    float bm[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      float x = sacc[2 * g][0];
+#pragma unroll
+      for (int v = 1; v < 16; ++v) x = smax(x, sacc[2 * g][v]);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) x = smax(x, sacc[2 * g + 1][v]);
+      bm[g] = x;
+    }
+    float tl = bm[0];
+#pragma unroll
+    for (int g = 1; g < NG; ++g) tl = smax(tl, bm[g]);
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(tl), __float_as_uint(tl), false, false);
+    const float t = smax(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    const float m_new = smax(m, t);
+    const float tc = t * c2;
+    const float mc = m_new * c2;
+    const float delta = tc - mc;
+    const float kf = __builtin_floorf(delta);
+    const float f = delta - kf;
+    const float gam = __builtin_amdgcn_exp2f((mc_old - mc) + (f_old - f));
+    const int kfold = (int)__builtin_fmaxf(kf, -300.0f);
+    const float bias = log6 - tc;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) oacc[db][v] *= gam;
+
+    // V^T scale bytes of this lane's dim rows: dword h of the row's 8 bytes holds blocks 4h .. 4h + 3
+    uint32_t vsw[NDB][2];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const uint2 w2 = *reinterpret_cast<const uint2*>(L + T::VS_OFF + (32 * db + col) * 8);
+      vsw[db][0] = w2.x >> (8 * hi);
+      vsw[db][1] = w2.y >> (8 * hi);
+    }
+    float ps[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    static_for<NG>([&](auto G_) {
+      constexpr int g = decltype(G_)::value;
+      const int e = (int)__builtin_fmaxf(__builtin_ceilf((bm[g] - t) * c2), -126.0f);
+      const float escale = __builtin_ldexpf(1.0f, e);
+      uint32_t w[4];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int tt = 2 * g + half;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          uint32_t word = 0;
+          static_for<4>([&](auto I_) {
+            constexpr int i = decltype(I_)::value;
+            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[tt][8 * q + 2 * i], c2, bias));
+            const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[tt][8 * q + 2 * i + 1], c2, bias));
+            ps[(2 * half + q) & 3] += p0;
+            ps[(2 * half + q) & 3] += p1;
+            if constexpr (i == 0) word = __float_as_uint(p0);
+            word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, p0, p1, escale, i);
+          });
+          w[2 * half + q] = word;
+        }
+      }
+      const v4i pw = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
+      const int sb = e + kfold + 127;
+      const int psb = sb < 0 ? 0 : sb;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const v4i a = *reinterpret_cast<const v4i*>(L + T::VC_OFF + (db * NG + g) * 1024 + lane * 16);
+        oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(pw), oacc[db], 4, 4, 2 * (g & 1),
+                                                                   (int)vsw[db][g >> 1], 0, psb);
+      }
+    });
+    const float psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
+    lsum_acc = lsum_acc * gam + __builtin_ldexpf(psum, kfold);
+    m = m_new;
+    mc_old = mc;
+    f_old = f;
+  }
+
+  const float ltot = lsum_acc + __shfl_xor(lsum_acc, 32, 64);
+  const float inv = 1.0f / ltot;
+  if (qi < N) {
+    uint8_t* obase = reinterpret_cast<uint8_t*>(o);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int d0 = 32 * db + 8 * g + 4 * hi;
+        const size_t idx = ((size_t)bh * N + qi) * D + d0;
+        const float a0 = oacc[db][4 * g] * inv, a1 = oacc[db][4 * g + 1] * inv;
+        const float a2 = oacc[db][4 * g + 2] * inv, a3 = oacc[db][4 * g + 3] * inv;
+        if (OUT == 0) {
+          *reinterpret_cast<float4*>(obase + idx * 4) = make_float4(a0, a1, a2, a3);
+        } else {
+          uint16_t h0, h1, h2, h3;
+          if (OUT == 1) { h0 = f32_to_bf16_rne(a0); h1 = f32_to_bf16_rne(a1); h2 = f32_to_bf16_rne(a2); h3 = f32_to_bf16_rne(a3); }
+          else { h0 = f32_to_fp16_rne(a0); h1 = f32_to_fp16_rne(a1); h2 = f32_to_fp16_rne(a2); h3 = f32_to_fp16_rne(a3); }
+          *reinterpret_cast<uint2*>(obase + idx * 2) = make_uint2((uint32_t)h0 | ((uint32_t)h1 << 16), (uint32_t)h2 | ((uint32_t)h3 << 16));
+        }
+      }
+  }
+}
+
+template <int D, bool CAUSAL, int OUT, bool SQ>
+static hipError_t launch_fp4_256_t(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
+                                   const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2,
+                                   float log6, hipStream_t st) {
+  const int nqt = (N + AQ - 1) / AQ;
+  hipLaunchKernelGGL((attn_fp4_mx256_kernel<D, CAUSAL, OUT, SQ>), dim3((unsigned)(nqt * BH)), dim3(256), 0, st,
+                     (const uint8_t*)qc, (const uint8_t*)qs, (const uint8_t*)kc, (const uint8_t*)ks, (const uint8_t*)vc,
+                     (const uint8_t*)vs, qkb, o, BH, N, Np, nqt, c2, log6);
+  return hipGetLastError();
+}
+
+template <int D, bool CAUSAL, bool SQ>
+static hipError_t launch_fp4_256_o(int out, const void* qc, const void* qs, const void* kc, const void* ks,
+                                   const void* vc, const void* vs, const float* qkb, void* o, int BH, int N, int Np,
+                                   float c2, float log6, hipStream_t st) {
+  if (out == 0) return launch_fp4_256_t<D, CAUSAL, 0, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+  if (out == 1) return launch_fp4_256_t<D, CAUSAL, 1, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+  return launch_fp4_256_t<D, CAUSAL, 2, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+}
+
 template <int D, int BKV, bool CAUSAL, int OUT, bool SQ>
 static hipError_t launch_fp4_t(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
                                const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2, float log6,
@@ -407,6 +711,14 @@ hipError_t launch_attn_fp4_mx(const void* qc, const void* qs, const void* kc, co
 #define SAGE_A(DD, BB)                                                                                    \
   return causal ? launch_fp4_s<DD, BB, true>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st) \
                 : launch_fp4_s<DD, BB, false>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st)
+  if (bkv == 256) {
+#define SAGE_A256(DD, CC)                                                                                      \
+  return qkb ? launch_fp4_256_o<DD, CC, true>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st) \
+             : launch_fp4_256_o<DD, CC, false>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st)
+    if (D == 128) { if (causal) { SAGE_A256(128, true); } else { SAGE_A256(128, false); } }
+    else { if (causal) { SAGE_A256(64, true); } else { SAGE_A256(64, false); } }
+#undef SAGE_A256
+  }
   if (D == 128) { if (bkv == 128) { SAGE_A(128, 128); } else { SAGE_A(128, 64); } }
   else { if (bkv == 128) { SAGE_A(64, 128); } else { SAGE_A(64, 64); } }
 #undef SAGE_A

@@ -57,6 +57,7 @@ int check_shape(int B, int H, int N, int D, unsigned fmt) {
   if (B <= 0 || H <= 0 || N <= 0) return SAGE_ERR_INVALID_ARG;
   if (D != 64 && D != 128) return SAGE_ERR_INVALID_ARG;
   if (fmt & ~SAGE_FMT_ALL_BITS) return SAGE_ERR_INVALID_ARG;
+  if ((fmt & SAGE_BKV64) && (fmt & SAGE_BKV256)) return SAGE_ERR_INVALID_ARG;
   const int f = fmt_of(fmt);
   if (f != SAGE_FMT_MXFP4 && f != SAGE_FMT_NV16_E4M3) return SAGE_ERR_INVALID_ARG;
   if ((long long)B * H > (1LL << 30)) return SAGE_ERR_INVALID_ARG;
@@ -139,6 +140,7 @@ int attn_args(const void* q, const void* k, const void* v, const void* o, int B,
               unsigned fmt) {
   int rc = check_shape(B, H, N, D, fmt);
   if (rc != SAGE_OK) return rc;
+  if ((fmt & SAGE_BKV256) && fmt_of(fmt) != SAGE_FMT_MXFP4) return SAGE_ERR_UNSUPPORTED;
   if (!q || !k || !v || !o) return SAGE_ERR_INVALID_ARG;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return SAGE_ERR_INVALID_ARG;
   if (causal != 0 && causal != 1) return SAGE_ERR_INVALID_ARG;
@@ -153,10 +155,12 @@ inline int out_kind(unsigned fmt) { return (fmt & SAGE_OUT_F32) ? 0 : ((fmt & SA
 int attn_prequant_impl(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc, const void* vs,
                        const float* qkb, void* o, int B, int H, int N, int D, int causal, unsigned fmt,
                        hipStream_t st) {
-  const int bkv = (fmt & SAGE_BKV64) ? 64 : 128;
-  if (fmt_of(fmt) == SAGE_FMT_NV16_E4M3)
+  const int bkv = (fmt & SAGE_BKV64) ? 64 : ((fmt & SAGE_BKV256) ? 256 : 128);
+  if (fmt_of(fmt) == SAGE_FMT_NV16_E4M3) {
+    if (bkv == 256) return SAGE_ERR_UNSUPPORTED;
     return hip_status(sage::launch_attn_nv16(qc, qs, kc, ks, vc, vs, qkb, o, B * H, N, pad128(N), D, bkv,
                                              causal != 0, out_kind(fmt), softmax_c2(D), log2_of_2688(), st));
+  }
   return hip_status(sage::launch_attn_fp4_mx(qc, qs, kc, ks, vc, vs, qkb, o, B * H, N, pad128(N), D, bkv,
                                              causal != 0, out_kind(fmt), softmax_c2(D), log2_of_6(), st));
 }

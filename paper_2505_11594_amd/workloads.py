@@ -53,10 +53,12 @@ class Workload:
 # The five benchmark configurations, in order.
 CONFIGS = [
     Workload("b1h1n128d64_fp16", 1, 1, 128, 64, False, IN_FP16, (FMT_MX,), bkv=64, seed=1000),
-    Workload("b4h32n4096d128_kbias4", 4, 32, 4096, 128, False, IN_BF16, (FMT_MX,), k_bias_var=4.0, seed=1001),
-    Workload("b1h32n32768d128_outliers", 1, 32, 32768, 128, False, IN_BF16, (FMT_MX,),
+    Workload("b4h32n4096d128_kbias4", 4, 32, 4096, 128, False, IN_BF16, (FMT_MX,), bkv=256, k_bias_var=4.0,
+             seed=1001),
+    Workload("b1h32n32768d128_outliers", 1, 32, 32768, 128, False, IN_BF16, (FMT_MX,), bkv=256,
              outlier_frac=0.01, outlier_scale=20.0, seed=1002),
-    Workload("b8h32n8192d128_causal_kbias1", 8, 32, 8192, 128, True, IN_BF16, (FMT_MX,), k_bias_var=1.0, seed=1003),
+    Workload("b8h32n8192d128_causal_kbias1", 8, 32, 8192, 128, True, IN_BF16, (FMT_MX,), bkv=256, k_bias_var=1.0,
+             seed=1003),
     Workload("b1h24n76800d64_kbias4", 1, 24, 76800, 64, False, IN_BF16, (FMT_NV16, FMT_MX), k_bias_var=4.0, seed=1004),
 ]
 

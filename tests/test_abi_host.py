@@ -49,8 +49,8 @@ def _attn(L, **kw):
 
 
 @pytest.mark.parametrize("bad", [dict(q=None), dict(o=None), dict(q=FAKE + 2), dict(B=0), dict(H=-1), dict(N=0),
-                                 dict(D=96), dict(D=256), dict(causal=2), dict(fmt=0x80), dict(fmt=0x3),
-                                 dict(N=1 << 30)])
+                                 dict(D=96), dict(D=256), dict(causal=2), dict(fmt=0x100), dict(fmt=0x3),
+                                 dict(fmt=0x40 | 0x80), dict(N=1 << 30)])
 def test_attn_invalid_args_rejected_on_host(L, bad):
     assert _attn(L, **bad) == bd.SAGE_ERR_INVALID_ARG
 
@@ -60,6 +60,10 @@ def test_attn_unsupported(L):
     for f in (0, bd.SAGE_FMT_NV16_E4M3):
         assert L.sage_attn_fp4_fwd_prequant(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 128, 0,
                                             f | bd.SAGE_SMOOTH_Q, None) == bd.SAGE_ERR_UNSUPPORTED
+    # 256-key tiles exist for MXFP4 only; rejected before any allocation or launch
+    assert _attn(L, fmt=bd.SAGE_FMT_NV16_E4M3 | bd.SAGE_BKV256) == bd.SAGE_ERR_UNSUPPORTED
+    assert L.sage_attn_fp4_fwd_prequant(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 128, 128, 0,
+                                        bd.SAGE_FMT_NV16_E4M3 | bd.SAGE_BKV256, None) == bd.SAGE_ERR_UNSUPPORTED
 
 
 def test_smooth_q_workspace_and_quant_arguments(L):

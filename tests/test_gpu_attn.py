@@ -22,7 +22,7 @@ TOL = 2e-3
 
 def gpu_attn(q, k, v, in_dtype, causal, fmt, bkv, out_f32=True, **kw):
     torch = torch_dev()
-    f = fmt | (bd.SAGE_BKV64 if bkv == 64 else 0)
+    f = fmt | bd.bkv_flag(bkv)
     o = bd.sage_attn_fp4_fwd(to_dev(q, in_dtype), to_dev(k, in_dtype), to_dev(v, in_dtype), causal=causal, fmt=f,
                              out_f32=out_f32, **kw)
     torch.cuda.synchronize()
@@ -61,6 +61,34 @@ def test_attn_edge_shapes(fmt, N, D, causal, bkv):
     check(o.cpu().numpy().reshape(-1, D), ref, tie, "edge")
 
 
+@pytest.mark.parametrize("N", [1, 100, 257, 300, 512, 640, 1000])
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("out_f32", [True, False])
+def test_attn_bkv256_edge_shapes(N, D, causal, out_f32):
+    """256-key tiles (MXFP4): tails that end inside the tile's lower or upper
+    128 keys (N = 100, 300, 640, 1000), an exact multiple of the tile (512),
+    one token; 16-bit and fp32 outputs."""
+    say("attn bkv256 edge N=%d D=%d causal=%d out_f32=%d" % (N, D, causal, out_f32))
+    in_dtype = 1 if (N + D) % 2 else 0
+    q, k, v = wl.make_inputs(1, 2, N, D, in_dtype, seed=300 + N, k_bias_var=4.0, outlier_frac=0.02)
+    o = gpu_attn(q, k, v, in_dtype, causal, 0, 256, out_f32=out_f32)
+    ref, tie, _ = oracle.attn(q, k, v, in_dtype, causal, oracle.FMT_MX, 256)
+    got = o.float().cpu().numpy().reshape(-1, D)
+    # a 16-bit output adds its own rounding: half an ulp of |O| <= max|V|
+    extra = None if out_f32 else np.abs(ref).max(axis=1) * (2.0 ** -8 if in_dtype == 1 else 2.0 ** -11)
+    check(got, ref, tie, "bkv256 edge", extra)
+
+
+def test_attn_bkv256_rejected_for_nv16_and_with_bkv64():
+    torch = torch_dev()
+    q = torch.zeros((1, 1, 128, 64), dtype=torch.float16, device="cuda:0")
+    with pytest.raises(RuntimeError):
+        bd.sage_attn_fp4_fwd(q, q, q, fmt=bd.SAGE_FMT_NV16_E4M3 | bd.SAGE_BKV256)
+    with pytest.raises(RuntimeError):
+        bd.sage_attn_fp4_fwd(q, q, q, fmt=bd.SAGE_BKV64 | bd.SAGE_BKV256)
+
+
 def test_attn_config0_all_rows():
     w = wl.CONFIGS[0]
     q, k, v = wl.generate(w)
@@ -71,19 +99,23 @@ def test_attn_config0_all_rows():
     say("accuracy vs exact", oracle.metrics(ex, o.cpu().numpy().reshape(-1, w.D)))
 
 
-@pytest.mark.parametrize("ci,fmt", [(1, 0), (2, 0), (3, 0), (4, 1), (4, 0)])
-def test_attn_configs_full_size_sampled_rows(ci, fmt):
-    """The benchmark's launch configuration at full size; the oracle computes a
-    seeded sample of rows (first/last/random query tiles of sampled heads)."""
+@pytest.mark.parametrize("ci,fmt,bkv", [(1, 0, None), (2, 0, None), (3, 0, None), (4, 1, None), (4, 0, None),
+                                        (2, 0, 128), (3, 0, 128), (4, 0, 256)])
+def test_attn_configs_full_size_sampled_rows(ci, fmt, bkv):
+    """The benchmark's launch configuration at full size (each workload's own
+    KV tile, plus the other tile on the long, causal and D = 64 workloads); the
+    oracle computes a seeded sample of rows (first/last/random query tiles of
+    sampled heads)."""
     w = wl.CONFIGS[ci]
     assert fmt in w.fmts
-    say("attn config", ci, w.name, "fmt", fmt)
+    bkv = bkv or w.bkv
+    say("attn config", ci, w.name, "fmt", fmt, "bkv", bkv)
     q, k, v = wl.generate(w)
-    o = gpu_attn(q, k, v, w.in_dtype, w.causal, fmt, w.bkv)
+    o = gpu_attn(q, k, v, w.in_dtype, w.causal, fmt, bkv)
     BH = w.B * w.H
     heads = sorted({0, BH - 1} | set(np.random.default_rng(ci).choice(BH, min(BH, 6), replace=False).tolist()))
     rows = wl.sample_rows(w, per_head_tiles=4, tile=128, rows_per_tile=8, heads=heads, seed=ci)
-    ref, tie, cnt = oracle.attn(q, k, v, w.in_dtype, w.causal, fmt, w.bkv, rows=rows)
+    ref, tie, cnt = oracle.attn(q, k, v, w.in_dtype, w.causal, fmt, bkv, rows=rows)
     got = o_rows(o, rows, w.D)
     check(got, ref, tie, w.name)
     ex = oracle.exact_attn(q, k, v, w.in_dtype, w.causal, rows=rows)

@@ -45,7 +45,7 @@ def test_quant_q_smooth_bit_exact(fmt, shape, in_dtype):
 
 def gpu_attn_sq(q, k, v, in_dtype, causal, bkv, extra=0, fmt=0):
     torch = torch_dev()
-    f = fmt | bd.SAGE_SMOOTH_Q | extra | (bd.SAGE_BKV64 if bkv == 64 else 0)
+    f = fmt | bd.SAGE_SMOOTH_Q | extra | bd.bkv_flag(bkv)
     o = bd.sage_attn_fp4_fwd(to_dev(q, in_dtype), to_dev(k, in_dtype), to_dev(v, in_dtype), causal=causal, fmt=f)
     torch.cuda.synchronize()
     return o
@@ -63,6 +63,18 @@ def test_attn_smooth_q_edge_shapes(fmt, N, D, causal, bkv):
     o = gpu_attn_sq(q, k, v, in_dtype, causal, bkv, fmt=fmt)
     ref, tie, _ = oracle.attn(q, k, v, in_dtype, causal, fmt, bkv, flags=oracle.SMOOTH_Q)
     check(o.cpu().numpy().reshape(-1, D), ref, tie, "smooth-Q edge")
+
+
+@pytest.mark.parametrize("N", [1, 100, 300, 512, 640])
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("causal", [False, True])
+def test_attn_smooth_q_bkv256_edge_shapes(N, D, causal):
+    say("attn smooth-Q bkv256 edge N=%d D=%d causal=%d" % (N, D, causal))
+    in_dtype = 1 if (N + D) % 2 else 0
+    q, k, v = q_bias_inputs(1, 2, N, D, in_dtype, seed=530 + N)
+    o = gpu_attn_sq(q, k, v, in_dtype, causal, 256)
+    ref, tie, _ = oracle.attn(q, k, v, in_dtype, causal, oracle.FMT_MX, 256, flags=oracle.SMOOTH_Q)
+    check(o.cpu().numpy().reshape(-1, D), ref, tie, "smooth-Q bkv256 edge")
 
 
 def test_attn_smooth_q_without_smoothing_k():

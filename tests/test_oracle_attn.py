@@ -30,7 +30,7 @@ def widen(bits, dt):
     return wl.from_bits(bits, dt)
 
 
-@pytest.mark.parametrize("bkv", [16, 64, 128])
+@pytest.mark.parametrize("bkv", [16, 64, 128, 256])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("N", [200, 256])
 def test_identity_quantizer_equals_textbook_softmax(bkv, causal, N):
