@@ -32,6 +32,12 @@ typedef enum {
   SAGE_ERR_WORKSPACE = 4     /* caller workspace smaller than the size query returned   */
 } sage_status;
 
+/* ---- shapes ------------------------------------------------------------ */
+/* Every entry point takes B, H, N, D with B, H, N >= 1 and D in {64, 128}. */
+/* Np = N rounded up to 128.  Per head, Np * D <= 2^31 (N <= 2^24 at        */
+/* D = 128, 2^25 at D = 64); in total, B * H * Np * D <= 2^40.  Larger      */
+/* shapes return SAGE_ERR_INVALID_ARG.                                      */
+
 /* ---- fmt bitfield ----------------------------------------------------- */
 /* Microscaling format (Sec. 3.1, "Data type determination"):              */
 #define SAGE_FMT_MXFP4      0x0u  /* E2M1 codes, 1x32 blocks, E8M0 scales (gfx950 native) */

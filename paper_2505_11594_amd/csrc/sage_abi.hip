@@ -62,6 +62,8 @@ int check_shape(int B, int H, int N, int D, unsigned fmt) {
   if (f != SAGE_FMT_MXFP4 && f != SAGE_FMT_NV16_E4M3) return SAGE_ERR_INVALID_ARG;
   if ((long long)B * H > (1LL << 30)) return SAGE_ERR_INVALID_ARG;
   if (N > (1 << 30) - 128) return SAGE_ERR_INVALID_ARG;
+  // one head's tensors are indexed with 32-bit offsets (row * Np, key * D)
+  if ((long long)pad128(N) * D > (1LL << 31)) return SAGE_ERR_INVALID_ARG;
   if ((long long)B * H * (long long)pad128(N) * D > kMaxElems) return SAGE_ERR_INVALID_ARG;
   return SAGE_OK;
 }

@@ -50,7 +50,8 @@ def _attn(L, **kw):
 
 @pytest.mark.parametrize("bad", [dict(q=None), dict(o=None), dict(q=FAKE + 2), dict(B=0), dict(H=-1), dict(N=0),
                                  dict(D=96), dict(D=256), dict(causal=2), dict(fmt=0x100), dict(fmt=0x3),
-                                 dict(fmt=0x40 | 0x80), dict(N=1 << 30)])
+                                 dict(fmt=0x40 | 0x80), dict(N=1 << 30),
+                                 dict(N=(1 << 24) + 1), dict(D=64, N=(1 << 25) + 1)])
 def test_attn_invalid_args_rejected_on_host(L, bad):
     assert _attn(L, **bad) == bd.SAGE_ERR_INVALID_ARG
 
@@ -192,3 +193,15 @@ def test_product_path_does_not_import_oracle():
             if f.endswith((".py", ".hip", ".h", ".cpp")):
                 src = open(os.path.join(root, f)).read()
                 assert "import oracle" not in src and "from oracle" not in src and "sage_oracle" not in src, f
+
+
+def test_per_head_size_limit(L):
+    """One head may hold Np * D <= 2^31 elements: the largest accepted N at
+    D = 128 is 2^24, at D = 64 2^25; one token more is rejected by every size
+    query."""
+    for D, nmax in ((128, 1 << 24), (64, 1 << 25)):
+        assert L.sage_attn_fp4_workspace_size(1, 1, nmax, D, 0) > 0
+        assert L.sage_attn_fp4_workspace_size(1, 1, nmax + 1, D, 0) == 0
+        assert L.sage_attn_int8_workspace_size(1, 1, nmax, D, 0) > 0
+        assert L.sage_attn_int8_workspace_size(1, 1, nmax + 1, D, 0) == 0
+        assert bd.attn_int8_bwd_min_workspace_size(1, 1, nmax + 1, D) == 0
