@@ -47,6 +47,15 @@ __device__ __forceinline__ void lds_load4(const void* src, void* dst) {
 }
 __device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
 
+// A workgroup-uniform address, pinned to scalar registers, so that base +
+// 32-bit lane offset selects the scalar-base form of a global load.
+__device__ __forceinline__ const uint8_t* sbase(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+  return reinterpret_cast<const uint8_t*>((hi << 32) | lo);
+}
+
 // One LDS stage of a KV tile, in MFMA-operand order (plus, with smoothing Q,
 // the tile's BKV entries of the query block's GEMV bias).
 template <int D, int BKV, bool SQ>
@@ -439,63 +448,57 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx256_kernel(
   int ntiles = (N + BKV - 1) / BKV;
   if (CAUSAL) ntiles = min(ntiles, min(q0 + AQ - 1, N - 1) / BKV + 1);
 
+  // Load jobs: wave w loads K^ operand blocks b = w + 4i (key row 32t + col,
+  // bytes [32s + 16hi, +16) with t = b / NKS, s = b % NKS), V^T operand blocks
+  // b = w + 4i (dim row 32i + col, bytes [32w + 16hi, +16) of the tile, since
+  // NG = 4) and scale dword jobs jb = w + 4i: K^ scale dwords 64jb + lane,
+  // then V^T scale dwords 64(jb - NKSJ) + lane (dim row d / 2, half d & 1).
+  // Each address is a uniform base -- head, tile, job and the tail redirect
+  // -- plus one of five fixed lane offsets, so a load costs no VALU.
+  static_assert(4 % NKS == 0 && NG == 4, "job layout");
   constexpr int KJ = T::NKB / 4, VJ = T::NVB / 4;
+  const uint32_t ko0 = (uint32_t)((32 * (wave / NKS) + col) * (D / 2) + 32 * (wave % NKS) + 16 * hi);
+  const uint32_t vo0 = (uint32_t)(col * (Np / 2) + 32 * wave + 16 * hi);
+  const uint32_t kso = (uint32_t)(4 * lane);
+  const uint32_t vso = (uint32_t)((lane >> 1) * (Np / 32) + 4 * (lane & 1));
+  const uint32_t vso_hi = (uint32_t)(4 * (lane & 1));   // the second dword: subtracted when it lies past Np
   const uint8_t* kbase = kc + (size_t)bh * Np * (D / 2);
   const uint8_t* vbase = vc + (size_t)bh * D * (Np / 2);
   const uint8_t* ksbase = ks + (size_t)bh * Np * (D / 32);
   const uint8_t* vsbase = vs + (size_t)bh * D * (Np / 32);
-  uint32_t ko[KJ], vo[VJ], so[T::SJ];
-#pragma unroll
-  for (int i = 0; i < KJ; ++i) {
-    const int b = wave + 4 * i, t = b / NKS, s = b % NKS;
-    ko[i] = (32 * t + col) * (D / 2) + 32 * s + 16 * hi;
-  }
-#pragma unroll
-  for (int i = 0; i < VJ; ++i) {
-    const int b = wave + 4 * i, db = b / NG, g = b % NG;
-    vo[i] = (32 * db + col) * (Np / 2) + 32 * g + 16 * hi;
-  }
-#pragma unroll
-  for (int i = 0; i < T::SJ; ++i) {
-    const int jb = wave + 4 * i;
-    if (jb < T::NKSJ) {
-      so[i] = (64 * jb + lane) * 4;                        // K^ scale dword of the tile
-    } else {
-      const int d = 64 * (jb - T::NKSJ) + lane;            // V^T scale dword d: dim row d / 2, half d & 1
-      so[i] = (d >> 1) * (Np / 32) + 4 * (d & 1);
-    }
-  }
   const float* brow = SQ ? qkb + ((size_t)bh * nqt + qt) * Np : nullptr;
   auto issue = [&](int j, int stage) {
     const int kb = j * BKV;
     const bool short_tail = kb + BKV > Np;                 // keys [kb + 128, kb + 256) lie past Np
+    const uint8_t* kt = kbase + (size_t)kb * (D / 2);
+    const uint8_t* vt = vbase + kb / 2;
+    const uint8_t* kst = ksbase + (size_t)kb * (D / 32);
+    const uint8_t* vst = vsbase + kb / 32;
     uint8_t* L = lds[stage];
-    const uint32_t kto = (uint32_t)kb * (D / 2), vto = (uint32_t)kb / 2;
 #pragma unroll
     for (int i = 0; i < KJ; ++i) {
       const int b = wave + 4 * i, t = b / NKS;
-      const uint32_t back = (short_tail && t >= NSUB / 2) ? 128u * (D / 2) : 0u;
-      lds_load16(kbase + (ko[i] + kto - back), L + T::KC_OFF + b * 1024);
+      const long long back = (short_tail && t >= NSUB / 2) ? 128LL * (D / 2) : 0;
+      lds_load16(sbase(kt + ((long long)i * (128 / NKS) * (D / 2) - back)) + ko0, L + T::KC_OFF + b * 1024);
     }
 #pragma unroll
     for (int i = 0; i < VJ; ++i) {
-      const int b = wave + 4 * i, g = b % NG;
-      const uint32_t back = (short_tail && g >= NG / 2) ? 64u : 0u;
-      lds_load16(vbase + (vo[i] + vto - back), L + T::VC_OFF + b * 1024);
+      const long long back = (short_tail && wave >= NG / 2) ? 64 : 0;
+      lds_load16(sbase(vt + ((long long)i * 32 * (Np / 2) - back)) + vo0, L + T::VC_OFF + (wave + 4 * i) * 1024);
     }
 #pragma unroll
     for (int i = 0; i < T::SJ; ++i) {
       const int jb = wave + 4 * i;
       if (jb < T::NKSJ) {
-        const uint32_t back = (short_tail && 64 * jb * 4 >= T::KS_BYTES / 2) ? (uint32_t)(T::KS_BYTES / 2) : 0u;
-        lds_load4(ksbase + (size_t)kb * (D / 32) + so[i] - back, L + T::KS_OFF + jb * 256);
+        const long long back = (short_tail && 64 * jb * 4 >= T::KS_BYTES / 2) ? T::KS_BYTES / 2 : 0;
+        lds_load4(sbase(kst + (256LL * jb - back)) + kso, L + T::KS_OFF + jb * 256);
       } else {
-        const uint32_t back = (short_tail && (lane & 1)) ? 4u : 0u;
-        lds_load4(vsbase + kb / 32 + so[i] - back, L + T::VS_OFF + (jb - T::NKSJ) * 256);
+        lds_load4(sbase(vst + (long long)(jb - T::NKSJ) * Np) + (vso - (short_tail ? vso_hi : 0u)),
+                  L + T::VS_OFF + (jb - T::NKSJ) * 256);
       }
     }
     if constexpr (SQ) {
-      if (wave == 0) lds_load16(brow + min(kb + 4 * lane, Np - 4), L + T::BIAS_OFF);
+      if (wave == 0) lds_load16(brow + (uint32_t)min(kb + 4 * lane, Np - 4), L + T::BIAS_OFF);
     }
   };
 
