@@ -52,7 +52,7 @@ struct Nv16Stage {
 
   // 32 codes + two E4M3 scales -> 32 bf16 values in four 16-byte chunks
   __device__ __forceinline__ static void dequant32(const v4i codes, uint32_t sc2, v4i out[4]) {
-    const float s0 = e4m3_decode(sc2 & 0xFFu), s1 = e4m3_decode((sc2 >> 8) & 0xFFu);
+    const float s0 = e4m3_decode_hw<0>(sc2), s1 = e4m3_decode_hw<1>(sc2);
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const float s = (w < 2) ? s0 : s1;
@@ -108,6 +108,7 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   constexpr int NDB = D / 32;
   constexpr int BIAS_OFF = T::BYTES, LBYTES = T::BYTES + (SQ ? BKV * 4 : 0);   // bias of the tile's keys
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][LBYTES];
+  __shared__ float rtab[128];   // fl32(1 / s) of every E4M3 code s (0 for s = 0): the second level's reciprocal
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 31, hi = lane >> 5;
 
@@ -128,7 +129,7 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
 #pragma unroll
     for (int s = 0; s < NKS; ++s) {
       const uint32_t word = *reinterpret_cast<const uint32_t*>(crow + 8 * s + 4 * hi);
-      const float sc = (qi < N) ? e4m3_decode(srow[s]) : 0.0f;
+      const float sc = (qi < N) ? e4m3_decode_hw<0>(srow[s]) : 0.0f;
       uint32_t w[4];
       static_for<4>([&](auto B_) {
         constexpr int b = decltype(B_)::value;
@@ -153,6 +154,7 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   for (int db = 0; db < NDB; ++db) oacc[db] = v16f{};
   float m = -INFINITY, mc_old = -INFINITY, f_old = 0.0f, lsum_acc = 0.0f;
 
+  if (tid < 128) rtab[tid] = tid == 0 ? 0.0f : 1.0f / e4m3_decode_hw<0>((uint32_t)tid);   // visible after the first barrier
   Nv16Stage<D, BKV> stg;
   // smoothing Q: threads tid < BKV/4 stage 4 bias entries of the next tile
   const float* brow = SQ ? qkb + ((size_t)bh * nqt + qt) * Np : nullptr;
@@ -244,9 +246,9 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
       for (int t = 0; t < NSUB; ++t) {
         // second level: E4M3 scale of this lane's 16-key block
         const float amax = (bm[t] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(__builtin_fmaf(bm[t], c2, bias));
-        const uint32_t sb = e4m3_encode(amax / 6.0f);
-        const float s2 = e4m3_decode(sb);
-        const float r = (s2 == 0.0f) ? 0.0f : 1.0f / s2;
+        const uint32_t sb = e4m3_encode_hw(amax / 6.0f);
+        const float s2 = e4m3_decode_hw<0>(sb);
+        const float r = rtab[sb];
         const float s2k = __builtin_ldexpf(s2, kfold);   // k_j folded into the dequantized P
 #pragma unroll
         for (int w = 0; w < 2; ++w) {

@@ -38,6 +38,23 @@ __global__ __launch_bounds__(256) void cvt_u8_kernel(const float* __restrict__ x
   if (i < n) y[i] = (uint8_t)(__builtin_amdgcn_cvt_pk_u8_f32(x[i], 0, 0u) & 0xFFu);
 }
 
+// the E4M3 byte v_cvt_pk_fp8_f32 makes of x[i], and v_cvt_f32_fp8 of every byte value
+__global__ __launch_bounds__(256) void cvt_fp8_kernel(const float* __restrict__ x, uint8_t* __restrict__ y, int n,
+                                                      float* __restrict__ dec) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] = (uint8_t)(__builtin_amdgcn_cvt_pk_fp8_f32(x[i], 0.0f, 0, false) & 0xFF);
+  if (i < 256) dec[i] = __builtin_amdgcn_cvt_f32_fp8(i, 0);
+}
+
+// bf16 pairs of v_cvt_scalef32_pk_bf16_fp4: code byte c[i] (two E2M1 codes) times scale s[i]
+__global__ __launch_bounds__(256) void cvt_bf16_fp4_kernel(const uint8_t* __restrict__ c, const float* __restrict__ s,
+                                                           uint32_t* __restrict__ y, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const auto r = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4((uint32_t)c[i], s[i], 0);
+  y[i] = __builtin_bit_cast(uint32_t, r);
+}
+
 __global__ __launch_bounds__(256) void exp2_kernel(const float* __restrict__ x, float* __restrict__ y, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) y[i] = __builtin_amdgcn_exp2f(x[i]);
@@ -118,6 +135,20 @@ int sage_probe_cvt_fp4(const float* x, uint8_t* codes, int n, float scale, hipSt
 int sage_probe_cvt_u8(const float* x, uint8_t* y, int n, hipStream_t stream) {
   if (!x || !y || n < 1) return 1;
   hipLaunchKernelGGL(cvt_u8_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, x, y, n);
+  return st(hipGetLastError());
+}
+
+// y: n bytes, the E4M3 byte of x[i]; dec: 256 floats, the decoded value of every byte
+int sage_probe_cvt_fp8(const float* x, uint8_t* y, int n, float* dec, hipStream_t stream) {
+  if (!x || !y || !dec || n < 256) return 1;
+  hipLaunchKernelGGL(cvt_fp8_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, x, y, n, dec);
+  return st(hipGetLastError());
+}
+
+// y: n words, the two bf16 values (low half: low nibble of c[i]) scaled by s[i]
+int sage_probe_cvt_bf16_fp4(const uint8_t* c, const float* s, uint32_t* y, int n, hipStream_t stream) {
+  if (!c || !s || !y || n < 1) return 1;
+  hipLaunchKernelGGL(cvt_bf16_fp4_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, c, s, y, n);
   return st(hipGetLastError());
 }
 

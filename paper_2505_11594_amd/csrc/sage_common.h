@@ -83,6 +83,16 @@ __device__ __forceinline__ float e4m3_decode(uint32_t b) {
   if (e == 0) return __builtin_ldexpf((float)m, -9);
   return __builtin_ldexpf((float)(8u + m), (int)e - 10);
 }
+// The same codec in one instruction each: gfx950's v_cvt_pk_fp8_f32 (OCP
+// E4M3, nearest even) equals e4m3_encode on [0, 448] -- every rounding
+// midpoint and the subnormal range included -- and v_cvt_f32_fp8 equals
+// e4m3_decode on every code; values >= 448 are clamped first, as e4m3_encode
+// saturates.  Byte `sel` of `word` is decoded.
+__device__ __forceinline__ uint32_t e4m3_encode_hw(float s) {
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(__builtin_fminf(s, 448.0f), 0.0f, 0, false) & 0xFFu;
+}
+template <int SEL>
+__device__ __forceinline__ float e4m3_decode_hw(uint32_t word) { return __builtin_amdgcn_cvt_f32_fp8((int)word, SEL); }
 
 // ---- FP4 (E2M1) conversion ----------------------------------------------
 // v_cvt_scalef32_pk_fp4_f32 rounds to nearest even, saturates at +-6 and keeps

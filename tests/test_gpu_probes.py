@@ -9,6 +9,11 @@ checked against independent CPU definitions.
   treats an FP4 or INT8 code of P as tie-ambiguous; and it must never decrease
   its output as its argument grows, on every fp32 in [-130, 0];
 - v_cvt_pk_u8_f32 against rint with clamping to [0, 255];
+- v_cvt_pk_fp8_f32 / v_cvt_f32_fp8 against the oracle's E4M3 codec (the NV16
+  kernel encodes and decodes its second-level P scales with them), on every
+  rounding midpoint of [0, 448] and a sweep of the range;
+- v_cvt_scalef32_pk_bf16_fp4: it applies only the power-of-two part of its
+  scale operand, so an E4M3 scale cannot be folded into it;
 - the register layouts of the FP4 block-scaled, int8 and bf16 32x32 MFMAs
   against numpy products (and, for FP4, the oracle's exact FP4MM).
 """
@@ -37,6 +42,8 @@ def P():
     L.sage_probe_cvt_fp4.argtypes = [vp, vp, ctypes.c_int, ctypes.c_float, vp]
     L.sage_probe_exp2.argtypes = [vp, vp, ctypes.c_int, vp]
     L.sage_probe_cvt_u8.argtypes = [vp, vp, ctypes.c_int, vp]
+    L.sage_probe_cvt_fp8.argtypes = [vp, vp, ctypes.c_int, vp, vp]
+    L.sage_probe_cvt_bf16_fp4.argtypes = [vp, vp, vp, ctypes.c_int, vp]
     L.sage_probe_mfma_fp4.argtypes = [vp] * 6
     L.sage_probe_mfma_i8.argtypes = [vp] * 4
     L.sage_probe_mfma_bf16.argtypes = [vp] * 4
@@ -197,3 +204,50 @@ def test_mfma_bf16_layout(P):
     run(P.sage_probe_mfma_bf16, dptr(ad), dptr(bd_), dptr(cd))
     af, bf = wl.from_bits(a, 1).astype(np.float64), wl.from_bits(b, 1).astype(np.float64)
     assert np.array_equal(cd.cpu().numpy(), (af @ bf.T).astype(np.float32))
+
+
+def e4m3_values():
+    return np.array([oracle.e4m3_decode(c) for c in range(127)], dtype=np.float64)
+
+
+def test_cvt_fp8_matches_the_e4m3_definition(P):
+    """Every midpoint between neighbouring E4M3 values (and 3 ulp either side),
+    a strided sweep of [2^-12, 460], zero and the saturation region [448, 460]:
+    the hardware byte equals the oracle's encoder (nearest even, saturation at
+    448); every code decodes to the oracle's value."""
+    torch = torch_dev()
+    vals = e4m3_values()
+    xs = []
+    for m in (vals[:-1] + vals[1:]) / 2:
+        b = int(np.float32(m).view(np.uint32))
+        xs.append((np.arange(-3, 4, dtype=np.int64) + b).astype(np.uint32).view(np.float32))
+    lo, hi = int(np.float32(2.0 ** -12).view(np.uint32)), int(np.float32(460.0).view(np.uint32))
+    xs.append(np.arange(lo, hi, 997, dtype=np.int64).astype(np.uint32).view(np.float32))
+    xs.append(np.array([0.0, 448.0, 450.0, 459.0, 2.0 ** -10, 2.0 ** -11, 1e-30], dtype=np.float32))
+    x = np.concatenate(xs)
+    xd = torch.from_numpy(x).cuda()
+    y = torch.zeros(x.size, dtype=torch.uint8, device="cuda:0")
+    dec = torch.zeros(256, dtype=torch.float32, device="cuda:0")
+    run(P.sage_probe_cvt_fp8, dptr(xd), dptr(y), x.size, dptr(dec))
+    ref = np.array([oracle.e4m3_encode(float(v)) for v in x], dtype=np.uint8)
+    got = y.cpu().numpy()
+    bad = np.flatnonzero(got != ref)
+    assert bad.size == 0, "x=%r: hardware %02x, oracle %02x" % (float(x[bad[0]]), got[bad[0]], ref[bad[0]])
+    d = dec.cpu().numpy()[:127]
+    assert np.array_equal(d, vals.astype(np.float32))
+
+
+def test_cvt_bf16_fp4_applies_only_the_power_of_two_part_of_the_scale(P):
+    torch = torch_dev()
+    e2 = np.array([oracle.e2m1_decode(c) for c in range(16)])
+    vals = e4m3_values()[1:]
+    byte = np.tile(np.arange(256), vals.size).astype(np.uint8)
+    sc = np.repeat(vals, 256).astype(np.float32)
+    pow2 = 2.0 ** np.floor(np.log2(sc.astype(np.float64)))
+    lo = (e2[byte & 15] * pow2).astype(np.float32).view(np.uint32) >> 16      # exact in bf16
+    hi = (e2[byte >> 4] * pow2).astype(np.float32).view(np.uint32) >> 16
+    y = torch.zeros(byte.size, dtype=torch.int32, device="cuda:0")
+    bd_, sd = torch.from_numpy(byte).cuda(), torch.from_numpy(sc).cuda()      # held until the kernel has run
+    run(P.sage_probe_cvt_bf16_fp4, dptr(bd_), dptr(sd), dptr(y), byte.size)
+    got = y.cpu().numpy().view(np.uint32)
+    assert np.array_equal(got, (lo | (hi << 16)).astype(np.uint32))
