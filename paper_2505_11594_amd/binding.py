@@ -120,6 +120,27 @@ def _shape(t):
     return tuple(int(s) for s in t.shape)
 
 
+def _check_tensor(t, what: str, shape, dtype, device):
+    """A caller-supplied buffer must match what the kernels will write or read
+    (the C ABI receives bare pointers and cannot check it)."""
+    if not t.is_contiguous() or t.device != device or t.dtype != dtype or tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must be a contiguous %s tensor of shape %s on %s, got %s %s on %s"
+                         % (what, dtype, tuple(shape), device, t.dtype, tuple(t.shape), t.device))
+
+
+def _check_workspace(ws, device):
+    import torch
+    if ws.dtype != torch.uint8 or ws.dim() != 1 or not ws.is_contiguous() or ws.device != device:
+        raise ValueError("workspace must be a contiguous 1-d uint8 tensor on %s" % device)
+
+
+def _check_quantized(pair, what: str, nbytes, device):
+    import torch
+    for t, n, part in zip(pair[:2], nbytes, ("codes", "scales")):
+        if t.dtype != torch.uint8 or not t.is_contiguous() or t.device != device or t.numel() != n:
+            raise ValueError("%s %s must be %d contiguous uint8 bytes on %s" % (what, part, n, device))
+
+
 def quant_sizes(role: int, B: int, H: int, N: int, D: int, fmt: int):
     c, s = ctypes.c_size_t(), ctypes.c_size_t()
     _check("sage_quant_sizes", lib().sage_quant_sizes(role, B, H, N, D, fmt, ctypes.byref(c), ctypes.byref(s)))
@@ -159,6 +180,11 @@ def _out(q, out_f32: bool):
     return torch.empty(q.shape, dtype=torch.float32 if out_f32 else q.dtype, device=q.device)
 
 
+def _check_o(o, q, out_f32: bool):
+    import torch
+    _check_tensor(o, "out", q.shape, torch.float32 if out_f32 else q.dtype, q.device)
+
+
 def sage_attn_fp4_fwd(q, k, v, causal: bool = False, fmt: int = SAGE_FMT_MXFP4, out_f32: bool = True,
                       out=None, workspace=None):
     """O = attention(Q, K, V) through the FP4 path.  With ``workspace`` (a uint8 device
@@ -168,6 +194,9 @@ def sage_attn_fp4_fwd(q, k, v, causal: bool = False, fmt: int = SAGE_FMT_MXFP4, 
         raise ValueError("q, k, v must have the same shape")
     fmt = fmt | _in_flag(q) | (SAGE_OUT_F32 if out_f32 else 0)
     o = _out(q, out_f32) if out is None else out
+    _check_o(o, q, out_f32)
+    if workspace is not None:
+        _check_workspace(workspace, q.device)
     if workspace is None:
         rc = lib().sage_attn_fp4_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, H, N, D, int(bool(causal)), fmt, _stream())
         _check("sage_attn_fp4_fwd", rc)
@@ -185,9 +214,12 @@ def sage_attn_fp4_fwd_prequant(qq, kq, vq, shape, causal: bool = False, fmt: int
     B, H, N, D = shape
     fmt = fmt | (SAGE_IN_BF16 if in_bf16 else SAGE_IN_FP16) | (SAGE_OUT_F32 if out_f32 else 0)
     dev = qq[0].device
+    for pair, role, what in ((qq, SAGE_ROLE_Q, "q"), (kq, SAGE_ROLE_K, "k"), (vq, SAGE_ROLE_V, "v")):
+        _check_quantized(pair, what, quant_sizes(role, B, H, N, D, fmt), dev)
+    odt = torch.float32 if out_f32 else (torch.bfloat16 if in_bf16 else torch.float16)
     if out is None:
-        out = torch.empty(shape, dtype=torch.float32 if out_f32 else (torch.bfloat16 if in_bf16 else torch.float16),
-                          device=dev)
+        out = torch.empty(shape, dtype=odt, device=dev)
+    _check_tensor(out, "out", shape, odt, dev)
     rc = lib().sage_attn_fp4_fwd_prequant(_ptr(qq[0]), _ptr(qq[1]), _ptr(kq[0]), _ptr(kq[1]), _ptr(vq[0]),
                                           _ptr(vq[1]), _ptr(out), B, H, N, D, int(bool(causal)), fmt, _stream())
     _check("sage_attn_fp4_fwd_prequant", rc)
@@ -199,6 +231,7 @@ def sage_attn_bf16_fwd(q, k, v, causal: bool = False, out_f32: bool = True, out=
     B, H, N, D = _shape(q)
     flags = _in_flag(q) | (SAGE_OUT_F32 if out_f32 else 0)
     o = _out(q, out_f32) if out is None else out
+    _check_o(o, q, out_f32)
     rc = lib().sage_attn_bf16_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, H, N, D, int(bool(causal)), flags, _stream())
     _check("sage_attn_bf16_fwd", rc)
     return o
@@ -247,9 +280,13 @@ def sage_attn_int8_fwd(q, k, v, causal: bool = False, flags: int = 0, out_f32: b
         raise ValueError("q, k, v must have the same shape")
     flags = flags | _in_flag(q) | (SAGE_OUT_F32 if out_f32 else 0)
     o = _out(q, out_f32) if out is None else out
+    _check_o(o, q, out_f32)
     L = None
     if lse:
         L = torch.empty((B, H, N), dtype=torch.float32, device=q.device) if lse_out is None else lse_out
+        _check_tensor(L, "lse_out", (B, H, N), torch.float32, q.device)
+    if workspace is not None:
+        _check_workspace(workspace, q.device)
     if workspace is None:
         rc = lib().sage_attn_int8_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(L), B, H, N, D, int(bool(causal)),
                                       flags, _stream())
@@ -269,6 +306,11 @@ def sage_attn_int8_fwd_prequant(qq, kq, vq, shape, causal: bool = False, in_bf16
     B, H, N, D = shape
     flags = flags | (SAGE_IN_BF16 if in_bf16 else SAGE_IN_FP16) | (SAGE_OUT_F32 if out_f32 else 0)
     dev = qq[0].device
+    for pair, role, what in ((qq, SAGE_ROLE_Q, "q"), (kq, SAGE_ROLE_K, "k"), (vq, SAGE_ROLE_V, "v")):
+        cb, sb = quant_int8_sizes(role, B, H, N, D, flags & SAGE_BKV64)
+        for t, n, part, dt in ((pair[0], cb, "codes", torch.int8), (pair[1], sb // 4, "scales", torch.float32)):
+            if t.dtype != dt or not t.is_contiguous() or t.device != dev or t.numel() != n:
+                raise ValueError("%s %s must be %d contiguous %s elements on %s" % (what, part, n, dt, dev))
     out = torch.empty(shape, dtype=torch.float32 if out_f32 else (torch.bfloat16 if in_bf16 else torch.float16),
                       device=dev)
     L = torch.empty((B, H, N), dtype=torch.float32, device=dev) if lse else None
@@ -300,9 +342,16 @@ def sage_attn_int8_bwd(q, k, v, o, lse, dout, causal: bool = False, flags: int =
         raise ValueError("o must be the fp32 forward output")
     if tuple(lse.shape) != (B, H, N) or lse.dtype != torch.float32 or not lse.is_contiguous():
         raise ValueError("lse must be fp32 [B,H,N]")
+    for t, what in ((k, "k"), (v, "v"), (dout, "dout"), (o, "o"), (lse, "lse")):
+        if t.device != q.device:
+            raise ValueError("%s must be on %s" % (what, q.device))
     flags = flags | _in_flag(q)
     dq, dk, dv = out if out is not None else [torch.empty((B, H, N, D), dtype=torch.float32, device=q.device)
                                               for _ in range(3)]
+    for t, what in ((dq, "dq"), (dk, "dk"), (dv, "dv")):
+        _check_tensor(t, what, (B, H, N, D), torch.float32, q.device)
+    if workspace is not None:
+        _check_workspace(workspace, q.device)
     ptrs = [_ptr(t) for t in (q, k, v, o, lse, dout, dq, dk, dv)]
     if workspace is None:
         _check("sage_attn_int8_bwd", lib().sage_attn_int8_bwd(*ptrs, B, H, N, D, int(bool(causal)), flags, _stream()))

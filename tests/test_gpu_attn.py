@@ -171,3 +171,31 @@ def test_attn_closed_form_q_zero():
     vdeq = E2M1[vc[0, 0]] * np.repeat(2.0 ** (vs[0, 0].astype(np.float64) - 127), 32, axis=1)
     expect = vdeq[:, :300].mean(axis=1)
     assert np.abs(o - expect[None, :]).max() < 1e-5
+
+
+def test_binding_rejects_mismatched_buffers():
+    """The C ABI takes bare pointers, so the binding checks every caller-supplied
+    buffer against what the kernels will write or read; nothing is launched."""
+    torch = torch_dev()
+    q = torch.zeros((1, 2, 100, 64), dtype=torch.bfloat16, device="cuda:0")
+    bad_out = [torch.zeros((1, 2, 100, 64), dtype=torch.bfloat16, device="cuda:0"),      # fp32 expected
+               torch.zeros((1, 2, 100, 32), dtype=torch.float32, device="cuda:0"),
+               torch.zeros((1, 2, 64, 100), dtype=torch.float32, device="cuda:0").transpose(2, 3)]
+    for o in bad_out:
+        with pytest.raises(ValueError):
+            bd.sage_attn_fp4_fwd(q, q, q, out=o)
+        with pytest.raises(ValueError):
+            bd.sage_attn_bf16_fwd(q, q, q, out=o)
+    with pytest.raises(ValueError):
+        bd.sage_attn_fp4_fwd(q, q, q, workspace=torch.zeros(1 << 20, dtype=torch.float32, device="cuda:0"))
+    qq = bd.sage_quant_fp4(q, bd.SAGE_ROLE_Q)
+    kq = bd.sage_quant_fp4(q, bd.SAGE_ROLE_K)
+    vq = bd.sage_quant_fp4(q, bd.SAGE_ROLE_V)
+    with pytest.raises(ValueError):      # K^ holds Np = 128 rows, Q^ holds N = 100
+        bd.sage_attn_fp4_fwd_prequant(kq[:2], kq[:2], vq[:2], (1, 2, 100, 64))
+    with pytest.raises(ValueError):
+        bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (1, 2, 100, 64), out_f32=False,
+                                      out=torch.zeros((1, 2, 100, 64), dtype=torch.float32, device="cuda:0"))
+    o = bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (1, 2, 100, 64))      # the matching call runs
+    torch.cuda.synchronize()
+    assert o.shape == (1, 2, 100, 64) and o.dtype == torch.float32

@@ -201,3 +201,22 @@ def test_attn_int8_workloads_sampled_rows(ci):
     check_lse(L.reshape(-1)[torch_dev().from_numpy(rows).to(L.device)].cpu().numpy(), lref, w.name + " int8")
     ex = oracle.exact_attn(q, k, v, w.in_dtype, w.causal, rows=rows)
     say("int8 accuracy vs exact (sampled rows)", oracle.metrics(ex, got), cnt)
+
+
+def test_binding_rejects_mismatched_buffers():
+    torch = torch_dev()
+    q = torch.zeros((1, 2, 100, 64), dtype=torch.bfloat16, device="cuda:0")
+    f32 = lambda *s: torch.zeros(s, dtype=torch.float32, device="cuda:0")
+    with pytest.raises(ValueError):
+        bd.sage_attn_int8_fwd(q, q, q, out=torch.zeros_like(q))
+    with pytest.raises(ValueError):
+        bd.sage_attn_int8_fwd(q, q, q, lse_out=f32(1, 2, 64))
+    qq = bd.sage_quant_int8(q, bd.SAGE_ROLE_Q)
+    kq = bd.sage_quant_int8(q, bd.SAGE_ROLE_K)
+    vq = bd.sage_quant_int8(q, bd.SAGE_ROLE_V)
+    with pytest.raises(ValueError):      # K^ holds Np = 128 rows, Q^ holds N = 100
+        bd.sage_attn_int8_fwd_prequant(kq[:2], kq[:2], vq[:2], (1, 2, 100, 64))
+    o, L = bd.sage_attn_int8_fwd(q, q, q)
+    with pytest.raises(ValueError):
+        bd.sage_attn_int8_bwd(q, q, q, o, L, q, out=[f32(1, 2, 100, 64), f32(1, 2, 100, 64), torch.zeros_like(q)])
+    torch.cuda.synchronize()
