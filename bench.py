@@ -43,6 +43,18 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def warm(torch, fn, min_calls: int = 3, min_s: float = 0.1):
+    """Run fn until at least min_calls launches and min_s seconds have passed, so
+    that a timed block after host-side work (input generation, quantization)
+    does not start on a GPU whose clocks are still ramping."""
+    t0 = time.perf_counter()
+    n = 0
+    while n < min_calls or time.perf_counter() - t0 < min_s:
+        fn()
+        torch.cuda.synchronize()
+        n += 1
+
+
 def kernel_source_sha() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
@@ -189,8 +201,7 @@ def other_configs(torch, bd, wl, steps):
             fk = fmt | (bd.bkv_flag(w.bkv) if f == wl.FMT_MX else 0)
             run = lambda: bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (w.B, w.H, w.N, w.D), causal=w.causal,
                                                          fmt=fk, out=o)
-            run()
-            torch.cuda.synchronize()
+            warm(torch, run)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             n = max(3, min(steps, 10))
             e0.record()
@@ -291,7 +302,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the attention-kernel timings of the other workloads")
@@ -447,8 +458,7 @@ def main():
                             dtype=torch.uint8, device=dev)
         step_sq = lambda: bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=fmt_sq, out_f32=True, out=o,
                                                workspace=ws_sq)
-        step_sq()
-        torch.cuda.synchronize()
+        warm(torch, step_sq)
         n_sq = max(3, min(args.steps, 10))
         e0.record()
         for _ in range(n_sq):
