@@ -130,8 +130,8 @@ size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt);
  * per row and tile, then phi of P~/s_P1 with R = 6 for E8M0 scales and
  * 448*6 for E4M3 scales) and O += FP4MM(P^, V^) * s_P1; O = O / l.
  * MXFP4 runs on block-scaled FP4 MFMA; NV16 (whose E4M3 scales at 16-element
- * granularity the MFMA cannot take) dequantizes exactly to bf16 and runs on
- * bf16 MFMA.
+ * granularity the MFMA cannot take) dequantizes exactly to f16 and runs on
+ * f16 MFMA.
  * With SAGE_SMOOTH_Q the scores get the smoothing-Q GEMV term described above
  * (both formats).
  * KV tiles (the granularity of s_P1) are 128 keys; SAGE_BKV64 takes 64,

@@ -1,15 +1,22 @@
 // NV16 (E2M1 codes, 16-element blocks, E4M3 scales -- the paper's NVFP4,
 // Sec. 3.1) attention forward for gfx950.  The block-scaled MFMA only takes
 // E8M0 scales at 32-element granularity, so this path dequantizes exactly to
-// bf16 (an E2M1 value times an E4M3 scale has at most 6 significant bits) and
-// runs both products on v_mfma_f32_32x32x16_bf16:
+// f16 and runs both products on v_mfma_f32_32x32x16_f16.  An E2M1 value times
+// an E4M3 scale has at most 6 significant bits and lies in [2^-10, 2688], so
+// f16 holds it exactly.  An E4M3 scale s is M * 2^X with an integer M < 16,
+// so code * s is v_cvt_scalef32_pk_f16_fp4 (code * 2^X, exact) times M
+// (v_pk_mul_f16, exact): one convert and one packed multiply per two values.
 //   * Q^ is dequantized once into the B-operand registers;
 //   * each K^ / V^T tile arrives as codes + scales (4.5 bits per element),
-//     staged in registers a tile ahead and dequantized into bf16 LDS tiles;
+//     staged in registers a tile ahead and dequantized into f16 LDS tiles;
 //   * P~ gets the two-level quantization of Sec. 3.2 with R = 448 * 6 in
 //     registers: the first level as in the MXFP4 kernel, the second level an
 //     E4M3 scale per 16 keys (round to nearest even of blockmax/6), E2M1 codes
-//     of P~2 / s, and the dequantized code * s fed to the MFMA in bf16.
+//     of P~2 / s, and the dequantized code * s * 2^k fed to the MFMA in f16.
+//     This is exact unless the tile's max lies more than 9 / c2 below the
+//     running max; then values under 2^-9 of the row's largest round into
+//     f16's subnormal range (an absolute error below 2^-25 there), and a
+//     tile with k < -31 contributes zero.
 // K^ is stored with the tokens of every 32-token group permuted (offset
 // 16h + 4g + r at position 8g + 4h + r), so the 16 scores a lane holds for one
 // 32-key subtile are one 16-key block of original keys and, split in halves,
@@ -20,6 +27,10 @@
 namespace sage {
 
 constexpr int NQ = 128;   // queries per workgroup (4 waves x 32)
+
+typedef _Float16 v2h __attribute__((ext_vector_type(2)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ v8h as_h(const v4i x) { return __builtin_bit_cast(v8h, x); }
 
 template <int D, int BKV>
 struct Nv16Stage {
@@ -50,32 +61,32 @@ struct Nv16Stage {
     }
   }
 
-  // 32 codes + two E4M3 scales -> 32 bf16 values in four 16-byte chunks
-  __device__ __forceinline__ static void dequant32(const v4i codes, uint32_t sc2, v4i out[4]) {
-    const float s0 = e4m3_decode_hw<0>(sc2), s1 = e4m3_decode_hw<1>(sc2);
+  // 32 codes + two E4M3 scales -> 32 f16 values in four 16-byte chunks
+  __device__ __forceinline__ static void dequant32(const v4i codes, uint32_t sc2, const float* ptab,
+                                                   const uint32_t* mtab, v4i out[4]) {
+    const uint32_t b0 = sc2 & 0xFFu, b1 = (sc2 >> 8) & 0xFFu;
+    const float x0 = ptab[b0], x1 = ptab[b1];
+    const v2h m0 = __builtin_bit_cast(v2h, mtab[b0]), m1 = __builtin_bit_cast(v2h, mtab[b1]);
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      const float s = (w < 2) ? s0 : s1;
       const uint32_t word = (uint32_t)codes[w];
       uint32_t o[4];
       static_for<4>([&](auto B_) {
         constexpr int b = decltype(B_)::value;
-        const auto f = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(word, 1.0f, b);   // exact E2M1 values
-        typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
-        const v2bf pb = {(__bf16)(f[0] * s), (__bf16)(f[1] * s)};                 // exact in bf16
-        o[b] = __builtin_bit_cast(uint32_t, pb);
+        const v2h h = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(word, w < 2 ? x0 : x1, b) * (w < 2 ? m0 : m1);
+        o[b] = __builtin_bit_cast(uint32_t, h);
       });
       out[w] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
     }
   }
 
-  __device__ __forceinline__ void store(uint8_t* lds, int tid) const {
+  __device__ __forceinline__ void store(uint8_t* lds, int tid, const float* ptab, const uint32_t* mtab) const {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int u = (tid + 256 * i) % KU;
       const int row = u / (D / 32), c = u % (D / 32);
       v4i q[4];
-      dequant32(kc[i], ksc[i], q);
+      dequant32(kc[i], ksc[i], ptab, mtab, q);
 #pragma unroll
       for (int w = 0; w < 4; ++w)
         *reinterpret_cast<v4i*>(lds + T::K_OFF + row * T::KROW + bswz<T::KCH>(row, 4 * c + w) * 16) = q[w];
@@ -85,7 +96,7 @@ struct Nv16Stage {
       const int u = (tid + 256 * i) % VU;
       const int d = u / (BKV / 32), c = u % (BKV / 32);
       v4i q[4];
-      dequant32(vc[i], vsc[i], q);
+      dequant32(vc[i], vsc[i], ptab, mtab, q);
 #pragma unroll
       for (int w = 0; w < 4; ++w)
         *reinterpret_cast<v4i*>(lds + T::V_OFF + d * T::VROW + bswz<T::VCH>(d, 4 * c + w) * 16) = q[w];
@@ -108,7 +119,10 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   constexpr int NDB = D / 32;
   constexpr int BIAS_OFF = T::BYTES, LBYTES = T::BYTES + (SQ ? BKV * 4 : 0);   // bias of the tile's keys
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][LBYTES];
-  __shared__ float rtab[128];   // fl32(1 / s) of every E4M3 code s (0 for s = 0): the second level's reciprocal
+  // per E4M3 code b (s = M * 2^X): rtab = fl32(1 / s) (0 for s = 0), the second
+  // level's reciprocal; ptab = 2^X; mtab = {M, M} in f16
+  __shared__ float rtab[128], ptab[128];
+  __shared__ uint32_t mtab[128];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 31, hi = lane >> 5;
 
@@ -134,9 +148,8 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
       static_for<4>([&](auto B_) {
         constexpr int b = decltype(B_)::value;
         const auto f = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(word, 1.0f, b);
-        typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
-        const v2bf pb = {(__bf16)(f[0] * sc), (__bf16)(f[1] * sc)};
-        w[b] = __builtin_bit_cast(uint32_t, pb);
+        const v2h ph = {(_Float16)(f[0] * sc), (_Float16)(f[1] * sc)};   // exact in f16
+        w[b] = __builtin_bit_cast(uint32_t, ph);
       });
       qreg[s] = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
     }
@@ -154,7 +167,14 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   for (int db = 0; db < NDB; ++db) oacc[db] = v16f{};
   float m = -INFINITY, mc_old = -INFINITY, f_old = 0.0f, lsum_acc = 0.0f;
 
-  if (tid < 128) rtab[tid] = tid == 0 ? 0.0f : 1.0f / e4m3_decode_hw<0>((uint32_t)tid);   // visible after the first barrier
+  if (tid < 128) {
+    const int E = tid >> 3, man = tid & 7;
+    rtab[tid] = tid == 0 ? 0.0f : 1.0f / e4m3_decode_hw<0>((uint32_t)tid);
+    ptab[tid] = __builtin_ldexpf(1.0f, E ? E - 10 : -9);
+    const _Float16 M = (_Float16)(E ? 8 + man : man);
+    mtab[tid] = __builtin_bit_cast(uint32_t, v2h{M, M});
+  }
+  __syncthreads();
   Nv16Stage<D, BKV> stg;
   // smoothing Q: threads tid < BKV/4 stage 4 bias entries of the next tile
   const float* brow = SQ ? qkb + ((size_t)bh * nqt + qt) * Np : nullptr;
@@ -167,7 +187,7 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   };
   stg.load(kc, ks, vc, vs, bh, Np, 0, tid);
   bias_load(0);
-  stg.store(lds[0], tid);
+  stg.store(lds[0], tid, ptab, mtab);
   bias_store(lds[0]);
   __syncthreads();
 
@@ -189,7 +209,7 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
 #pragma unroll
         for (int s = 0; s < NKS; ++s) {
           const v4i a = *reinterpret_cast<const v4i*>(L + T::K_OFF + row * T::KROW + bswz<T::KCH>(row, 2 * s + hi) * 16);
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf(a), as_bf(qreg[s]), acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h(a), as_h(qreg[s]), acc, 0, 0, 0);
         }
         sacc[t] = acc;
       }
@@ -247,9 +267,10 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
         // second level: E4M3 scale of this lane's 16-key block
         const float amax = (bm[t] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(__builtin_fmaf(bm[t], c2, bias));
         const uint32_t sb = e4m3_encode_hw(amax / 6.0f);
-        const float s2 = e4m3_decode_hw<0>(sb);
         const float r = rtab[sb];
-        const float s2k = __builtin_ldexpf(s2, kfold);   // k_j folded into the dequantized P
+        // k_j folded into the power of two of the dequantized P; below 2^-31 the block is dropped
+        const float x2k = __builtin_ldexpf(ptab[sb], kfold < -31 ? -31 : kfold);
+        const v2h m2 = kfold < -31 ? v2h{(_Float16)0.0f, (_Float16)0.0f} : __builtin_bit_cast(v2h, mtab[sb]);
 #pragma unroll
         for (int w = 0; w < 2; ++w) {
           uint32_t pw[4];
@@ -263,10 +284,7 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
             // byte 0 gets the two codes; the other bytes are never read
             const float y0 = p0 * r;
             const uint32_t code = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(__float_as_uint(y0), y0, p1 * r, 1.0f, 0);
-            const auto dq = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(code, 1.0f, 0);
-            typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
-            const v2bf pb = {(__bf16)(dq[0] * s2k), (__bf16)(dq[1] * s2k)};
-            pw[i] = __builtin_bit_cast(uint32_t, pb);
+            pw[i] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(code, x2k, 0) * m2);
           }
           pk[2 * t + w] = v4i{(int)pw[0], (int)pw[1], (int)pw[2], (int)pw[3]};
         }
@@ -281,14 +299,14 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
 #pragma unroll
         for (int u = 0; u < NPK; ++u) {
           const v4i a = *reinterpret_cast<const v4i*>(L + vo[u] + 32 * db * T::VROW);
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf(a), as_bf(pk[u]), oacc[db], 0, 0, 0);
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h(a), as_h(pk[u]), oacc[db], 0, 0, 0);
         }
       m = m_new;
       mc_old = mc;
       f_old = f;
     }
     if (more) {
-      stg.store(lds[buf ^ 1], tid);
+      stg.store(lds[buf ^ 1], tid, ptab, mtab);
       bias_store(lds[buf ^ 1]);
     }
     __syncthreads();

@@ -55,6 +55,15 @@ __global__ __launch_bounds__(256) void cvt_bf16_fp4_kernel(const uint8_t* __rest
   y[i] = __builtin_bit_cast(uint32_t, r);
 }
 
+// f16 pairs of v_cvt_scalef32_pk_f16_fp4: code byte c[i] (two E2M1 codes) times scale s[i]
+__global__ __launch_bounds__(256) void cvt_f16_fp4_kernel(const uint8_t* __restrict__ c, const float* __restrict__ s,
+                                                          uint32_t* __restrict__ y, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const auto r = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4((uint32_t)c[i], s[i], 0);
+  y[i] = __builtin_bit_cast(uint32_t, r);
+}
+
 __global__ __launch_bounds__(256) void exp2_kernel(const float* __restrict__ x, float* __restrict__ y, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) y[i] = __builtin_amdgcn_exp2f(x[i]);
@@ -149,6 +158,13 @@ int sage_probe_cvt_fp8(const float* x, uint8_t* y, int n, float* dec, hipStream_
 int sage_probe_cvt_bf16_fp4(const uint8_t* c, const float* s, uint32_t* y, int n, hipStream_t stream) {
   if (!c || !s || !y || n < 1) return 1;
   hipLaunchKernelGGL(cvt_bf16_fp4_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, c, s, y, n);
+  return st(hipGetLastError());
+}
+
+// y: n words, the two f16 values (low half: low nibble of c[i]) scaled by s[i]
+int sage_probe_cvt_f16_fp4(const uint8_t* c, const float* s, uint32_t* y, int n, hipStream_t stream) {
+  if (!c || !s || !y || n < 1) return 1;
+  hipLaunchKernelGGL(cvt_f16_fp4_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, c, s, y, n);
   return st(hipGetLastError());
 }
 

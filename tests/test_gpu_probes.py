@@ -251,3 +251,26 @@ def test_cvt_bf16_fp4_applies_only_the_power_of_two_part_of_the_scale(P):
     run(P.sage_probe_cvt_bf16_fp4, dptr(bd_), dptr(sd), dptr(y), byte.size)
     got = y.cpu().numpy().view(np.uint32)
     assert np.array_equal(got, (lo | (hi << 16)).astype(np.uint32))
+
+
+def test_cvt_f16_fp4_applies_the_power_of_two_scale_exactly(P):
+    """v_cvt_scalef32_pk_f16_fp4 with power-of-two scales: E2M1 value times the
+    scale, exact in f16 (the NV16 kernel splits an E4M3 scale into this power of
+    two and an integer mantissa), nearest even into f16's subnormal range and to
+    zero below it."""
+    torch = torch_dev()
+    e2 = np.array([oracle.e2m1_decode(c) for c in range(16)])
+    exps = np.arange(-40, 6)
+    byte = np.tile(np.arange(256), exps.size).astype(np.uint8)
+    sc = np.repeat(2.0 ** exps, 256).astype(np.float32)
+    lo = (e2[byte & 15] * sc.astype(np.float64)).astype(np.float16).view(np.uint16).astype(np.uint32)
+    hi = (e2[byte >> 4] * sc.astype(np.float64)).astype(np.float16).view(np.uint16).astype(np.uint32)
+    y = torch.zeros(byte.size, dtype=torch.int32, device="cuda:0")
+    bd_, sd = torch.from_numpy(byte).cuda(), torch.from_numpy(sc).cuda()      # held until the kernel has run
+    P.sage_probe_cvt_f16_fp4.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_int, ctypes.c_void_p]
+    run(P.sage_probe_cvt_f16_fp4, dptr(bd_), dptr(sd), dptr(y), byte.size)
+    got = y.cpu().numpy().view(np.uint32)
+    exp = (lo | (hi << 16)).astype(np.uint32)
+    bad = np.flatnonzero(got != exp)
+    assert bad.size == 0, "byte %02x scale 2^%d: got %08x expected %08x" % (
+        byte[bad[0]], int(np.log2(sc[bad[0]])), got[bad[0]], exp[bad[0]])
