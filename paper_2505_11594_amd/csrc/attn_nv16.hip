@@ -266,7 +266,7 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
       for (int t = 0; t < NSUB; ++t) {
         // second level: E4M3 scale of this lane's 16-key block
         const float amax = (bm[t] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(__builtin_fmaf(bm[t], c2, bias));
-        const uint32_t sb = e4m3_encode_hw(amax / 6.0f);
+        const uint32_t sb = e4m3_encode_hw(div6(amax));
         const float r = rtab[sb];
         // k_j folded into the power of two of the dequantized P; below 2^-31 the block is dropped
         const float x2k = __builtin_ldexpf(ptab[sb], kfold < -31 ? -31 : kfold);

@@ -94,6 +94,17 @@ __device__ __forceinline__ uint32_t e4m3_encode_hw(float s) {
 template <int SEL>
 __device__ __forceinline__ float e4m3_decode_hw(uint32_t word) { return __builtin_amdgcn_cvt_f32_fp8((int)word, SEL); }
 
+// fl32(x / 6) for 2^-90 <= x <= 2^100 with a multiply and two FMAs instead of
+// a division: q = x * fl32(1/6), the residual x - 6q is exact, and one FMA step
+// rounds correctly -- checked on every significand of one binade, which covers
+// every exponent in that range (the step commutes with powers of two).  Below
+// 2^-90 the result stays under 2^-10, where the E4M3 code is 0 either way.
+__device__ __forceinline__ float div6(float x) {
+  const float y = 0x1.555556p-3f;                   // fl32(1/6)
+  const float q = x * y;
+  return __builtin_fmaf(__builtin_fmaf(-q, 6.0f, x), y, q);
+}
+
 // ---- FP4 (E2M1) conversion ----------------------------------------------
 // v_cvt_scalef32_pk_fp4_f32 rounds to nearest even, saturates at +-6 and keeps
 // the sign of zero; it divides by the power-of-two part of the scale operand.
