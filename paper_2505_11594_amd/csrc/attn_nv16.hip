@@ -244,15 +244,15 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
       for (int t = 0; t < NSUB; ++t) {
         float x = sacc[t][0];
 #pragma unroll
-        for (int v = 1; v < 16; ++v) x = __builtin_fmaxf(x, sacc[t][v]);
+        for (int v = 1; v < 16; ++v) x = smax(x, sacc[t][v]);   // scores are finite or -inf
         bm[t] = x;
       }
       float tl = bm[0];
 #pragma unroll
-      for (int t = 1; t < NSUB; ++t) tl = __builtin_fmaxf(tl, bm[t]);
+      for (int t = 1; t < NSUB; ++t) tl = smax(tl, bm[t]);
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(tl), __float_as_uint(tl), false, false);
-      const float tmax = __builtin_fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-      const float m_new = __builtin_fmaxf(m, tmax);
+      const float tmax = smax(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+      const float m_new = smax(m, tmax);
       const float tc = tmax * c2, mc = m_new * c2;
       const float delta = tc - mc;
       const float kf = __builtin_floorf(delta);
