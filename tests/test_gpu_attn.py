@@ -122,22 +122,25 @@ def test_attn_configs_full_size_sampled_rows(ci, fmt, bkv):
     say("accuracy vs exact (sampled rows)", oracle.metrics(ex, got), cnt)
 
 
-@pytest.mark.parametrize("fmt", [0, 1])
-def test_attn_deterministic_and_entry_points_agree(fmt):
+@pytest.mark.parametrize("fmt,bkv", [(0, 128), (1, 128), (0, 256), (0, 64)])
+def test_attn_deterministic_and_entry_points_agree(fmt, bkv):
+    """Two calls, the caller-workspace entry point and the prequantized one give
+    the same bits (each KV tile size of the format)."""
     torch = torch_dev()
     w = wl.CONFIGS[1]
     q, k, v = wl.generate(w, B=1, H=4, N=2048)
-    a = gpu_attn(q, k, v, w.in_dtype, False, fmt, 128)
-    b = gpu_attn(q, k, v, w.in_dtype, False, fmt, 128)
+    a = gpu_attn(q, k, v, w.in_dtype, False, fmt, bkv)
+    b = gpu_attn(q, k, v, w.in_dtype, False, fmt, bkv)
     assert torch.equal(a, b)
+    f = fmt | bd.bkv_flag(bkv)
     qd, kd, vd = (to_dev(x, w.in_dtype) for x in (q, k, v))
-    ws = torch.empty(bd.attn_fp4_workspace_size(1, 4, 2048, 128, fmt | bd.SAGE_IN_BF16 | bd.SAGE_OUT_F32),
+    ws = torch.empty(bd.attn_fp4_workspace_size(1, 4, 2048, 128, f | bd.SAGE_IN_BF16 | bd.SAGE_OUT_F32),
                      dtype=torch.uint8, device="cuda")
-    c = bd.sage_attn_fp4_fwd(qd, kd, vd, causal=False, fmt=fmt, workspace=ws)
+    c = bd.sage_attn_fp4_fwd(qd, kd, vd, causal=False, fmt=f, workspace=ws)
     qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q, fmt)
     kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K, fmt)
     vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V, fmt)
-    e = bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (1, 4, 2048, 128), fmt=fmt)
+    e = bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (1, 4, 2048, 128), fmt=f)
     torch.cuda.synchronize()
     assert torch.equal(a, c) and torch.equal(a, e)
 
