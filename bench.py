@@ -307,8 +307,10 @@ def main():
     ap.add_argument("--no-bf16", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the attention-kernel timings of the other workloads")
     ap.add_argument("--no-int8", action="store_true", help="skip the 8-bit attention forward")
-    ap.add_argument("--mode", choices=["full", "attn", "attn_int8", "attn_int8_bwd", "copy", "rates"], default="full",
-                    help="attn: only the attention kernel (for counter runs); attn_int8: only the 8-bit one; "
+    ap.add_argument("--mode", choices=["full", "attn", "attn_nv16", "attn_int8", "attn_int8_bwd", "copy", "rates"],
+                    default="full",
+                    help="attn: only the attention kernel (for counter runs); attn_nv16: only the NV16 kernel on "
+                         "B1 H24 N76800 D64; attn_int8: only the 8-bit one; "
                          "attn_int8_bwd: only the 8-bit backward (after one 8-bit forward for O and L); "
                          "copy: a plain 1 GiB device copy (calibrates FETCH_SIZE / WRITE_SIZE); "
                          "rates: instruction issue-rate microbenchmarks behind the VALU co-bound")
@@ -334,6 +336,23 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"mode": "copy", "bytes_per_copy": nbytes, "copies": args.warmup + args.steps}))
+        return
+
+    if args.mode == "attn_nv16":
+        w = wl.CONFIGS[4]
+        assert wl.FMT_NV16 in w.fmts
+        B, H, N, D = w.B, w.H, w.N, w.D
+        dt = torch.bfloat16 if w.in_dtype == wl.IN_BF16 else torch.float16
+        xs = [torch.from_numpy(a.view(np.int16)).view(dt).to("cuda:0") for a in wl.generate(w)]
+        nv = bd.SAGE_FMT_NV16_E4M3
+        qq, kq, vq = (bd.sage_quant_fp4(x, r, nv) for x, r in zip(xs, (bd.SAGE_ROLE_Q, bd.SAGE_ROLE_K, bd.SAGE_ROLE_V)))
+        o = torch.empty((B, H, N, D), dtype=torch.float32, device="cuda:0")
+        for _ in range(args.warmup + args.steps):
+            bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal,
+                                          fmt=nv | bd.bkv_flag(w.bkv), out=o)
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "attn_nv16", "workload": w.name, "launches": args.warmup + args.steps,
+                          "ops_per_launch": w.ops}))
         return
 
     w = wl.CONFIGS[2]
