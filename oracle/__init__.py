@@ -25,8 +25,14 @@ FMT_MX, FMT_NV16, FMT_NONE = 0, 1, 2
 IN_FP16, IN_BF16 = 0, 1
 ROLE_Q, ROLE_K, ROLE_V = 0, 1, 2
 NO_SMOOTH_K, DIRECT_P, R_LITERAL, SMOOTH_Q, OCP_SCALE = 1, 2, 4, 8, 16
+# the P step in the fused order a GPU evaluates it (orc_p_tile; for the test that bounds its differences)
+FUSED_P = 256
 # 8-bit attention (Algorithm 2) flags: NO_SMOOTH_K, and
 I8_STATIC_P, I8_IDENTITY, I8_DP_INT8 = 32, 64, 128
+# P^ of Algorithm 2 in the fused order a GPU evaluates it (for the test that bounds its differences)
+I8_FUSED_P = 512
+# P of Algorithm 3 in the fused order (for the test that bounds its differences)
+I8_FUSED_BWD = 1024
 
 _lib = None
 
@@ -90,7 +96,7 @@ def lib():
                                      [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int])
         L.orc_p_tile.restype = ctypes.c_int
         L.orc_p_tile.argtypes = ([ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_int, ctypes.c_int,
-                                  ctypes.c_uint] + [ctypes.c_void_p] * 9)
+                                  ctypes.c_uint] + [ctypes.c_void_p] * 12)
         L.orc_fp4mm.restype = ctypes.c_long
         L.orc_fp4mm.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_int] * 4 + [ctypes.c_void_p]
         L.orc_psi_block.restype = ctypes.c_float
@@ -231,13 +237,14 @@ def attn(q_bits, k_bits, v_bits, in_dtype: int, causal: bool, fmt: int, bkv: int
     rows = np.ascontiguousarray(rows, dtype=np.int64)
     out = np.zeros((rows.size, D), dtype=np.float32)
     tol = np.zeros(rows.size, dtype=np.float32)
-    cnt = np.zeros(4, dtype=np.int64)
+    cnt = np.zeros(5, dtype=np.int64)
     rc = lib().orc_attn2(_ptr(q_bits), _ptr(k_bits), _ptr(v_bits), in_dtype, B, H, N, D, int(bool(causal)),
                          fmt, bkv, bq, flags, _ptr(rows), rows.size, _ptr(out), _ptr(tol), _ptr(cnt),
                          nthreads or default_threads())
     if rc != 0:
         raise ValueError("orc_attn2: invalid arguments")
-    counters = dict(inexact_s=int(cnt[0]), inexact_o=int(cnt[1]), tie_codes=int(cnt[2]), skipped_tiles=int(cnt[3]))
+    counters = dict(inexact_s=int(cnt[0]), inexact_o=int(cnt[1]), tie_codes=int(cnt[2]), skipped_tiles=int(cnt[3]),
+                    alt_scales=int(cnt[4]))
     return out, tol, counters
 
 
@@ -259,24 +266,31 @@ def exact_attn(q_bits, k_bits, v_bits, in_dtype: int, causal: bool, rows=None, n
 
 
 def p_tile(S, m_old: float, D: int, fmt: int, flags: int = 0):
-    """One tile of the online softmax and the two-level quantization of P~.
+    """One tile of the online softmax and the two-level quantization of P~,
+    in Algorithm 1's order (FUSED_P: the fused order).
 
-    Returns dict(m_new, alpha, s1, rowsum, p2, codes, sbytes, tie_step, scale_tie)."""
+    Returns dict(m_new, alpha, s1, rowsum, p2, codes, sbytes, lo, hi, sb_lo, sb_hi, cont):
+    lo/hi bound every accepted P~2 value per key, sb_lo/sb_hi every accepted
+    block scale byte, cont = sum(hi - lo)."""
     S = np.ascontiguousarray(S, dtype=np.float32)
     bkv = S.size
     n = 1 if fmt == FMT_NONE else block_size(fmt)
     outs = [np.zeros(1, dtype=np.float32) for _ in range(4)]
     p2 = np.zeros(bkv, dtype=np.float32)
     codes = np.zeros(bkv, dtype=np.uint8)
-    sbytes = np.zeros(bkv // n, dtype=np.uint8)
-    tie = np.zeros(bkv, dtype=np.float64)
-    stie = np.zeros(bkv // n, dtype=np.uint8)
+    sbytes = np.zeros(max(bkv // n, 1), dtype=np.uint8)
+    lo = np.zeros(bkv, dtype=np.float64)
+    hi = np.zeros(bkv, dtype=np.float64)
+    sb_lo = np.zeros(max(bkv // n, 1), dtype=np.uint8)
+    sb_hi = np.zeros(max(bkv // n, 1), dtype=np.uint8)
+    cont = np.zeros(1, dtype=np.float64)
     rc = lib().orc_p_tile(_ptr(S), bkv, float(m_old), D, fmt, flags, *[_ptr(o) for o in outs],
-                          _ptr(p2), _ptr(codes), _ptr(sbytes), _ptr(tie), _ptr(stie))
+                          _ptr(p2), _ptr(codes), _ptr(sbytes), _ptr(lo), _ptr(hi), _ptr(sb_lo), _ptr(sb_hi),
+                          _ptr(cont))
     if rc != 0:
         raise ValueError("orc_p_tile: fully masked tile")
     return dict(m_new=float(outs[0][0]), alpha=float(outs[1][0]), s1=float(outs[2][0]), rowsum=float(outs[3][0]),
-                p2=p2, codes=codes, sbytes=sbytes, tie_step=tie, scale_tie=stie)
+                p2=p2, codes=codes, sbytes=sbytes, lo=lo, hi=hi, sb_lo=sb_lo, sb_hi=sb_hi, cont=float(cont[0]))
 
 
 def fp4mm(ac, as_, bc, bs, fmt: int):

@@ -59,6 +59,8 @@
 #define ORC_OCP_SCALE 16u    /* ablation (MX only): E8M0 block scales by the floor
                                 rule 2^(floor(log2 amax) - 2) for Q, K, V and the
                                 second level of P, values above 6 s clip to 6    */
+#define ORC_FUSED_P 256u     /* P~2 in the fused order a GPU evaluates it (for the
+                                test that bounds its differences; orc_p_tile)     */
 
 /* ------------------------------------------------------------------------ */
 /* 16-bit input widening (exact)                                             */
@@ -376,12 +378,13 @@ typedef struct {
   int64_t nrows;
   float* out;        /* [nrows][D] */
   float* tie_tol;    /* [nrows] extra tolerance from tie-ambiguous P codes, or NULL */
-  int64_t* counters; /* [4]: inexact S sums, inexact O sums, ambiguous P codes, skipped tiles */
+  int64_t* counters; /* [5]: inexact S sums, inexact O sums, ambiguous P codes, skipped tiles,
+                        P blocks with another accepted scale */
   head_t* heads;     /* [B*H], only the ones used are filled */
   char* head_used;
   int64_t next;
   pthread_mutex_t mu;
-  int64_t cnt[4];
+  int64_t cnt[5];
 } attn_job_t;
 
 static void two_code(float v, int* c2) {
@@ -476,169 +479,238 @@ static void free_head(head_t* h) {
 /* correctly rounded (to fp32) exp2: the fp64 exp2 rounded once */
 static float exp2_f32(float x) { return (float)exp2((double)x); }
 
+/* half an fp32 ulp at magnitude |x|: the largest error of one fp32 rounding
+   to a result of that size (subnormal results: half the smallest step) */
+static double hulp32(double x) {
+  x = fabs(x);
+  if (x < 0x1p-126) return 0x1p-150;
+  int e;
+  frexp(x, &e);                      /* x = f 2^e, f in [0.5, 1): ulp = 2^(e-24) */
+  return ldexp(1.0, e - 25);
+}
+
 /* ------------------------------------------------------------------------ */
-/* One query row of Algorithm 1 (smoothing Q optional, flag ORC_SMOOTH_Q).   */
+/* orc_p_tile: one KV tile of one query row -- the online-softmax step and   */
+/* the two-level quantization of P~ (Algorithm 1; Sec. 3.2, Eq. two-level),  */
+/* evaluated in the order the paper writes them:                             */
 /*                                                                           */
-/* Readings (the paper does not fix these):                                  */
-/*  - smoothing Q: the block mean qbar_i is taken over the B_q rows of the   */
-/*    row's query block; the GEMV(qbar_i, K_j^T) uses the unquantized K' of  */
-/*    the smoothing-K step in fp32, as a chain of fp32 fused multiply-adds   */
-/*    in order of d starting from 0, and is added to the fp32 FP4MM result:  */
-/*    S = fl32(fl32(FP4MM) + GEMV).                                          */
-/*  - softmax scale 1/sqrt(D) is applied and exp is taken base 2:            */
-/*    P~_k = 2^{c2 (S_k - m)} with c2 = fl32(log2(e)/sqrt(D)).                */
-/*  - running max m and tile max t are kept in the raw score domain S.        */
-/*  - two-level (Sec. 3.2): s_P1 = rowmax(P~)/R, P~2 = P~ / s_P1.  Since      */
-/*    rowmax(P~) = 2^{c2 (t - m)}, P~2_k = R 2^{c2 (S_k - t)}; it is computed  */
-/*    in fp32 as exp2(fma(S_k, c2, fl32(log2 R - fl32(t c2)))).  R = 448*6    */
-/*    for E4M3 scales; with E8M0 scales R = 6 (maps the tile row max onto    */
-/*    the largest FP4 value; ORC_R_LITERAL keeps 448*6 as an ablation).       */
-/*  - the second level is phi over each n-key block of P~2.  For MX the      */
-/*    block's E8M0 exponent is the smallest e with 6 2^e >= blockmax(P~2),    */
-/*    where blockmax(P~2) = 6 2^{c2 (bm - t)} (bm = block max of S) is read   */
-/*    in the score domain: e = ceil(fl32(fl32(bm - t) c2)) (for R = 6), so    */
-/*    the decision does not depend on the exp implementation.  Values that    */
-/*    round above 6 2^e saturate to code 6 (E2M1 saturation).                */
-/*  - l accumulates the unquantized P~ (Algorithm 1): the tile's            */
-/*    rowsum(P~) is fl32(s_P1 * sum_k P~2_k) with a sequential fp32 sum.      */
-/*  - O_new = fl32(fl32(alpha O) + fl32(FP4MM(P^2, V^) s_P1)),               */
-/*    alpha = 2^{c2 (m_old - m_new)} (0 on the first visited tile).          */
-/*  - the final O = fl32(O / l).                                             */
-/*  - causal: key k is visible to query i iff k <= i; fully masked tiles are  */
-/*    skipped; keys >= N are masked.                                         */
-/* tie_tol: the bound on |O| change if any P code whose pre-rounding value   */
-/* lies within TIE_REL of an E2M1 rounding boundary took the other            */
-/* neighbouring code (both are valid results when exp is evaluated in fp32   */
-/* to within a few ulp, which the paper leaves unspecified).                  */
-/* ------------------------------------------------------------------------ */
-#define TIE_REL (1.0 / 1048576.0) /* 8 ulp of fp32 */
-
-static int e2m1_tie_step(float y, double* step) {
-  /* y >= 0: if y lies within TIE_REL (relative) of a rounding midpoint,
-     return 1 and the distance between the two neighbouring grid values */
-  for (int i = 0; i < 7; ++i) {
-    double mid = 0.5 * ((double)E2M1_VAL[i] + E2M1_VAL[i + 1]);
-    if (fabs((double)y - mid) <= TIE_REL * mid) { *step = (double)E2M1_VAL[i + 1] - E2M1_VAL[i]; return 1; }
-  }
-  return 0;
-}
-
-static int e4m3_tie(float s) {
-  /* s > 0: within TIE_REL of a midpoint between two adjacent E4M3 values */
-  if (!(s > 0.0f) || s >= 448.0f) return 0;
-  for (int c = 0; c < 0x7E; ++c) {
-    double lo = orc_e4m3_decode((uint8_t)c), hi = orc_e4m3_decode((uint8_t)(c + 1));
-    double mid = 0.5 * (lo + hi);
-    if (fabs((double)s - mid) <= TIE_REL * mid) return 1;
-    if (hi > s * 2.0) break;
-  }
-  return 0;
-}
-
-/* ------------------------------------------------------------------------ */
-/* orc_p_tile: online-softmax update and two-level quantization of P~ for    */
-/* one query row and one KV tile (Algorithm 1; Sec. 3.2, Eq. two-level).     */
-/*  S[bkv]  : the tile's scores (fp32), -inf for masked keys; at least one    */
-/*            key is unmasked                                                */
-/*  m_old   : running max (raw score domain), -inf before the first tile      */
-/* outputs:                                                                  */
-/*  m_new, alpha = 2^{c2 (m_old - m_new)} (0 on the first tile),              */
-/*  s1 = rowmax(P~)/R (1 for direct quantization), rowsum = rowsum(P~),       */
-/*  p2[bkv] = P~2 (fp32), codes[bkv] (one per byte), sbytes[bkv/n] scale      */
-/*  bytes, tie_step[bkv] (0, or the grid step if the code is tie-ambiguous),  */
-/*  scale_tie[bkv/n] (NV16: the block scale is tie-ambiguous).               */
-/* fmt NONE: codes/sbytes untouched, p2 holds P~2 unquantized.               */
+/*   m_new = max(m_old, rowmax(S))                                           */
+/*   P~_k  = exp(S_k - m_new)        base 2 with the softmax scale (R7):     */
+/*           fl32(exp2(fl32(fl32(S_k c2) - fl32(m_new c2))))                  */
+/*   rowsum(P~) = sequential fp32 sum of the P~_k (l takes it unquantized)   */
+/*   alpha = exp(m_old - m_new) = fl32(exp2(fl32(fl32(m_old c2) - fl32(m_new c2)))), */
+/*           0 on the first visited tile                                     */
+/*   rho   = rowmax(P~) over the tile (R9)                                   */
+/*   s_P1  = fl32(rho / R)                                                   */
+/*   P~2_k = P~_k / s_P1, read as fl32(P~_k fl32(1/s_P1)) (R4)               */
+/*   (s_P2, P^2) = phi(P~2) over the n-key blocks of the tile (Sec. 3.1):    */
+/*           MX: e = smallest e with 6 2^e >= max of the block's P~2 values, */
+/*               clamped to [-127, 127] (R2); codes E2M1(P~2 2^-e);          */
+/*           NV16: s = E4M3(fl32(amax/6)), codes E2M1(fl32(P~2 fl32(1/s)))   */
+/*   s_P1 < 2^-126 (below the normal fp32 range, its reciprocal would       */
+/*           overflow) -> the tile adds nothing to O: s_P1 = 0, P^ = 0.      */
+/*                                                                           */
+/* R = 6 with E8M0 scales, 448*6 with E4M3 scales (R8); ORC_R_LITERAL keeps  */
+/* 448*6 with E8M0 (ablation).  ORC_DIRECT_P quantizes P~ itself (s_P1 = 1,  */
+/* ablation of Table 1(b)).                                                  */
+/*                                                                           */
+/* ORC_FUSED_P evaluates the same quantities in the fused order a GPU uses:  */
+/* P~2_k = exp2(fma(S_k, c2, fl32(fl32(log2 R) - fl32(t c2)))), the MX block */
+/* exponent from scores, e = max(ceil(fl32(fl32(bm - t) c2)), -126) with bm  */
+/* the block's largest score, s_P1 = fl32(exp2(fl32(t c2) - fl32(m c2))/R),  */
+/* rowsum = fl32(s_P1 sum P~2).  Equal in exact arithmetic; it exists so     */
+/* that a test can show every difference it makes lies inside the set of     */
+/* results the intervals below accept.                                       */
+/*                                                                           */
+/* Acceptance intervals (the paper fixes no fp32 evaluation order).  For     */
+/* each key, [lo, hi] holds every P~2 value that either evaluation can       */
+/* produce: the plain value above, and the fused value, whose log2 differs   */
+/* from the exact log2 R + c2 (S_k - t) (fp64 here) by at most               */
+/*   W_k = h(log2 R) + h(t c2) + h(B) + h(arg_k) + 2^-22/ln 2,               */
+/* h = half an fp32 ulp of each rounded intermediate (B = fl32(log2 R - t c2),*/
+/* arg_k = fl32(fma(S_k, c2, B))), the last term a 1-ulp exp2 plus its own   */
+/* rounding.  [sb_lo, sb_hi] holds every block scale byte either evaluation  */
+/* can choose: MX -- the plain exponent and ceil of the score-domain         */
+/* exponent c2 (bm - t) within its two roundings; NV16 -- E4M3 of amax/6 for */
+/* amax anywhere in the block max's interval (and the plain one).  The       */
+/* block holding the tile max has c2 (bm - t) = 0 exactly, so the fused      */
+/* choice there is 2^0, while the plain P~2 of that key lands within an ulp  */
+/* of 6 on either side: when it lands above, the plain rule takes 2^1 and    */
+/* both bytes are in the range.                                              */
+/* cont_out: sum over keys of (hi - lo), the bound on the move of the tile's */
+/* unquantized row sum between the two evaluations (in P~2 units).           */
 /* ------------------------------------------------------------------------ */
 int orc_p_tile(const float* S, int bkv, float m_old, int D, int fmt, unsigned flags,
                float* m_new_out, float* alpha_out, float* s1_out, float* rowsum_out,
-               float* p2, uint8_t* codes, uint8_t* sbytes, double* tie_step, uint8_t* scale_tie) {
+               float* p2, uint8_t* codes, uint8_t* sbytes, double* lo, double* hi,
+               uint8_t* sb_lo, uint8_t* sb_hi, double* cont_out) {
   const int n = (fmt == ORC_FMT_NONE) ? 1 : block_of(fmt);
-  const int direct = (flags & ORC_DIRECT_P) != 0;
+  const int direct = (flags & ORC_DIRECT_P) != 0, fused = (flags & ORC_FUSED_P) != 0;
   const float c2 = (float)(1.0 / (log(2.0) * sqrt((double)D)));
   const float R = (fmt == ORC_FMT_NV16 || (flags & ORC_R_LITERAL)) ? 448.0f * 6.0f : 6.0f;
   const float logR = (float)log2((double)R);
 
-  float t = -INFINITY;
+  float t = -INFINITY;                                  /* rowmax(S) of the tile */
   for (int kk = 0; kk < bkv; ++kk) if (S[kk] > t) t = S[kk];
   if (t == -INFINITY) return -1;
   const float m_new = m_old > t ? m_old : t;
-  volatile float tc = t * c2;
+  volatile float tc = t * c2;                           /* u = S c2 is monotone in S */
   volatile float mc_new = m_new * c2;
   float alpha = 0.0f;
   if (m_old != -INFINITY) { volatile float mc_old = m_old * c2; volatile float d = mc_old - mc_new; alpha = exp2_f32(d); }
 
-  /* first level: s_P1 = rowmax(P~)/R with rowmax(P~) = 2^{c2 (t - m_new)} */
-  float s1;
-  volatile float bias;
-  if (direct) { s1 = 1.0f; bias = -mc_new; }
-  else {
-    volatile float dt = tc - mc_new;
-    float rho = exp2_f32(dt);
-    volatile float q = rho / R;
-    s1 = q;
-    bias = logR - tc;
+  float s1, psum = 0.0f, rowsum;
+  if (fused) {
+    volatile float bias;
+    if (direct) { s1 = 1.0f; bias = -mc_new; }
+    else { volatile float dt = tc - mc_new; volatile float q = exp2_f32(dt) / R; s1 = q; bias = logR - tc; }
+    for (int kk = 0; kk < bkv; ++kk) {
+      p2[kk] = (S[kk] == -INFINITY) ? 0.0f : exp2_f32(fmaf(S[kk], c2, bias));
+      psum += p2[kk];
+    }
+    volatile float rs = s1 * psum;
+    rowsum = rs;
+  } else {
+    /* P~ = exp(S - m_new), its row sum and its row max */
+    float rho = 0.0f;
+    for (int kk = 0; kk < bkv; ++kk) {
+      float p = 0.0f;
+      if (S[kk] != -INFINITY) { volatile float u = S[kk] * c2; volatile float d = u - mc_new; p = exp2_f32(d); }
+      p2[kk] = p;
+      psum += p;
+      if (p > rho) rho = p;
+    }
+    rowsum = psum;
+    if (direct) s1 = 1.0f;
+    else {
+      /* s_P1 = rowmax(P~)/R; P~2 = P~/s_P1 */
+      volatile float q = rho / R;
+      s1 = q;
+    }
+    if (!direct && s1 < 0x1p-126f) {
+      /* s_P1 below the normal fp32 range (P~ underflows, or the tile lies
+         more than 126 binades under the running max): 1/s_P1 would overflow,
+         and the tile adds nothing to O */
+      s1 = 0.0f;
+      for (int kk = 0; kk < bkv; ++kk) p2[kk] = 0.0f;
+    } else if (!direct) {
+      volatile float r = 1.0f / s1;
+      for (int kk = 0; kk < bkv; ++kk) { volatile float y = p2[kk] * r; p2[kk] = y; }
+    }
   }
-  /* P~2 = R 2^{c2 (S - t)}, and the unquantized row sum */
-  float psum = 0.0f;
-  for (int kk = 0; kk < bkv; ++kk) {
-    p2[kk] = (S[kk] == -INFINITY) ? 0.0f : exp2_f32(fmaf(S[kk], c2, bias));
-    psum += p2[kk];
-    if (tie_step) tie_step[kk] = 0.0;
+  *m_new_out = m_new; *alpha_out = alpha; *s1_out = s1; *rowsum_out = rowsum;
+  if (cont_out) *cont_out = 0.0;
+
+  /* acceptance intervals of the P~2 values */
+  if (lo) {
+    volatile float B = logR - tc;
+    const double wfix = hulp32(logR) + hulp32(tc) + hulp32(B) + 0x1p-22 / log(2.0);
+    double cont = 0.0;
+    for (int kk = 0; kk < bkv; ++kk) {
+      if (S[kk] == -INFINITY) { lo[kk] = hi[kk] = 0.0; continue; }
+      if (direct) { lo[kk] = hi[kk] = p2[kk]; continue; }
+      const double pex = (double)R * exp2((double)c2 * ((double)S[kk] - (double)t));
+      const double W = wfix + hulp32(fmaf(S[kk], c2, B));
+      double flo = pex * exp2(-W), fhi = pex * exp2(W);
+      if (fhi < 0x1p-120) { flo = 0.0; fhi += 0x1p-147; } /* fp32 flushes or rounds to subnormal steps there */
+      lo[kk] = flo < p2[kk] ? flo : p2[kk];
+      hi[kk] = fhi > p2[kk] ? fhi : p2[kk];
+      cont += hi[kk] - lo[kk];
+    }
+    if (cont_out) *cont_out = cont;
   }
-  volatile float rs = s1 * psum;
-  *m_new_out = m_new; *alpha_out = alpha; *s1_out = s1; *rowsum_out = rs;
   if (fmt == ORC_FMT_NONE) return 0;
 
   /* second level: (s_P2, P^2) = phi(P~2) over n-key blocks */
   for (int b0 = 0; b0 < bkv; b0 += n) {
     const int blk = b0 / n;
-    if (scale_tie) scale_tie[blk] = 0;
+    float am = 0.0f, bm = -INFINITY;
+    for (int kk = b0; kk < b0 + n; ++kk) { if (p2[kk] > am) am = p2[kk]; if (S[kk] > bm) bm = S[kk]; }
     if (fmt == ORC_FMT_MX) {
-      float bm = -INFINITY;
-      for (int kk = b0; kk < b0 + n; ++kk) if (S[kk] > bm) bm = S[kk];
       int e;
-      if (bm == -INFINITY) e = -126;
-      else if (direct || (flags & (ORC_R_LITERAL | ORC_OCP_SCALE))) {
-        float am = 0.0f;
-        for (int kk = b0; kk < b0 + n; ++kk) if (p2[kk] > am) am = p2[kk];
-        e = (flags & ORC_OCP_SCALE) ? orc_e8m0_exponent_floor(am) : orc_e8m0_exponent(am);
+      if (fused && !direct && !(flags & (ORC_R_LITERAL | ORC_OCP_SCALE))) {
+        if (bm == -INFINITY) e = -126;
+        else { volatile float dd = bm - t; volatile float d2 = dd * c2; e = (int)ceilf(d2); }
+        if (e < -126) e = -126;
       } else {
-        /* blockmax(P~2) = 6 2^{c2 (bm - t)}; smallest e with 6 2^e >= it */
-        volatile float dd = bm - t;
-        volatile float d2 = dd * c2;
-        e = (int)ceilf(d2);
+        e = (flags & ORC_OCP_SCALE) ? orc_e8m0_exponent_floor(am) : orc_e8m0_exponent(am);
       }
-      /* P scales stay in the normal fp32 range: blocks below 2^-126 of the
-         tile max hold values that vanish next to it */
-      if (e < -126) e = -126;
       sbytes[blk] = (uint8_t)(e + 127);
-      for (int kk = b0; kk < b0 + n; ++kk) {
-        float y = ldexpf(p2[kk], -e);
-        codes[kk] = orc_e2m1_encode(y);
-        double step;
-        if (tie_step && e2m1_tie_step(y, &step)) tie_step[kk] = step;
+      for (int kk = b0; kk < b0 + n; ++kk) codes[kk] = orc_e2m1_encode(ldexpf(p2[kk], -e));
+      if (sb_lo) {
+        int elo = e, ehi = e;
+        if (!direct && bm != -INFINITY && !(flags & (ORC_R_LITERAL | ORC_OCP_SCALE))) {
+          /* the score-domain exponent: c2 (bm - t) after the roundings of
+             bm - t and of the product */
+          volatile float dd = bm - t;
+          const double x = (double)c2 * ((double)bm - (double)t);
+          /* bm = t (the block holding the tile max): both roundings are exact */
+          const double w = dd == 0.0f ? 0.0 : hulp32(dd) * (double)c2 + hulp32((double)dd * c2);
+          int a = (int)ceil(x - w), b = (int)ceil(x + w);
+          if (a < -126) a = -126;
+          if (b < -126) b = -126;
+          if (a < elo) elo = a;
+          if (b > ehi) ehi = b;
+        } else if (!direct && bm != -INFINITY) {
+          /* ablation rules on the value maximum: any value in the block max's interval */
+          double hm = 0.0, lm = 0.0;
+          for (int kk = b0; kk < b0 + n; ++kk) { if (hi[kk] > hm) hm = hi[kk]; if (lo[kk] > lm) lm = lo[kk]; }
+          int a = (flags & ORC_OCP_SCALE) ? orc_e8m0_exponent_floor((float)lm) : orc_e8m0_exponent((float)lm);
+          int b = (flags & ORC_OCP_SCALE) ? orc_e8m0_exponent_floor((float)hm) : orc_e8m0_exponent((float)hm);
+          if (a < elo) elo = a;
+          if (b > ehi) ehi = b;
+        }
+        sb_lo[blk] = (uint8_t)(elo + 127);
+        sb_hi[blk] = (uint8_t)(ehi + 127);
       }
     } else {
       uint8_t sb = orc_phi_block(p2 + b0, n, fmt, codes + b0);
       sbytes[blk] = sb;
-      float scale = orc_e4m3_decode(sb);
-      float am = 0.0f;
-      for (int kk = b0; kk < b0 + n; ++kk) if (p2[kk] > am) am = p2[kk];
-      volatile float q6 = am / 6.0f;
-      if (scale_tie && e4m3_tie(q6)) scale_tie[blk] = 1;
-      if (tie_step && scale > 0.0f) {
-        volatile float r = 1.0f / scale;
-        for (int kk = b0; kk < b0 + n; ++kk) {
-          volatile float y = p2[kk] * r;
-          double step;
-          if (e2m1_tie_step(y, &step)) tie_step[kk] = step;
-        }
+      if (sb_lo) {
+        /* E4M3(fl32(amax/6)) for amax anywhere in the block max's interval;
+           the division's own rounding widens it by an ulp */
+        double hm = 0.0, lm = 0.0;
+        for (int kk = b0; kk < b0 + n; ++kk) { if (hi[kk] > hm) hm = hi[kk]; if (lo[kk] > lm) lm = lo[kk]; }
+        uint8_t a = orc_e4m3_encode((float)(lm / 6.0 * (1.0 - 0x1p-23)));
+        uint8_t b = orc_e4m3_encode((float)(hm / 6.0 * (1.0 + 0x1p-23)));
+        sb_lo[blk] = a < sb ? a : sb;
+        sb_hi[blk] = b > sb ? b : sb;
       }
     }
   }
   return 0;
 }
 
+/* dequantized V^ of key k, channel c (zero past the padded tail) */
+static double vhat(const head_t* h, int c, int k) {
+  if (k >= h->Np) return 0.0;
+  return 0.5 * (double)h->vc2[(long)c * h->Np + k] * (double)h->vs[(long)c * (h->Np / h->n) + k / h->n];
+}
+
+/* the E2M1 code of a P~2 value at block scale byte sb: MX divides by the
+   power of two exactly, NV16 multiplies by fl32(1/s) (R4) */
+static uint8_t p_code(float y, uint8_t sb, int fmt) {
+  if (fmt == ORC_FMT_MX) return orc_e2m1_encode(ldexpf(y, -((int)sb - 127)));
+  const float s = orc_e4m3_decode(sb);
+  if (!(s > 0.0f)) return 0;
+  volatile float r = 1.0f / s;
+  volatile float q = y * r;
+  return orc_e2m1_encode(q);
+}
+
+/* largest change of a code's value (times the scale sc) when its P~2 value
+   is anywhere in [lo, hi], against the code c; the interval is widened by
+   2^-21 so that the rounding of y/sc to fp32 and of NV16's reciprocal never
+   narrows it */
+static double code_dev(double lo, double hi, double sc, uint8_t c) {
+  if (!(sc > 0.0)) return 0.0;
+  const double v = orc_e2m1_decode(c);
+  const double a = orc_e2m1_decode(orc_e2m1_encode((float)(lo * (1.0 - 0x1p-21) / sc)));
+  const double b = orc_e2m1_decode(orc_e2m1_encode((float)(hi * (1.0 + 0x1p-21) / sc)));
+  const double d = fabs(a - v) > fabs(b - v) ? fabs(a - v) : fabs(b - v);
+  return d * sc;
+}
+
 /* ------------------------------------------------------------------------ */
 /* One query row of Algorithm 1 (smoothing Q optional, flag ORC_SMOOTH_Q).   */
 /*                                                                           */
@@ -648,32 +720,26 @@ int orc_p_tile(const float* S, int bkv, float m_old, int D, int fmt, unsigned fl
 /*    the smoothing-K step in fp32, as a chain of fp32 fused multiply-adds   */
 /*    in order of d starting from 0, and is added to the fp32 FP4MM result:  */
 /*    S = fl32(fl32(FP4MM) + GEMV).                                          */
-/*  - softmax scale 1/sqrt(D) is applied and exp is taken base 2:            */
-/*    P~_k = 2^{c2 (S_k - m)} with c2 = fl32(log2(e)/sqrt(D)).                */
-/*  - running max m and tile max t are kept in the raw score domain S.        */
-/*  - two-level (Sec. 3.2): s_P1 = rowmax(P~)/R, P~2 = P~ / s_P1.  Since      */
-/*    rowmax(P~) = 2^{c2 (t - m)}, P~2_k = R 2^{c2 (S_k - t)}; it is computed  */
-/*    in fp32 as exp2(fma(S_k, c2, fl32(log2 R - fl32(t c2)))).  R = 448*6    */
-/*    for E4M3 scales; with E8M0 scales R = 6 (maps the tile row max onto    */
-/*    the largest FP4 value; ORC_R_LITERAL keeps 448*6 as an ablation).       */
-/*  - the second level is phi over each n-key block of P~2.  For MX the      */
-/*    block's E8M0 exponent is the smallest e with 6 2^e >= blockmax(P~2),    */
-/*    where blockmax(P~2) = 6 2^{c2 (bm - t)} (bm = block max of S) is read   */
-/*    in the score domain: e = ceil(fl32(fl32(bm - t) c2)) (for R = 6), so    */
-/*    the decision does not depend on the exp implementation.  Values that    */
-/*    round above 6 2^e saturate to code 6 (E2M1 saturation).                */
-/*  - l accumulates the unquantized P~ (Algorithm 1): the tile's            */
-/*    rowsum(P~) is fl32(s_P1 * sum_k P~2_k) with a sequential fp32 sum.      */
-/*  - O_new = fl32(fl32(alpha O) + fl32(FP4MM(P^2, V^) s_P1)),               */
-/*    alpha = 2^{c2 (m_old - m_new)} (0 on the first visited tile).          */
+/*  - the softmax step and the two-level quantization of each tile follow    */
+/*    Algorithm 1's order (orc_p_tile): P~, its row sum and row max, s_P1,   */
+/*    P~2 = P~/s_P1, phi(P~2).                                               */
+/*  - l = fl32(fl32(alpha l) + rowsum(P~)), over the unquantized P~.         */
+/*  - O_new = fl32(fl32(alpha O) + fl32(FP4MM(P^2, V^) s_P1)).               */
 /*  - the final O = fl32(O / l).                                             */
 /*  - causal: key k is visible to query i iff k <= i; fully masked tiles are  */
 /*    skipped; keys >= N are masked.                                         */
-/* tie_tol: the bound on |O| change if any P code whose pre-rounding value   */
-/* lies within TIE_REL of an E2M1 rounding boundary took the other            */
-/* neighbouring code (both are valid results when exp is evaluated in fp32   */
-/* to within a few ulp, which the paper leaves unspecified), or if an NV16   */
-/* block scale is itself tie-ambiguous.                                      */
+/* tie_tol: a bound on |O_c| - over the channels c - of the change between  */
+/* this result and any other accepted evaluation of the P step (orc_p_tile's */
+/* intervals).  Per tile and block it takes the larger of (a) the codes that */
+/* any value in a key's interval maps to at the block's own scale, and (b)   */
+/* for every other accepted block scale, the exact change of that block's    */
+/* contribution to O_c when its codes are re-derived at that scale, plus     */
+/* (a) at that scale; both weigh |V^_kc| and are scaled by s_P1, carried    */
+/* through alpha like O and divided by l at the end.  The row sum moves by   */
+/* at most s_P1 sum_k (hi - lo) per tile between evaluations (plus 2^-20 of  */
+/* the tile's row sum for the fp32 roundings of s_P1 and alpha); that moves  */
+/* O by at most max|V^| times it over l.  Tiles whose s_P1 lies below     */
+/* 2^-126 add a bound of bkv 2^-110 max|V^| (R 2^-126 per key, both ways).  */
 /* ------------------------------------------------------------------------ */
 static void attn_row(attn_job_t* J, long bh, int i, float* out, float* tol_out, int64_t* cnt) {
   head_t* h = &J->heads[bh];
@@ -709,10 +775,14 @@ static void attn_row(attn_job_t* J, long bh, int i, float* out, float* tol_out, 
   float* P2 = (float*)malloc(sizeof(float) * bkv);
   uint8_t* pc = (uint8_t*)malloc((size_t)bkv);
   uint8_t* psb = (uint8_t*)malloc((size_t)nblk + 1);
-  uint8_t* stie = (uint8_t*)malloc((size_t)nblk + 1);
-  double* tstep = (double*)malloc(sizeof(double) * bkv);
+  double* plo = (double*)malloc(sizeof(double) * bkv);
+  double* phi = (double*)malloc(sizeof(double) * bkv);
+  uint8_t* sblo = (uint8_t*)malloc((size_t)nblk + 1);
+  uint8_t* sbhi = (uint8_t*)malloc((size_t)nblk + 1);
+  double* tolc = (double*)calloc(D, sizeof(double));
+  double* blkc = (double*)calloc(D, sizeof(double));
+  double tolcont = 0.0;
   float* O = (float*)calloc(D, sizeof(float));
-  double tol = 0.0;
   float m = -INFINITY, l = 0.0f;
 
   const int ntiles = (N + bkv - 1) / bkv;
@@ -749,23 +819,57 @@ static void attn_row(attn_job_t* J, long bh, int i, float* out, float* tol_out, 
     if (nvalid == 0) { cnt[3]++; continue; }
 
     float m_new, alpha, s1, rowsum;
+    double cont = 0.0;
     orc_p_tile(S, bkv, m, D, fmt, J->flags, &m_new, &alpha, &s1, &rowsum, P2, pc, psb,
-               tol_out ? tstep : NULL, tol_out ? stie : NULL);
+               tol_out ? plo : NULL, tol_out ? phi : NULL, tol_out ? sblo : NULL, tol_out ? sbhi : NULL, &cont);
     volatile float al = alpha * l;
     l = al + rowsum;
-    tol = (double)alpha * tol;
 
     if (fmt != ORC_FMT_NONE && tol_out) {
-      for (int blk = 0; blk < nblk; ++blk) {
-        double sc = fmt == ORC_FMT_MX ? orc_e8m0_decode(psb[blk]) : orc_e4m3_decode(psb[blk]);
-        if (fmt == ORC_FMT_NV16 && stie[blk]) {
-          cnt[2]++;
-          double sc2 = orc_e4m3_decode(psb[blk] < 0x7E ? psb[blk] + 1 : psb[blk]);
-          tol += (double)n * 2.0 * sc2 * (double)s1 * h->vabs_max;
+      for (int c = 0; c < D; ++c) tolc[c] *= (double)alpha;
+      tolcont = (double)alpha * tolcont + (double)s1 * cont + (double)rowsum * 0x1p-20 +
+                (s1 == 0.0f ? (double)bkv * 0x1p-110 : 0.0);
+      for (int blk = 0; blk < nblk && s1 > 0.0f; ++blk) {
+        const int b0 = blk * n;
+        if (k0 + b0 >= h->Np) break;                   /* V^ is zero past the padded tail */
+        if (fmt == ORC_FMT_MX && sbhi[blk] < 127 - 120) {
+          /* every accepted scale is below 2^-120: bound the block's whole
+             contribution instead of enumerating it */
+          const double bnd = (double)s1 * n * 6.0 * ldexp(1.0, (int)sbhi[blk] - 127) * h->vabs_max;
+          for (int c = 0; c < D; ++c) tolc[c] += bnd;
           continue;
         }
-        for (int kk = blk * n; kk < blk * n + n; ++kk)
-          if (tstep[kk] != 0.0) { cnt[2]++; tol += tstep[kk] * sc * (double)s1 * h->vabs_max; }
+        const double sc = scale_value(psb[blk], fmt);
+        /* (a) at the block's own scale */
+        for (int c = 0; c < D; ++c) blkc[c] = 0.0;
+        for (int kk = b0; kk < b0 + n; ++kk) {
+          const double dv = code_dev(plo[kk], phi[kk], sc, pc[kk]);
+          if (dv == 0.0) continue;
+          cnt[2]++;
+          for (int c = 0; c < D; ++c) blkc[c] += dv * fabs(vhat(h, c, k0 + kk));
+        }
+        /* (b) every other accepted block scale */
+        for (int sb = sblo[blk]; sb <= sbhi[blk]; ++sb) {
+          if (sb == psb[blk]) continue;
+          cnt[4]++;
+          const double sa = scale_value((uint8_t)sb, fmt);
+          uint8_t ca[32];
+          double dva[32];
+          for (int kk = b0; kk < b0 + n; ++kk) {
+            ca[kk - b0] = p_code(P2[kk], (uint8_t)sb, fmt);
+            dva[kk - b0] = code_dev(plo[kk], phi[kk], sa, ca[kk - b0]);
+          }
+          for (int c = 0; c < D; ++c) {
+            double d = 0.0, w = 0.0;
+            for (int kk = b0; kk < b0 + n; ++kk) {
+              const double v = vhat(h, c, k0 + kk);
+              d += ((double)orc_e2m1_decode(ca[kk - b0]) * sa - (double)orc_e2m1_decode(pc[kk]) * sc) * v;
+              w += dva[kk - b0] * fabs(v);
+            }
+            if (fabs(d) + w > blkc[c]) blkc[c] = fabs(d) + w;
+          }
+        }
+        for (int c = 0; c < D; ++c) tolc[c] += (double)s1 * blkc[c];
       }
     }
 
@@ -798,13 +902,18 @@ static void attn_row(attn_job_t* J, long bh, int i, float* out, float* tol_out, 
     m = m_new;
   }
   for (int c = 0; c < D; ++c) { volatile float o = O[c] / l; out[c] = o; }
-  if (tol_out) *tol_out = (float)(tol / (double)l);
-  free(qf); free(qc2); free(qs); free(qbar); free(S); free(P2); free(pc); free(psb); free(stie); free(tstep); free(O);
+  if (tol_out) {
+    double tmax = 0.0;
+    for (int c = 0; c < D; ++c) if (tolc[c] > tmax) tmax = tolc[c];
+    *tol_out = (float)((tmax + h->vabs_max * tolcont) / (double)l);
+  }
+  free(qf); free(qc2); free(qs); free(qbar); free(S); free(P2); free(pc); free(psb); free(O);
+  free(plo); free(phi); free(sblo); free(sbhi); free(tolc); free(blkc);
 }
 
 static void* attn_worker(void* arg) {
   attn_job_t* J = (attn_job_t*)arg;
-  int64_t cnt[4] = {0, 0, 0, 0};
+  int64_t cnt[5] = {0, 0, 0, 0, 0};
   for (;;) {
     pthread_mutex_lock(&J->mu);
     int64_t r = J->next++;
@@ -816,7 +925,7 @@ static void* attn_worker(void* arg) {
     attn_row(J, bh, i, J->out + r * J->D, J->tie_tol ? J->tie_tol + r : NULL, cnt);
   }
   pthread_mutex_lock(&J->mu);
-  for (int c = 0; c < 4; ++c) J->cnt[c] += cnt[c];
+  for (int c = 0; c < 5; ++c) J->cnt[c] += cnt[c];
   pthread_mutex_unlock(&J->mu);
   return NULL;
 }
@@ -840,8 +949,9 @@ static void* head_worker(void* arg) {
 /*  q, k, v : 16-bit [B,H,N,D] host arrays (in_dtype fp16/bf16)              */
 /*  rows    : flat row ids ((b*H + h)*N + i), nrows of them                   */
 /*  out     : [nrows][D] fp32;  tie_tol: [nrows] or NULL;                     */
-/*  counters: [4] or NULL (inexact S sums, inexact O sums, tie-ambiguous P    */
-/*            codes, skipped tiles)                                          */
+/*  counters: [5] or NULL (inexact S sums, inexact O sums, P codes with an   */
+/*            accepted alternative, skipped tiles, P blocks with an accepted */
+/*            alternative scale)                                             */
 /* Returns 0, or -1 for invalid arguments.                                   */
 /* ------------------------------------------------------------------------ */
 int orc_attn2(const uint16_t* q, const uint16_t* k, const uint16_t* v, int in_dtype,
@@ -876,7 +986,7 @@ int orc_attn2(const uint16_t* q, const uint16_t* k, const uint16_t* v, int in_dt
   for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
   for (int t = 0; t < nthreads; ++t) pthread_create(&th[t], NULL, attn_worker, &J);
   for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
-  if (counters) for (int c = 0; c < 4; ++c) counters[c] = J.cnt[c];
+  if (counters) for (int c = 0; c < 5; ++c) counters[c] = J.cnt[c];
   for (long i = 0; i < HJ.nlist; ++i) free_head(&J.heads[HJ.list[i]]);
   free(HJ.list); free(J.heads); free(J.head_used);
   pthread_mutex_destroy(&J.mu); pthread_mutex_destroy(&HJ.mu);

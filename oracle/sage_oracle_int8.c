@@ -27,13 +27,24 @@
  *     c_t = fl32(fl32(s_Q s_K) c2), c2 = fl32(log2(e)/sqrt(D)), acc the exact
  *     integer product of the codes (|acc| < 2^24 for D <= 128, so fl32(acc)
  *     is exact).  The running max m and the tile max t are in this domain.
- *   - P^ = P~/s_P = 127 * 2^{u - t}, evaluated as
- *     exp2(fma(fl32(acc), c_t, fl32(log2 127 - t))) and rounded to the
- *     nearest integer (ties to even); s_P = fl32(2^{t - m}/127).
+ *   - the per-token quantization of P~ in Algorithm 2's order:
+ *     P~_k = fl32(exp2(fl32(u_k - m_new))), s_P = fl32(exp(rowmax(S) - m)/127)
+ *     = fl32(fl32(exp2(fl32(t - m_new)))/127), P^_k = P~_k/s_P read as
+ *     rint(fl32(P~_k fl32(1/s_P))) (ties to even, at most 127).  A tile whose
+ *     s_P lies below the normal fp32 range adds nothing (1/s_P would overflow).
  *   - l accumulates the unquantized P~ as Algorithm 2 writes it:
- *     l = fl32(fl32(alpha l) + fl32(s_P sum_k P~_k/s_P)), the sum sequential
- *     in fp32; alpha = 2^{m_old - m_new}, 0 on the first visited tile (the
- *     running max starts at -inf).
+ *     l = fl32(fl32(alpha l) + rowsum(P~)), the row sum sequential in fp32;
+ *     alpha = 2^{m_old - m_new}, 0 on the first visited tile (the running max
+ *     starts at -inf).
+ *   - tolerance: a GPU may evaluate P^ in the fused order
+ *     exp2(fma(fl32(acc), c_t, fl32(log2 127 - t))); per key, [lo, hi] holds
+ *     every value either order can reach before rounding -- the plain value
+ *     and 127 2^{acc c_t - t} (fp64) within the fused order's roundings,
+ *     W = h(log2 127) + h(t) + h(B) + h(arg) + 2^-22/ln 2 in log2 units
+ *     (h = half an fp32 ulp of each rounded intermediate).  Every code that
+ *     [lo, hi] reaches adds its distance to the plain code times s_P s_V
+ *     max|V^ row|, and the row sum's move s_P sum (hi - lo) adds max|V^|
+ *     times it; both are carried through alpha and divided by l.
  *   - O = fma(fl32(MM(P^, V^)), fl32(s_P s_V), fl32(alpha O)) per tile, the
  *     integer product exact; O = fl32(O / l) at the end.
  *   - L is the natural-log log-sum-exp of the scaled scores S/sqrt(D):
@@ -45,7 +56,9 @@
  * Flags: ORC_NO_SMOOTH_K (1) skips smoothing K; ORC_I8_STATIC_P (32) is the
  * ablation the paper argues against: P~ = 2^{u - m} quantized with the static
  * scale 1/127; ORC_I8_IDENTITY (64) skips every quantization (pins the
- * tiling, the online softmax and L against textbook attention).
+ * tiling, the online softmax and L against textbook attention);
+ * ORC_I8_FUSED_P (512) evaluates P^ in the fused order (a test shows the
+ * difference stays inside the tolerance).
  */
 #include <math.h>
 #include <stdint.h>
@@ -59,12 +72,14 @@ long orc_kmean(const uint16_t* k, int in_dtype, int B, int H, int N, int D, floa
 #define ORC_NO_SMOOTH_K 1u
 #define ORC_I8_STATIC_P 32u
 #define ORC_I8_IDENTITY 64u
+#define ORC_I8_FUSED_P 512u   /* P^ in the fused order a GPU evaluates it (for the test
+                                 that bounds its differences): rint(exp2(fma(fl32(acc),
+                                 c_t, fl32(log2 127 - t)))), l += fl32(s_P sum of them) */
 
 #define ORC_ROLE_Q 0
 #define ORC_ROLE_K 1
 #define ORC_ROLE_V 2
 
-#define I8_TIE_REL (1.0 / 1048576.0) /* 8 ulp of fp32, as for the FP4 codes of P */
 
 /* ------------------------------------------------------------------------ */
 /* psi on one block of n values (Eq. psi).  Returns the scale.               */
@@ -122,7 +137,7 @@ typedef struct {
   float *qs, *ks, *vs;        /* block scales                               */
   int* vrow_max;              /* [N] max_d |V^[k,d]| (tie bound)            */
   float *qf, *kf, *vf;        /* identity mode: Q, K', V in fp32            */
-  double vabs_max;            /* identity mode: max |V|                     */
+  double vabs_max;            /* max |V| (identity), max |deq(V^)| otherwise */
 } i8head_t;
 
 typedef struct {
@@ -173,10 +188,13 @@ static void i8_build_head(i8job_t* J, long bh) {
   orc_quant_int8(kb, J->in_dtype, ORC_ROLE_K, 1, 1, N, D, J->bkv, smooth, h->kc, h->ks, mu);
   orc_quant_int8(vb, J->in_dtype, ORC_ROLE_V, 1, 1, N, D, J->bkv, 0, h->vc, h->vs, NULL);
   h->vrow_max = (int*)malloc(sizeof(int) * N);
+  h->vabs_max = 0.0;
   for (int k = 0; k < N; ++k) {
     int m = 0;
     for (int c = 0; c < D; ++c) { int a = abs(h->vc[(long)k * D + c]); if (a > m) m = a; }
     h->vrow_max[k] = m;
+    const double a = (double)m * h->vs[k / J->bkv];
+    if (a > h->vabs_max) h->vabs_max = a;
   }
   free(mu);
 }
@@ -190,6 +208,18 @@ static void i8_free_head(i8head_t* h) {
 static float exp2_cr(float x) { return (float)exp2((double)x); }   /* correctly rounded fp32 exp2 */
 static float log2_cr(float x) { return (float)log2((double)x); }
 
+/* half an fp32 ulp at magnitude |x| (subnormal results: half the smallest step) */
+static double i8_hulp(double x) {
+  x = fabs(x);
+  if (x < 0x1p-126) return 0x1p-150;
+  int e;
+  frexp(x, &e);
+  return ldexp(1.0, e - 25);
+}
+
+/* rint clamped to the code range [0, 127] of P^ */
+static double i8_pcode(double y) { double c = rint(y); return c > 127.0 ? 127.0 : c; }
+
 /* One query row of Algorithm 2. */
 static void i8_row(i8job_t* J, long bh, int i, float* out, float* lse, float* tol_out, int64_t* cnt) {
   const i8head_t* h = &J->heads[bh];
@@ -199,11 +229,12 @@ static void i8_row(i8job_t* J, long bh, int i, float* out, float* lse, float* to
   const float log127 = (float)log2(127.0);
   const float sQ = ident ? 1.0f : h->qs[i / J->bq];
   float* accf = (float*)malloc(sizeof(float) * bkv);
+  float* ub = (float*)malloc(sizeof(float) * bkv);      /* u = fl32(acc) c_t */
+  float* pt = (float*)malloc(sizeof(float) * bkv);      /* P~ */
   float* code = (float*)malloc(sizeof(float) * bkv);    /* P^ (identity: P~/s_P unrounded) */
   char* valid = (char*)malloc((size_t)bkv);
-  char* tie = (char*)malloc((size_t)bkv);
   float* O = (float*)calloc(D, sizeof(float));
-  double tol = 0.0;
+  double tol = 0.0, tolcont = 0.0;
   float m = -INFINITY, l = 0.0f;
 
   const int ntiles = (N + bkv - 1) / bkv;
@@ -229,39 +260,79 @@ static void i8_row(i8job_t* J, long bh, int i, float* out, float* lse, float* to
         accf[kk] = (float)a;                 /* exact: |a| <= 127^2 D < 2^24 */
       }
       volatile float u = accf[kk] * ct;
+      ub[kk] = u;
       if (u > t) t = u;
     }
     if (t == -INFINITY) { cnt[1]++; continue; }
     const float m_new = m > t ? m : t;
     float alpha = 0.0f;
     if (m != -INFINITY) { volatile float d = m - m_new; alpha = exp2_cr(d); }
-    /* per-token scale of P~ from the reused maxima: s_P = rowmax(P~)/127 */
-    float sP;
-    volatile float bias;
-    if (stat) { sP = 1.0f / 127.0f; bias = log127 - m_new; }
-    else { volatile float d = t - m_new; float rho = exp2_cr(d); volatile float q = rho / 127.0f; sP = q; bias = log127 - t; }
+    /* P~ = exp(S - m_new) and its row sum */
     float psum = 0.0f;
     for (int kk = 0; kk < bkv; ++kk) {
-      tie[kk] = 0;
-      if (!valid[kk]) { code[kk] = 0.0f; continue; }
-      const float p = exp2_cr(fmaf(accf[kk], ct, bias));
+      float p = 0.0f;
+      if (valid[kk]) { volatile float d = ub[kk] - m_new; p = exp2_cr(d); }
+      pt[kk] = p;
       psum += p;
-      if (ident) { code[kk] = p; continue; }
-      float c = rintf(p);
-      if (c > 127.0f) c = 127.0f;
-      code[kk] = c;
-      const double mid = floor((double)p) + 0.5;
-      if (fabs((double)p - mid) <= I8_TIE_REL * mid) tie[kk] = 1;
     }
-    volatile float rs = sP * psum;
+    /* per-token scale of P~ from the reused maxima: s_P = exp(rowmax(S) - m)/127 */
+    float sP, r;
+    if (stat) { sP = 1.0f / 127.0f; r = 127.0f; }
+    else { volatile float d = t - m_new; volatile float q = exp2_cr(d) / 127.0f; sP = q; volatile float rr = 1.0f / sP; r = rr; }
+    if (!stat && sP < 0x1p-126f) { sP = 0.0f; r = 0.0f; }   /* the tile adds nothing to O */
+    /* P^ = P~/s_P */
+    for (int kk = 0; kk < bkv; ++kk) {
+      volatile float y = pt[kk] * r;
+      code[kk] = ident ? y : (float)i8_pcode(y);
+    }
+    if ((J->flags & ORC_I8_FUSED_P) && !stat && !ident && sP > 0.0f) {
+      volatile float B = log127 - t;
+      float ys = 0.0f;
+      for (int kk = 0; kk < bkv; ++kk) {
+        const float y = valid[kk] ? exp2_cr(fmaf(accf[kk], ct, B)) : 0.0f;
+        ys += y;
+        code[kk] = (float)i8_pcode(y);
+      }
+      volatile float rs = sP * ys;
+      psum = rs;
+    }
     volatile float al = alpha * l;
-    l = al + rs;
+    l = al + psum;
     const float sV = ident ? 1.0f : h->vs[j];
     volatile float spv = sP * sV;
     tol = (double)alpha * tol;
-    if (!ident && tol_out)
-      for (int kk = 0; kk < bkv; ++kk)
-        if (tie[kk]) { cnt[0]++; tol += (double)spv * h->vrow_max[k0 + kk]; }
+    tolcont = (double)alpha * tolcont;
+    if (!ident && tol_out) {
+      if (!stat) {
+        /* values the fused order reaches: 127 2^{acc c_t - t} within W */
+        volatile float B = log127 - t;
+        const double wfix = i8_hulp(log127) + i8_hulp(t) + i8_hulp(B) + 0x1p-22 / log(2.0);
+        double cont = 0.0;
+        for (int kk = 0; kk < bkv; ++kk) {
+          if (!valid[kk]) continue;
+          const double y = (double)pt[kk] * (double)r;
+          const double pex = 127.0 * exp2((double)accf[kk] * (double)ct - (double)t);
+          const double W = wfix + i8_hulp(fmaf(accf[kk], ct, B));
+          double flo = pex * exp2(-W), fhi = pex * exp2(W);
+          if (fhi < 0x1p-120) { flo = 0.0; fhi += 0x1p-147; }
+          const double lo = flo < y ? flo : y, hi = fhi > y ? fhi : y;
+          cont += hi - lo;
+          const double c0 = code[kk], d1 = fabs(i8_pcode(lo) - c0), d2 = fabs(i8_pcode(hi) - c0);
+          const double dv = d1 > d2 ? d1 : d2;
+          if (dv > 0.0) { cnt[0]++; tol += dv * (double)spv * h->vrow_max[k0 + kk]; }
+        }
+        tolcont += (double)sP * cont;
+        if (sP == 0.0f) tolcont += (double)bkv * 0x1p-110;
+      } else {
+        for (int kk = 0; kk < bkv; ++kk) {
+          if (!valid[kk]) continue;
+          const double y = (double)pt[kk] * 127.0;
+          const double mid = floor(y) + 0.5;
+          if (fabs(y - mid) <= mid * 0x1p-20) { cnt[0]++; tol += (double)spv * h->vrow_max[k0 + kk]; }
+        }
+      }
+      tolcont += (double)psum * 0x1p-20;
+    }
     /* O = diag(alpha) O + MM(P^, V^) s_P s_V */
     for (int c = 0; c < D; ++c) {
       float pv;
@@ -283,8 +354,8 @@ static void i8_row(i8job_t* J, long bh, int i, float* out, float* lse, float* to
   volatile float ml = m + log2_cr(l);
   volatile float L = ml * (float)log(2.0);
   *lse = L;
-  if (tol_out) *tol_out = (float)(tol / (double)l);
-  free(accf); free(code); free(valid); free(tie); free(O);
+  if (tol_out) *tol_out = (float)((tol + h->vabs_max * tolcont) / (double)l);
+  free(accf); free(ub); free(pt); free(code); free(valid); free(O);
 }
 
 static void* i8_worker(void* arg) {
@@ -354,8 +425,13 @@ int orc_attn_int8(const uint16_t* q, const uint16_t* k, const uint16_t* v, int i
 /*    dP = fl32 of the exact dot product.                                   */
 /*  - D_q = fl32(sum_d dO[q,d] O[q,d]) (exact sum, rounded once).           */
 /*  - scores as in the forward: u = fl32(fl32(acc) c_t) in the log2 domain; */
-/*    P = exp(S/sqrt(D) - L) = exp2(fma(fl32(acc), c_t, -Lb)),             */
-/*    Lb = fl32(L fl32(log2 e)); masked entries have P = 0.                 */
+/*    P = exp(S/sqrt(D) - L) in Algorithm 3's order: fl32(exp2(fl32(u -    */
+/*    Lb))), Lb = fl32(L fl32(log2 e)); masked entries have P = 0.  A GPU   */
+/*    may fuse it as exp2(fma(fl32(acc), c_t, -Lb)) (flag ORC_I8_FUSED_BWD  */
+/*    evaluates that order); the two differ by at most a relative          */
+/*    e_P = ln 2 (h(u) + h(u - Lb) + h(fused argument)) + 2^-22 (h = half  */
+/*    an fp32 ulp of each rounded intermediate; the last term the two exp2 */
+/*    evaluations, one correctly rounded, one within 1 ulp).                */
 /*  - psi of P, dO and dS per (B_q x B_kv) block, (B_q x D) block and      */
 /*    (B_q x B_kv) block, as psi of the forward (s = fl32(max|x|/127),      */
 /*    codes rint(fl32(x fl32(1/s)))).  A block with no visible entry is     */
@@ -373,19 +449,22 @@ int orc_attn_int8(const uint16_t* q, const uint16_t* k, const uint16_t* v, int i
 /*    window of a rounding midpoint may take either neighbour on a GPU      */
 /*    (exp2 to 1 ulp; dP and D summed in another order); each such code     */
 /*    adds the size of its effect to the per-element tolerance of dV, dK,   */
-/*    dQ.  The window: 8 ulp of the value for P^, and for dS^ the bound     */
-/*    |P| (e_dP + e_D) + |dP - D| |P| 2^-21 (e_x = 2^-17 times the sum of   */
-/*    |terms| of x) over s_dS, plus 8 ulp; block scales that move by an ulp */
-/*    shift every code by a relative 2^-22, also inside the window.  The    */
+/*    dQ.  The window: for P^ a relative e_P of the value plus e_P of the  */
+/*    block max (it moves s_P) plus 8 ulp; for dS^ the bound                */
+/*    |P| (e_dP + e_D) + |dP - D| |P| (2^-21 + e_P) (e_x = 2^-17 times the  */
+/*    sum of |terms| of x) over s_dS, plus 8 ulp; block scales that move by */
+/*    an ulp shift every code by a relative 2^-22, also inside it.  The     */
 /*    same dS error also reaches dQ and dK continuously -- through s_dS     */
 /*    (its bound is the largest element bound over 127: every code's value */
 /*    and the fold factor move with it) and through rowsum(dS) in the       */
 /*    smoothing-K term -- and is added to their tolerance.                  */
 /* Flags: ORC_NO_SMOOTH_K, ORC_I8_IDENTITY (no psi anywhere: the exact      */
 /* gradients of softmax attention up to fp32 rounding), ORC_I8_DP_INT8      */
-/* (ablation, Table 1(c): dP = MM(dO^, V^) with per-block INT8 dO and V).    */
+/* (ablation, Table 1(c): dP = MM(dO^, V^) with per-block INT8 dO and V),    */
+/* ORC_I8_FUSED_BWD (P in the fused order, for the test that bounds it).     */
 /* ======================================================================== */
 #define ORC_I8_DP_INT8 128u
+#define ORC_I8_FUSED_BWD 1024u
 
 typedef struct {
   const uint16_t *q, *k, *v, *dout;
@@ -460,6 +539,7 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
   float* Pc = (float*)malloc(sizeof(float) * (size_t)bq * bkv);     /* P^ (identity: P)  */
   float* Sc = (float*)malloc(sizeof(float) * (size_t)bq * bkv);     /* dS^ (identity: dS) */
   double* win = (double*)malloc(sizeof(double) * (size_t)bq * bkv);
+  double* eP = (double*)calloc((size_t)bq * bkv, sizeof(double));     /* relative window of P */
   char* vis = (char*)malloc((size_t)bq * bkv);
   double* acc = (double*)malloc(sizeof(double) * (size_t)(bq > bkv ? bq : bkv) * D);
 
@@ -483,6 +563,7 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
       volatile float ct = sqk * c2;
       /* P = exp(S - L) and dS = P (dP - D) */
       float pmax = 0.0f;
+      double ePmax = 0.0;
       for (int a = 0; a < nq; ++a)
         for (int b = 0; b < nk; ++b) {
           const int q = q0 + a, k = k0 + b, e = a * bkv + b;
@@ -497,8 +578,11 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
             for (int c = 0; c < D; ++c) s += (long)qc[(long)q * D + c] * kc[(long)k * D + c];
             accf = (float)s;
           }
-          P[e] = exp2_cr(fmaf(accf, ct, -Lb[q]));
-          if (P[e] > pmax) pmax = P[e];
+          volatile float u = accf * ct;
+          volatile float d = u - Lb[q];
+          P[e] = (J->flags & ORC_I8_FUSED_BWD) ? exp2_cr(fmaf(accf, ct, -Lb[q])) : exp2_cr(d);
+          eP[e] = log(2.0) * (i8_hulp(u) + i8_hulp(d) + i8_hulp(fmaf(accf, ct, -Lb[q]))) + 0x1p-22;
+          if (P[e] > pmax) { pmax = P[e]; ePmax = eP[e]; }
         }
       float dsmax = 0.0f;
       for (int a = 0; a < nq; ++a)
@@ -521,7 +605,8 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
           dS[e] = ds;
           if (fabsf(ds) > dsmax) dsmax = fabsf(ds);
           /* error window of dS from the GPU's other summation orders and exp2 */
-          win[e] = fabs((double)P[e]) * (ldexp(sa, -17) + ldexp(Dabs[q], -17)) + fabs((double)d) * fabs((double)P[e]) * ldexp(1.0, -21);
+          win[e] = fabs((double)P[e]) * (ldexp(sa, -17) + ldexp(Dabs[q], -17)) +
+                   fabs((double)d) * fabs((double)P[e]) * (ldexp(1.0, -21) + eP[e]);
         }
       /* psi(P) over the block, psi(dS) over the block */
       float sP = 1.0f, sdS = 1.0f;
@@ -540,7 +625,7 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
           Sc[e] = rintf(y2);
           if (tq) {
             /* flag codes near a midpoint; the effect goes into the tolerance */
-            const double w1 = fabs((double)y1) * ldexp(1.0, -20) + ldexp(1.0, -20);
+            const double w1 = fabs((double)y1) * (eP[e] + ePmax + ldexp(1.0, -20)) + ldexp(1.0, -20);
             const double w2 = win[e] * (double)r2 + fabs((double)y2) * (es * (double)r2 + ldexp(1.0, -20)) +
                               ldexp(1.0, -20);
             const int a = e / bkv, b = e % bkv;
@@ -615,7 +700,7 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
   }
   free(mu); free(qc); free(kc); free(gc); free(vc8); free(qs); free(ks); free(gs); free(vs8);
   free(qf); free(kf); free(vf); free(gf); free(Dr); free(Lb); free(Dabs);
-  free(P); free(dS); free(Pc); free(Sc); free(win); free(vis); free(acc);
+  free(P); free(dS); free(Pc); free(Sc); free(win); free(eP); free(vis); free(acc);
 }
 
 static void* i8_bwd_worker(void* arg) {

@@ -2,10 +2,14 @@
 smoothing Q, two-level P quantization of Sec. 3.2) against the oracle.
 
 Bar: |O_gpu - O_oracle| <= 2e-3 per element (fp32 output), plus, per row, the
-oracle's bound for P codes whose pre-rounding value lies within 8 ulp of an
-E2M1 rounding boundary (the GPU evaluates exp2 with v_exp_f32, within 1 ulp
-of the correctly rounded value the oracle uses; such codes may legitimately
-take either neighbour)."""
+oracle's tie_tol: the largest change any other accepted evaluation of the P
+step can make.  The oracle evaluates P~, s_P1 and P~2 = P~/s_P1 in Algorithm
+1's order; the kernel evaluates P~2 fused (exp2 of one fma, v_exp_f32 within
+1 ulp) and takes the E8M0 exponent of each block from scores.  Codes whose
+value lies within the two orders' difference of a rounding boundary, and
+block scales within it of a boundary (notably the block of the tile max,
+whose plain-order P~2 lands one ulp above 6 on a few percent of tiles and
+then takes 2^1), may legitimately differ; tie_tol sums their effect."""
 import numpy as np
 import pytest
 
@@ -36,13 +40,18 @@ def o_rows(o, rows, D):
     return flat.index_select(0, idx).float().cpu().numpy()
 
 
+ALT = 1e-4    # a row whose tie_tol exceeds this has an accepted alternative P code or block scale
+
+
 def check(got, ref, tie_tol, label, extra=None):
     err = np.abs(got - ref).max(axis=1)
     lim = TOL + tie_tol + (0 if extra is None else extra)
     bad = err > lim
-    say("%s: rows=%d max_err=%.3g (%.3g without tie rows) tie_rows=%d" %
-        (label, len(err), float(err.max()), float(err[tie_tol == 0].max()) if (tie_tol == 0).any() else 0.0,
-         int((tie_tol > 0).sum())))
+    one = tie_tol <= ALT
+    say("%s: rows=%d max_err=%.3g; rows with one accepted P step: %d, max_err %.3g; rows with alternatives: %d, "
+        "max_err %.3g, max err/(2e-3 + tie_tol) %.3f" %
+        (label, len(err), float(err.max()), int(one.sum()), float(err[one].max()) if one.any() else 0.0,
+         int((~one).sum()), float(err[~one].max()) if (~one).any() else 0.0, float((err / lim).max())))
     assert not bad.any(), "%s: %d rows over the bar, worst err %.3g at row %d" % (
         label, int(bad.sum()), float(err[bad].max()), int(np.flatnonzero(bad)[0]))
 
@@ -99,27 +108,65 @@ def test_attn_config0_all_rows():
     say("accuracy vs exact", oracle.metrics(ex, o.cpu().numpy().reshape(-1, w.D)))
 
 
-@pytest.mark.parametrize("ci,fmt,bkv", [(1, 0, None), (2, 0, None), (3, 0, None), (4, 1, None), (4, 0, None),
-                                        (2, 0, 128), (3, 0, 128), (4, 0, 256)])
-def test_attn_configs_full_size_sampled_rows(ci, fmt, bkv):
+_GEN = {}
+
+
+def generate_cached(ci):
+    """Full-size inputs of workload ci, generated once per test session."""
+    if ci not in _GEN:
+        _GEN.clear()
+        _GEN[ci] = wl.generate(wl.CONFIGS[ci])
+    return _GEN[ci]
+
+
+@pytest.mark.parametrize("b", [0, 1, 2, 3])
+def test_attn_config1_all_rows(b):
+    """B4 H32 N4096 D128 (K channel bias of variance 4) in the benchmark's launch
+    configuration (one launch over all four batches, 256-key tiles): every
+    row of batch b against the oracle."""
+    ci = 1
+    w = wl.CONFIGS[ci]
+    say("attn config", ci, w.name, "batch", b, "all rows")
+    q, k, v = generate_cached(ci)
+    o = gpu_attn(q, k, v, w.in_dtype, w.causal, 0, w.bkv)
+    rows = np.arange(b * w.H * w.N, (b + 1) * w.H * w.N, dtype=np.int64)
+    ref, tie, cnt = oracle.attn(q, k, v, w.in_dtype, w.causal, 0, w.bkv, rows=rows)
+    got = o_rows(o, rows, w.D)
+    check(got, ref, tie, "%s batch %d" % (w.name, b))
+    if b == 0:
+        sub = rows[:: 64]
+        ex = oracle.exact_attn(q, k, v, w.in_dtype, w.causal, rows=sub)
+        say("accuracy vs exact (every 64th row)", oracle.metrics(ex, got[:: 64]), cnt)
+
+
+@pytest.mark.parametrize("ci,fmt,bkv,whole", [(2, 0, None, True), (2, 0, 128, False), (3, 0, None, True),
+                                              (3, 0, 128, False), (4, 1, None, True), (4, 0, None, True),
+                                              (4, 0, 256, False)])
+def test_attn_configs_full_size_sampled_rows(ci, fmt, bkv, whole):
     """The benchmark's launch configuration at full size (each workload's own
-    KV tile, plus the other tile on the long, causal and D = 64 workloads); the
-    oracle computes a seeded sample of rows (first/last/random query tiles of
-    sampled heads)."""
+    KV tile, plus the other tile on the long, causal and D = 64 workloads).
+    With whole=True the oracle computes 8 whole 128-row query tiles on each
+    of 8 heads (first and last tile always, the tile ending on a KV-tile
+    boundary when causal, the rest seeded); otherwise 8 rows of 4 tiles."""
     w = wl.CONFIGS[ci]
     assert fmt in w.fmts
     bkv = bkv or w.bkv
-    say("attn config", ci, w.name, "fmt", fmt, "bkv", bkv)
-    q, k, v = wl.generate(w)
+    say("attn config", ci, w.name, "fmt", fmt, "bkv", bkv, "whole tiles" if whole else "sampled rows")
+    q, k, v = generate_cached(ci)
     o = gpu_attn(q, k, v, w.in_dtype, w.causal, fmt, bkv)
     BH = w.B * w.H
-    heads = sorted({0, BH - 1} | set(np.random.default_rng(ci).choice(BH, min(BH, 6), replace=False).tolist()))
-    rows = wl.sample_rows(w, per_head_tiles=4, tile=128, rows_per_tile=8, heads=heads, seed=ci)
+    rng = np.random.default_rng(ci)
+    heads = sorted({0, BH - 1} | set(rng.choice(np.arange(1, BH - 1), min(BH - 2, 6), replace=False).tolist()))
+    if whole:
+        rows = wl.sample_rows(w, per_head_tiles=8, tile=128, rows_per_tile=128, heads=heads, seed=ci)
+    else:
+        rows = wl.sample_rows(w, per_head_tiles=4, tile=128, rows_per_tile=8, heads=heads, seed=ci)
     ref, tie, cnt = oracle.attn(q, k, v, w.in_dtype, w.causal, fmt, bkv, rows=rows)
     got = o_rows(o, rows, w.D)
     check(got, ref, tie, w.name)
-    ex = oracle.exact_attn(q, k, v, w.in_dtype, w.causal, rows=rows)
-    say("accuracy vs exact (sampled rows)", oracle.metrics(ex, got), cnt)
+    sub = rows[:: 16] if whole else rows
+    ex = oracle.exact_attn(q, k, v, w.in_dtype, w.causal, rows=sub)
+    say("accuracy vs exact (sampled rows)", oracle.metrics(ex, got[:: 16] if whole else got), cnt)
 
 
 @pytest.mark.parametrize("fmt,bkv", [(0, 128), (1, 128), (0, 256), (0, 64)])
