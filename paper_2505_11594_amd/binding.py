@@ -120,6 +120,18 @@ def _shape(t):
     return tuple(int(s) for s in t.shape)
 
 
+def _check_qkv(q, k, v):
+    """q, k and v must share shape, 16-bit dtype and device: the kernels read
+    all three with q's element type and size."""
+    shp = _shape(q)
+    _in_flag(q)
+    for t, what in ((k, "k"), (v, "v")):
+        if _shape(t) != shp or t.dtype != q.dtype or t.device != q.device:
+            raise ValueError("%s must match q: shape %s, dtype %s, device %s; got %s, %s, %s"
+                             % (what, shp, q.dtype, q.device, tuple(t.shape), t.dtype, t.device))
+    return shp
+
+
 def _check_tensor(t, what: str, shape, dtype, device):
     """A caller-supplied buffer must match what the kernels will write or read
     (the C ABI receives bare pointers and cannot check it)."""
@@ -189,9 +201,7 @@ def sage_attn_fp4_fwd(q, k, v, causal: bool = False, fmt: int = SAGE_FMT_MXFP4, 
                       out=None, workspace=None):
     """O = attention(Q, K, V) through the FP4 path.  With ``workspace`` (a uint8 device
     tensor of at least attn_fp4_workspace_size bytes) no allocation happens inside."""
-    B, H, N, D = _shape(q)
-    if _shape(k) != (B, H, N, D) or _shape(v) != (B, H, N, D):
-        raise ValueError("q, k, v must have the same shape")
+    B, H, N, D = _check_qkv(q, k, v)
     fmt = fmt | _in_flag(q) | (SAGE_OUT_F32 if out_f32 else 0)
     o = _out(q, out_f32) if out is None else out
     _check_o(o, q, out_f32)
@@ -228,7 +238,7 @@ def sage_attn_fp4_fwd_prequant(qq, kq, vq, shape, causal: bool = False, fmt: int
 
 def sage_attn_bf16_fwd(q, k, v, causal: bool = False, out_f32: bool = True, out=None):
     """bf16-MFMA comparison kernel of the same structure."""
-    B, H, N, D = _shape(q)
+    B, H, N, D = _check_qkv(q, k, v)
     flags = _in_flag(q) | (SAGE_OUT_F32 if out_f32 else 0)
     o = _out(q, out_f32) if out is None else out
     _check_o(o, q, out_f32)
@@ -275,9 +285,7 @@ def sage_attn_int8_fwd(q, k, v, causal: bool = False, flags: int = 0, out_f32: b
     [B,H,N] fp32 (None when ``lse`` is False).  With ``workspace`` (uint8, at
     least attn_int8_workspace_size bytes) no allocation happens inside."""
     import torch
-    B, H, N, D = _shape(q)
-    if _shape(k) != (B, H, N, D) or _shape(v) != (B, H, N, D):
-        raise ValueError("q, k, v must have the same shape")
+    B, H, N, D = _check_qkv(q, k, v)
     flags = flags | _in_flag(q) | (SAGE_OUT_F32 if out_f32 else 0)
     o = _out(q, out_f32) if out is None else out
     _check_o(o, q, out_f32)

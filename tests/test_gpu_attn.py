@@ -238,6 +238,17 @@ def test_binding_rejects_mismatched_buffers():
             bd.sage_attn_bf16_fwd(q, q, q, out=o)
     with pytest.raises(ValueError):
         bd.sage_attn_fp4_fwd(q, q, q, workspace=torch.zeros(1 << 20, dtype=torch.float32, device="cuda:0"))
+    # k and v of another dtype with the right shape (fp16 or fp32 read as bf16,
+    # a 1-byte dtype read past its end) or on the host
+    others = [torch.zeros((1, 2, 100, 64), dtype=dt, device="cuda:0")
+              for dt in (torch.float16, torch.float32, torch.uint8, torch.int8, torch.bool)]
+    others.append(torch.zeros((1, 2, 100, 64), dtype=torch.bfloat16))
+    for x in others:
+        for fwd in (bd.sage_attn_fp4_fwd, bd.sage_attn_bf16_fwd, bd.sage_attn_int8_fwd):
+            with pytest.raises((ValueError, TypeError)):
+                fwd(q, x, q)
+            with pytest.raises((ValueError, TypeError)):
+                fwd(q, q, x)
     qq = bd.sage_quant_fp4(q, bd.SAGE_ROLE_Q)
     kq = bd.sage_quant_fp4(q, bd.SAGE_ROLE_K)
     vq = bd.sage_quant_fp4(q, bd.SAGE_ROLE_V)

@@ -394,3 +394,82 @@ def test_fused_order_attention_within_tie_tol(fmt, N, D, causal, bkv):
     assert np.all(err <= ta + 2e-6 * np.abs(a).max())
     if fmt == oracle.FMT_MX:
         assert ca["alt_scales"] > 0
+
+
+# ------------------------------------------------------------------ error bound against exact attention
+def _deq(codes, scales, n, fmt):
+    """Dequantize one-code-per-byte E2M1 codes with their block scale bytes
+    (blocks of n along the last axis)."""
+    e2m1 = np.array([oracle.e2m1_decode(c) for c in range(16)])
+    sv = np.array([2.0 ** (b - 127) if fmt == oracle.FMT_MX else oracle.e4m3_decode(b) for b in range(256)])
+    return e2m1[codes] * np.repeat(sv[scales], n, axis=-1)
+
+
+@pytest.mark.parametrize("fmt", [oracle.FMT_MX, oracle.FMT_NV16])
+@pytest.mark.parametrize("N,D,causal,bkv", [(100, 64, False, 64), (256, 128, False, 128), (256, 64, True, 64),
+                                            (200, 128, True, 128)])
+def test_error_bound_against_exact_attention(fmt, N, D, causal, bkv):
+    """The oracle stays within an fp64 bound of exact softmax attention, built
+    from the errors of each quantization step (Sec. 3.1, phi; Sec. 3.2):
+      |O - O_exact| <= T1 + T2 + T3 per element, with
+      T1 = sum_k eps_k |V^_kc|: the P step -- each P~2 block error is at most
+           blockmax/3 with E8M0 scales (the grid's largest half-step is 2^e and
+           6 2^(e-1) < blockmax), blockmax (1 + 2^-4)/6 with E4M3 scales, in
+           units of the row's softmax weights of the quantized scores;
+      T2 = sum_k |pi^_k - pi_k| |V^_kc|: the scores' quantization (pi^ the
+           softmax of S^ = Q^ K^'T, pi that of Q K^T, both fp64);
+      T3 = sum_k pi_k |V^_kc - V_kc|: V's quantization;
+    plus 4e-6 max|V^| for the oracle's fp32 arithmetic.  The P step alone
+    (O against pi^ V^) is checked against T1, and must use a visible part of
+    it, so the bound is not vacuous."""
+    n = oracle.block_size(fmt)
+    q, k, v = wl.make_inputs(1, 1, N, D, wl.IN_BF16, seed=80 + N + D, k_bias_var=4.0, outlier_frac=0.03)
+    out, _, _ = oracle.attn(q, k, v, wl.IN_BF16, causal, fmt, bkv)
+    qf, kf, vf = (wl.from_bits(x, 1)[0, 0].astype(np.float64) for x in (q, k, v))
+    qc, qs, _, _ = oracle.quant(q, wl.IN_BF16, oracle.ROLE_Q, fmt)
+    kc, ks, _, _ = oracle.quant(k, wl.IN_BF16, oracle.ROLE_K, fmt)
+    vc, vs, _, _ = oracle.quant(v, wl.IN_BF16, oracle.ROLE_V, fmt)
+    qh, kh = _deq(qc[0, 0], qs[0, 0], n, fmt), _deq(kc[0, 0], ks[0, 0], n, fmt)
+    vh = _deq(vc[0, 0], vs[0, 0], n, fmt).T[:N]                 # [N, D]
+    mask = np.tril(np.ones((N, N), bool)) if causal else np.ones((N, N), bool)
+
+    def softmax(s):
+        s = np.where(mask, s / np.sqrt(D), -np.inf)
+        e = np.exp(s - s.max(axis=1, keepdims=True))
+        return e / e.sum(axis=1, keepdims=True)
+    pi, pih = softmax(qf @ kf.T), softmax(qh @ kh.T)
+    # per key: the largest quantized-score weight of its n-key block within its KV tile
+    bm = np.zeros_like(pih)
+    for b0 in range(0, N, n):
+        bm[:, b0:b0 + n] = pih[:, b0:b0 + n].max(axis=1, keepdims=True)
+    eps = bm / 3.0 if fmt == oracle.FMT_MX else bm * (1 + 2.0 ** -4) / 6.0 + bm * 2.0 ** -16
+    eps = np.where(mask, eps, 0.0)
+    av = np.abs(vh)
+    T1 = eps @ av
+    T2 = np.abs(pih - pi) @ av
+    T3 = pi @ np.abs(vh - vf)
+    slack = 4e-6 * av.max()
+    p_err = np.abs(out - pih @ vh)
+    assert np.all(p_err <= T1 + slack)
+    assert (p_err / (T1 + slack)).max() > 0.05
+    ex = pi @ vf
+    assert np.all(np.abs(out - ex) <= T1 + T2 + T3 + slack)
+    # the oracle's own exact attention is the same fp64 reference
+    ex2 = oracle.exact_attn(q, k, v, wl.IN_BF16, causal)
+    assert np.abs(ex2 - ex).max() <= 1e-12 * np.abs(ex).max()
+
+
+def test_metrics_hand_worked():
+    """Appendix accuracy metrics on hand-worked vectors: an exact copy gives
+    CosSim 1, relative L1 0, RMSE 0; doubling gives CosSim 1, relative L1 1 and
+    RMSE = rms(O); for O = (3, 4) against O' = (4, 3): CosSim 24/25, L1 2/7,
+    RMSE 1."""
+    o = np.array([[1.0, -2.0, 2.0], [0.5, 0.0, -4.0]])
+    m = oracle.metrics(o, o)
+    assert m["cossim"] == pytest.approx(1.0, abs=1e-15) and m["l1"] == 0.0 and m["rmse"] == 0.0
+    m = oracle.metrics(o, 2 * o)
+    assert m["cossim"] == pytest.approx(1.0, abs=1e-15) and m["l1"] == pytest.approx(1.0, abs=1e-15)
+    assert m["rmse"] == pytest.approx(np.sqrt((o ** 2).mean()), rel=1e-15)
+    m = oracle.metrics(np.array([3.0, 4.0]), np.array([4.0, 3.0]))
+    assert m["cossim"] == pytest.approx(24 / 25, rel=1e-15)
+    assert m["l1"] == pytest.approx(2 / 7, rel=1e-15) and m["rmse"] == pytest.approx(1.0, rel=1e-15)
