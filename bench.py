@@ -106,10 +106,50 @@ RATE_TESTS = [  # (name, what one loop iteration issues, instructions of the cou
     ("mfma_fp4+exp", "4 FP4 MFMA + 8 v_exp_f32", 4), ("mfma_bf16", "4 v_mfma_f32_32x32x16_bf16", 4),
     ("mfma_bf16+fma", "4 bf16 MFMA + 32 v_fma_f32", 4), ("mfma16_fp4", "8 v_mfma_scale_f32_16x16x128_f8f6f4 (FP4)", 8),
     ("mfma16_fp4+fma", "8 FP4 16x16x128 MFMA + 32 v_fma_f32", 8),
-    ("split", "even SIMD slots: 4 FP4 MFMA; odd slots: 32 v_fma_f32", None),
+    ("split_unverified", "even HW wave slots: 4 FP4 MFMA; odd: 32 v_fma_f32 (placement unchecked)", None),
     ("exp+fma", "8 v_exp_f32 + 32 independent v_fma_f32", 8),
     ("cvt_fp4+fma", "8 v_cvt_scalef32_pk_fp4_f32 + 32 independent v_fma_f32", 8),
-    ("chain", "8 x (v_fma_f32 -> v_exp_f32 -> v_add_f32) + 4 FP4 packs", 8)]
+    ("chain", "8 x (v_fma_f32 -> v_exp_f32 -> v_add_f32) + 4 FP4 packs", 8),
+    ("inter_fma", "4 x (1 FP4 MFMA, 8 v_fma_f32), order pinned", 4),
+    ("inter_exp", "4 x (1 FP4 MFMA, 2 v_exp_f32), order pinned", 4),
+    ("inter_chain", "4 x (1 FP4 MFMA, 2 chain links + 1 FP4 pack), order pinned", 4)]
+
+SPLIT_OTHER = [("fma", "32 v_fma_f32"), ("exp", "8 v_exp_f32"), ("chain", "8 chain links + 4 FP4 packs")]
+
+
+def split_rates(torch, lib, iters):
+    """MFMA waves and VALU waves sharing each SIMD, placement verified: one
+    workgroup per CU, waves ranked per SIMD from their HW_ID; the time is
+    reported only when every SIMD holds W/2 waves of each role."""
+    import ctypes
+    import numpy as np
+    lib.sage_rates_split.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                     ctypes.POINTER(ctypes.c_float)]
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    res = {}
+    for w in (2, 4):
+        nw = 4 * w
+        out = torch.empty(256 * 64 * nw, dtype=torch.float32, device="cuda:0")
+        place = torch.zeros(2 * 256 * nw, dtype=torch.int32, device="cuda:0")
+        for o, (name, what) in enumerate(SPLIT_OTHER):
+            ms = ctypes.c_float()
+            rc = lib.sage_rates_split(o, w, ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(place.data_ptr()), stream,
+                                      ctypes.byref(ms))
+            if rc != 0:
+                raise RuntimeError("sage_rates_split(%d, %d) failed: %d" % (o, w, rc))
+            pl = place.cpu().numpy().view(np.uint32).reshape(256, nw, 2)
+            simd = (pl[:, :, 0] >> 4) & 3
+            ok = True
+            for b in range(256):
+                for sd in range(4):
+                    roles = pl[b, simd[b] == sd, 1]
+                    if roles.size != w or int(roles.sum()) != w // 2:
+                        ok = False
+            cyc = ms.value * 1e-3 * 2.4e9 / (iters * (w // 2))   # per (1 MFMA + 1 other) wave-iteration pair
+            res["split_%s@%d" % (name, w)] = dict(cycles=cyc, placement_verified=ok)
+            log("waves/SIMD %d  split MFMA | %-30s %8.1f cycles per pair of iterations, placement %s"
+                % (w, what, cyc, "verified" if ok else "NOT verified"))
+    return res
 
 
 def issue_rates(torch):
@@ -133,6 +173,7 @@ def issue_rates(torch):
             cyc = ms.value * 1e-3 * 2.4e9 / (iters * w)     # cycles per loop iteration per SIMD
             res["%s@%d" % (name, w)] = cyc
             log("waves/SIMD %d  %-16s %-52s %8.1f cycles/iteration" % (w, name, what, cyc))
+    split = split_rates(torch, lib, iters)
     summary = {}
     for w in (2, 4):
         g = lambda k: res["%s@%d" % (k, w)]
@@ -146,16 +187,25 @@ def issue_rates(torch):
             "exp_hidden_under_fp4_mfma": (g("mfma_fp4") + g("exp") - g("mfma_fp4+exp")) / g("exp"),
             "fma_hidden_under_bf16_mfma": (g("mfma_bf16") + g("fma") - g("mfma_bf16+fma")) / g("fma"),
             "fma_hidden_under_fp4_16x16x128": (g("mfma16_fp4") + g("fma") - g("mfma16_fp4+fma")) / g("fma"),
-            # split: half the waves of a SIMD run only MFMAs, the other half only fma
-            "split_vs_serial": g("split") / ((g("mfma_fp4") + g("fma")) / 2),
             # transcendental / pack work against plain VALU work on independent registers
             "exp_hidden_under_fma": (g("fma") + g("exp") - g("exp+fma")) / g("exp"),
             "cvt_fp4_hidden_under_fma": (g("fma") + g("cvt_fp4") - g("cvt_fp4+fma")) / g("cvt_fp4"),
             # the attention kernel's per-score work (fma, exp, add, half a pack), as measured
             "chain_cycles_per_score": g("chain") / 8,
-            "chain_vs_isolated_rates": g("chain") / (16 * g("fma") / 32 + g("exp") + 4 * g("cvt_fp4") / 8)}
+            "chain_vs_isolated_rates": g("chain") / (16 * g("fma") / 32 + g("exp") + 4 * g("cvt_fp4") / 8),
+            # the same mixes with the interleave pinned (one MFMA, then its share of the other work)
+            "fma_hidden_under_fp4_mfma_pinned": (g("mfma_fp4") + g("fma") - g("inter_fma")) / g("fma"),
+            "exp_hidden_under_fp4_mfma_pinned": (g("mfma_fp4") + g("exp") - g("inter_exp")) / g("exp"),
+            "chain_hidden_under_fp4_mfma_pinned": (g("mfma_fp4") + g("chain") - g("inter_chain")) / g("chain")}
+        for name, _ in SPLIT_OTHER:
+            sp = split["split_%s@%d" % (name, w)]
+            other = g({"fma": "fma", "exp": "exp", "chain": "chain"}[name])
+            summary["w%d" % w]["split_%s_hidden" % name] = (
+                (g("mfma_fp4") + other - sp["cycles"]) / min(g("mfma_fp4"), other) if sp["placement_verified"] else None)
+            summary["w%d" % w]["split_%s_vs_serial" % name] = (
+                sp["cycles"] / (g("mfma_fp4") + other) if sp["placement_verified"] else None)
     print(json.dumps({"mode": "rates", "clock_assumed_ghz": 2.4, "iterations": iters,
-                      "cycles_per_iteration": res, "derived": summary}), flush=True)
+                      "cycles_per_iteration": res, "split": split, "derived": summary}), flush=True)
 
 
 def accuracy_vs_exact(torch, q, k, v, o, w, nrows=512, seed=7):

@@ -449,12 +449,13 @@ int orc_attn_int8(const uint16_t* q, const uint16_t* k, const uint16_t* v, int i
 /*    window of a rounding midpoint may take either neighbour on a GPU      */
 /*    (exp2 to 1 ulp; dP and D summed in another order); each such code     */
 /*    adds the size of its effect to the per-element tolerance of dV, dK,   */
-/*    dQ.  The window: for P^ a relative e_P of the value plus e_P of the  */
-/*    block max (it moves s_P) plus 8 ulp; for dS^ the bound                */
+/*    dQ.  The window: for P^ a relative e_P of the value plus the block's */
+/*    largest e_P (it bounds the move of s_P) plus 8 ulp; for dS^ the bound */
 /*    |P| (e_dP + e_D) + |dP - D| |P| (2^-21 + e_P) (e_x = 2^-17 times the  */
 /*    sum of |terms| of x) over s_dS, plus 8 ulp; block scales that move by */
 /*    an ulp shift every code by a relative 2^-22, also inside it.  The     */
-/*    same dS error also reaches dQ and dK continuously -- through s_dS     */
+/*    move of s_P reaches dV continuously, and the                          */
+/*    same dS error reaches dQ and dK continuously -- through s_dS          */
 /*    (its bound is the largest element bound over 127: every code's value */
 /*    and the fold factor move with it) and through rowsum(dS) in the       */
 /*    smoothing-K term -- and is added to their tolerance.                  */
@@ -563,7 +564,7 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
       volatile float ct = sqk * c2;
       /* P = exp(S - L) and dS = P (dP - D) */
       float pmax = 0.0f;
-      double ePmax = 0.0;
+      double ePmax = 0.0;                     /* largest relative window of P in the block */
       for (int a = 0; a < nq; ++a)
         for (int b = 0; b < nk; ++b) {
           const int q = q0 + a, k = k0 + b, e = a * bkv + b;
@@ -582,7 +583,8 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
           volatile float d = u - Lb[q];
           P[e] = (J->flags & ORC_I8_FUSED_BWD) ? exp2_cr(fmaf(accf, ct, -Lb[q])) : exp2_cr(d);
           eP[e] = log(2.0) * (i8_hulp(u) + i8_hulp(d) + i8_hulp(fmaf(accf, ct, -Lb[q]))) + 0x1p-22;
-          if (P[e] > pmax) { pmax = P[e]; ePmax = eP[e]; }
+          if (P[e] > pmax) pmax = P[e];
+          if (eP[e] > ePmax) ePmax = eP[e];     /* bounds the move of the block max */
         }
       float dsmax = 0.0f;
       for (int a = 0; a < nq; ++a)
@@ -658,6 +660,8 @@ static void i8_bwd_head(i8bwd_t* J, long bh) {
               s += (double)Pc[a * bkv + b] * (ident ? (double)gf[(long)(q0 + a) * D + c] : (double)gc[(long)(q0 + a) * D + c]);
             const long o = (long)(k0 + b) * D + c;
             dv[o] = fmaf((float)s, f, dv[o]);
+            /* s_P moves with the block max by at most ePmax (relative) */
+            if (tv && !ident) tv[o] += (float)(fabs(s) * (double)f * ePmax);
           }
       }
       /* dK_j += MM(dS^T, Q^) s_dS s_Q / sqrt(D) */
