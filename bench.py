@@ -343,7 +343,9 @@ def int8_backward(torch, bd, w, qd, kd, vd, o, L, steps):
                                                                                       100 * floor / t))
     del ws, grads, dout
     return {"step_ms": t * 1e3, "tops": ops / t / 1e12, "ops": ops,
-            "kernels": ["attn_i8_bwd_dv_kernel<128,false>", "attn_i8_bwd_dk_kernel<128,false,true>", "attn_i8_bwd_dq_kernel<128,false,true>"],
+            # the recommended workspace stores dS^: dK writes it, dQ sums from it
+            "kernels": ["i8_bwd_prep_kernel<128,true>", "attn_i8_bwd_dv_kernel<128,false>",
+                        "attn_i8_bwd_dk_kernel<128,false,true,true>", "attn_i8_bwd_dq_ds_kernel<128,false>"],
             "frac_of_mixed_peak": floor / t,
             "peak_note": "8/10 of the work at the int8 peak (5000 TOPS), 2/10 (dO V^T) at the bf16 peak (2500 TFLOP/s)"}
 
