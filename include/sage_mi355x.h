@@ -154,6 +154,24 @@ int sage_attn_fp4_fwd_ws(const void* q, const void* k, const void* v, void* o,
                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * sage_attn_fp4_fwd_noalloc -- sage_attn_fp4_fwd for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same arguments, kernels and results
+ * as sage_attn_fp4_fwd, with no hipMalloc, hipFree or allocating library call.
+ * Its workspace is a fixed scratch of SAGE_NOALLOC_SCRATCH_BYTES inside the
+ * library, one per GPU, held until the process ends; shapes whose
+ * sage_attn_fp4_workspace_size() exceeds it return SAGE_ERR_WORKSPACE before
+ * any HIP call (256 MiB holds B = 1, H = 32, N = 32768, D = 128).
+ * `stream` must belong to the current device (else SAGE_ERR_INVALID_ARG).
+ * All calls on one GPU share its scratch: calls that overlap on one GPU
+ * (other streams, other host threads) race and must be serialized by the
+ * caller; consecutive calls on one stream are safe.
+ */
+#define SAGE_NOALLOC_SCRATCH_BYTES (256ull << 20)
+int sage_attn_fp4_fwd_noalloc(const void* q, const void* k, const void* v, void* o,
+                              int B, int H, int N, int D, int causal, unsigned fmt, hipStream_t stream);
+
+/*
  * sage_attn_fp4_fwd_prequant -- the attention kernel alone, on tensors
  * produced by sage_quant_fp4 (layouts above).  kmean is not needed: the
  * smoothing is already inside K^ (softmax is invariant to it).  SAGE_SMOOTH_Q

@@ -60,6 +60,7 @@ def lib():
         L.sage_attn_fp4_workspace_size.restype = sz
         L.sage_attn_fp4_fwd.argtypes = [vp, vp, vp, vp, i, i, i, i, i, u, vp]
         L.sage_attn_fp4_fwd_ws.argtypes = [vp, vp, vp, vp, i, i, i, i, i, u, vp, sz, vp]
+        L.sage_attn_fp4_fwd_noalloc.argtypes = [vp, vp, vp, vp, i, i, i, i, i, u, vp]
         L.sage_attn_fp4_fwd_prequant.argtypes = [vp] * 7 + [i, i, i, i, i, u, vp]
         L.sage_attn_bf16_fwd.argtypes = [vp, vp, vp, vp, i, i, i, i, i, u, vp]
         L.sage_quant_int8_sizes.argtypes = [i, i, i, i, i, u, ctypes.POINTER(sz), ctypes.POINTER(sz)]
@@ -79,7 +80,7 @@ def lib():
         L.sage_status_string.restype = ctypes.c_char_p
         L.sage_version.restype = ctypes.c_char_p
         for name in ("sage_quant_sizes", "sage_quant_fp4", "sage_attn_fp4_fwd", "sage_attn_fp4_fwd_ws",
-                     "sage_attn_fp4_fwd_prequant", "sage_attn_bf16_fwd", "sage_quant_int8_sizes",
+                     "sage_attn_fp4_fwd_noalloc", "sage_attn_fp4_fwd_prequant", "sage_attn_bf16_fwd", "sage_quant_int8_sizes",
                      "sage_quant_int8", "sage_attn_int8_fwd", "sage_attn_int8_fwd_ws",
                      "sage_attn_int8_fwd_prequant", "sage_attn_int8_bwd", "sage_attn_int8_bwd_ws"):
             getattr(L, name).restype = i
@@ -214,6 +215,20 @@ def sage_attn_fp4_fwd(q, k, v, causal: bool = False, fmt: int = SAGE_FMT_MXFP4, 
         rc = lib().sage_attn_fp4_fwd_ws(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, H, N, D, int(bool(causal)), fmt,
                                         _ptr(workspace), workspace.numel(), _stream())
         _check("sage_attn_fp4_fwd_ws", rc)
+    return o
+
+
+def sage_attn_fp4_fwd_noalloc(q, k, v, causal: bool = False, fmt: int = SAGE_FMT_MXFP4, out_f32: bool = True,
+                              out=None):
+    """sage_attn_fp4_fwd on the library's fixed per-GPU scratch (no device allocation
+    inside the C call; ``out`` may be preallocated).  Calls that overlap on one GPU race."""
+    B, H, N, D = _check_qkv(q, k, v)
+    fmt = fmt | _in_flag(q) | (SAGE_OUT_F32 if out_f32 else 0)
+    o = _out(q, out_f32) if out is None else out
+    _check_o(o, q, out_f32)
+    rc = lib().sage_attn_fp4_fwd_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(o), B, H, N, D, int(bool(causal)), fmt,
+                                         _stream())
+    _check("sage_attn_fp4_fwd_noalloc", rc)
     return o
 
 

@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "sage_common.h"
 #include "sage_mi355x.h"
@@ -42,6 +43,9 @@ hipError_t launch_attn_int8_bwd(const void* qc, const float* qs, const void* qt,
                                 float rsd, hipStream_t st);
 size_t i8_bwd_ds_bytes_per_head(int N);
 }  // namespace sage
+
+// the scratch of sage_attn_fp4_fwd_noalloc (see the no-allocation entry point below)
+__device__ __align__(256) uint8_t sage_noalloc_scratch[SAGE_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -186,6 +190,19 @@ int attn_ws_impl(const void* q, const void* k, const void* v, void* o, int B, in
                             H, N, D, causal, fmt, st);
   return rc;
 }
+
+// ---- the no-allocation entry point -----------------------------------------
+// sage_attn_fp4_fwd_noalloc runs attn_ws_impl on a fixed scratch: a file-scope
+// device array, one copy per GPU, held until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it is a stand-in, not a
+// device address): the address comes from hipGetSymbolAddress, once per
+// device with that device current, and is kept per device.  Every call on a
+// GPU shares that GPU's scratch, so calls that overlap on one GPU (two streams,
+// two host threads) race.  Nothing in it needs to start at zero: every byte
+// attn_ws_impl reads is written earlier in the same call.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];   // device address of sage_noalloc_scratch, per device
 
 // ---- 8-bit attention (Algorithm 2) ----------------------------------------
 constexpr unsigned kI8Flags = SAGE_IN_BF16 | SAGE_OUT_F32 | SAGE_NO_SMOOTH_K | SAGE_BKV64;
@@ -442,6 +459,30 @@ int sage_attn_fp4_fwd(const void* q, const void* k, const void* v, void* o, int 
   rc = attn_ws_impl(q, k, v, o, B, H, N, D, causal, fmt, ws, stream);
   if (hipFreeAsync(ws, stream) != hipSuccess && rc == SAGE_OK) rc = SAGE_ERR_HIP;
   return rc;
+}
+
+int sage_attn_fp4_fwd_noalloc(const void* q, const void* k, const void* v, void* o, int B, int H, int N, int D,
+                              int causal, unsigned fmt, hipStream_t stream) {
+  int rc = attn_args(q, k, v, o, B, H, N, D, causal, fmt);
+  if (rc != SAGE_OK) return rc;
+  if (!smooth_q_supported(fmt)) return SAGE_ERR_UNSUPPORTED;
+  if (attn_ws_layout(B, H, N, D, fmt).total > (size_t)SAGE_NOALLOC_SCRATCH_BYTES) return SAGE_ERR_WORKSPACE;
+  int dev = -1;
+  hipDevice_t sdev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return SAGE_ERR_HIP;
+  if (hipStreamGetDevice(stream, &sdev) != hipSuccess) return SAGE_ERR_HIP;
+  if (sdev != dev || dev >= kMaxDevices) return SAGE_ERR_INVALID_ARG;   // the stream must be on the current device
+  void* ws = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+      void* p = nullptr;
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(sage_noalloc_scratch)) != hipSuccess || !p) return SAGE_ERR_HIP;
+      g_scratch_ptr[dev] = p;
+    }
+    ws = g_scratch_ptr[dev];
+  }
+  return attn_ws_impl(q, k, v, o, B, H, N, D, causal, fmt, ws, stream);
 }
 
 int sage_attn_fp4_fwd_prequant(const void* q_codes, const void* q_scales, const void* k_codes, const void* k_scales,
