@@ -59,16 +59,17 @@ def kernel_source_sha() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def traffic_from_counters(n_launch_units: float):
-    """HBM bytes per launch from committed rocprofv3 FETCH_SIZE/WRITE_SIZE runs
-    (scaled by the copy-kernel calibration), or None when the kernel source
-    changed since they were taken."""
+def traffic_from_counters(variant: str = "default"):
+    """HBM bytes per launch of the bench kernel ("default": 128-query
+    workgroups, "wg256": 256-query workgroups) from committed rocprofv3
+    FETCH_SIZE/WRITE_SIZE runs scaled by the copy-kernel calibration, or None
+    when the kernel source changed since they were taken."""
     if not os.path.exists(COUNTERS):
         return None
     c = json.load(open(COUNTERS))
-    if c.get("source_sha") != kernel_source_sha():
+    if c.get("source_sha") != kernel_source_sha() or variant not in c:
         return None
-    return float(c["hbm_bytes_per_launch"])
+    return float(c[variant]["hbm_bytes_per_launch"])
 
 
 def cpu_baseline(w, q, k, v, budget_s: float = 15.0):
@@ -146,7 +147,9 @@ def split_rates(torch, lib, iters):
                     if roles.size != w or int(roles.sum()) != w // 2:
                         ok = False
             cyc = ms.value * 1e-3 * 2.4e9 / (iters * (w // 2))   # per (1 MFMA + 1 other) wave-iteration pair
-            res["split_%s@%d" % (name, w)] = dict(cycles=cyc, placement_verified=ok)
+            # how the SPI spreads a workgroup's waves: SIMD of wave i against i % 4
+            rr = float(np.mean(simd == (np.arange(nw)[None, :] % 4)))
+            res["split_%s@%d" % (name, w)] = dict(cycles=cyc, placement_verified=ok, simd_is_wave_mod_4=rr)
             log("waves/SIMD %d  split MFMA | %-30s %8.1f cycles per pair of iterations, placement %s"
                 % (w, what, cyc, "verified" if ok else "NOT verified"))
     return res
@@ -359,6 +362,7 @@ def main():
     ap.add_argument("--no-bf16", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the attention-kernel timings of the other workloads")
     ap.add_argument("--no-int8", action="store_true", help="skip the 8-bit attention forward")
+    ap.add_argument("--wg256", action="store_true", help="--mode attn: 256-query workgroups (SAGE_WG256)")
     ap.add_argument("--mode", choices=["full", "attn", "attn_nv16", "attn_int8", "attn_int8_bwd", "copy", "rates"],
                     default="full",
                     help="attn: only the attention kernel (for counter runs); attn_nv16: only the NV16 kernel on "
@@ -453,8 +457,9 @@ def main():
         qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q)
         kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K)
         vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V)
+        fa = tile | (bd.SAGE_WG256 if args.wg256 else 0)
         for _ in range(args.warmup + args.steps):
-            bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, fmt=tile, out=o)
+            bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, fmt=fa, out=o)
         torch.cuda.synchronize()
         print(json.dumps({"mode": "attn", "launches": args.warmup + args.steps, "ops_per_launch": ops}))
         return
@@ -503,6 +508,23 @@ def main():
     t_quant = e0.elapsed_time(e1) / 1e3 / args.steps
     n_el = B * H * N * D
     quant_bytes = n_el * (2 + 2 + 2 + 2) + 3 * n_el * (0.5 + 1.0 / 32)   # K read twice (mean + quantize)
+
+    # the same kernel with 256-query workgroups (SAGE_WG256): half the K^/V^T fetches, same bits
+    wg256 = None
+    if w.bkv == 256 and not w.causal:
+        run_wg = lambda: bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal,
+                                                       fmt=tile | bd.SAGE_WG256, out=o)
+        warm(torch, run_wg)
+        e0.record()
+        for _ in range(args.steps):
+            run_wg()
+        e1.record()
+        torch.cuda.synchronize()
+        t_wg = e0.elapsed_time(e1) / 1e3 / args.steps
+        wg256 = {"kernel": "attn_fp4_mx256_kernel<%d,false,0,false,8>" % D, "kernel_ms": t_wg * 1e3,
+                 "tops": ops / t_wg / 1e12, "frac_of_mxfp4_peak": ops / t_wg / 1e12 / PEAK_FP4_TFLOPS,
+                 "traffic": traffic_from_counters("wg256")}
+        log("attention kernel, 256-query workgroups %.3f ms = %.1f TFLOP/s" % (t_wg * 1e3, ops / t_wg / 1e12))
 
     bf16 = None
     if not args.no_bf16:
@@ -570,13 +592,14 @@ def main():
                    "format": "MXFP4 (E2M1, 1x32 blocks, E8M0 scales)", "kv_tile": w.bkv, "parallelism": "none",
                    "step": "kmean + quantize Q/K/V + FP4 attention (sage_attn_fp4_fwd_ws)"},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
-                     "frac": attn_tflops / PEAK_FP4_TFLOPS, "traffic": traffic_from_counters(1),
-                     "kernel": ("attn_fp4_mx256_kernel<128,false,0,false>" if w.bkv == 256 else
+                     "frac": attn_tflops / PEAK_FP4_TFLOPS, "traffic": traffic_from_counters("default"),
+                     "kernel": ("attn_fp4_mx256_kernel<128,false,0,false,4>" if w.bkv == 256 else
                                 "attn_fp4_mx_kernel<%d,%d,false,0,false>" % (D, w.bkv)), "kernel_ms": t_attn * 1e3},
         "accuracy_vs_exact": acc,
         "quantize": {"ms": t_quant * 1e3, "algorithmic_GBs": quant_bytes / t_quant / 1e9,
                      "frac_of_hbm_peak": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS},
         "bf16_kernel": bf16,
+        "attn_wg256": wg256,
         "smooth_q_step": smooth_q,
         "int8_fwd": int8,
         "int8_bwd": int8_bwd,

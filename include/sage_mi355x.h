@@ -51,7 +51,12 @@ typedef enum {
 #define SAGE_SMOOTH_Q       0x20u /* smoothing Q (Algorithm 1), see below                   */
 #define SAGE_BKV64          0x40u /* KV tile of 64 tokens instead of 128                   */
 #define SAGE_BKV256         0x80u /* KV tile of 256 tokens (MXFP4 attention only)          */
-#define SAGE_FMT_ALL_BITS   0xFFu
+#define SAGE_WG256          0x100u /* 256 queries per workgroup instead of 128: each K^/V^T
+                                      tile is fetched from L2 once per 256 queries (about
+                                      half the fetch traffic) for slightly more time.  Only
+                                      with SAGE_BKV256, non-causal, without SAGE_SMOOTH_Q;
+                                      otherwise SAGE_ERR_UNSUPPORTED.  Same results.      */
+#define SAGE_FMT_ALL_BITS   0x1FFu
 
 /* ---- quantization roles ------------------------------------------------ */
 #define SAGE_ROLE_Q 0

@@ -20,6 +20,7 @@ SAGE_NO_SMOOTH_K = 0x10
 SAGE_SMOOTH_Q = 0x20
 SAGE_BKV64 = 0x40
 SAGE_BKV256 = 0x80
+SAGE_WG256 = 0x100       # 256 queries per workgroup (MXFP4, 256-key tiles, non-causal, no smoothing Q)
 
 
 def bkv_flag(bkv: int) -> int:

@@ -405,17 +405,24 @@ struct Fp4Stage256 {
   static constexpr int BIAS_OFF = VS_OFF + D * 8;
   static constexpr int BYTES = BIAS_OFF + (SQ ? BKV * 4 : 0);
   static constexpr int NKSJ = KS_BYTES / 4 / 64, NVSJ = D * 2 / 64;   // dword-load jobs of 64 lanes
-  static constexpr int SJ = (NKSJ + NVSJ) / 4;                        // per wave
-  static_assert((NKSJ + NVSJ) % 4 == 0 && NKB % 4 == 0 && NVB % 4 == 0, "even split over 4 waves");
+  static_assert(NKB % 8 == 0 && NVB % 8 == 0, "operand blocks split evenly over 4 or 8 waves");
 };
 
-template <int D, bool CAUSAL, int OUT, bool SQ>
-__global__ __launch_bounds__(256, 2) void attn_fp4_mx256_kernel(
+// W waves per workgroup (32 queries each).  W = 4 is the default.  W = 8
+// (flag SAGE_WG256; non-causal, without smoothing Q, whose GEMV bias rows
+// belong to 128-query blocks) shares each K^/V^T tile in LDS between 256
+// queries, so a tile is fetched from L2 once per 256 queries instead of per
+// 128: about half the fetch traffic, for slightly more time (the two waves on
+// a SIMD then meet at the same barrier).
+template <int D, bool CAUSAL, int OUT, bool SQ, int W>
+__global__ __launch_bounds__(64 * W, 8 / W) void attn_fp4_mx256_kernel(
     const uint8_t* __restrict__ qc, const uint8_t* __restrict__ qs, const uint8_t* __restrict__ kc,
     const uint8_t* __restrict__ ks, const uint8_t* __restrict__ vc, const uint8_t* __restrict__ vs,
     const float* __restrict__ qkb, void* __restrict__ o, int BH, int N, int Np, int nqt, float c2, float log6) {
   using T = Fp4Stage256<D, SQ>;
   constexpr int BKV = T::BKV, NSUB = T::NSUB, NKS = T::NKS, NDB = T::NDB, NG = T::NG;
+  constexpr int AQW = 32 * W;
+  static_assert((W == 4 || W == 8) && (!SQ || W == 4), "4 or 8 waves; smoothing Q blocks are 128 queries");
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][T::BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -427,7 +434,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx256_kernel(
   const long long bh = lin / nqt;
   int qt = lin % nqt;
   if (CAUSAL) qt = nqt - 1 - qt;
-  const int q0 = qt * AQ;
+  const int q0 = qt * AQW;
   const int qw = q0 + wave * 32;
   const int qi = qw + col;
 
@@ -446,7 +453,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx256_kernel(
   qsc >>= 8 * hi;
 
   int ntiles = (N + BKV - 1) / BKV;
-  if (CAUSAL) ntiles = min(ntiles, min(q0 + AQ - 1, N - 1) / BKV + 1);
+  if (CAUSAL) ntiles = min(ntiles, min(q0 + AQW - 1, N - 1) / BKV + 1);
 
   // Load jobs: wave w loads K^ operand blocks b = w + 4i (key row 32t + col,
   // bytes [32s + 16hi, +16) with t = b / NKS, s = b % NKS), V^T operand blocks
@@ -455,10 +462,10 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx256_kernel(
   // then V^T scale dwords 64(jb - NKSJ) + lane (dim row d / 2, half d & 1).
   // Each address is a uniform base -- head, tile, job and the tail redirect
   // -- plus one of five fixed lane offsets, so a load costs no VALU.
-  static_assert(4 % NKS == 0 && NG == 4, "job layout");
-  constexpr int KJ = T::NKB / 4, VJ = T::NVB / 4;
+  static_assert(W % NKS == 0 && NG == 4 && W % NG == 0, "job layout");
+  constexpr int KJ = T::NKB / W, VJ = T::NVB / W, NSJ = T::NKSJ + T::NVSJ, SJ = (NSJ + W - 1) / W;
   const uint32_t ko0 = (uint32_t)((32 * (wave / NKS) + col) * (D / 2) + 32 * (wave % NKS) + 16 * hi);
-  const uint32_t vo0 = (uint32_t)(col * (Np / 2) + 32 * wave + 16 * hi);
+  const uint32_t vo0 = (uint32_t)((32 * (wave / NG) + col) * (Np / 2) + 32 * (wave % NG) + 16 * hi);
   const uint32_t kso = (uint32_t)(4 * lane);
   const uint32_t vso = (uint32_t)((lane >> 1) * (Np / 32) + 4 * (lane & 1));
   const uint32_t vso_hi = (uint32_t)(4 * (lane & 1));   // the second dword: subtracted when it lies past Np
@@ -477,22 +484,22 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx256_kernel(
     uint8_t* L = lds[stage];
 #pragma unroll
     for (int i = 0; i < KJ; ++i) {
-      const int b = wave + 4 * i, t = b / NKS;
+      const int b = wave + W * i, t = b / NKS;
       const long long back = (short_tail && t >= NSUB / 2) ? 128LL * (D / 2) : 0;
-      lds_load16(sbase(kt + ((long long)i * (128 / NKS) * (D / 2) - back)) + ko0, L + T::KC_OFF + b * 1024);
+      lds_load16(sbase(kt + ((long long)i * (32 * W / NKS) * (D / 2) - back)) + ko0, L + T::KC_OFF + b * 1024);
     }
 #pragma unroll
     for (int i = 0; i < VJ; ++i) {
-      const long long back = (short_tail && wave >= NG / 2) ? 64 : 0;
-      lds_load16(sbase(vt + ((long long)i * 32 * (Np / 2) - back)) + vo0, L + T::VC_OFF + (wave + 4 * i) * 1024);
+      const long long back = (short_tail && (wave % NG) >= NG / 2) ? 64 : 0;
+      lds_load16(sbase(vt + ((long long)i * 8 * W * (Np / 2) - back)) + vo0, L + T::VC_OFF + (wave + W * i) * 1024);
     }
 #pragma unroll
-    for (int i = 0; i < T::SJ; ++i) {
-      const int jb = wave + 4 * i;
+    for (int i = 0; i < SJ; ++i) {
+      const int jb = wave + W * i;
       if (jb < T::NKSJ) {
         const long long back = (short_tail && 64 * jb * 4 >= T::KS_BYTES / 2) ? T::KS_BYTES / 2 : 0;
         lds_load4(sbase(kst + (256LL * jb - back)) + kso, L + T::KS_OFF + jb * 256);
-      } else {
+      } else if (jb < NSJ) {
         lds_load4(sbase(vst + (long long)(jb - T::NKSJ) * Np) + (vso - (short_tail ? vso_hi : 0u)),
                   L + T::VS_OFF + (jb - T::NKSJ) * 256);
       }
@@ -659,24 +666,24 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx256_kernel(
   }
 }
 
-template <int D, bool CAUSAL, int OUT, bool SQ>
+template <int D, bool CAUSAL, int OUT, bool SQ, int W>
 static hipError_t launch_fp4_256_t(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
                                    const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2,
                                    float log6, hipStream_t st) {
-  const int nqt = (N + AQ - 1) / AQ;
-  hipLaunchKernelGGL((attn_fp4_mx256_kernel<D, CAUSAL, OUT, SQ>), dim3((unsigned)(nqt * BH)), dim3(256), 0, st,
+  const int nqt = (N + 32 * W - 1) / (32 * W);
+  hipLaunchKernelGGL((attn_fp4_mx256_kernel<D, CAUSAL, OUT, SQ, W>), dim3((unsigned)(nqt * BH)), dim3(64 * W), 0, st,
                      (const uint8_t*)qc, (const uint8_t*)qs, (const uint8_t*)kc, (const uint8_t*)ks, (const uint8_t*)vc,
                      (const uint8_t*)vs, qkb, o, BH, N, Np, nqt, c2, log6);
   return hipGetLastError();
 }
 
-template <int D, bool CAUSAL, bool SQ>
+template <int D, bool CAUSAL, bool SQ, int W>
 static hipError_t launch_fp4_256_o(int out, const void* qc, const void* qs, const void* kc, const void* ks,
                                    const void* vc, const void* vs, const float* qkb, void* o, int BH, int N, int Np,
                                    float c2, float log6, hipStream_t st) {
-  if (out == 0) return launch_fp4_256_t<D, CAUSAL, 0, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
-  if (out == 1) return launch_fp4_256_t<D, CAUSAL, 1, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
-  return launch_fp4_256_t<D, CAUSAL, 2, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+  if (out == 0) return launch_fp4_256_t<D, CAUSAL, 0, SQ, W>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+  if (out == 1) return launch_fp4_256_t<D, CAUSAL, 1, SQ, W>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+  return launch_fp4_256_t<D, CAUSAL, 2, SQ, W>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
 }
 
 template <int D, int BKV, bool CAUSAL, int OUT, bool SQ>
@@ -710,14 +717,19 @@ static hipError_t launch_fp4_s(int out, const void* qc, const void* qs, const vo
 // qkb: smoothing-Q bias [BH, ceil(N/128), Np] fp32, or null without smoothing Q.
 hipError_t launch_attn_fp4_mx(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
                               const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
-                              bool causal, int out, float c2, float log6, hipStream_t st) {
+                              bool causal, int out, float c2, float log6, bool wg256, hipStream_t st) {
 #define SAGE_A(DD, BB)                                                                                    \
   return causal ? launch_fp4_s<DD, BB, true>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st) \
                 : launch_fp4_s<DD, BB, false>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st)
   if (bkv == 256) {
-#define SAGE_A256(DD, CC)                                                                                      \
-  return qkb ? launch_fp4_256_o<DD, CC, true>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st) \
-             : launch_fp4_256_o<DD, CC, false>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st)
+    // 256-query workgroups: non-causal, without smoothing Q (checked by the caller)
+    if (wg256) {
+      if (D == 128) return launch_fp4_256_o<128, false, false, 8>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+      return launch_fp4_256_o<64, false, false, 8>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st);
+    }
+#define SAGE_A256(DD, CC)                                                                                         \
+  return qkb ? launch_fp4_256_o<DD, CC, true, 4>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st) \
+             : launch_fp4_256_o<DD, CC, false, 4>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, log6, st)
     if (D == 128) { if (causal) { SAGE_A256(128, true); } else { SAGE_A256(128, false); } }
     else { if (causal) { SAGE_A256(64, true); } else { SAGE_A256(64, false); } }
 #undef SAGE_A256

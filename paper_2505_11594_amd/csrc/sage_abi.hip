@@ -22,7 +22,7 @@ hipError_t launch_qk_bias(const void* k, const float* mu, const float* qbar, flo
                           bool bf16, hipStream_t st);
 hipError_t launch_attn_fp4_mx(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
                               const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
-                              bool causal, int out, float c2, float log6, hipStream_t st);
+                              bool causal, int out, float c2, float log6, bool wg256, hipStream_t st);
 hipError_t launch_attn_nv16(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
                             const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
                             bool causal, int out, float c2, float logR, hipStream_t st);
@@ -147,6 +147,7 @@ int attn_args(const void* q, const void* k, const void* v, const void* o, int B,
   int rc = check_shape(B, H, N, D, fmt);
   if (rc != SAGE_OK) return rc;
   if ((fmt & SAGE_BKV256) && fmt_of(fmt) != SAGE_FMT_MXFP4) return SAGE_ERR_UNSUPPORTED;
+  if ((fmt & SAGE_WG256) && (!(fmt & SAGE_BKV256) || causal || (fmt & SAGE_SMOOTH_Q))) return SAGE_ERR_UNSUPPORTED;
   if (!q || !k || !v || !o) return SAGE_ERR_INVALID_ARG;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return SAGE_ERR_INVALID_ARG;
   if (causal != 0 && causal != 1) return SAGE_ERR_INVALID_ARG;
@@ -168,7 +169,8 @@ int attn_prequant_impl(const void* qc, const void* qs, const void* kc, const voi
                                              causal != 0, out_kind(fmt), softmax_c2(D), log2_of_2688(), st));
   }
   return hip_status(sage::launch_attn_fp4_mx(qc, qs, kc, ks, vc, vs, qkb, o, B * H, N, pad128(N), D, bkv,
-                                             causal != 0, out_kind(fmt), softmax_c2(D), log2_of_6(), st));
+                                             causal != 0, out_kind(fmt), softmax_c2(D), log2_of_6(),
+                                             (fmt & SAGE_WG256) != 0, st));
 }
 
 int attn_ws_impl(const void* q, const void* k, const void* v, void* o, int B, int H, int N, int D, int causal,
@@ -495,6 +497,8 @@ int sage_attn_fp4_fwd_prequant(const void* q_codes, const void* q_scales, const 
   if (!aligned(q_scales, 4) || !aligned(k_scales, 4) || !aligned(vt_scales, 4)) return SAGE_ERR_INVALID_ARG;
   if (causal != 0 && causal != 1) return SAGE_ERR_INVALID_ARG;
   if (fmt & SAGE_SMOOTH_Q) return SAGE_ERR_UNSUPPORTED;   // the GEMV bias is not an input of this entry point
+  if ((fmt & SAGE_WG256) && (!(fmt & SAGE_BKV256) || fmt_of(fmt) != SAGE_FMT_MXFP4 || causal))
+    return SAGE_ERR_UNSUPPORTED;
   return attn_prequant_impl(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, nullptr, o, B, H, N, D, causal,
                             fmt, stream);
 }

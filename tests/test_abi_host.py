@@ -49,7 +49,7 @@ def _attn(L, **kw):
 
 
 @pytest.mark.parametrize("bad", [dict(q=None), dict(o=None), dict(q=FAKE + 2), dict(B=0), dict(H=-1), dict(N=0),
-                                 dict(D=96), dict(D=256), dict(causal=2), dict(fmt=0x100), dict(fmt=0x3),
+                                 dict(D=96), dict(D=256), dict(causal=2), dict(fmt=0x200), dict(fmt=0x3),
                                  dict(fmt=0x40 | 0x80), dict(N=1 << 30),
                                  dict(N=(1 << 24) + 1), dict(D=64, N=(1 << 25) + 1)])
 def test_attn_invalid_args_rejected_on_host(L, bad):
@@ -205,3 +205,16 @@ def test_per_head_size_limit(L):
         assert L.sage_attn_int8_workspace_size(1, 1, nmax, D, 0) > 0
         assert L.sage_attn_int8_workspace_size(1, 1, nmax + 1, D, 0) == 0
         assert bd.attn_int8_bwd_min_workspace_size(1, 1, nmax + 1, D) == 0
+
+
+def test_wg256_only_where_implemented(L):
+    """256-query workgroups need MXFP4 with 256-key tiles, non-causal, no smoothing Q."""
+    W, B256 = bd.SAGE_WG256, bd.SAGE_BKV256
+    assert _attn(L, fmt=W) == bd.SAGE_ERR_UNSUPPORTED                                  # 128-key tiles
+    assert _attn(L, fmt=W | bd.SAGE_BKV64) == bd.SAGE_ERR_UNSUPPORTED
+    assert _attn(L, fmt=W | B256, causal=1) == bd.SAGE_ERR_UNSUPPORTED
+    assert _attn(L, fmt=W | B256 | bd.SAGE_SMOOTH_Q) == bd.SAGE_ERR_UNSUPPORTED
+    assert _attn(L, fmt=W | B256 | bd.SAGE_FMT_NV16_E4M3) == bd.SAGE_ERR_UNSUPPORTED
+    args = [FAKE] * 7 + [1, 1, 128, 128]
+    assert L.sage_attn_fp4_fwd_prequant(*args, 1, W | B256, None) == bd.SAGE_ERR_UNSUPPORTED
+    assert L.sage_attn_fp4_fwd_prequant(*args, 0, W, None) == bd.SAGE_ERR_UNSUPPORTED

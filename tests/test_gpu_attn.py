@@ -260,3 +260,38 @@ def test_binding_rejects_mismatched_buffers():
     o = bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (1, 2, 100, 64))      # the matching call runs
     torch.cuda.synchronize()
     assert o.shape == (1, 2, 100, 64) and o.dtype == torch.float32
+
+
+@pytest.mark.parametrize("N,D", [(1, 64), (100, 128), (257, 64), (300, 128), (640, 128), (1000, 64)])
+def test_attn_wg256_same_bits_as_default(N, D):
+    """SAGE_WG256 (256 queries per workgroup, each K^/V^T tile shared by 8
+    waves) changes who loads a tile, not what any wave computes: the output is
+    bit-identical to the default 128-query workgroups, fp32 and 16-bit."""
+    torch = torch_dev()
+    say("attn wg256 N=%d D=%d" % (N, D))
+    in_dtype = 1 if N % 2 else 0
+    q, k, v = wl.make_inputs(2, 3, N, D, in_dtype, seed=700 + N, k_bias_var=4.0, outlier_frac=0.02)
+    got = None
+    for out_f32 in (True, False):
+        a = gpu_attn(q, k, v, in_dtype, False, 0, 256, out_f32=out_f32)
+        qd, kd, vd = (to_dev(x, in_dtype) for x in (q, k, v))
+        b = bd.sage_attn_fp4_fwd(qd, kd, vd, causal=False, fmt=bd.SAGE_BKV256 | bd.SAGE_WG256, out_f32=out_f32)
+        torch.cuda.synchronize()
+        assert torch.equal(a, b)
+        if out_f32:
+            got = b.cpu().numpy().reshape(-1, D)
+    ref, tie, _ = oracle.attn(q, k, v, in_dtype, False, oracle.FMT_MX, 256)
+    check(got, ref, tie, "wg256")
+
+
+def test_attn_wg256_bench_workload_same_bits():
+    """The bench workload (B1 H32 N32768 D128, outlier rows) with SAGE_WG256:
+    every output bit equal to the default launch."""
+    torch = torch_dev()
+    w = wl.CONFIGS[2]
+    q, k, v = generate_cached(2)
+    a = gpu_attn(q, k, v, w.in_dtype, False, 0, 256)
+    qd, kd, vd = (to_dev(x, w.in_dtype) for x in (q, k, v))
+    b = bd.sage_attn_fp4_fwd(qd, kd, vd, causal=False, fmt=bd.SAGE_BKV256 | bd.SAGE_WG256)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
