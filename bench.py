@@ -211,6 +211,56 @@ def issue_rates(torch):
                       "cycles_per_iteration": res, "split": split, "derived": summary}), flush=True)
 
 
+def issue_ceilings(torch, kernel_ms: float):
+    """Ceilings of the 256-key FP4 kernel on the bench workload from instruction
+    issue: the issue rates measured live (register-only loops, 2 waves per SIMD
+    as in the kernel) times the kernel's instructions per tile-wave (one wave x
+    one 256-key tile) from the committed SQ counters of the same source.  Each
+    ceiling is the MFMA time per tile-wave at the spec peak (32 MFMAs x 32
+    cycles) over the cycles that one kind of work, or a combination, needs; the
+    achieved figure puts the measured kernel time in the same units at 2.4 GHz.
+    None when the counters were taken on another kernel source."""
+    import ctypes
+    if not os.path.exists(COUNTERS):
+        return None
+    c = json.load(open(COUNTERS))
+    if c.get("source_sha") != kernel_source_sha() or "sq_per_tile_wave" not in c.get("default", {}):
+        return None
+    sq = c["default"]["sq_per_tile_wave"]
+    n_mfma, n_exp, n_pack = sq["SQ_INSTS_MFMA"], sq["SQ_INSTS_VALU_TRANS_F32"], c["fp4_packs_per_tile_wave"]
+    n_valu = sq["SQ_INSTS_VALU"] - n_mfma - n_exp - n_pack     # SQ_INSTS_VALU counts MFMA and transcendentals too
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2505_11594_amd", "libsage_rates.so"))
+    lib.sage_rates_run.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                   ctypes.POINTER(ctypes.c_float)]
+    iters = lib.sage_rates_iterations()
+    out = torch.empty(1024 * 8 * 64, dtype=torch.float32, device="cuda:0")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    names = [t[0] for t in RATE_TESTS]
+    cyc = {}
+    for name in ("fma", "exp", "cvt_fp4", "mfma_fp4"):
+        ms = ctypes.c_float()
+        for _ in range(2):                                  # the first launch warms the clocks
+            rc = lib.sage_rates_run(names.index(name), 2, ctypes.c_void_p(out.data_ptr()), stream, ctypes.byref(ms))
+            if rc != 0:
+                raise RuntimeError("sage_rates_run(%s) failed: %d" % (name, rc))
+        per_iter = ms.value * 1e-3 * 2.4e9 / (iters * 2)
+        cyc[name] = per_iter / [t[2] for t in RATE_TESTS if t[0] == name][0]
+    t_mfma, t_exp = n_mfma * cyc["mfma_fp4"], n_exp * cyc["exp"]
+    t_valu = n_valu * cyc["fma"] + n_pack * cyc["cvt_fp4"]
+    spec = n_mfma * 32.0
+    tile_waves_per_simd = c["tile_waves_per_launch"] / 1024.0
+    measured = kernel_ms * 1e-3 * 2.4e9 / tile_waves_per_simd
+    return {"cycles_per_instruction": {k: round(v, 3) for k, v in cyc.items()},
+            "per_tile_wave": {"mfma": n_mfma, "exp": n_exp, "fp4_pack": n_pack, "other_valu": round(n_valu, 1)},
+            "cycles_per_tile_wave": {"mfma": round(t_mfma, 1), "exp": round(t_exp, 1), "valu_and_packs": round(t_valu, 1),
+                                     "all_in_series": round(t_mfma + t_exp + t_valu, 1),
+                                     "measured_at_2.4GHz": round(measured, 1)},
+            "frac_of_peak": {"mfma_alone": spec / t_mfma, "exp_alone": spec / t_exp, "valu_alone": spec / t_valu,
+                             "exp_hidden_under_mfma": spec / (t_valu + max(t_mfma, t_exp)),
+                             "all_in_series": spec / (t_mfma + t_exp + t_valu), "achieved": spec / measured},
+            "counters": "profiles/attn_fp4_mx_counters.json (rocprofv3 SQ counters; 64 FP4 packs per tile-wave from the code)"}
+
+
 def accuracy_vs_exact(torch, q, k, v, o, w, nrows=512, seed=7):
     """CosSim, relative L1 and RMSE of an attention output against fp64 softmax(QK^T/sqrt(D))V
     (the paper's accuracy metrics), on a seeded sample of query rows of every head; the
@@ -570,6 +620,13 @@ def main():
         int8 = int8_forward(torch, bd, w, qd, kd, vd, o, args.steps)
         int8_bwd = int8_backward(torch, bd, w, qd, kd, vd, o, int8_forward.lse, args.steps)
 
+    ceilings = None
+    if w.bkv == 256 and D == 128:
+        ceilings = issue_ceilings(torch, t_attn * 1e3)
+        if ceilings:
+            log("issue ceilings (fraction of the MXFP4 peak): " +
+                ", ".join("%s %.3f" % kv for kv in ceilings["frac_of_peak"].items()))
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
@@ -594,7 +651,8 @@ def main():
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
                      "frac": attn_tflops / PEAK_FP4_TFLOPS, "traffic": traffic_from_counters("default"),
                      "kernel": ("attn_fp4_mx256_kernel<128,false,0,false,4>" if w.bkv == 256 else
-                                "attn_fp4_mx_kernel<%d,%d,false,0,false>" % (D, w.bkv)), "kernel_ms": t_attn * 1e3},
+                                "attn_fp4_mx_kernel<%d,%d,false,0,false>" % (D, w.bkv)), "kernel_ms": t_attn * 1e3,
+                     "issue_ceilings": ceilings},
         "accuracy_vs_exact": acc,
         "quantize": {"ms": t_quant * 1e3, "algorithmic_GBs": quant_bytes / t_quant / 1e9,
                      "frac_of_hbm_peak": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS},
