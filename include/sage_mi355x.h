@@ -123,8 +123,9 @@ int sage_quant_fp4(const void* x, int role, int B, int H, int N, int D, unsigned
 
 /* Workspace bytes for sage_attn_fp4_fwd_ws (quantized Q, K, V, the mean and
  * its partial sums; with SAGE_SMOOTH_Q also the query-block means and the
- * GEMV term, B*H*ceil(N/128)*(D + Np)*4 bytes).  0 for invalid arguments.
- * Host only. */
+ * GEMV term, B*H*ceil(N/128)*(D + Np)*4 bytes; with NV16 also the exact f16
+ * expansion of K^ and V^T the attention kernel reads, 4*B*H*Np*D bytes).
+ * 0 for invalid arguments.  Host only. */
 size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt);
 
 /*
@@ -135,7 +136,8 @@ size_t sage_attn_fp4_workspace_size(int B, int H, int N, int D, unsigned fmt);
  * per row and tile, then phi of P~/s_P1 with R = 6 for E8M0 scales and
  * 448*6 for E4M3 scales) and O += FP4MM(P^, V^) * s_P1; O = O / l.
  * MXFP4 runs on block-scaled FP4 MFMA; NV16 (whose E4M3 scales at 16-element
- * granularity the MFMA cannot take) dequantizes exactly to f16 and runs on
+ * granularity the MFMA cannot take) expands K^ and V^T exactly to f16 once
+ * per call, dequantizes Q^ and P^ exactly to f16 in registers, and runs on
  * f16 MFMA.
  * With SAGE_SMOOTH_Q the scores get the smoothing-Q GEMV term described above
  * (both formats).
@@ -180,7 +182,9 @@ int sage_attn_fp4_fwd_noalloc(const void* q, const void* k, const void* v, void*
  * sage_attn_fp4_fwd_prequant -- the attention kernel alone, on tensors
  * produced by sage_quant_fp4 (layouts above).  kmean is not needed: the
  * smoothing is already inside K^ (softmax is invariant to it).  SAGE_SMOOTH_Q
- * returns SAGE_ERR_UNSUPPORTED (its GEMV term is not an input here).
+ * returns SAGE_ERR_UNSUPPORTED (its GEMV term is not an input here).  With
+ * NV16 the f16 expansion of K^ and V^T (4*B*H*Np*D bytes) comes from
+ * hipMallocAsync on `stream` and is freed with hipFreeAsync on it.
  */
 int sage_attn_fp4_fwd_prequant(const void* q_codes, const void* q_scales,
                                const void* k_codes, const void* k_scales,

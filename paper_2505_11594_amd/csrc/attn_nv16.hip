@@ -7,8 +7,9 @@
 // so code * s is v_cvt_scalef32_pk_f16_fp4 (code * 2^X, exact) times M
 // (v_pk_mul_f16, exact): one convert and one packed multiply per two values.
 //   * Q^ is dequantized once into the B-operand registers;
-//   * each K^ / V^T tile arrives as codes + scales (4.5 bits per element),
-//     staged in registers a tile ahead and dequantized into f16 LDS tiles;
+//   * K^ and V^T are expanded once per call into f16 copies in HBM (the same
+//     exact values), and each tile of them is copied into LDS with
+//     direct-to-LDS loads a tile ahead: no per-workgroup dequantization;
 //   * P~ gets the two-level quantization of Sec. 3.2 with R = 448 * 6 in
 //     registers: the first level as in the MXFP4 kernel, the second level an
 //     E4M3 scale per 16 keys (round to nearest even of blockmax/6), E2M1 codes
@@ -32,86 +33,71 @@ typedef _Float16 v2h __attribute__((ext_vector_type(2)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
 __device__ __forceinline__ v8h as_h(const v4i x) { return __builtin_bit_cast(v8h, x); }
 
-template <int D, int BKV>
-struct Nv16Stage {
-  using T = Bf16TileT<D, BKV>;
-  static constexpr int KU = BKV * D / 32, VU = D * BKV / 32;   // 32-element units
-  static constexpr int KPT = (KU + 255) / 256, VPT = (VU + 255) / 256;
-  v4i kc[KPT], vc[VPT];
-  uint32_t ksc[KPT], vsc[VPT];
+// Direct-to-LDS 16-byte load: lane l's bytes land at dst + 16 l.
+__device__ __forceinline__ void nv_lds_load16(const void* src, void* dst) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+}
+__device__ __forceinline__ void nv_wait_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
+// a workgroup-uniform address in scalar registers (scalar base + lane offset)
+__device__ __forceinline__ const uint8_t* nv_sbase(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+  return reinterpret_cast<const uint8_t*>((hi << 32) | lo);
+}
 
-  __device__ __forceinline__ void load(const uint8_t* __restrict__ kcg, const uint8_t* __restrict__ ksg,
-                                       const uint8_t* __restrict__ vcg, const uint8_t* __restrict__ vsg, long long bh,
-                                       int Np, int kb, int tid) {
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int u = (tid + 256 * i) % KU;          // units past the tile repeat a valid one
-      const int row = u / (D / 32), c = u % (D / 32);
-      const size_t r = (size_t)bh * Np + kb + row;
-      kc[i] = *reinterpret_cast<const v4i*>(kcg + r * (D / 2) + c * 16);
-      ksc[i] = *reinterpret_cast<const uint16_t*>(ksg + r * (D / 16) + c * 2);
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int u = (tid + 256 * i) % VU;
-      const int d = u / (BKV / 32), c = u % (BKV / 32);
-      const size_t r = (size_t)bh * D + d;
-      vc[i] = *reinterpret_cast<const v4i*>(vcg + r * (Np / 2) + kb / 2 + c * 16);
-      vsc[i] = *reinterpret_cast<const uint16_t*>(vsg + r * (Np / 16) + kb / 16 + c * 2);
-    }
+// Exact f16 expansion of K^ and V^T.  Both are flat arrays of 32-element
+// units (16 code bytes, two E4M3 scale bytes, one per 16 elements); unit u of
+// K^ (row-major [BH, Np, D]) and of V^T ([BH, D, Np]) expands to the 32 f16
+// values at element 32 u of K~ / V~^T, so the token order of K^ is kept.
+// code * s = v_cvt_scalef32_pk_f16_fp4(code, 2^X) * M (s = M * 2^X), both
+// steps exact.  One thread per unit; K units first, then V units.
+__global__ __launch_bounds__(256) void nv16_expand_kernel(const uint8_t* __restrict__ kc, const uint8_t* __restrict__ ks,
+                                                          const uint8_t* __restrict__ vc, const uint8_t* __restrict__ vs,
+                                                          uint8_t* __restrict__ kh, uint8_t* __restrict__ vth,
+                                                          long long units) {
+  __shared__ float ptab[128];
+  __shared__ uint32_t mtab[128];
+  const int tid = threadIdx.x;
+  if (tid < 128) {
+    const int E = tid >> 3, man = tid & 7;
+    ptab[tid] = __builtin_ldexpf(1.0f, E ? E - 10 : -9);
+    const _Float16 M = (_Float16)(E ? 8 + man : man);
+    mtab[tid] = __builtin_bit_cast(uint32_t, v2h{M, M});
   }
-
-  // 32 codes + two E4M3 scales -> 32 f16 values in four 16-byte chunks
-  __device__ __forceinline__ static void dequant32(const v4i codes, uint32_t sc2, const float* ptab,
-                                                   const uint32_t* mtab, v4i out[4]) {
-    const uint32_t b0 = sc2 & 0xFFu, b1 = (sc2 >> 8) & 0xFFu;
-    const float x0 = ptab[b0], x1 = ptab[b1];
-    const v2h m0 = __builtin_bit_cast(v2h, mtab[b0]), m1 = __builtin_bit_cast(v2h, mtab[b1]);
+  __syncthreads();
+  long long u = (long long)blockIdx.x * 256 + tid;
+  if (u >= 2 * units) return;
+  const bool isv = u >= units;
+  if (isv) u -= units;
+  const uint8_t* c = (isv ? vc : kc) + 16 * u;
+  const uint32_t sc2 = *reinterpret_cast<const uint16_t*>((isv ? vs : ks) + 2 * u);
+  const v4i codes = *reinterpret_cast<const v4i*>(c);
+  const uint32_t b0 = sc2 & 0x7Fu, b1 = (sc2 >> 8) & 0x7Fu;   // scales are non-negative E4M3 codes
+  const float x0 = ptab[b0], x1 = ptab[b1];
+  const v2h m0 = __builtin_bit_cast(v2h, mtab[b0]), m1 = __builtin_bit_cast(v2h, mtab[b1]);
+  v4i* out = reinterpret_cast<v4i*>((isv ? vth : kh) + 64 * u);
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const uint32_t word = (uint32_t)codes[w];
-      uint32_t o[4];
-      static_for<4>([&](auto B_) {
-        constexpr int b = decltype(B_)::value;
-        const v2h h = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(word, w < 2 ? x0 : x1, b) * (w < 2 ? m0 : m1);
-        o[b] = __builtin_bit_cast(uint32_t, h);
-      });
-      out[w] = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
-    }
+  for (int w = 0; w < 4; ++w) {
+    const uint32_t word = (uint32_t)codes[w];
+    uint32_t ov[4];
+    static_for<4>([&](auto B_) {
+      constexpr int b = decltype(B_)::value;
+      const v2h h = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(word, w < 2 ? x0 : x1, b) * (w < 2 ? m0 : m1);
+      ov[b] = __builtin_bit_cast(uint32_t, h);
+    });
+    out[w] = v4i{(int)ov[0], (int)ov[1], (int)ov[2], (int)ov[3]};
   }
-
-  __device__ __forceinline__ void store(uint8_t* lds, int tid, const float* ptab, const uint32_t* mtab) const {
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int u = (tid + 256 * i) % KU;
-      const int row = u / (D / 32), c = u % (D / 32);
-      v4i q[4];
-      dequant32(kc[i], ksc[i], ptab, mtab, q);
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-        *reinterpret_cast<v4i*>(lds + T::K_OFF + row * T::KROW + bswz<T::KCH>(row, 4 * c + w) * 16) = q[w];
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int u = (tid + 256 * i) % VU;
-      const int d = u / (BKV / 32), c = u % (BKV / 32);
-      v4i q[4];
-      dequant32(vc[i], vsc[i], ptab, mtab, q);
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-        *reinterpret_cast<v4i*>(lds + T::V_OFF + d * T::VROW + bswz<T::VCH>(d, 4 * c + w) * 16) = q[w];
-    }
-  }
-};
+}
 
 // OUT: 0 = fp32, 1 = bf16, 2 = fp16.  SQ: smoothing Q -- S += qkb[bh, query
 // block, key] (Algorithm 1's GEMV of the block mean with K'; one row of Np
 // floats per 128-query block, this workgroup's query tile).
 template <int D, int BKV, bool CAUSAL, int OUT, bool SQ>
 __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
-    const uint8_t* __restrict__ qc, const uint8_t* __restrict__ qs, const uint8_t* __restrict__ kc,
-    const uint8_t* __restrict__ ks, const uint8_t* __restrict__ vc, const uint8_t* __restrict__ vs,
-    const float* __restrict__ qkb, void* __restrict__ o, int BH, int N, int Np, int nqt, float c2, float logR) {
+    const uint8_t* __restrict__ qc, const uint8_t* __restrict__ qs, const uint8_t* __restrict__ kh,
+    const uint8_t* __restrict__ vth, const float* __restrict__ qkb, void* __restrict__ o, int BH, int N, int Np,
+    int nqt, float c2, float logR) {
   using T = Bf16TileT<D, BKV>;
   constexpr int NSUB = BKV / 32;   // 32-key subtiles = P blocks per lane
   constexpr int NKS = D / 16;      // QK K-steps
@@ -119,11 +105,11 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   constexpr int NDB = D / 32;
   constexpr int BIAS_OFF = T::BYTES, LBYTES = T::BYTES + (SQ ? BKV * 4 : 0);   // bias of the tile's keys
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][LBYTES];
-  // per E4M3 code b (s = M * 2^X): rtab = fl32(1 / s) (0 for s = 0), the second
-  // level's reciprocal; ptab = 2^X; mtab = {M, M} in f16
+  // per E4M3 code b (s = M * 2^X) of P's second level: rtab = fl32(1 / s) (0 for
+  // s = 0), ptab = 2^X, mtab = {M, M} in f16
   __shared__ float rtab[128], ptab[128];
   __shared__ uint32_t mtab[128];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31, hi = lane >> 5;
 
   const int total = nqt * BH;
@@ -175,31 +161,47 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
     mtab[tid] = __builtin_bit_cast(uint32_t, v2h{M, M});
   }
   __syncthreads();
-  Nv16Stage<D, BKV> stg;
-  // smoothing Q: threads tid < BKV/4 stage 4 bias entries of the next tile
+  // Tile loads, direct to LDS in the swizzled f16 layout.  Job J of a tile
+  // (1 KiB, wave J % 4) covers K~ rows J * KRJ .. + KRJ (V~^T rows J * VRJ ..);
+  // lane l fills LDS chunk l of the job, which holds logical chunk
+  // bswz(row, l % KCH) of its row.  For J = wave + 4 i that chunk and the
+  // lane's row within the job do not depend on i, so every load is a uniform
+  // base plus one fixed lane offset per operand.
+  constexpr int KRJ = 1024 / T::KROW, VRJ = 1024 / T::VROW;
+  constexpr int NKJ = BKV * T::KROW / 1024 / 4, NVJ = D * T::VROW / 1024 / 4;   // jobs per wave
+  static_assert(BKV * T::KROW % 4096 == 0 && D * T::VROW % 4096 == 0, "jobs split evenly over 4 waves");
+  uint32_t klo, vlo;
+  {
+    const int kr = wave * KRJ + lane / T::KCH, vr = wave * VRJ + lane / T::VCH;
+    klo = (uint32_t)((lane / T::KCH) * (D * 2) + bswz<T::KCH>(kr, lane % T::KCH) * 16);
+    vlo = (uint32_t)((lane / T::VCH) * (Np * 2) + bswz<T::VCH>(vr, lane % T::VCH) * 16);
+  }
+  const uint8_t* kbase = kh + ((size_t)bh * Np + wave * KRJ) * (D * 2);
+  const uint8_t* vbase = vth + ((size_t)bh * D + wave * VRJ) * ((size_t)Np * 2);
+  // smoothing Q: the tile's BKV bias entries, 16 bytes per lane of wave 0
   const float* brow = SQ ? qkb + ((size_t)bh * nqt + qt) * Np : nullptr;
-  v4f bst = v4f{0.f, 0.f, 0.f, 0.f};
-  auto bias_load = [&](int kb) {
-    if (SQ && tid < BKV / 4) bst = *reinterpret_cast<const v4f*>(brow + kb + 4 * tid);
+  auto issue = [&](int kb, uint8_t* L) {
+#pragma unroll
+    for (int i = 0; i < NKJ; ++i)
+      nv_lds_load16(nv_sbase(kbase + ((size_t)kb + (size_t)4 * KRJ * i) * (D * 2)) + klo,
+                    L + T::K_OFF + (wave + 4 * i) * 1024);
+#pragma unroll
+    for (int i = 0; i < NVJ; ++i)
+      nv_lds_load16(nv_sbase(vbase + (size_t)4 * VRJ * i * ((size_t)Np * 2) + (size_t)kb * 2) + vlo,
+                    L + T::V_OFF + (wave + 4 * i) * 1024);
+    if constexpr (SQ) {
+      if (wave == 0 && lane < BKV / 4) nv_lds_load16(brow + kb + 4 * lane, L + BIAS_OFF);
+    }
   };
-  auto bias_store = [&](uint8_t* L) {
-    if (SQ && tid < BKV / 4) *reinterpret_cast<v4f*>(L + BIAS_OFF + 16 * tid) = bst;
-  };
-  stg.load(kc, ks, vc, vs, bh, Np, 0, tid);
-  bias_load(0);
-  stg.store(lds[0], tid, ptab, mtab);
-  bias_store(lds[0]);
-  __syncthreads();
+  issue(0, lds[0]);
 
   auto tile = [&](auto BUF_, int j) {
     constexpr int buf = decltype(BUF_)::value;
     const uint8_t* L = lds[buf];
     const int kb = j * BKV;
-    const bool more = j + 1 < ntiles;
-    if (more) {
-      stg.load(kc, ks, vc, vs, bh, Np, kb + BKV, tid);
-      bias_load(kb + BKV);
-    }
+    nv_wait_loads();                                   // this wave's loads of tile j have landed
+    __syncthreads();                                   // everyone's; every wave is past tile j - 1
+    if (j + 1 < ntiles) issue(kb + BKV, lds[buf ^ 1]);
     if (!CAUSAL || kb <= qw + 31) {
       v16f sacc[NSUB];
 #pragma unroll
@@ -305,11 +307,6 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
       mc_old = mc;
       f_old = f;
     }
-    if (more) {
-      stg.store(lds[buf ^ 1], tid, ptab, mtab);
-      bias_store(lds[buf ^ 1]);
-    }
-    __syncthreads();
   };
   for (int j = 0; j < ntiles; j += 2) {
     tile(ic<0>{}, j);
@@ -341,40 +338,47 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
 }
 
 template <int D, int BKV, bool CAUSAL, int OUT, bool SQ>
-static hipError_t launch_nv16_t(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                                const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2, float logR,
-                                hipStream_t st) {
+static hipError_t launch_nv16_t(const void* qc, const void* qs, const uint8_t* kh, const uint8_t* vth, const float* qkb,
+                                void* o, int BH, int N, int Np, float c2, float logR, hipStream_t st) {
   const int nqt = (N + NQ - 1) / NQ;
   hipLaunchKernelGGL((attn_nv16_kernel<D, BKV, CAUSAL, OUT, SQ>), dim3((unsigned)(nqt * BH)), dim3(256), 0, st,
-                     (const uint8_t*)qc, (const uint8_t*)qs, (const uint8_t*)kc, (const uint8_t*)ks, (const uint8_t*)vc,
-                     (const uint8_t*)vs, qkb, o, BH, N, Np, nqt, c2, logR);
+                     (const uint8_t*)qc, (const uint8_t*)qs, kh, vth, qkb, o, BH, N, Np, nqt, c2, logR);
   return hipGetLastError();
 }
 
 template <int D, int BKV, bool CAUSAL, bool SQ>
-static hipError_t launch_nv16_o(int out, const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                                const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2, float logR,
-                                hipStream_t st) {
-  if (out == 0) return launch_nv16_t<D, BKV, CAUSAL, 0, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st);
-  if (out == 1) return launch_nv16_t<D, BKV, CAUSAL, 1, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st);
-  return launch_nv16_t<D, BKV, CAUSAL, 2, SQ>(qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st);
+static hipError_t launch_nv16_o(int out, const void* qc, const void* qs, const uint8_t* kh, const uint8_t* vth,
+                                const float* qkb, void* o, int BH, int N, int Np, float c2, float logR, hipStream_t st) {
+  if (out == 0) return launch_nv16_t<D, BKV, CAUSAL, 0, SQ>(qc, qs, kh, vth, qkb, o, BH, N, Np, c2, logR, st);
+  if (out == 1) return launch_nv16_t<D, BKV, CAUSAL, 1, SQ>(qc, qs, kh, vth, qkb, o, BH, N, Np, c2, logR, st);
+  return launch_nv16_t<D, BKV, CAUSAL, 2, SQ>(qc, qs, kh, vth, qkb, o, BH, N, Np, c2, logR, st);
 }
 
 template <int D, int BKV, bool CAUSAL>
-static hipError_t launch_nv16_s(int out, const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                                const void* vs, const float* qkb, void* o, int BH, int N, int Np, float c2, float logR,
-                                hipStream_t st) {
-  return qkb ? launch_nv16_o<D, BKV, CAUSAL, true>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st)
-             : launch_nv16_o<D, BKV, CAUSAL, false>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st);
+static hipError_t launch_nv16_s(int out, const void* qc, const void* qs, const uint8_t* kh, const uint8_t* vth,
+                                const float* qkb, void* o, int BH, int N, int Np, float c2, float logR, hipStream_t st) {
+  return qkb ? launch_nv16_o<D, BKV, CAUSAL, true>(out, qc, qs, kh, vth, qkb, o, BH, N, Np, c2, logR, st)
+             : launch_nv16_o<D, BKV, CAUSAL, false>(out, qc, qs, kh, vth, qkb, o, BH, N, Np, c2, logR, st);
 }
 
+size_t nv16_expand_bytes(int BH, int Np, int D) { return 2 * (size_t)BH * Np * D * sizeof(uint16_t); }
+
+// kv16: nv16_expand_bytes(BH, Np, D) bytes of device memory (256-byte aligned)
+// for the f16 expansion of K^ (first half) and V^T (second half).
 // qkb: smoothing-Q bias [BH, ceil(N/128), Np] fp32, or null without smoothing Q.
 hipError_t launch_attn_nv16(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                            const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
-                            bool causal, int out, float c2, float logR, hipStream_t st) {
-#define SAGE_N(DD, BB)                                                                                      \
-  return causal ? launch_nv16_s<DD, BB, true>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st) \
-                : launch_nv16_s<DD, BB, false>(out, qc, qs, kc, ks, vc, vs, qkb, o, BH, N, Np, c2, logR, st)
+                            const void* vs, void* kv16, const float* qkb, void* o, int BH, int N, int Np, int D,
+                            int bkv, bool causal, int out, float c2, float logR, hipStream_t st) {
+  const long long units = (long long)BH * Np * (D / 32);   // 32-element units of K^, and of V^T
+  uint8_t* kh = static_cast<uint8_t*>(kv16);
+  uint8_t* vth = kh + nv16_expand_bytes(BH, Np, D) / 2;
+  hipLaunchKernelGGL(nv16_expand_kernel, dim3((unsigned)((2 * units + 255) / 256)), dim3(256), 0, st,
+                     (const uint8_t*)kc, (const uint8_t*)ks, (const uint8_t*)vc, (const uint8_t*)vs, kh, vth, units);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+#define SAGE_N(DD, BB)                                                                              \
+  return causal ? launch_nv16_s<DD, BB, true>(out, qc, qs, kh, vth, qkb, o, BH, N, Np, c2, logR, st) \
+                : launch_nv16_s<DD, BB, false>(out, qc, qs, kh, vth, qkb, o, BH, N, Np, c2, logR, st)
   if (D == 128) { if (bkv == 128) { SAGE_N(128, 128); } else { SAGE_N(128, 64); } }
   else { if (bkv == 128) { SAGE_N(64, 128); } else { SAGE_N(64, 64); } }
 #undef SAGE_N

@@ -24,8 +24,9 @@ hipError_t launch_attn_fp4_mx(const void* qc, const void* qs, const void* kc, co
                               const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
                               bool causal, int out, float c2, float log6, bool wg256, hipStream_t st);
 hipError_t launch_attn_nv16(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc,
-                            const void* vs, const float* qkb, void* o, int BH, int N, int Np, int D, int bkv,
-                            bool causal, int out, float c2, float logR, hipStream_t st);
+                            const void* vs, void* kv16, const float* qkb, void* o, int BH, int N, int Np, int D,
+                            int bkv, bool causal, int out, float c2, float logR, hipStream_t st);
+size_t nv16_expand_bytes(int BH, int Np, int D);
 hipError_t launch_attn_bf16(const void* q, const void* k, const void* vt, void* o, int BH, int N, int Np, int D,
                             bool causal, bool out_f32, float c2, hipStream_t st);
 hipError_t launch_transpose_v_bf16(const void* v, void* vt, int BH, int N, int Np, int D, hipStream_t st);
@@ -94,7 +95,7 @@ size_t kmean_ws_bytes(int B, int H, int N, int D) {
 }
 
 struct AttnWs {
-  size_t qc, qs, kc, ks, vc, vs, mu, part, qbar, bias, total;
+  size_t qc, qs, kc, ks, vc, vs, mu, part, qbar, bias, kv16, total;
 };
 
 AttnWs attn_ws_layout(int B, int H, int N, int D, unsigned fmt) {
@@ -111,6 +112,9 @@ AttnWs attn_ws_layout(int B, int H, int N, int D, unsigned fmt) {
   const size_t nqb = (fmt & SAGE_SMOOTH_Q) ? (size_t)sage::qmean_blocks(N) : 0;
   w.qbar = off; off += up256((size_t)B * H * nqb * D * sizeof(float));
   w.bias = off; off += up256((size_t)B * H * nqb * pad128(N) * sizeof(float));
+  // NV16: the exact f16 expansion of K^ and V^T that the attention kernel reads
+  w.kv16 = off;
+  if (fmt_of(fmt) == SAGE_FMT_NV16_E4M3) off += up256(sage::nv16_expand_bytes(B * H, pad128(N), D));
   w.total = off;
   return w;
 }
@@ -159,14 +163,23 @@ inline float log2_of_6() { return (float)std::log2(6.0); }
 inline float log2_of_2688() { return (float)std::log2(448.0 * 6.0); }
 inline int out_kind(unsigned fmt) { return (fmt & SAGE_OUT_F32) ? 0 : ((fmt & SAGE_IN_BF16) ? 1 : 2); }
 
+// kv16: for NV16, device memory of nv16_expand_bytes() for the f16 expansion of
+// K^ and V^T, or null to take it from hipMallocAsync on st for this call.
 int attn_prequant_impl(const void* qc, const void* qs, const void* kc, const void* ks, const void* vc, const void* vs,
-                       const float* qkb, void* o, int B, int H, int N, int D, int causal, unsigned fmt,
+                       void* kv16, const float* qkb, void* o, int B, int H, int N, int D, int causal, unsigned fmt,
                        hipStream_t st) {
   const int bkv = (fmt & SAGE_BKV64) ? 64 : ((fmt & SAGE_BKV256) ? 256 : 128);
   if (fmt_of(fmt) == SAGE_FMT_NV16_E4M3) {
     if (bkv == 256) return SAGE_ERR_UNSUPPORTED;
-    return hip_status(sage::launch_attn_nv16(qc, qs, kc, ks, vc, vs, qkb, o, B * H, N, pad128(N), D, bkv,
-                                             causal != 0, out_kind(fmt), softmax_c2(D), log2_of_2688(), st));
+    void* own = nullptr;
+    if (!kv16) {
+      if (hipMallocAsync(&own, sage::nv16_expand_bytes(B * H, pad128(N), D), st) != hipSuccess) return SAGE_ERR_HIP;
+      kv16 = own;
+    }
+    int rc = hip_status(sage::launch_attn_nv16(qc, qs, kc, ks, vc, vs, kv16, qkb, o, B * H, N, pad128(N), D, bkv,
+                                               causal != 0, out_kind(fmt), softmax_c2(D), log2_of_2688(), st));
+    if (own && hipFreeAsync(own, st) != hipSuccess && rc == SAGE_OK) rc = SAGE_ERR_HIP;
+    return rc;
   }
   return hip_status(sage::launch_attn_fp4_mx(qc, qs, kc, ks, vc, vs, qkb, o, B * H, N, pad128(N), D, bkv,
                                              causal != 0, out_kind(fmt), softmax_c2(D), log2_of_6(),
@@ -188,8 +201,8 @@ int attn_ws_impl(const void* q, const void* k, const void* v, void* o, int B, in
     rc = hip_status(sage::launch_qk_bias(k, smooth_k ? mu : nullptr, qbar, bias, B * H, N, pad128(N), D,
                                          (fmt & SAGE_IN_BF16) != 0, st));
   if (rc == SAGE_OK)
-    rc = attn_prequant_impl(base + w.qc, base + w.qs, base + w.kc, base + w.ks, base + w.vc, base + w.vs, bias, o, B,
-                            H, N, D, causal, fmt, st);
+    rc = attn_prequant_impl(base + w.qc, base + w.qs, base + w.kc, base + w.ks, base + w.vc, base + w.vs, base + w.kv16,
+                            bias, o, B, H, N, D, causal, fmt, st);
   return rc;
 }
 
@@ -499,8 +512,8 @@ int sage_attn_fp4_fwd_prequant(const void* q_codes, const void* q_scales, const 
   if (fmt & SAGE_SMOOTH_Q) return SAGE_ERR_UNSUPPORTED;   // the GEMV bias is not an input of this entry point
   if ((fmt & SAGE_WG256) && (!(fmt & SAGE_BKV256) || fmt_of(fmt) != SAGE_FMT_MXFP4 || causal))
     return SAGE_ERR_UNSUPPORTED;
-  return attn_prequant_impl(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, nullptr, o, B, H, N, D, causal,
-                            fmt, stream);
+  return attn_prequant_impl(q_codes, q_scales, k_codes, k_scales, vt_codes, vt_scales, nullptr, nullptr, o, B, H, N, D,
+                            causal, fmt, stream);
 }
 
 int sage_attn_bf16_fwd(const void* q, const void* k, const void* v, void* o, int B, int H, int N, int D, int causal,
