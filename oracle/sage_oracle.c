@@ -518,9 +518,14 @@ static double hulp32(double x) {
 /* P~2_k = exp2(fma(S_k, c2, fl32(fl32(log2 R) - fl32(t c2)))), the MX block */
 /* exponent from scores, e = max(ceil(fl32(fl32(bm - t) c2)), -126) with bm  */
 /* the block's largest score, s_P1 = fl32(exp2(fl32(t c2) - fl32(m c2))/R),  */
-/* rowsum = fl32(s_P1 sum P~2).  Equal in exact arithmetic; it exists so     */
-/* that a test can show every difference it makes lies inside the set of     */
-/* results the intervals below accept.                                       */
+/* rowsum = fl32(s_P1 sum P~2).  NV16 takes the block scale s = M 2^X from   */
+/* the fused P~2 values as above, and folds the division by s into the      */
+/* exponent: y_k = exp2(fma(S_k, c2, fl32(B - fl32(log2 M)))), codes         */
+/* E2M1(y_k 2^-X) (exact), the row sum s_P1 sum over blocks of M sum y_k (a  */
+/* block with s = 0 keeps its P~2 values in the row sum and gets zero codes).*/
+/* Equal in exact arithmetic; it exists so that a test can show every       */
+/* difference it makes lies inside the set of results the intervals below   */
+/* accept.                                                                   */
 /*                                                                           */
 /* Acceptance intervals (the paper fixes no fp32 evaluation order).  For     */
 /* each key, [lo, hi] holds every P~2 value that either evaluation can       */
@@ -529,7 +534,10 @@ static double hulp32(double x) {
 /*   W_k = h(log2 R) + h(t c2) + h(B) + h(arg_k) + 2^-22/ln 2,               */
 /* h = half an fp32 ulp of each rounded intermediate (B = fl32(log2 R - t c2),*/
 /* arg_k = fl32(fma(S_k, c2, B))), the last term a 1-ulp exp2 plus its own   */
-/* rounding.  [sb_lo, sb_hi] holds every block scale byte either evaluation  */
+/* rounding.  NV16 adds the roundings of the folded division (log2 M with   */
+/* M <= 15 to within an ulp, B - log2 M, and the fma at that argument), each */
+/* bounded by half an ulp at |B| + 4 or |arg_k| + 4, or an ulp at 4.          */
+/* [sb_lo, sb_hi] holds every block scale byte either evaluation             */
 /* can choose: MX -- the plain exponent and ceil of the score-domain         */
 /* exponent c2 (bm - t) within its two roundings; NV16 -- E4M3 of amax/6 for */
 /* amax anywhere in the block max's interval (and the plain one).  The       */
@@ -569,7 +577,7 @@ int orc_p_tile(const float* S, int bkv, float m_old, int D, int fmt, unsigned fl
       psum += p2[kk];
     }
     volatile float rs = s1 * psum;
-    rowsum = rs;
+    rowsum = rs;                          /* NV16 without DIRECT_P: replaced below */
   } else {
     /* P~ = exp(S - m_new), its row sum and its row max */
     float rho = 0.0f;
@@ -610,7 +618,9 @@ int orc_p_tile(const float* S, int bkv, float m_old, int D, int fmt, unsigned fl
       if (S[kk] == -INFINITY) { lo[kk] = hi[kk] = 0.0; continue; }
       if (direct) { lo[kk] = hi[kk] = p2[kk]; continue; }
       const double pex = (double)R * exp2((double)c2 * ((double)S[kk] - (double)t));
-      const double W = wfix + hulp32(fmaf(S[kk], c2, B));
+      const float arg = fmaf(S[kk], c2, B);
+      double W = wfix + hulp32(arg);
+      if (fmt == ORC_FMT_NV16) W += hulp32(4.0) + hulp32(fabs((double)B) + 4.0) + hulp32(fabs((double)arg) + 4.0);
       double flo = pex * exp2(-W), fhi = pex * exp2(W);
       if (fhi < 0x1p-120) { flo = 0.0; fhi += 0x1p-147; } /* fp32 flushes or rounds to subnormal steps there */
       lo[kk] = flo < p2[kk] ? flo : p2[kk];
@@ -622,6 +632,7 @@ int orc_p_tile(const float* S, int bkv, float m_old, int D, int fmt, unsigned fl
   if (fmt == ORC_FMT_NONE) return 0;
 
   /* second level: (s_P2, P^2) = phi(P~2) over n-key blocks */
+  float fsum_nv = 0.0f;                 /* NV16, fused order: sum over blocks of M sum y */
   for (int b0 = 0; b0 < bkv; b0 += n) {
     const int blk = b0 / n;
     float am = 0.0f, bm = -INFINITY;
@@ -666,6 +677,22 @@ int orc_p_tile(const float* S, int bkv, float m_old, int D, int fmt, unsigned fl
     } else {
       uint8_t sb = orc_phi_block(p2 + b0, n, fmt, codes + b0);
       sbytes[blk] = sb;
+      if (fused && !direct) {
+        /* the division by s = M 2^X folded into the exponent (see above) */
+        const int E = sb >> 3, man = sb & 7;
+        const int M = E ? 8 + man : man, X = E ? E - 10 : -9;
+        const float lgm = M ? (float)log2((double)M) : 0.0f;
+        volatile float Bf = logR - tc;
+        volatile float bb = Bf - lgm;
+        float ys = 0.0f;
+        for (int kk = b0; kk < b0 + n; ++kk) {
+          const float y = (S[kk] == -INFINITY) ? 0.0f : exp2_f32(fmaf(S[kk], c2, bb));
+          ys += y;
+          codes[kk] = M ? orc_e2m1_encode(ldexpf(y, -X)) : 0;
+        }
+        volatile float wsum = (float)(M ? M : 1) * ys;
+        fsum_nv += wsum;
+      }
       if (sb_lo) {
         /* E4M3(fl32(amax/6)) for amax anywhere in the block max's interval;
            the division's own rounding widens it by an ulp */
@@ -678,6 +705,7 @@ int orc_p_tile(const float* S, int bkv, float m_old, int D, int fmt, unsigned fl
       }
     }
   }
+  if (fused && !direct && fmt == ORC_FMT_NV16) { volatile float rs = s1 * fsum_nv; *rowsum_out = rs; }
   return 0;
 }
 

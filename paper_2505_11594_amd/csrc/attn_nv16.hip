@@ -12,8 +12,10 @@
 //     direct-to-LDS loads a tile ahead: no per-workgroup dequantization;
 //   * P~ gets the two-level quantization of Sec. 3.2 with R = 448 * 6 in
 //     registers: the first level as in the MXFP4 kernel, the second level an
-//     E4M3 scale per 16 keys (round to nearest even of blockmax/6), E2M1 codes
-//     of P~2 / s, and the dequantized code * s * 2^k fed to the MFMA in f16.
+//     E4M3 scale s = M * 2^X per 16 keys (round to nearest even of
+//     blockmax/6), E2M1 codes of P~2 / s with the division by M folded into
+//     the exponent and the one by 2^X into the convert, and the dequantized
+//     code * s * 2^k fed to the MFMA in f16.
 //     This is exact unless the tile's max lies more than 9 / c2 below the
 //     running max; then values under 2^-9 of the row's largest round into
 //     f16's subnormal range (an absolute error below 2^-25 there), and a
@@ -105,9 +107,10 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   constexpr int NDB = D / 32;
   constexpr int BIAS_OFF = T::BYTES, LBYTES = T::BYTES + (SQ ? BKV * 4 : 0);   // bias of the tile's keys
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][LBYTES];
-  // per E4M3 code b (s = M * 2^X) of P's second level: rtab = fl32(1 / s) (0 for
-  // s = 0), ptab = 2^X, mtab = {M, M} in f16
-  __shared__ float rtab[128], ptab[128];
+  // per E4M3 code b (s = M * 2^X) of P's second level: ptab = 2^X, mtab = {M, M}
+  // in f16, wtab = M and lgtab = fl32(log2 M) (1 and 0 for s = 0, whose codes
+  // are multiplied by M = 0 and whose values still enter the row sum)
+  __shared__ float ptab[128], wtab[128], lgtab[128];
   __shared__ uint32_t mtab[128];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31, hi = lane >> 5;
@@ -155,7 +158,9 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
 
   if (tid < 128) {
     const int E = tid >> 3, man = tid & 7;
-    rtab[tid] = tid == 0 ? 0.0f : 1.0f / e4m3_decode_hw<0>((uint32_t)tid);
+    const int Mi = E ? 8 + man : man;
+    wtab[tid] = (float)(Mi ? Mi : 1);
+    lgtab[tid] = (float)log2((double)(Mi ? Mi : 1));
     ptab[tid] = __builtin_ldexpf(1.0f, E ? E - 10 : -9);
     const _Float16 M = (_Float16)(E ? 8 + man : man);
     mtab[tid] = __builtin_bit_cast(uint32_t, v2h{M, M});
@@ -266,30 +271,34 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
       v4i pk[NPK];
 #pragma unroll
       for (int t = 0; t < NSUB; ++t) {
-        // second level: E4M3 scale of this lane's 16-key block
+        // second level: E4M3 scale s = M 2^X of this lane's 16-key block, from its largest P~2
         const float amax = (bm[t] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(__builtin_fmaf(bm[t], c2, bias));
         const uint32_t sb = e4m3_encode_hw(div6(amax));
-        const float r = rtab[sb];
+        // the division by s folded into the exponent: y = 2^{fma(S, c2, B - log2 M)} = P~2 / M,
+        // codes E2M1(y 2^-X) (the convert divides by the power of two exactly), row sum M sum y
+        const float bb = bias - lgtab[sb];
+        const float x2 = ptab[sb];
         // k_j folded into the power of two of the dequantized P; below 2^-31 the block is dropped
         const float x2k = __builtin_ldexpf(ptab[sb], kfold < -31 ? -31 : kfold);
         const v2h m2 = kfold < -31 ? v2h{(_Float16)0.0f, (_Float16)0.0f} : __builtin_bit_cast(v2h, mtab[sb]);
+        float bs[2] = {0.0f, 0.0f};
 #pragma unroll
         for (int w = 0; w < 2; ++w) {
           uint32_t pw[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int v = 8 * w + 2 * i;
-            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v], c2, bias));
-            const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v + 1], c2, bias));
-            ps[i & 1] += p0;
-            ps[i & 1] += p1;
+            const float y0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v], c2, bb));
+            const float y1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[t][v + 1], c2, bb));
+            bs[i & 1] += y0;
+            bs[i & 1] += y1;
             // byte 0 gets the two codes; the other bytes are never read
-            const float y0 = p0 * r;
-            const uint32_t code = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(__float_as_uint(y0), y0, p1 * r, 1.0f, 0);
+            const uint32_t code = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(__float_as_uint(y0), y0, y1, x2, 0);
             pw[i] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(code, x2k, 0) * m2);
           }
           pk[2 * t + w] = v4i{(int)pw[0], (int)pw[1], (int)pw[2], (int)pw[3]};
         }
+        ps[t & 1] = __builtin_fmaf(bs[0] + bs[1], wtab[sb], ps[t & 1]);
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db)

@@ -272,9 +272,12 @@ def test_fused_p_step_lies_inside_the_accepted_set(fmt):
     the MX exponent from scores) differs from Algorithm 1's order only inside
     the sets orc_p_tile accepts: on 3000 random tiles (varied score scales up
     to the outlier workload's, running max above the tile or not, masked
-    keys, 64/128/256 keys) every fused P~2 value lies in its key's [lo, hi]
-    and every fused block scale byte in [sb_lo, sb_hi].  The counts of codes
-    and scales that actually differ are reported."""
+    keys, 64/128/256 keys) every fused P~2 value lies in its key's [lo, hi],
+    every fused block scale byte in [sb_lo, sb_hi], and every fused code is
+    the code of some value in [lo, hi] at the fused scale (for NV16, whose
+    fused order folds the division by the block scale into the exponent, this
+    is the check that matters).  The counts of codes and scales that actually
+    differ are reported."""
     rng = np.random.default_rng(51)
     n = oracle.block_size(fmt)
     R = 6.0 if fmt == oracle.FMT_MX else 2688.0
@@ -296,6 +299,18 @@ def test_fused_p_step_lies_inside_the_accepted_set(fmt):
         assert np.all(a["sb_lo"] <= f["sbytes"]) and np.all(f["sbytes"] <= a["sb_hi"])
         for b in range(bkv // n):
             blk = slice(b * n, b * n + n)
+            # every fused code is one that a value in its key's interval reaches at the
+            # fused block scale (NV16 folds the division by that scale into the exponent)
+            sc = oracle.e8m0_decode(int(f["sbytes"][b])) if fmt == oracle.FMT_MX else \
+                oracle.e4m3_decode(int(f["sbytes"][b]))
+            for kk in range(b * n, b * n + n):
+                c = int(f["codes"][kk])
+                if sc == 0.0:
+                    assert c == 0
+                    continue
+                clo = oracle.e2m1_encode(float(a["lo"][kk] * (1 - 2.0 ** -21) / sc))
+                chi = oracle.e2m1_encode(float(a["hi"][kk] * (1 + 2.0 ** -21) / sc))
+                assert clo <= c <= chi, (trial, kk, clo, c, chi)
             am = float(a["p2"][blk].max())
             if f["sbytes"][b] != a["sbytes"][b]:
                 if a["s1"] == 0.0 or am < R * 2.0 ** -100:
