@@ -168,7 +168,8 @@ int sage_attn_fp4_fwd_ws(const void* q, const void* k, const void* v, void* o,
  * Its workspace is a fixed scratch of SAGE_NOALLOC_SCRATCH_BYTES inside the
  * library, one per GPU, held until the process ends; shapes whose
  * sage_attn_fp4_workspace_size() exceeds it return SAGE_ERR_WORKSPACE before
- * any HIP call (256 MiB holds B = 1, H = 32, N = 32768, D = 128).
+ * any HIP call (256 MiB holds B = 1, H = 32, N = 32768, D = 128 in MXFP4;
+ * NV16 also needs the f16 expansion of K^ and V^T, 4*B*H*Np*D bytes).
  * `stream` must belong to the current device (else SAGE_ERR_INVALID_ARG).
  * All calls on one GPU share its scratch: calls that overlap on one GPU
  * (other streams, other host threads) race and must be serialized by the
