@@ -443,20 +443,20 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp4_mx256_kernel(
   if (qi < N) {
     const uint8_t* qrow = qc + ((size_t)bh * N + qi) * (D / 2);
 #pragma unroll
-    for (int s = 0; s < NKS; ++s) qreg[s] = *reinterpret_cast<const v4i*>(qrow + (2 * s + hi) * 16);
+    for (int s = 0; s < NKS; ++s) qreg[s] = *reinterpret_cast<const v4i*>(qrow + (s + NKS * hi) * 16);
     const uint8_t* srow = qs + ((size_t)bh * N + qi) * (D / 32);
     qsc = (D == 128) ? *reinterpret_cast<const uint32_t*>(srow) : (uint32_t)*reinterpret_cast<const uint16_t*>(srow);
   } else {
 #pragma unroll
     for (int s = 0; s < NKS; ++s) qreg[s] = v4i{0, 0, 0, 0};
   }
-  qsc >>= 8 * hi;
+  qsc >>= 8 * NKS * hi;
 
   int ntiles = (N + BKV - 1) / BKV;
   if (CAUSAL) ntiles = min(ntiles, min(q0 + AQW - 1, N - 1) / BKV + 1);
 
   // Load jobs: wave w loads K^ operand blocks b = w + 4i (key row 32t + col,
-  // bytes [32s + 16hi, +16) with t = b / NKS, s = b % NKS), V^T operand blocks
+  // bytes [16s + 16 NKS hi, +16) with t = b / NKS, s = b % NKS), V^T operand blocks
   // b = w + 4i (dim row 32i + col, bytes [32w + 16hi, +16) of the tile, since
   // NG = 4) and scale dword jobs jb = w + 4i: K^ scale dwords 64jb + lane,
   // then V^T scale dwords 64(jb - NKSJ) + lane (dim row d / 2, half d & 1).
@@ -464,7 +464,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp4_mx256_kernel(
   // -- plus one of five fixed lane offsets, so a load costs no VALU.
   static_assert(W % NKS == 0 && NG == 4 && W % NG == 0, "job layout");
   constexpr int KJ = T::NKB / W, VJ = T::NVB / W, NSJ = T::NKSJ + T::NVSJ, SJ = (NSJ + W - 1) / W;
-  const uint32_t ko0 = (uint32_t)((32 * (wave / NKS) + col) * (D / 2) + 32 * (wave % NKS) + 16 * hi);
+  const uint32_t ko0 = (uint32_t)((32 * (wave / NKS) + col) * (D / 2) + 16 * (wave % NKS) + 16 * NKS * hi);
   const uint32_t vo0 = (uint32_t)((32 * (wave / NG) + col) * (Np / 2) + 32 * (wave % NG) + 16 * hi);
   const uint32_t kso = (uint32_t)(4 * lane);
   const uint32_t vso = (uint32_t)((lane >> 1) * (Np / 32) + 4 * (lane & 1));
@@ -524,19 +524,23 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp4_mx256_kernel(
     const int kb = j * BKV;
     if (CAUSAL && kb > qw + 31) continue;                  // the whole tile is above this wave's diagonal
 
-    // S^T = K^ . Q^T for the tile
+    // S^T = K^ . Q^T for the tile.  K-step s takes channel block s + NKS hi in
+    // lane half hi (blocks s and s + NKS), so each lane's K and Q scale bytes
+    // for the NKS steps are one 16-bit half of the row's scale word, selected by
+    // op_sel s.  S is exact, so the grouping of blocks into steps does not
+    // change it.
     v16f sacc[NSUB];
 #pragma unroll
     for (int t = 0; t < NSUB; ++t) {
       uint32_t ksc;
-      if constexpr (D == 128) ksc = *reinterpret_cast<const uint32_t*>(L + T::KS_OFF + (32 * t + col) * 4) >> (8 * hi);
+      if constexpr (D == 128) ksc = *reinterpret_cast<const uint16_t*>(L + T::KS_OFF + (32 * t + col) * 4 + 2 * hi);
       else ksc = L[T::KS_OFF + (32 * t + col) * 2 + hi];
       v16f acc = v16f{};
       static_for<NKS>([&](auto S_) {
         constexpr int s = decltype(S_)::value;
         const v4i a = *reinterpret_cast<const v4i*>(L + T::KC_OFF + (t * NKS + s) * 1024 + lane * 16);
-        acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(qreg[s]), acc, 4, 4, 2 * s, (int)ksc,
-                                                              2 * s, (int)qsc);
+        acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(as_op(a), as_op(qreg[s]), acc, 4, 4, s, (int)ksc, s,
+                                                              (int)qsc);
       });
       sacc[t] = acc;
     }
@@ -587,6 +591,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp4_mx256_kernel(
     const float f = delta - kf;
     const float gam = __builtin_amdgcn_exp2f((mc_old - mc) + (f_old - f));
     const int kfold = (int)__builtin_fmaxf(kf, -300.0f);
+    const int kf127 = kfold + 127;                         // P's scale byte is e + kfold + 127, clamped at 0
     const float bias = log6 - tc;
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
@@ -626,7 +631,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp4_mx256_kernel(
         }
       }
       const v4i pw = v4i{(int)w[0], (int)w[1], (int)w[2], (int)w[3]};
-      const int sb = e + kfold + 127;
+      const int sb = e + kf127;
       const int psb = sb < 0 ? 0 : sb;
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
