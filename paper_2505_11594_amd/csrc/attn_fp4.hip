@@ -47,13 +47,19 @@ __device__ __forceinline__ void lds_load4(const void* src, void* dst) {
 }
 __device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
 
-// A workgroup-uniform address, pinned to scalar registers, so that base +
-// 32-bit lane offset selects the scalar-base form of a global load.
-__device__ __forceinline__ const uint8_t* sbase(const void* p) {
-  const uint64_t v = reinterpret_cast<uint64_t>(p);
-  const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
-  const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
-  return reinterpret_cast<const uint8_t*>((hi << 32) | lo);
+// A raw buffer resource over `bytes` bytes at `base` (reads past the end return
+// zero), and direct-to-LDS buffer loads from it: lane l's bytes land at
+// dst + size * l; the byte address is base + voff (per lane) + soff (uniform).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+}
+__device__ __forceinline__ void buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, void* dst) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16, voff,
+                                           (uint32_t)__builtin_amdgcn_readfirstlane((int)soff), 0, 0);
+}
+__device__ __forceinline__ void buf_load4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, void* dst) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 4, voff,
+                                           (uint32_t)__builtin_amdgcn_readfirstlane((int)soff), 0, 0);
 }
 
 // One LDS stage of a KV tile, in MFMA-operand order (plus, with smoothing Q,
@@ -135,7 +141,9 @@ __global__ __launch_bounds__(256, 2) void attn_fp4_mx_kernel(
   // w, w + 4, ... (b = (db, g) = (b / NG, b % NG): dim row 32db + col, bytes
   // [32g + 16hi, +16) of the tile) and scale job w: K^ scale dwords c = w for
   // w < NKSJ (64 per job), then V^T scale dwords (one per dim row).  Each
-  // load is a wave-uniform tile base plus a fixed 32-bit lane offset.
+  // load is a wave-uniform tile base plus a fixed 32-bit lane offset.  (The
+  // buffer-resource form of the 256-key kernel made this kernel 4% slower at
+  // D = 64, so it keeps global loads.)
   constexpr int KJ = (T::NKB + 3) / 4, VJ = (T::NVB + 3) / 4;
   static_assert(T::NKSJ + T::NVSJ <= 4, "one scale job per wave");
   const uint8_t* kbase = kc + (size_t)bh * Np * (D / 2);
@@ -460,8 +468,9 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp4_mx256_kernel(
   // b = w + 4i (dim row 32i + col, bytes [32w + 16hi, +16) of the tile, since
   // NG = 4) and scale dword jobs jb = w + 4i: K^ scale dwords 64jb + lane,
   // then V^T scale dwords 64(jb - NKSJ) + lane (dim row d / 2, half d & 1).
-  // Each address is a uniform base -- head, tile, job and the tail redirect
-  // -- plus one of five fixed lane offsets, so a load costs no VALU.
+  // Each load is a buffer resource over the head's tensor, a uniform offset --
+  // tile, job and the tail redirect -- and one of five fixed lane offsets, so
+  // a load costs no VALU and no 64-bit address arithmetic.
   static_assert(W % NKS == 0 && NG == 4 && W % NG == 0, "job layout");
   constexpr int KJ = T::NKB / W, VJ = T::NVB / W, NSJ = T::NKSJ + T::NVSJ, SJ = (NSJ + W - 1) / W;
   const uint32_t ko0 = (uint32_t)((32 * (wave / NKS) + col) * (D / 2) + 16 * (wave % NKS) + 16 * NKS * hi);
@@ -474,34 +483,34 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp4_mx256_kernel(
   const uint8_t* ksbase = ks + (size_t)bh * Np * (D / 32);
   const uint8_t* vsbase = vs + (size_t)bh * D * (Np / 32);
   const float* brow = SQ ? qkb + ((size_t)bh * nqt + qt) * Np : nullptr;
+  // buffer resources over this head's K^, V^T codes and scales: every load is
+  // the resource, a uniform byte offset and one fixed lane offset
+  const __amdgpu_buffer_rsrc_t rk = make_rsrc(kbase, Np * (D / 2)), rv = make_rsrc(vbase, D * (Np / 2));
+  const __amdgpu_buffer_rsrc_t rks = make_rsrc(ksbase, Np * (D / 32)), rvs = make_rsrc(vsbase, D * (Np / 32));
   auto issue = [&](int j, int stage) {
     const int kb = j * BKV;
     const bool short_tail = kb + BKV > Np;                 // keys [kb + 128, kb + 256) lie past Np
-    const uint8_t* kt = kbase + (size_t)kb * (D / 2);
-    const uint8_t* vt = vbase + kb / 2;
-    const uint8_t* kst = ksbase + (size_t)kb * (D / 32);
-    const uint8_t* vst = vsbase + kb / 32;
     uint8_t* L = lds[stage];
 #pragma unroll
     for (int i = 0; i < KJ; ++i) {
       const int b = wave + W * i, t = b / NKS;
-      const long long back = (short_tail && t >= NSUB / 2) ? 128LL * (D / 2) : 0;
-      lds_load16(sbase(kt + ((long long)i * (32 * W / NKS) * (D / 2) - back)) + ko0, L + T::KC_OFF + b * 1024);
+      const uint32_t back = (short_tail && t >= NSUB / 2) ? 128u * (D / 2) : 0u;
+      buf_load16(rk, ko0, (uint32_t)kb * (D / 2) + (uint32_t)i * (32 * W / NKS) * (D / 2) - back, L + T::KC_OFF + b * 1024);
     }
 #pragma unroll
     for (int i = 0; i < VJ; ++i) {
-      const long long back = (short_tail && (wave % NG) >= NG / 2) ? 64 : 0;
-      lds_load16(sbase(vt + ((long long)i * 8 * W * (Np / 2) - back)) + vo0, L + T::VC_OFF + (wave + W * i) * 1024);
+      const uint32_t back = (short_tail && (wave % NG) >= NG / 2) ? 64u : 0u;
+      buf_load16(rv, vo0, (uint32_t)kb / 2 + (uint32_t)i * 8 * W * (Np / 2) - back, L + T::VC_OFF + (wave + W * i) * 1024);
     }
 #pragma unroll
     for (int i = 0; i < SJ; ++i) {
       const int jb = wave + W * i;
       if (jb < T::NKSJ) {
-        const long long back = (short_tail && 64 * jb * 4 >= T::KS_BYTES / 2) ? T::KS_BYTES / 2 : 0;
-        lds_load4(sbase(kst + (256LL * jb - back)) + kso, L + T::KS_OFF + jb * 256);
+        const uint32_t back = (short_tail && 64 * jb * 4 >= T::KS_BYTES / 2) ? T::KS_BYTES / 2 : 0u;
+        buf_load4(rks, kso, (uint32_t)kb * (D / 32) + 256u * jb - back, L + T::KS_OFF + jb * 256);
       } else if (jb < NSJ) {
-        lds_load4(sbase(vst + (long long)(jb - T::NKSJ) * Np) + (vso - (short_tail ? vso_hi : 0u)),
-                  L + T::VS_OFF + (jb - T::NKSJ) * 256);
+        buf_load4(rvs, vso - (short_tail ? vso_hi : 0u), (uint32_t)kb / 32 + (uint32_t)(jb - T::NKSJ) * Np,
+              L + T::VS_OFF + (jb - T::NKSJ) * 256);
       }
     }
     if constexpr (SQ) {
