@@ -60,8 +60,9 @@ def kernel_source_sha() -> str:
 
 
 def traffic_from_counters(variant: str = "default"):
-    """HBM bytes per launch of the bench kernel ("default": 128-query
-    workgroups, "wg256": 256-query workgroups) from committed rocprofv3
+    """HBM bytes per launch of the 256-key attention kernel on the bench
+    workload ("default": 128-query workgroups, the library's shape without
+    SAGE_WG256; "wg256": 256-query workgroups) from committed rocprofv3
     FETCH_SIZE/WRITE_SIZE runs scaled by the copy-kernel calibration, or None
     when the kernel source changed since they were taken."""
     if not os.path.exists(COUNTERS):
@@ -211,7 +212,7 @@ def issue_rates(torch):
                       "cycles_per_iteration": res, "split": split, "derived": summary}), flush=True)
 
 
-def issue_ceilings(torch, kernel_ms: float):
+def issue_ceilings(torch, kernel_ms: float, variant: str = "default"):
     """Ceilings of the 256-key FP4 kernel on the bench workload from instruction
     issue: the issue rates measured live (register-only loops, 2 waves per SIMD
     as in the kernel) times the kernel's instructions per tile-wave (one wave x
@@ -224,9 +225,9 @@ def issue_ceilings(torch, kernel_ms: float):
     if not os.path.exists(COUNTERS):
         return None
     c = json.load(open(COUNTERS))
-    if c.get("source_sha") != kernel_source_sha() or "sq_per_tile_wave" not in c.get("default", {}):
+    if c.get("source_sha") != kernel_source_sha() or "sq_per_tile_wave" not in c.get(variant, {}):
         return None
-    sq = c["default"]["sq_per_tile_wave"]
+    sq = c[variant]["sq_per_tile_wave"]
     n_mfma, n_exp, n_pack = sq["SQ_INSTS_MFMA"], sq["SQ_INSTS_VALU_TRANS_F32"], c["fp4_packs_per_tile_wave"]
     n_valu = sq["SQ_INSTS_VALU"] - n_mfma - n_exp - n_pack     # SQ_INSTS_VALU counts MFMA and transcendentals too
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2505_11594_amd", "libsage_rates.so"))
@@ -470,13 +471,17 @@ def main():
     to_dev = lambda a: torch.from_numpy(a.view(np.int16)).view(dt).to(dev)
     qd, kd, vd = to_dev(q), to_dev(k), to_dev(v)
     tile = bd.bkv_flag(w.bkv)
-    fmt = bd.SAGE_FMT_MXFP4 | tile | (bd.SAGE_IN_BF16 if w.in_dtype == wl.IN_BF16 else 0) | bd.SAGE_OUT_F32
+    # 256-query workgroups where the kernel has them (256-key tiles, non-causal, no smoothing Q): each K^/V^T
+    # tile in LDS then serves 8 waves, which halves the HBM fetches at the same or slightly lower time
+    wg = w.bkv == 256 and not w.causal
+    shape = tile | (bd.SAGE_WG256 if wg else 0)
+    fmt = bd.SAGE_FMT_MXFP4 | shape | (bd.SAGE_IN_BF16 if w.in_dtype == wl.IN_BF16 else 0) | bd.SAGE_OUT_F32
     ws = torch.empty(bd.attn_fp4_workspace_size(B, H, N, D, fmt), dtype=torch.uint8, device=dev)
     o = torch.empty((B, H, N, D), dtype=torch.float32, device=dev)
     ops = w.ops
 
     def step():
-        bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=bd.SAGE_FMT_MXFP4 | tile, out_f32=True, out=o,
+        bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=bd.SAGE_FMT_MXFP4 | shape, out_f32=True, out=o,
                              workspace=ws)
 
     if args.mode == "attn_int8":
@@ -533,7 +538,7 @@ def main():
     vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V)
 
     def attn_only():
-        bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, fmt=tile, out=o)
+        bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, fmt=shape, out=o)
 
     for _ in range(2):
         attn_only()
@@ -559,11 +564,11 @@ def main():
     n_el = B * H * N * D
     quant_bytes = n_el * (2 + 2 + 2 + 2) + 3 * n_el * (0.5 + 1.0 / 32)   # K read twice (mean + quantize)
 
-    # the same kernel with 256-query workgroups (SAGE_WG256): half the K^/V^T fetches, same bits
-    wg256 = None
-    if w.bkv == 256 and not w.causal:
+    # the same kernel with 128-query workgroups (the shape without SAGE_WG256): same bits, twice the fetches
+    wg128 = None
+    if wg:
         run_wg = lambda: bd.sage_attn_fp4_fwd_prequant(qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal,
-                                                       fmt=tile | bd.SAGE_WG256, out=o)
+                                                       fmt=tile, out=o)
         warm(torch, run_wg)
         e0.record()
         for _ in range(args.steps):
@@ -571,10 +576,10 @@ def main():
         e1.record()
         torch.cuda.synchronize()
         t_wg = e0.elapsed_time(e1) / 1e3 / args.steps
-        wg256 = {"kernel": "attn_fp4_mx256_kernel<%d,false,0,false,8>" % D, "kernel_ms": t_wg * 1e3,
+        wg128 = {"kernel": "attn_fp4_mx256_kernel<%d,false,0,false,4>" % D, "kernel_ms": t_wg * 1e3,
                  "tops": ops / t_wg / 1e12, "frac_of_mxfp4_peak": ops / t_wg / 1e12 / PEAK_FP4_TFLOPS,
-                 "traffic": traffic_from_counters("wg256")}
-        log("attention kernel, 256-query workgroups %.3f ms = %.1f TFLOP/s" % (t_wg * 1e3, ops / t_wg / 1e12))
+                 "traffic": traffic_from_counters("default")}
+        log("attention kernel, 128-query workgroups %.3f ms = %.1f TFLOP/s" % (t_wg * 1e3, ops / t_wg / 1e12))
 
     bf16 = None
     if not args.no_bf16:
@@ -622,7 +627,7 @@ def main():
 
     ceilings = None
     if w.bkv == 256 and D == 128:
-        ceilings = issue_ceilings(torch, t_attn * 1e3)
+        ceilings = issue_ceilings(torch, t_attn * 1e3, "wg256" if wg else "default")
         if ceilings:
             log("issue ceilings (fraction of the MXFP4 peak): " +
                 ", ".join("%s %.3f" % kv for kv in ceilings["frac_of_peak"].items()))
@@ -647,17 +652,20 @@ def main():
         "data": "synthetic (seeded normal Q/K/V, 1% of Q and K rows x20)",
         "config": {"workload": w.name, "B": B, "H": H, "N": N, "D": D, "causal": w.causal,
                    "format": "MXFP4 (E2M1, 1x32 blocks, E8M0 scales)", "kv_tile": w.bkv, "parallelism": "none",
-                   "step": "kmean + quantize Q/K/V + FP4 attention (sage_attn_fp4_fwd_ws)"},
+                   "step": "kmean + quantize Q/K/V + FP4 attention (sage_attn_fp4_fwd_ws)",
+                   "query_workgroup": 256 if wg else 128},
         "roofline": {"bound": "mfma", "achieved": attn_tflops, "peak": PEAK_FP4_TFLOPS, "unit": "TFLOP/s",
-                     "frac": attn_tflops / PEAK_FP4_TFLOPS, "traffic": traffic_from_counters("default"),
-                     "kernel": ("attn_fp4_mx256_kernel<128,false,0,false,4>" if w.bkv == 256 else
-                                "attn_fp4_mx_kernel<%d,%d,false,0,false>" % (D, w.bkv)), "kernel_ms": t_attn * 1e3,
+                     "frac": attn_tflops / PEAK_FP4_TFLOPS,
+                     "traffic": traffic_from_counters("wg256" if wg else "default") if w.bkv == 256 else None,
+                     "kernel": ("attn_fp4_mx256_kernel<%d,false,0,false,%d>" % (D, 8 if wg else 4) if w.bkv == 256
+                                else "attn_fp4_mx_kernel<%d,%d,false,0,false>" % (D, w.bkv)),
+                     "kernel_ms": t_attn * 1e3,
                      "issue_ceilings": ceilings},
         "accuracy_vs_exact": acc,
         "quantize": {"ms": t_quant * 1e3, "algorithmic_GBs": quant_bytes / t_quant / 1e9,
                      "frac_of_hbm_peak": quant_bytes / t_quant / 1e9 / PEAK_HBM_GBS},
         "bf16_kernel": bf16,
-        "attn_wg256": wg256,
+        "attn_wg128": wg128,
         "smooth_q_step": smooth_q,
         "int8_fwd": int8,
         "int8_bwd": int8_bwd,

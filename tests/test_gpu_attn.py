@@ -139,21 +139,28 @@ def test_attn_config1_all_rows(b):
         say("accuracy vs exact (every 64th row)", oracle.metrics(ex, got[:: 64]), cnt)
 
 
-@pytest.mark.parametrize("ci,fmt,bkv,whole", [(2, 0, None, True), (2, 0, 128, False), (3, 0, None, True),
-                                              (3, 0, 128, False), (4, 1, None, True), (4, 0, None, True),
-                                              (4, 0, 256, False)])
-def test_attn_configs_full_size_sampled_rows(ci, fmt, bkv, whole):
+WG = bd.SAGE_WG256
+
+
+@pytest.mark.parametrize("ci,fmt,bkv,whole,shape", [(2, 0, None, True, WG), (2, 0, None, False, 0),
+                                                    (2, 0, 128, False, 0), (3, 0, None, True, 0),
+                                                    (3, 0, 128, False, 0), (4, 1, None, True, 0),
+                                                    (4, 0, None, True, 0), (4, 0, 256, False, 0)])
+def test_attn_configs_full_size_sampled_rows(ci, fmt, bkv, whole, shape):
     """The benchmark's launch configuration at full size (each workload's own
-    KV tile, plus the other tile on the long, causal and D = 64 workloads).
-    With whole=True the oracle computes 8 whole 128-row query tiles on each
-    of 8 heads (first and last tile always, the tile ending on a KV-tile
-    boundary when causal, the rest seeded); otherwise 8 rows of 4 tiles."""
+    KV tile, plus the other tile on the long, causal and D = 64 workloads;
+    on the B1 H32 N32768 D128 workload 256-query workgroups as the bench step
+    launches them, and the 128-query shape on sampled rows).  With whole=True
+    the oracle computes 8 whole 128-row query tiles on each of 8 heads (first
+    and last tile always, the tile ending on a KV-tile boundary when causal,
+    the rest seeded); otherwise 8 rows of 4 tiles."""
     w = wl.CONFIGS[ci]
     assert fmt in w.fmts
     bkv = bkv or w.bkv
-    say("attn config", ci, w.name, "fmt", fmt, "bkv", bkv, "whole tiles" if whole else "sampled rows")
+    say("attn config", ci, w.name, "fmt", fmt, "bkv", bkv, "whole tiles" if whole else "sampled rows",
+        "256-query workgroups" if shape else "")
     q, k, v = generate_cached(ci)
-    o = gpu_attn(q, k, v, w.in_dtype, w.causal, fmt, bkv)
+    o = gpu_attn(q, k, v, w.in_dtype, w.causal, fmt | shape, bkv)
     BH = w.B * w.H
     rng = np.random.default_rng(ci)
     heads = sorted({0, BH - 1} | set(rng.choice(np.arange(1, BH - 1), min(BH - 2, 6), replace=False).tolist()))
