@@ -107,11 +107,11 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   constexpr int NDB = D / 32;
   constexpr int BIAS_OFF = T::BYTES, LBYTES = T::BYTES + (SQ ? BKV * 4 : 0);   // bias of the tile's keys
   __shared__ __attribute__((aligned(16))) uint8_t lds[2][LBYTES];
-  // per E4M3 code b (s = M * 2^X) of P's second level: ptab = 2^X, mtab = {M, M}
-  // in f16, wtab = M and lgtab = fl32(log2 M) (1 and 0 for s = 0, whose codes
-  // are multiplied by M = 0 and whose values still enter the row sum)
-  __shared__ float ptab[128], wtab[128], lgtab[128];
-  __shared__ uint32_t mtab[128];
+  // per E4M3 code b (s = M * 2^X) of P's second level, one 16-byte record (one
+  // LDS read): {2^X, M, fl32(log2 M), {M, M} in f16} -- M = 1 and log2 M = 0
+  // for s = 0, whose codes are multiplied by the f16 M = 0 and whose values
+  // still enter the row sum
+  __shared__ float4 stab[128];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int col = lane & 31, hi = lane >> 5;
 
@@ -159,11 +159,9 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
   if (tid < 128) {
     const int E = tid >> 3, man = tid & 7;
     const int Mi = E ? 8 + man : man;
-    wtab[tid] = (float)(Mi ? Mi : 1);
-    lgtab[tid] = (float)log2((double)(Mi ? Mi : 1));
-    ptab[tid] = __builtin_ldexpf(1.0f, E ? E - 10 : -9);
     const _Float16 M = (_Float16)(E ? 8 + man : man);
-    mtab[tid] = __builtin_bit_cast(uint32_t, v2h{M, M});
+    stab[tid] = make_float4(__builtin_ldexpf(1.0f, E ? E - 10 : -9), (float)(Mi ? Mi : 1),
+                            (float)log2((double)(Mi ? Mi : 1)), __builtin_bit_cast(float, v2h{M, M}));
   }
   __syncthreads();
   // Tile loads, direct to LDS in the swizzled f16 layout.  Job J of a tile
@@ -267,20 +265,26 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
       const float gam = __builtin_amdgcn_exp2f((mc_old - mc) + (f_old - f));
       const int kfold = (int)__builtin_fmaxf(kf, -300.0f);
       const float bias = logR - tc;                    // P~2 = 2^{fma(S, c2, log2 R - t c2)}, R = 448 * 6
+      // k_j folded into the power of two of the dequantized P; below 2^-31 the
+      // tile's blocks are dropped (their f16 M becomes 0)
+      const int kfl = kfold < -31 ? -31 : kfold;
+      const uint32_t mkeep = kfold < -31 ? 0u : 0xFFFFFFFFu;
       float ps[2] = {0.0f, 0.0f};
       v4i pk[NPK];
 #pragma unroll
       for (int t = 0; t < NSUB; ++t) {
         // second level: E4M3 scale s = M 2^X of this lane's 16-key block, from its largest P~2
-        const float amax = (bm[t] == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f(__builtin_fmaf(bm[t], c2, bias));
+        // tmax and so bias are finite (every row of a tile that is computed has
+        // a key of it that is not masked), so a masked block's bm = -inf gives 0
+        const float amax = __builtin_amdgcn_exp2f(__builtin_fmaf(bm[t], c2, bias));
         const uint32_t sb = e4m3_encode_hw(div6(amax));
+        const float4 rec = stab[sb];
         // the division by s folded into the exponent: y = 2^{fma(S, c2, B - log2 M)} = P~2 / M,
         // codes E2M1(y 2^-X) (the convert divides by the power of two exactly), row sum M sum y
-        const float bb = bias - lgtab[sb];
-        const float x2 = ptab[sb];
-        // k_j folded into the power of two of the dequantized P; below 2^-31 the block is dropped
-        const float x2k = __builtin_ldexpf(ptab[sb], kfold < -31 ? -31 : kfold);
-        const v2h m2 = kfold < -31 ? v2h{(_Float16)0.0f, (_Float16)0.0f} : __builtin_bit_cast(v2h, mtab[sb]);
+        const float bb = bias - rec.z;
+        const float x2 = rec.x;
+        const float x2k = __builtin_ldexpf(rec.x, kfl);
+        const v2h m2 = __builtin_bit_cast(v2h, __builtin_bit_cast(uint32_t, rec.w) & mkeep);
         float bs[2] = {0.0f, 0.0f};
 #pragma unroll
         for (int w = 0; w < 2; ++w) {
@@ -298,7 +302,7 @@ __global__ __launch_bounds__(256, 2) void attn_nv16_kernel(
           }
           pk[2 * t + w] = v4i{(int)pw[0], (int)pw[1], (int)pw[2], (int)pw[3]};
         }
-        ps[t & 1] = __builtin_fmaf(bs[0] + bs[1], wtab[sb], ps[t & 1]);
+        ps[t & 1] = __builtin_fmaf(bs[0] + bs[1], rec.y, ps[t & 1]);
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db)

@@ -87,9 +87,10 @@ __device__ __forceinline__ float e4m3_decode(uint32_t b) {
 // E4M3, nearest even) equals e4m3_encode on [0, 448] -- every rounding
 // midpoint and the subnormal range included -- and v_cvt_f32_fp8 equals
 // e4m3_decode on every code; values >= 448 are clamped first, as e4m3_encode
-// saturates.  Byte `sel` of `word` is decoded.
+// saturates.  Byte `sel` of `word` is decoded.  The encoder converts the pair
+// (s, +0) into the low half of a zero word, so bytes 1..3 of its result are 0.
 __device__ __forceinline__ uint32_t e4m3_encode_hw(float s) {
-  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(__builtin_fminf(s, 448.0f), 0.0f, 0, false) & 0xFFu;
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(__builtin_fminf(s, 448.0f), 0.0f, 0, false);
 }
 template <int SEL>
 __device__ __forceinline__ float e4m3_decode_hw(uint32_t word) { return __builtin_amdgcn_cvt_f32_fp8((int)word, SEL); }
