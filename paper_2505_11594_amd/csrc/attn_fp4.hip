@@ -422,7 +422,7 @@ struct Fp4Stage256 {
 // queries, so a tile is fetched from L2 once per 256 queries instead of per
 // 128: about half the fetch traffic.  The two waves on a SIMD then belong to
 // one workgroup and meet at the same barrier, so they overlap less; with the
-// tile loads as buffer loads the time is the same as with W = 4.
+// tile loads as buffer loads the time stays within 2% of W = 4.
 template <int D, bool CAUSAL, int OUT, bool SQ, int W>
 __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp4_mx256_kernel(
     const uint8_t* __restrict__ qc, const uint8_t* __restrict__ qs, const uint8_t* __restrict__ kc,

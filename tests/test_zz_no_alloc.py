@@ -50,3 +50,21 @@ def test_noalloc_matches_the_allocating_entry_point(fmt, bkv):
         assert torch.equal(got, ref)
         assert torch.equal(out16, ref16)
         assert np.isfinite(got.cpu().numpy()).all()
+
+
+@pytest.mark.gpu
+def test_noalloc_256_query_workgroups():
+    """The bench step's launch shape (256-key tiles, 256-query workgroups,
+    non-causal) through the no-allocation entry point: two calls in a row, the
+    second smaller, each bit-equal to the allocating entry point."""
+    torch = torch_dev()
+    f = bd.SAGE_BKV256 | bd.SAGE_WG256
+    for (B, H, N, D, dtype, seed) in [(2, 3, 1000, 128, 1, 510), (1, 2, 300, 64, 0, 511)]:
+        say("noalloc wg256 B=%d H=%d N=%d D=%d" % (B, H, N, D))
+        q, k, v = wl.make_inputs(B, H, N, D, dtype, seed=seed, k_bias_var=4.0, outlier_frac=0.02)
+        qd, kd, vd = (to_dev(x, dtype) for x in (q, k, v))
+        ref = bd.sage_attn_fp4_fwd(qd, kd, vd, causal=False, fmt=f)
+        got = bd.sage_attn_fp4_fwd_noalloc(qd, kd, vd, causal=False, fmt=f)
+        torch.cuda.synchronize()
+        assert torch.equal(got, ref)
+        assert np.isfinite(got.cpu().numpy()).all()
