@@ -109,3 +109,18 @@ def test_quant_configs_full_size(ci):
                 assert np.array_equal(s, os_.reshape(s.shape)), (ci, role, fmt)
             else:
                 check_role(x, w.in_dtype, role, fmt)
+
+
+@pytest.mark.parametrize("fmt", [0, 1])
+def test_quant_work_split_ragged(fmt):
+    """The V quantizer walks contiguous ranges of (head, 128-token tile), one
+    workgroup per CU: 409 heads x 10 tiles = 4090 tiles make, on 256 CUs, 16
+    tiles per workgroup, a grid of 256 (so the XCD remap is on) and a last
+    workgroup with 10; the last tile of every head is partial (N = 1270).  The
+    K quantizer's steps of four units per thread end inside a workgroup's
+    range.  Every code, scale and the mean against the oracle, all roles."""
+    B, H, N, D = 1, 409, 1270, 64
+    say("quant work split", (B, H, N, D), "fmt", fmt)
+    q, k, v = wl.make_inputs(B, H, N, D, 1, seed=4090 + fmt, k_bias_var=4.0, outlier_frac=0.02)
+    for role, x in ((0, q), (1, k), (2, v)):
+        check_role(x, 1, role, fmt)
