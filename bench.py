@@ -73,6 +73,18 @@ def traffic_from_counters(variant: str = "default"):
     return float(c[variant]["hbm_bytes_per_launch"])
 
 
+def cpu_model() -> str:
+    """The host CPU's model name, as /proc/cpuinfo gives it."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, q, k, v, budget_s: float = 15.0):
     """The oracle, as is, on a bounded sample of query rows of head 0."""
     import oracle
@@ -97,7 +109,7 @@ def cpu_baseline(w, q, k, v, budget_s: float = 15.0):
     oracle.attn(q1, k1, v1, w.in_dtype, w.causal, oracle.FMT_MX, w.bkv, rows=rows, nthreads=threads)
     dt = time.perf_counter() - t0
     ops = 4.0 * nrows * N * D * (0.5 if w.causal else 1.0)
-    return {"value": ops / dt / 1e12, "unit": "TOPS", "cores": threads, "kind": "oracle",
+    return {"value": ops / dt / 1e12, "unit": "TOPS", "cores": threads, "cpu_model": cpu_model(), "kind": "oracle",
             "sample": "%d random query rows of head 0 (of %d x %d), K/V quantization of that head included, %.1f s"
                       % (nrows, w.B * w.H, N, dt)}
 
@@ -414,9 +426,12 @@ def main():
     ap.add_argument("--no-configs", action="store_true", help="skip the attention-kernel timings of the other workloads")
     ap.add_argument("--no-int8", action="store_true", help="skip the 8-bit attention forward")
     ap.add_argument("--wg256", action="store_true", help="--mode attn: 256-query workgroups (SAGE_WG256)")
-    ap.add_argument("--mode", choices=["full", "attn", "attn_nv16", "attn_int8", "attn_int8_bwd", "copy", "rates"],
+    ap.add_argument("--mode", choices=["full", "attn", "shapes", "attn_nv16", "attn_int8", "attn_int8_bwd", "copy",
+                                       "rates"],
                     default="full",
-                    help="attn: only the attention kernel (for counter runs); attn_nv16: only the NV16 kernel on "
+                    help="attn: only the attention kernel (for counter runs); shapes: the step and the attention "
+                         "kernel with 256- and 128-query workgroups, alternated in one process; "
+                         "attn_nv16: only the NV16 kernel on "
                          "B1 H24 N76800 D64; attn_int8: only the 8-bit one; "
                          "attn_int8_bwd: only the 8-bit backward (after one 8-bit forward for O and L); "
                          "copy: a plain 1 GiB device copy (calibrates FETCH_SIZE / WRITE_SIZE); "
@@ -508,6 +523,45 @@ def main():
                           "ops_per_launch": 10.0 * B * H * N * N * D * (0.5 if w.causal else 1.0)}))
         return
 
+    if args.mode == "shapes":
+        # the two workgroup shapes of the 256-key kernel, alternated args.warmup rounds (order swapped each
+        # round), args.steps launches per timing: the whole step and the attention kernel alone
+        qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q)
+        kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K)
+        vq = bd.sage_quant_fp4(vd, bd.SAGE_ROLE_V)
+        shapes = {"wg256": tile | bd.SAGE_WG256, "wg128": tile}
+        wss = {n: torch.empty(bd.attn_fp4_workspace_size(B, H, N, D, fmt | f), dtype=torch.uint8, device=dev)
+               for n, f in shapes.items()}
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+        def timed(fn):
+            e0.record()
+            for _ in range(args.steps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / args.steps
+
+        for n, f in shapes.items():
+            warm(torch, lambda: bd.sage_attn_fp4_fwd(qd, kd, vd, causal=w.causal, fmt=bd.SAGE_FMT_MXFP4 | f,
+                                                     out_f32=True, out=o, workspace=wss[n]))
+        res = {"step_" + n: [] for n in shapes}
+        res.update({"attn_" + n: [] for n in shapes})
+        for r in range(max(2, args.warmup)):
+            order = list(shapes) if r % 2 == 0 else list(shapes)[::-1]
+            for n in order:
+                f = shapes[n]
+                res["step_" + n].append(timed(lambda: bd.sage_attn_fp4_fwd(
+                    qd, kd, vd, causal=w.causal, fmt=bd.SAGE_FMT_MXFP4 | f, out_f32=True, out=o, workspace=wss[n])))
+            for n in order:
+                f = shapes[n]
+                res["attn_" + n].append(timed(lambda: bd.sage_attn_fp4_fwd_prequant(
+                    qq[:2], kq[:2], vq[:2], (B, H, N, D), causal=w.causal, fmt=f, out=o)))
+            log("round %d: %s" % (r, ", ".join("%s %.4f ms" % (k_, v_[-1]) for k_, v_ in res.items())))
+        print(json.dumps({"mode": "shapes", "workload": w.name, "launches_per_timing": args.steps,
+                          "ms": res, "mean_ms": {k_: sum(v_) / len(v_) for k_, v_ in res.items()}}))
+        return
+
     if args.mode == "attn":
         qq = bd.sage_quant_fp4(qd, bd.SAGE_ROLE_Q)
         kq = bd.sage_quant_fp4(kd, bd.SAGE_ROLE_K)
@@ -593,7 +647,9 @@ def main():
             torch.cuda.synchronize()
             t_bf = e0.elapsed_time(e1) / 1e3 / args.steps
             bf16 = {"tops": ops / t_bf / 1e12, "ms": t_bf * 1e3,
-                    "frac_of_bf16_peak": ops / t_bf / 1e12 / PEAK_BF16_TFLOPS}
+                    "frac_of_bf16_peak": ops / t_bf / 1e12 / PEAK_BF16_TFLOPS,
+                    "accuracy_vs_exact": accuracy_vs_exact(torch, qd, kd, vd, o, w)}
+            log("bf16 kernel %.3f ms, cossim %.5f" % (t_bf * 1e3, bf16["accuracy_vs_exact"]["cossim"]))
         except bd.SageError as ex:
             log("bf16 kernel unavailable:", ex)
 

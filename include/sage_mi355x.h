@@ -53,7 +53,7 @@ typedef enum {
 #define SAGE_BKV256         0x80u /* KV tile of 256 tokens (MXFP4 attention only)          */
 #define SAGE_WG256          0x100u /* 256 queries per workgroup instead of 128: each K^/V^T
                                       tile is fetched from L2 once per 256 queries (about
-                                      half the fetch traffic) within 2% of the time.  Only
+                                      half the fetch traffic) for about 1% more time.  Only
                                       with SAGE_BKV256, non-causal, without SAGE_SMOOTH_Q;
                                       otherwise SAGE_ERR_UNSUPPORTED.  Same results.      */
 #define SAGE_FMT_ALL_BITS   0x1FFu
