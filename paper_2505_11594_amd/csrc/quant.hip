@@ -329,7 +329,7 @@ constexpr int VT = 128;       // tokens per tile (a V^T row segment of 64 bytes)
 // One workgroup per CU, two tiles in flight: 79.7 us on B1 H32 N32768 D128,
 // against 96 us for one tile per workgroup and, with the same loop, 92 us at
 // two workgroups per CU (one tile ahead: 83.5 us at one per CU, 87, 96 and
-// 101 us at two, three and four).
+// 101 us at two, three and four); with the scale bytes staged, 71.4 us.
 constexpr int V_WG_PER_CU = 1;
 
 template <int D, bool BF16, int FMT>
@@ -339,6 +339,13 @@ __global__ __launch_bounds__(256) void quant_v_kernel(const uint16_t* __restrict
   constexpr int NB = (FMT == kFmtMX) ? 32 : 16;
   // all lanes of a wave read one row (consecutive channels): no padding needed
   __shared__ uint16_t tile[VT][D];
+  // The scale bytes of up to ST_TILES consecutive tiles of one head, per
+  // V^T row: one 128-byte segment of the row, stored whole (written one byte
+  // per block as they come, a row's line would fill over the workgroup's
+  // whole range and partly leave L2 before it is complete).  Rows are 132
+  // bytes apart, so the byte writes of a wave's channels fall in different banks.
+  constexpr int SPT = VT / NB, ST_TILES = 128 / SPT, ST_ROW = 132;
+  __shared__ __attribute__((aligned(16))) uint8_t sst[D * ST_ROW];
   const int ntt = (Np + VT - 1) / VT;
   // Workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous
   // range of (bh, tile), so the two 64-byte halves of every 128-byte V^T line
@@ -368,6 +375,20 @@ __global__ __launch_bounds__(256) void quant_v_kernel(const uint16_t* __restrict
   constexpr int BPT = VT / NB / TPG;         // token blocks per thread
   static_assert(BPT >= 1 && TPG * (D / CPT) == 256, "tile shape");
   const int c0 = (tid % (D / CPT)) * CPT, part = tid / (D / CPT);
+  int nst = 0;                               // tiles staged in sst (consecutive, one head)
+  auto flush = [&](int lin_last) {           // workgroup-uniform
+    __syncthreads();                         // every staged byte is written
+    const int lin0 = lin_last - nst + 1;
+    const int t0 = (lin0 % ntt) * VT;
+    const size_t bh = (size_t)(lin0 / ntt);
+    const int ndw = nst * SPT / 4;           // dwords per row (SPT is 4 or 8)
+    for (int e = tid; e < D * ndw; e += 256) {
+      const int c = e / ndw, i = e % ndw;
+      *reinterpret_cast<uint32_t*>(scales + (bh * D + c) * (Np / NB) + t0 / NB + 4 * i) =
+          *reinterpret_cast<const uint32_t*>(&sst[c * ST_ROW + 4 * i]);
+    }
+    nst = 0;                                 // sst is written again only after the next tile's barriers
+  };
   auto step = [&](int lin, uint4 (&raw)[LPT]) {
     __syncthreads();                         // every thread is done with the previous tile in LDS
 #pragma unroll
@@ -427,9 +448,11 @@ __global__ __launch_bounds__(256) void quant_v_kernel(const uint16_t* __restrict
         uint8_t* dst = codes + (bh * D + c) * (Np / 2) + (t0 + blk * NB) / 2;
         if (NB == 32) *reinterpret_cast<uint4*>(dst) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
         else *reinterpret_cast<uint2*>(dst) = make_uint2(wd[0], wd[1]);
-        scales[(bh * D + c) * (Np / NB) + (t0 + blk * NB) / NB] = (uint8_t)sbyte;
+        sst[c * ST_ROW + nst * SPT + blk] = (uint8_t)sbyte;
       }
     }
+    ++nst;
+    if (nst == ST_TILES || lin + 1 >= last || (lin + 1) / ntt != lin / ntt) flush(lin);
   };
   for (int lin = first; lin < last; lin += 2) {
     step(lin, ra);
